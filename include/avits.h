@@ -1,0 +1,210 @@
+/*
+ * avits.h — C ABI of the AViTS selective-upsampling step on AMD MI355X (gfx950).
+ *
+ * The library implements the hot path of spatiotemporal token selection for
+ * dynamic-resolution diffusion transformers (AViTS, Section 3): score every
+ * high-resolution latent token, select the top-K, gather them with the text
+ * (and reference) tokens into a compacted sequence while the other tokens are
+ * upsampled from the low-resolution latent, run one MMDiT joint-attention
+ * block on the compacted sequence, and scatter the result back.
+ *
+ * Conventions shared by every entry point:
+ *  - Every tensor argument is a DEVICE pointer owned by the caller, row-major
+ *    and contiguous, 16-byte aligned.  The library never allocates device
+ *    memory; scratch space comes through a caller-provided workspace whose
+ *    size the matching *_workspace_bytes() query returns.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Calls are
+ *    asynchronous: they enqueue kernels and return; no host<->device copy and
+ *    no synchronisation happens inside.
+ *  - Return value: AVITS_OK, or a negative error code.  Validation uses the
+ *    host-side arguments only (shapes, pointers, sizes); the contents of
+ *    device buffers are never inspected.  After an error nothing was
+ *    enqueued, except for AVITS_ERR_HIP, which reports a launch failure.
+ *    avits_last_error() returns the message of the calling thread's last
+ *    failure.
+ *  - `dtype` selects the storage type of every non-index tensor of a call:
+ *    AVITS_F32 or AVITS_BF16.  Scores, log-sum-exps and all accumulation are
+ *    fp32; indices and positions are int32.
+ *  - Calls that overlap on one stream are ordered; calls on different
+ *    streams that share a workspace race.
+ */
+#ifndef AVITS_H
+#define AVITS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  AVITS_OK = 0,
+  AVITS_ERR_INVALID_ARG = -1, /* bad shape, null pointer, k out of range, ... */
+  AVITS_ERR_UNSUPPORTED = -2, /* dtype / head dim / device not supported    */
+  AVITS_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required */
+  AVITS_ERR_HIP = -4          /* a kernel launch failed                      */
+};
+
+enum { AVITS_F32 = 0, AVITS_BF16 = 1 };
+enum { AVITS_UP_NEAREST = 0, AVITS_UP_BILINEAR = 1 };
+enum { AVITS_BLOCK_DOUBLE = 0, AVITS_BLOCK_SINGLE = 1 };
+
+/* Version string "major.minor.patch". */
+const char* avits_version(void);
+
+/* Message of the calling thread's last failed call ("" if none). */
+const char* avits_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * avits_score — spatiotemporal importance (Section 3.3; Eqs. spatial,
+ * dit_attn, zbar, step_var and joint).
+ *
+ * For each of the N scored image tokens i:
+ *   A_i = (1/H) sum_h sum_{j<L} exp(q_ih . k_jh / sqrt(d) - row_lse[h, i])
+ *       (the text share of the joint image->text attention of Eq. dit_attn;
+ *        row_lse is the log-sum-exp of token i's logits over the joint key
+ *        set, e.g. from avits_joint_lse),
+ *   V_i = (1/D_f) sum_c (feat_t[i,c] - feat_prev[i,c])^2 / 2
+ *       (Eq. step_var with the two consecutive steps as the snapshots),
+ *   S_i = alpha * (A_i - min A)/(max A - min A + eps)
+ *       + (1 - alpha) * (V_i - min V)/(max V - min V + eps).
+ *
+ * latent_q  [N, H, d]   image queries after QK-norm and RoPE   (dtype)
+ * text_k    [L, H, d]   text keys after QK-norm                (dtype)
+ * row_lse   [H, N]      fp32
+ * feat_t, feat_prev [N, D_f]                                   (dtype)
+ * scores    [N]         fp32 output S
+ * a_raw, v_raw [N]      fp32 outputs A and V; each may be NULL
+ * Requires N >= 1, L >= 1, H >= 1, d in {64, 128}, D_f >= 1,
+ * 0 <= alpha <= 1, eps >= 0.
+ * ---------------------------------------------------------------------- */
+size_t avits_score_workspace_bytes(int64_t N, int32_t H);
+int avits_score(const void* latent_q, const void* text_k, const float* row_lse,
+                const void* feat_t, const void* feat_prev,
+                int64_t N, int64_t L, int32_t H, int32_t d, int64_t D_f,
+                float alpha, float eps, int dtype,
+                float* scores, float* a_raw, float* v_raw,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_select — top-K selection (Eq. topk).
+ *
+ * Writes the indices of the k largest scores to idx[0..k) in strictly
+ * ascending order.  Order is (score descending, index ascending): among equal
+ * scores the lowest index wins, so the result is deterministic; -0.0 equals
+ * +0.0 and NaN ranks below every number.  k == 0 enqueues nothing.
+ * scores [N] fp32; idx [k] int32.  Requires N >= 1 and 0 <= k <= N.
+ * ---------------------------------------------------------------------- */
+size_t avits_select_workspace_bytes(int64_t N);
+int avits_select(const float* scores, int64_t N, int64_t k, int32_t* idx,
+                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_gather_upsample — Stage-2 re-layout (Section 3.2).
+ *
+ * With N = 4*H_lr*W_lr high-res tokens in raster order on a (2H_lr)x(2W_lr)
+ * grid and the selected indices idx[0..k) (ascending, unique, < N):
+ *   compact[0 .. n_prefix)        = prefix rows (text, then reference)
+ *   compact[n_prefix + j]         = highres_prev[idx[j]]
+ *   pos_sel[j]                    = (0, idx[j] / W_hr, idx[j] % W_hr)
+ *   canvas[p]                     = highres_prev[p]      if p is selected
+ *                                   upsample2x(lowres)[p] otherwise
+ * mode AVITS_UP_NEAREST copies the low-res cell (p's row/2, col/2);
+ * AVITS_UP_BILINEAR interpolates with half-pixel centres and edge clamping
+ * (fp32 arithmetic).  canvas may alias highres_prev (selected rows are then
+ * left in place); it may not overlap any other argument.
+ * lowres [H_lr*W_lr, D], highres_prev [N, D], prefix [n_prefix, D] (may be
+ * NULL when n_prefix == 0), compact [n_prefix + k, D], pos_sel [k, 3] int32,
+ * canvas [N, D].  The caller writes the prefix rows' positions itself.
+ * ---------------------------------------------------------------------- */
+int avits_gather_upsample(const void* lowres, const void* highres_prev, const void* prefix,
+                          const int32_t* idx, int64_t k, int32_t H_lr, int32_t W_lr,
+                          int64_t n_prefix, int64_t D, int mode, int dtype,
+                          void* compact, int32_t* pos_sel, void* canvas, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_block_forward — one MMDiT joint-attention block on the compacted
+ * sequence (Section 3.3.1: joint self-attention over [C; Z], Eq. joint_qk,
+ * with the model's QK-normalisation), FLUX-style:
+ *
+ * double (per stream s; rows [0, n_txt) use `txt`, the rest `img`):
+ *   h = LN(x)(1 + scale1) + shift1;  q,k,v = h W_qkv^T + b_qkv;
+ *   q,k = RMSNorm_d(.) * g;  RoPE(q, k) at pos;  o = softmax(q k^T/sqrt d) v
+ *   over all S rows;  x += gate1 (o W_o^T + b_o);
+ *   x += gate2 (GELU_tanh((LN(x)(1 + scale2) + shift2) W_1^T + b_1) W_2^T + b_2)
+ * single (one weight set):
+ *   h = LN(x)(1 + scale) + shift;  [q k v m] = h W_in^T + b_in;
+ *   q,k normalised and rotated;  x += gate ([attn(q,k,v); GELU_tanh(m)] W_out^T + b_out)
+ * LN has no affine and eps 1e-6; RMSNorm eps 1e-6.  RoPE: three axes
+ * (frame, row, col) over head-dim slices (d/8, 7d/16, 7d/16), theta 10000,
+ * adjacent pairs (2m, 2m+1) rotated by pos * theta^(-2m/n).
+ * Modulation rows: double (shift1, scale1, gate1, shift2, scale2, gate2);
+ * single (shift, scale, gate).  Weights use the [out, in] layout.
+ *
+ * x_in, x_out [S, D] with S = n_txt + n_img, D = H*d (x_out must not alias
+ * x_in); pos [S, 3] int32; lse_out [H, S] fp32 or NULL.  For the single kind
+ * n_txt only splits the count (both parts use the same weights).  S == 0 is a
+ * no-op.  Requires d in {64, 128}; all weight pointers of the used kind
+ * non-NULL.
+ * ---------------------------------------------------------------------- */
+typedef struct avits_double_stream_weights {
+  const void* mod;     /* [6, D]        */
+  const void* w_qkv;   /* [3D, D]       */
+  const void* b_qkv;   /* [3D]          */
+  const void* g_q;     /* [d]           */
+  const void* g_k;     /* [d]           */
+  const void* w_o;     /* [D, D]        */
+  const void* b_o;     /* [D]           */
+  const void* w_mlp1;  /* [F, D], F = mlp_hidden */
+  const void* b_mlp1;  /* [F]           */
+  const void* w_mlp2;  /* [D, F]        */
+  const void* b_mlp2;  /* [D]           */
+} avits_double_stream_weights;
+
+typedef struct avits_single_weights {
+  const void* mod;     /* [3, D]        */
+  const void* w_in;    /* [3D + F, D]   */
+  const void* b_in;    /* [3D + F]      */
+  const void* g_q;     /* [d]           */
+  const void* g_k;     /* [d]           */
+  const void* w_out;   /* [D, D + F]    */
+  const void* b_out;   /* [D]           */
+} avits_single_weights;
+
+typedef struct avits_block_weights {
+  int32_t kind;        /* AVITS_BLOCK_DOUBLE or AVITS_BLOCK_SINGLE */
+  int32_t mlp_hidden;  /* F (4*D for FLUX)                         */
+  avits_double_stream_weights txt, img;  /* kind == DOUBLE */
+  avits_single_weights single;           /* kind == SINGLE */
+} avits_block_weights;
+
+size_t avits_block_workspace_bytes(int32_t kind, int64_t S, int32_t H, int32_t d,
+                                   int32_t mlp_hidden, int dtype);
+int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos,
+                        int64_t n_txt, int64_t n_img, const avits_block_weights* w,
+                        int32_t H, int32_t d, int dtype, float* lse_out,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_scatter — Stage-3 re-layout: canvas[idx[j]] = out[row_offset + j]
+ * for j < k.  out [row_offset + k, D], idx [k] int32 (unique, < rows of
+ * canvas), canvas [*, D].  k == 0 enqueues nothing.
+ * ---------------------------------------------------------------------- */
+int avits_scatter(const void* out, const int32_t* idx, int64_t k, int64_t row_offset,
+                  int64_t D, int dtype, void* canvas, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_joint_lse — log-sum-exp of each image query's logits over the joint
+ * key set (the softmax normaliser of Eq. dit_attn):
+ *   lse[h, i] = log sum_{j < Nk} exp(q_ih . k_jh / sqrt(d))   (natural log)
+ * q [N, H, d], k_all [Nk, H, d] (dtype); lse [H, N] fp32.
+ * Requires N >= 1, Nk >= 1, d in {64, 128}.
+ * ---------------------------------------------------------------------- */
+int avits_joint_lse(const void* q, const void* k_all, int64_t N, int64_t Nk,
+                    int32_t H, int32_t d, int dtype, float* lse, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AVITS_H */

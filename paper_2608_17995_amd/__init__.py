@@ -1,0 +1,17 @@
+"""AViTS selective-upsampling step on MI355X: Python binding of libavits.so.
+
+Argument marshalling only.  Every entry point mirrors the C function of the
+same name in include/avits.h: tensors are passed as device pointers, the
+stream is torch's current HIP stream, and a non-zero return code raises
+AvitsError.  Every computation runs in the HIP kernels of libavits.so; there
+is no CPU fallback, and calling any entry point without the built library
+raises.
+"""
+from ._binding import (  # noqa: F401
+    AvitsError, load, lib_path, version,
+    F32, BF16, UP_NEAREST, UP_BILINEAR, BLOCK_DOUBLE, BLOCK_SINGLE,
+    avits_score_workspace_bytes, avits_score,
+    avits_select_workspace_bytes, avits_select,
+    avits_gather_upsample, avits_scatter, avits_joint_lse,
+    avits_block_workspace_bytes, avits_block_forward, BlockWeights,
+)

@@ -1,0 +1,227 @@
+"""ctypes binding of libavits.so (argument marshalling only)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+F32, BF16 = 0, 1
+UP_NEAREST, UP_BILINEAR = 0, 1
+BLOCK_DOUBLE, BLOCK_SINGLE = 0, 1
+
+_c_void_p, _i64, _i32, _f32, _size = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+
+
+class AvitsError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"avits error {code}: {msg}")
+        self.code = code
+
+
+class _DoubleStream(ctypes.Structure):
+    _fields_ = [(n, _c_void_p) for n in ("mod", "w_qkv", "b_qkv", "g_q", "g_k", "w_o", "b_o",
+                                          "w_mlp1", "b_mlp1", "w_mlp2", "b_mlp2")]
+
+
+class _Single(ctypes.Structure):
+    _fields_ = [(n, _c_void_p) for n in ("mod", "w_in", "b_in", "g_q", "g_k", "w_out", "b_out")]
+
+
+class _BlockWeights(ctypes.Structure):
+    _fields_ = [("kind", _i32), ("mlp_hidden", _i32), ("txt", _DoubleStream), ("img", _DoubleStream),
+                ("single", _Single)]
+
+
+_SIGS = {
+    "avits_version": (ctypes.c_char_p, []),
+    "avits_last_error": (ctypes.c_char_p, []),
+    "avits_score_workspace_bytes": (_size, [_i64, _i32]),
+    "avits_score": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i32, _i32,
+                                   _i64, _f32, _f32, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                   _size, _c_void_p]),
+    "avits_select_workspace_bytes": (_size, [_i64]),
+    "avits_select": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _size, _c_void_p]),
+    "avits_gather_upsample": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _i64, _i32, _i32, _i64,
+                                             _i64, ctypes.c_int, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p,
+                                             _c_void_p]),
+    "avits_block_workspace_bytes": (_size, [_i32, _i64, _i32, _i32, _i32, ctypes.c_int]),
+    "avits_block_forward": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _i64,
+                                           ctypes.POINTER(_BlockWeights), _i32, _i32, ctypes.c_int, _c_void_p,
+                                           _c_void_p, _size, _c_void_p]),
+    "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, ctypes.c_int, _c_void_p, _c_void_p]),
+    "avits_joint_lse": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i32, _i32, ctypes.c_int, _c_void_p,
+                                       _c_void_p]),
+}
+
+EXPORTS = tuple(_SIGS)
+
+
+def lib_path() -> str:
+    return os.path.join(_HERE, "libavits.so")
+
+
+def load():
+    """Load libavits.so (after torch, so both use torch's HIP runtime)."""
+    global _LIB
+    if _LIB is None:
+        import torch  # noqa: F401  (binds libamdhip64 before the library is loaded)
+        path = lib_path()
+        if not os.path.exists(path):
+            raise AvitsError(-2, f"{path} is missing; build it with `python -m paper_2608_17995_amd.build`")
+        lib = ctypes.CDLL(path)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(lib, name)
+            fn.restype, fn.argtypes = res, args
+        _LIB = lib
+    return _LIB
+
+
+def version() -> str:
+    return load().avits_version().decode()
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise AvitsError(rc, load().avits_last_error().decode())
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise AvitsError(-2, f"unsupported dtype {t.dtype}")
+
+
+def _dev(t, name, dtype=None):
+    """Device pointer of a contiguous GPU tensor (None passes NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise AvitsError(-1, f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise AvitsError(-1, f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise AvitsError(-1, f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _workspace(ws, nbytes, device):
+    import torch
+    if ws is None:
+        ws = torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+    return ws, _dev(ws, "workspace"), ws.numel() * ws.element_size()
+
+
+# ---------------------------------------------------------------------------
+
+def avits_score_workspace_bytes(N: int, H: int) -> int:
+    return load().avits_score_workspace_bytes(N, H)
+
+
+def avits_score(latent_q, text_k, row_lse, feat_t, feat_prev, alpha, eps, scores,
+                a_raw=None, v_raw=None, workspace=None, stream=None):
+    import torch
+    N, H, d = latent_q.shape
+    L = text_k.shape[0]
+    D_f = feat_t.shape[1]
+    dt = latent_q.dtype
+    ws, wsp, wsb = _workspace(workspace, avits_score_workspace_bytes(N, H), latent_q.device)
+    _check(load().avits_score(
+        _dev(latent_q, "latent_q"), _dev(text_k, "text_k", dt), _dev(row_lse, "row_lse", torch.float32),
+        _dev(feat_t, "feat_t", dt), _dev(feat_prev, "feat_prev", dt), N, L, H, d, D_f, alpha, eps,
+        _dtype_code(latent_q), _dev(scores, "scores", torch.float32), _dev(a_raw, "a_raw", torch.float32),
+        _dev(v_raw, "v_raw", torch.float32), wsp, wsb, _stream(stream)))
+    return scores
+
+
+def avits_select_workspace_bytes(N: int) -> int:
+    return load().avits_select_workspace_bytes(N)
+
+
+def avits_select(scores, k, idx, workspace=None, stream=None):
+    import torch
+    N = scores.shape[0]
+    ws, wsp, wsb = _workspace(workspace, avits_select_workspace_bytes(N), scores.device)
+    _check(load().avits_select(_dev(scores, "scores", torch.float32), N, k, _dev(idx, "idx", torch.int32),
+                               wsp, wsb, _stream(stream)))
+    return idx
+
+
+def avits_gather_upsample(lowres, highres_prev, prefix, idx, H_lr, W_lr, compact, pos_sel, canvas,
+                          mode=UP_NEAREST, stream=None):
+    import torch
+    dt = lowres.dtype
+    n_prefix = 0 if prefix is None else prefix.shape[0]
+    _check(load().avits_gather_upsample(
+        _dev(lowres, "lowres"), _dev(highres_prev, "highres_prev", dt),
+        _dev(prefix, "prefix", dt) if n_prefix else None, _dev(idx, "idx", torch.int32), idx.shape[0],
+        H_lr, W_lr, n_prefix, lowres.shape[1], mode, _dtype_code(lowres), _dev(compact, "compact", dt),
+        _dev(pos_sel, "pos_sel", torch.int32), _dev(canvas, "canvas", dt), _stream(stream)))
+    return compact, pos_sel, canvas
+
+
+def avits_scatter(out, idx, row_offset, canvas, stream=None):
+    import torch
+    _check(load().avits_scatter(_dev(out, "out"), _dev(idx, "idx", torch.int32), idx.shape[0], row_offset,
+                                out.shape[1], _dtype_code(out), _dev(canvas, "canvas", out.dtype), _stream(stream)))
+    return canvas
+
+
+def avits_joint_lse(q, k_all, lse, stream=None):
+    import torch
+    N, H, d = q.shape
+    _check(load().avits_joint_lse(_dev(q, "q"), _dev(k_all, "k_all", q.dtype), N, k_all.shape[0], H, d,
+                                  _dtype_code(q), _dev(lse, "lse", torch.float32), _stream(stream)))
+    return lse
+
+
+class BlockWeights:
+    """Device weights of one block, packed into the C struct (keeps the tensors alive)."""
+
+    def __init__(self, kind: int, txt: dict | None = None, img: dict | None = None, single: dict | None = None):
+        self.kind = kind
+        self.tensors = {"txt": txt or {}, "img": img or {}, "single": single or {}}
+        self.c = _BlockWeights()
+        self.c.kind = kind
+        if kind == BLOCK_DOUBLE:
+            ref = (txt or img)
+            self.c.mlp_hidden = ref["w_mlp1"].shape[0]
+            for part, w in (("txt", txt), ("img", img)):
+                if w:
+                    cs = getattr(self.c, part)
+                    for name, _ in _DoubleStream._fields_:
+                        setattr(cs, name, _dev(w[name], f"{part}.{name}"))
+        else:
+            D = single["w_out"].shape[0]
+            self.c.mlp_hidden = single["w_out"].shape[1] - D
+            for name, _ in _Single._fields_:
+                setattr(self.c.single, name, _dev(single[name], f"single.{name}"))
+
+
+def avits_block_workspace_bytes(kind: int, S: int, H: int, d: int, mlp_hidden: int, dtype: int) -> int:
+    return load().avits_block_workspace_bytes(kind, S, H, d, mlp_hidden, dtype)
+
+
+def avits_block_forward(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H, lse_out=None,
+                        workspace=None, stream=None):
+    import torch
+    S, D = x_in.shape
+    d = D // H
+    code = _dtype_code(x_in)
+    ws, wsp, wsb = _workspace(
+        workspace, avits_block_workspace_bytes(weights.kind, S, H, d, weights.c.mlp_hidden, code), x_in.device)
+    _check(load().avits_block_forward(
+        _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), n_txt, n_img,
+        ctypes.byref(weights.c), H, d, code, _dev(lse_out, "lse_out", torch.float32), wsp, wsb, _stream(stream)))
+    return x_out

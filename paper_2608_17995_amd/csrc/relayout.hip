@@ -1,0 +1,174 @@
+// Stage-2 gather / 2x upsample and Stage-3 scatter (Section 3.2).
+//
+// Pure data movement, HBM-bound.  Each wavefront moves one token row at a time
+// with 16-byte vector accesses; a row is D elements (6 KiB for D = 3072 bf16).
+// One launch covers every row job of the gather so small grids never idle the
+// chip: prefix copies, selected-row copies (+ their positions) and the
+// upsampled fill of unselected canvas rows.
+#include "common.h"
+
+namespace avits {
+namespace {
+
+constexpr int kRowsPerBlock = 4;  // one wavefront per row job
+
+// Copy `bytes` (multiple of 16) from src to dst with the 64 lanes of a wave.
+__device__ __forceinline__ void wave_copy_row(const char* __restrict__ src, char* __restrict__ dst,
+                                              int64_t bytes, int lane) {
+  const u32x4* s = reinterpret_cast<const u32x4*>(src);
+  u32x4* d = reinterpret_cast<u32x4*>(dst);
+  const int64_t n = bytes / 16;
+  for (int64_t i = lane; i < n; i += kWave) d[i] = s[i];
+}
+
+// First position in the ascending idx[0..k) not below p.
+__device__ __forceinline__ int64_t lower_bound(const int32_t* idx, int64_t k, int64_t p) {
+  int64_t lo = 0, hi = k;
+  while (lo < hi) {
+    int64_t mid = (lo + hi) >> 1;
+    if (idx[mid] < p) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+template <typename T>
+__device__ __forceinline__ void bilinear_row(const T* __restrict__ low, T* __restrict__ dst, int64_t p,
+                                             int H_lr, int W_lr, int64_t D, int lane) {
+  const int W_hr = 2 * W_lr;
+  const int r = int(p / W_hr), c = int(p % W_hr);
+  // Source coordinate (o + 0.5)/2 - 0.5 clamped at 0; taps clamped to the grid.
+  auto taps = [](int o, int n, int& i0, int& i1, float& w1) {
+    float src = fmaxf((o + 0.5f) * 0.5f - 0.5f, 0.f);
+    i0 = min(int(floorf(src)), n - 1);
+    i1 = min(i0 + 1, n - 1);
+    w1 = src - float(i0);
+  };
+  int r0, r1, c0, c1;
+  float wr1, wc1;
+  taps(r, H_lr, r0, r1, wr1);
+  taps(c, W_lr, c0, c1, wc1);
+  const float wr0 = 1.f - wr1, wc0 = 1.f - wc1;
+  const T* a = low + (int64_t(r0) * W_lr + c0) * D;
+  const T* b = low + (int64_t(r0) * W_lr + c1) * D;
+  const T* e = low + (int64_t(r1) * W_lr + c0) * D;
+  const T* f = low + (int64_t(r1) * W_lr + c1) * D;
+  for (int64_t i = lane; i < D; i += kWave) {
+    // Rows first, then columns (the order of the separable definition).
+    float left = wr0 * ld(a, i) + wr1 * ld(e, i);
+    float right = wr0 * ld(b, i) + wr1 * ld(f, i);
+    st(dst, i, wc0 * left + wc1 * right);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
+    const T* __restrict__ lowres, const T* highres, const T* __restrict__ prefix,
+    const int32_t* __restrict__ idx, int64_t k, int H_lr, int W_lr, int64_t n_prefix, int64_t D,
+    int mode, T* __restrict__ compact, int32_t* __restrict__ pos_sel, T* canvas, int canvas_aliases) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t job = int64_t(blockIdx.x) * kRowsPerBlock + threadIdx.x / kWave;
+  const int W_hr = 2 * W_lr;
+  const int64_t N = int64_t(4) * H_lr * W_lr;
+  const int64_t row_bytes = D * int64_t(sizeof(T));
+  if (job < n_prefix) {
+    wave_copy_row(reinterpret_cast<const char*>(prefix + job * D),
+                  reinterpret_cast<char*>(compact + job * D), row_bytes, lane);
+    return;
+  }
+  int64_t j = job - n_prefix;
+  if (j < k) {
+    const int64_t p = idx[j];
+    const char* src = reinterpret_cast<const char*>(highres + p * D);
+    wave_copy_row(src, reinterpret_cast<char*>(compact + (n_prefix + j) * D), row_bytes, lane);
+    if (!canvas_aliases) wave_copy_row(src, reinterpret_cast<char*>(canvas + p * D), row_bytes, lane);
+    if (lane == 0) {
+      pos_sel[3 * j + 0] = 0;
+      pos_sel[3 * j + 1] = int32_t(p / W_hr);
+      pos_sel[3 * j + 2] = int32_t(p % W_hr);
+    }
+    return;
+  }
+  const int64_t p = j - k;
+  if (p >= N) return;
+  const int64_t at = lower_bound(idx, k, p);
+  if (at < k && idx[at] == p) return;  // selected: handled by its own job
+  if (mode == AVITS_UP_NEAREST) {
+    const int64_t src_row = int64_t((p / W_hr) >> 1) * W_lr + ((p % W_hr) >> 1);
+    wave_copy_row(reinterpret_cast<const char*>(lowres + src_row * D),
+                  reinterpret_cast<char*>(canvas + p * D), row_bytes, lane);
+  } else {
+    bilinear_row(lowres, canvas + p * D, p, H_lr, W_lr, D, lane);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kWave * kRowsPerBlock) void scatter_kernel(
+    const T* __restrict__ out, const int32_t* __restrict__ idx, int64_t k, int64_t row_offset,
+    int64_t D, T* __restrict__ canvas) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t j = int64_t(blockIdx.x) * kRowsPerBlock + threadIdx.x / kWave;
+  if (j >= k) return;
+  wave_copy_row(reinterpret_cast<const char*>(out + (row_offset + j) * D),
+                reinterpret_cast<char*>(canvas + int64_t(idx[j]) * D), D * int64_t(sizeof(T)), lane);
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace
+}  // namespace avits
+
+using namespace avits;
+
+extern "C" int avits_gather_upsample(const void* lowres, const void* highres_prev, const void* prefix,
+                                     const int32_t* idx, int64_t k, int32_t H_lr, int32_t W_lr,
+                                     int64_t n_prefix, int64_t D, int mode, int dtype, void* compact,
+                                     int32_t* pos_sel, void* canvas, void* stream) {
+  AVITS_REQUIRE(H_lr >= 1 && W_lr >= 1, "gather_upsample: H_lr=%d W_lr=%d must be >= 1", H_lr, W_lr);
+  const int64_t N = int64_t(4) * H_lr * W_lr;
+  AVITS_REQUIRE(k >= 0 && k <= N, "gather_upsample: k=%lld outside [0, N=%lld]", (long long)k, (long long)N);
+  AVITS_REQUIRE(n_prefix >= 0, "gather_upsample: n_prefix=%lld < 0", (long long)n_prefix);
+  AVITS_REQUIRE(D >= 1, "gather_upsample: D=%lld < 1", (long long)D);
+  AVITS_REQUIRE(mode == AVITS_UP_NEAREST || mode == AVITS_UP_BILINEAR, "gather_upsample: bad mode %d", mode);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "gather_upsample: dtype %d unsupported", dtype);
+  const int64_t esz = dtype == AVITS_F32 ? 4 : 2;
+  AVITS_REQUIRE((D * esz) % 16 == 0, "gather_upsample: a row of D=%lld elements must be a multiple of 16 bytes", (long long)D);
+  AVITS_REQUIRE(lowres && highres_prev && canvas, "gather_upsample: null lowres/highres_prev/canvas");
+  AVITS_REQUIRE(n_prefix == 0 || prefix, "gather_upsample: null prefix with n_prefix=%lld", (long long)n_prefix);
+  AVITS_REQUIRE(n_prefix + k == 0 || compact, "gather_upsample: null compact");
+  AVITS_REQUIRE(k == 0 || (idx && pos_sel), "gather_upsample: null idx/pos_sel with k=%lld", (long long)k);
+  const int64_t jobs = n_prefix + k + N;
+  const dim3 grid(unsigned(ceil_div(jobs, kRowsPerBlock))), block(kWave * kRowsPerBlock);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int alias = canvas == highres_prev;
+  if (dtype == AVITS_F32)
+    hipLaunchKernelGGL(gather_upsample_kernel<float>, grid, block, 0, s, (const float*)lowres,
+                       (const float*)highres_prev, (const float*)prefix, idx, k, H_lr, W_lr, n_prefix, D,
+                       mode, (float*)compact, pos_sel, (float*)canvas, alias);
+  else
+    hipLaunchKernelGGL(gather_upsample_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)lowres,
+                       (const bf16_t*)highres_prev, (const bf16_t*)prefix, idx, k, H_lr, W_lr, n_prefix, D,
+                       mode, (bf16_t*)compact, pos_sel, (bf16_t*)canvas, alias);
+  return launch_status("gather_upsample");
+}
+
+extern "C" int avits_scatter(const void* out, const int32_t* idx, int64_t k, int64_t row_offset, int64_t D,
+                             int dtype, void* canvas, void* stream) {
+  AVITS_REQUIRE(k >= 0 && row_offset >= 0 && D >= 1, "scatter: bad k=%lld row_offset=%lld D=%lld",
+                (long long)k, (long long)row_offset, (long long)D);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "scatter: dtype %d unsupported", dtype);
+  const int64_t esz = dtype == AVITS_F32 ? 4 : 2;
+  AVITS_REQUIRE((D * esz) % 16 == 0, "scatter: a row of D=%lld elements must be a multiple of 16 bytes", (long long)D);
+  if (k == 0) return AVITS_OK;
+  AVITS_REQUIRE(out && idx && canvas, "scatter: null pointer");
+  const dim3 grid(unsigned(ceil_div(k, kRowsPerBlock))), block(kWave * kRowsPerBlock);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == AVITS_F32)
+    hipLaunchKernelGGL(scatter_kernel<float>, grid, block, 0, s, (const float*)out, idx, k, row_offset, D,
+                       (float*)canvas);
+  else
+    hipLaunchKernelGGL(scatter_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)out, idx, k, row_offset, D,
+                       (bf16_t*)canvas);
+  return launch_status("scatter");
+}

@@ -1,0 +1,130 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared
+symbol, and rejects invalid arguments before touching any device memory."""
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2608_17995_amd as avits
+from paper_2608_17995_amd import _binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "avits.h")
+
+INVALID, UNSUPPORTED, WORKSPACE = -1, -2, -3
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]*?\b(avits_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(avits.lib_path()):
+        pytest.fail("libavits.so is not built (python -m paper_2608_17995_amd.build)")
+    return avits.load()
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for want in ("avits_score", "avits_select", "avits_gather_upsample", "avits_block_forward",
+                 "avits_scatter", "avits_joint_lse", "avits_last_error", "avits_version"):
+        assert want in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", avits.lib_path()], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (avits_\w+)", out))
+    missing = [n for n in _declared() if n not in exported]
+    assert not missing, missing
+    assert set(_binding.EXPORTS) <= exported
+
+
+def test_version_and_error_text(lib):
+    assert avits.version().count(".") == 2
+    assert lib.avits_select(None, 10, 11, None, None, 0, None) == INVALID
+    assert b"k=11" in lib.avits_last_error()
+
+
+def test_select_validation(lib):
+    assert lib.avits_select(None, 0, 0, None, None, 0, None) == INVALID       # N < 1
+    assert lib.avits_select(None, 10, -1, None, None, 0, None) == INVALID     # k < 0
+    assert lib.avits_select(None, 10, 0, None, None, 0, None) == 0            # k == 0: no-op
+    assert lib.avits_select(None, 10, 3, None, None, 0, None) == INVALID      # null pointers
+    assert lib.avits_select_workspace_bytes(4096) == 0
+
+
+def _score(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, lse=FAKE, ft=FAKE, fp=FAKE, N=16, L=4, H=2, d=64, Df=8, alpha=0.5, eps=1e-8,
+             dtype=1, S=FAKE, ws=FAKE, wsb=1 << 30)
+    a.update(kw)
+    return lib.avits_score(a["q"], a["k"], a["lse"], a["ft"], a["fp"], a["N"], a["L"], a["H"], a["d"], a["Df"],
+                           a["alpha"], a["eps"], a["dtype"], a["S"], None, None, a["ws"], a["wsb"], None)
+
+
+def test_score_validation(lib):
+    assert _score(lib, N=0) == INVALID
+    assert _score(lib, L=0) == INVALID
+    assert _score(lib, alpha=1.5) == INVALID
+    assert _score(lib, alpha=-0.1) == INVALID
+    assert _score(lib, eps=-1.0) == INVALID
+    assert _score(lib, d=96) == UNSUPPORTED
+    assert _score(lib, dtype=7) == UNSUPPORTED
+    assert _score(lib, q=None) == INVALID
+    assert _score(lib, ws=None) == WORKSPACE
+    need = lib.avits_score_workspace_bytes(16, 2)
+    assert need >= 16 * 2 * 4
+    assert _score(lib, wsb=need - 1) == WORKSPACE
+
+
+def test_gather_and_scatter_validation(lib):
+    g = lib.avits_gather_upsample
+    # k > N (N = 4*2*2 = 16)
+    assert g(FAKE, FAKE, None, FAKE, 17, 2, 2, 0, 64, 0, 1, FAKE, FAKE, FAKE, None) == INVALID
+    assert g(FAKE, FAKE, None, FAKE, 3, 0, 2, 0, 64, 0, 1, FAKE, FAKE, FAKE, None) == INVALID   # H_lr
+    assert g(FAKE, FAKE, None, FAKE, 3, 2, 2, 0, 64, 5, 1, FAKE, FAKE, FAKE, None) == INVALID   # mode
+    assert g(FAKE, FAKE, None, FAKE, 3, 2, 2, 0, 60, 0, 1, FAKE, FAKE, FAKE, None) == INVALID   # 120-byte rows
+    assert g(FAKE, FAKE, None, FAKE, 3, 2, 2, 4, 64, 0, 1, FAKE, FAKE, FAKE, None) == INVALID   # null prefix
+    assert g(FAKE, FAKE, None, FAKE, 3, 2, 2, 0, 64, 0, 9, FAKE, FAKE, FAKE, None) == UNSUPPORTED
+    s = lib.avits_scatter
+    assert s(FAKE, FAKE, -1, 0, 64, 1, FAKE, None) == INVALID
+    assert s(FAKE, FAKE, 0, 0, 64, 1, FAKE, None) == 0        # k == 0: no-op
+    assert s(None, FAKE, 3, 0, 64, 1, FAKE, None) == INVALID
+    assert s(FAKE, FAKE, 3, 0, 64, 3, FAKE, None) == UNSUPPORTED
+
+
+def test_joint_lse_validation(lib):
+    f = lib.avits_joint_lse
+    assert f(FAKE, FAKE, 0, 5, 2, 64, 1, FAKE, None) == INVALID
+    assert f(FAKE, FAKE, 5, 0, 2, 64, 1, FAKE, None) == INVALID
+    assert f(FAKE, FAKE, 5, 5, 2, 32, 1, FAKE, None) == UNSUPPORTED
+    assert f(None, FAKE, 5, 5, 2, 64, 1, FAKE, None) == INVALID
+
+
+def test_block_validation(lib):
+    import ctypes
+    w = _binding._BlockWeights()
+    w.kind, w.mlp_hidden = 0, 256
+    f = lib.avits_block_forward
+    ws = lib.avits_block_workspace_bytes(0, 10, 1, 64, 256, 1)
+    assert ws > 0
+    assert f(FAKE, FAKE + 64, FAKE, 5, 5, None, 1, 64, 1, None, FAKE, ws, None) == INVALID          # null weights
+    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID  # missing weights
+    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 80, 1, None, FAKE, ws, None) == UNSUPPORTED
+    assert f(FAKE, FAKE + 64, FAKE, -1, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
+    assert f(FAKE, FAKE, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID  # alias
+    assert f(FAKE, FAKE + 64, FAKE, 0, 0, ctypes.byref(w), 1, 64, 1, None, None, 0, None) == 0    # S == 0
+    for part in ("txt", "img"):
+        for name, _ in _binding._DoubleStream._fields_:
+            setattr(getattr(w, part), name, FAKE)
+    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws - 1, None) == WORKSPACE
+    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, None, ws, None) == WORKSPACE
+    w.kind = 5
+    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
+    w.kind, w.mlp_hidden = 0, 100
+    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
+    assert lib.avits_block_workspace_bytes(1, 10, 1, 64, 256, 1) > 0
+    assert lib.avits_block_workspace_bytes(3, 10, 1, 64, 256, 1) == 0

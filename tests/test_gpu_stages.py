@@ -1,0 +1,243 @@
+"""Stage-by-stage parity of the HIP path against the oracle on identical inputs.
+
+Each stage's oracle runs on exactly the values the GPU stage consumed (the
+GPU's own upstream outputs copied to the host), so indices and layouts must
+match bit for bit and floats within the parity bar.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import configs as C
+from synth import generator as G
+
+from _gpu import assert_close, dev, double_weights_dev, host, rel_l2
+
+TINY = [C.TINY_F32, C.TINY_BF16, C.TINY_BF16_REF, C.TINY_F32_RAGGED]
+IDS = [w.name for w in TINY]
+
+pytestmark = pytest.mark.gpu
+
+
+def _k_all(si):
+    return np.concatenate([si["text_k"], si["ref_k"], si["latent_k"]])
+
+
+def _lse_gpu(gpu, w, si):
+    lse = torch.empty(w.H, w.N, device="cuda")
+    gpu.avits_joint_lse(dev(si["latent_q"], w.dtype), dev(_k_all(si), w.dtype), lse)
+    return lse
+
+
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+def test_joint_lse(gpu, w):
+    si = G.score_inputs(w)
+    lse = _lse_gpu(gpu, w, si)
+    torch.cuda.synchronize()
+    ref = oracle.joint_lse(si["latent_q"], _k_all(si))
+    assert_close(host(lse), ref, w.dtype, "joint_lse")
+    assert np.abs(host(lse) - ref).max() < 1e-3
+
+
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+def test_score(gpu, w):
+    si = G.score_inputs(w)
+    lse = _lse_gpu(gpu, w, si)
+    S = torch.empty(w.N, device="cuda")
+    A = torch.empty(w.N, device="cuda")
+    V = torch.empty(w.N, device="cuda")
+    gpu.avits_score(dev(si["latent_q"], w.dtype), dev(si["text_k"], w.dtype), lse, dev(si["feat_t"], w.dtype),
+                    dev(si["feat_prev"], w.dtype), w.alpha, w.eps_minmax, S, A, V)
+    torch.cuda.synchronize()
+    s_ref, a_ref, v_ref = oracle.score(si["latent_q"], si["text_k"], host(lse), si["feat_t"], si["feat_prev"],
+                                       w.alpha, w.eps_minmax)
+    assert_close(host(A), a_ref, w.dtype, "A")
+    assert_close(host(V), v_ref, w.dtype, "V")
+    assert_close(host(S), s_ref, w.dtype, "S")
+    # fp32 arithmetic on both bf16 and fp32 inputs: the fused score is tight either way.
+    assert np.abs(host(S) - s_ref).max() < 1e-4
+    np.testing.assert_allclose(host(A), a_ref, rtol=1e-4)
+    np.testing.assert_allclose(host(V), v_ref, rtol=1e-4)
+
+
+@pytest.mark.parametrize("w", [C.TINY_F32, C.TINY_BF16], ids=["f32", "bf16"])
+def test_score_without_optional_outputs_and_small_feature_width(gpu, w):
+    # D_f = 64 (the packed-latent reading of the snapshots); A/V outputs omitted.
+    w = w.replace(D_f=64)
+    si = G.score_inputs(w)
+    lse = _lse_gpu(gpu, w, si)
+    S = torch.empty(w.N, device="cuda")
+    gpu.avits_score(dev(si["latent_q"], w.dtype), dev(si["text_k"], w.dtype), lse, dev(si["feat_t"], w.dtype),
+                    dev(si["feat_prev"], w.dtype), w.alpha, w.eps_minmax, S)
+    torch.cuda.synchronize()
+    s_ref, _, _ = oracle.score(si["latent_q"], si["text_k"], host(lse), si["feat_t"], si["feat_prev"],
+                               w.alpha, w.eps_minmax)
+    assert np.abs(host(S) - s_ref).max() < 1e-4
+
+
+def _select(gpu, scores_np, k):
+    s = torch.from_numpy(np.ascontiguousarray(scores_np, dtype=np.float32)).cuda()
+    idx = torch.full((max(k, 1),), -7, dtype=torch.int32, device="cuda")
+    gpu.avits_select(s, k, idx[:k])
+    torch.cuda.synchronize()
+    return host(idx)[:k], host(idx)
+
+
+@pytest.mark.parametrize("n,k", [(1, 1), (5, 2), (1000, 1), (1024, 256), (1025, 1024), (4096, 1229),
+                                 (3001, 3001), (16384, 4915), (20000, 7)])
+def test_select_random(gpu, n, k):
+    s = np.random.default_rng(n * 7 + k).standard_normal(n).astype(np.float32)
+    got, _ = _select(gpu, s, k)
+    np.testing.assert_array_equal(got, oracle.select_topk(s, k))
+
+
+@pytest.mark.parametrize("n,k,levels", [(4096, 1229, 8), (1000, 500, 2), (2048, 2047, 1), (777, 300, 3)])
+def test_select_ties_lowest_index(gpu, n, k, levels):
+    s = G.quantised_scores(n, n, levels)
+    got, _ = _select(gpu, s, k)
+    np.testing.assert_array_equal(got, oracle.select_topk(s, k))
+
+
+def test_select_special_values_and_k0(gpu):
+    s = np.array([np.nan, -0.0, 0.0, -np.inf, np.inf, np.nan, -1.0, 3.0, -0.0], dtype=np.float32)
+    for k in range(len(s) + 1):
+        got, _ = _select(gpu, s, k)
+        np.testing.assert_array_equal(got, oracle.select_topk(s, k))
+    # k = 0 writes nothing.
+    _, raw = _select(gpu, s, 0)
+    assert raw[0] == -7
+
+
+def _gather(gpu, w, k, mode, alias, seed=0):
+    lay = G.layout_inputs(w)
+    idx = G.random_selection(w, k, seed)
+    prefix = np.concatenate([lay["text"], lay["ref"]])
+    t_low, t_high = dev(lay["lowres"], w.dtype), dev(lay["highres_prev"], w.dtype)
+    t_pre = dev(prefix, w.dtype) if w.LR else None
+    t_idx = dev(idx)
+    compact = torch.full((w.LR + k, w.D), 7.0, dtype=t_low.dtype, device="cuda")
+    pos = torch.full((k, 3), -1, dtype=torch.int32, device="cuda")
+    canvas = t_high if alias else torch.full_like(t_high, 7.0)
+    gpu.avits_gather_upsample(t_low, t_high, t_pre, t_idx, w.H_lr, w.W_lr, compact, pos, canvas, mode=mode)
+    torch.cuda.synchronize()
+    ref = oracle.gather_upsample(lay["lowres"], lay["highres_prev"], prefix, idx, w.H_lr, w.W_lr,
+                                 "nearest" if mode == 0 else "bilinear")
+    return (host(compact), host(pos), host(canvas)), ref, idx
+
+
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+@pytest.mark.parametrize("alias", [False, True], ids=["separate", "in_place"])
+def test_gather_nearest_bitexact(gpu, w, alias):
+    (compact, pos, canvas), (rc, rp, rcv), idx = _gather(gpu, w, w.k, 0, alias)
+    np.testing.assert_array_equal(compact, rc)
+    np.testing.assert_array_equal(pos, rp)
+    np.testing.assert_array_equal(canvas, rcv)
+
+
+@pytest.mark.parametrize("w", [C.TINY_BF16, C.TINY_F32], ids=["bf16", "f32"])
+def test_gather_keep_none_and_all(gpu, w):
+    for k in (0, w.N):
+        (compact, pos, canvas), (rc, rp, rcv), _ = _gather(gpu, w, k, 0, False)
+        np.testing.assert_array_equal(compact, rc)
+        np.testing.assert_array_equal(canvas, rcv)
+        if k == 0:  # pure upsampling
+            np.testing.assert_array_equal(canvas, oracle.upsample_nearest(G.layout_inputs(w)["lowres"], w.H_lr, w.W_lr))
+        else:       # dense fallback: every token keeps its high-res features
+            np.testing.assert_array_equal(canvas, G.layout_inputs(w)["highres_prev"])
+
+
+@pytest.mark.parametrize("w", [C.TINY_BF16, C.TINY_F32_RAGGED], ids=["bf16", "f32"])
+def test_gather_bilinear(gpu, w):
+    (compact, pos, canvas), (rc, rp, rcv), _ = _gather(gpu, w, w.k, 1, False)
+    np.testing.assert_array_equal(compact, rc)
+    np.testing.assert_array_equal(pos, rp)
+    if w.dtype == "bf16":
+        # fp32 interpolation of bf16 values, one final rounding: within one bf16 ulp.
+        ulp = np.abs(rcv) * 2.0 ** -7 + 1e-30
+        assert np.all(np.abs(canvas - rcv) <= ulp)
+    else:
+        assert np.abs(canvas - rcv).max() < 1e-5
+
+
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+def test_scatter_bitexact(gpu, w):
+    lay = G.layout_inputs(w)
+    idx = G.random_selection(w, w.k, 3)
+    out = G.block_input(w, w.S, 5)
+    t_canvas = dev(lay["highres_prev"], w.dtype)
+    gpu.avits_scatter(dev(out, w.dtype), dev(idx), w.LR, t_canvas)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(t_canvas), oracle.scatter(out, idx, w.LR, lay["highres_prev"]))
+
+
+def _block_inputs(w, n_txt, n_img, seed=0):
+    x = G.block_input(w, n_txt + n_img, seed)
+    g = np.random.default_rng(1000 + seed)
+    pos = np.zeros((n_txt + n_img, 3), np.int32)
+    pos[n_txt:, 0] = g.integers(0, 2, n_img)
+    pos[n_txt:, 1] = g.integers(0, w.H_hr, n_img)
+    pos[n_txt:, 2] = g.integers(0, w.W_hr, n_img)
+    return x, pos
+
+
+def _run_double(gpu, w, x, pos, n_txt, wt, wi):
+    t_x = dev(x, w.dtype)
+    out = torch.empty_like(t_x)
+    lse = torch.empty(w.H, x.shape[0], device="cuda")
+    bw = gpu.BlockWeights(gpu.BLOCK_DOUBLE, txt=double_weights_dev(wt, w.dtype), img=double_weights_dev(wi, w.dtype))
+    gpu.avits_block_forward(t_x, out, dev(pos), n_txt, x.shape[0] - n_txt, bw, w.H, lse_out=lse)
+    torch.cuda.synchronize()
+    return host(out), host(lse)
+
+
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+def test_double_block(gpu, w):
+    n_txt, n_img = w.L, w.R + w.k
+    x, pos = _block_inputs(w, n_txt, n_img)
+    wt, wi = G.double_stream_weights(w, 0, 0), G.double_stream_weights(w, 0, 1)
+    out, lse = _run_double(gpu, w, x, pos, n_txt, wt, wi)
+    ref, ref_lse = oracle.double_block(x, pos, n_txt, wt, wi, w.H)
+    assert_close(out, ref, w.dtype, "x_out")
+    assert_close(out - x, ref - x, w.dtype, "block update x_out - x_in")
+    assert_close(lse, ref_lse, w.dtype, "lse")
+
+
+@pytest.mark.parametrize("n_txt,n_img", [(40, 0), (0, 77), (1, 1), (129, 130)])
+def test_double_block_degenerate_streams(gpu, n_txt, n_img):
+    w = C.TINY_BF16
+    x, pos = _block_inputs(w, n_txt, n_img, seed=n_txt + n_img)
+    wt, wi = G.double_stream_weights(w, 0, 0), G.double_stream_weights(w, 0, 1)
+    out, lse = _run_double(gpu, w, x, pos, n_txt, wt, wi)
+    ref, ref_lse = oracle.double_block(x, pos, n_txt, wt, wi, w.H)
+    assert_close(out - x, ref - x, "bf16", "block update")
+    assert_close(lse, ref_lse, "bf16", "lse")
+
+
+@pytest.mark.parametrize("w", [C.TINY_F32, C.TINY_BF16], ids=["f32", "bf16"])
+def test_single_block(gpu, w):
+    S = w.L + w.k
+    x, pos = _block_inputs(w, w.L, w.k, seed=9)
+    ws = G.single_block_weights(w, 0)
+    t_x = dev(x, w.dtype)
+    out = torch.empty_like(t_x)
+    lse = torch.empty(w.H, S, device="cuda")
+    bw = gpu.BlockWeights(gpu.BLOCK_SINGLE, single=double_weights_dev(ws, w.dtype))
+    gpu.avits_block_forward(t_x, out, dev(pos), w.L, w.k, bw, w.H, lse_out=lse)
+    torch.cuda.synchronize()
+    ref, ref_lse = oracle.single_block(x, pos, ws, w.H)
+    assert_close(host(out), ref, w.dtype, "x_out")
+    assert_close(host(out) - x, ref - x, w.dtype, "block update")
+    assert_close(host(lse), ref_lse, w.dtype, "lse")
+
+
+def test_block_relayout_equivariance(gpu):
+    # RoPE reads positions, not sequence slots: shuffling image rows with their
+    # positions shuffles the outputs (bit-exact is not expected: summation order).
+    w = C.TINY_BF16
+    x, pos = _block_inputs(w, 16, 48, seed=4)
+    wt, wi = G.double_stream_weights(w, 0, 0), G.double_stream_weights(w, 0, 1)
+    out, _ = _run_double(gpu, w, x, pos, 16, wt, wi)
+    perm = np.concatenate([np.arange(16), 16 + np.random.default_rng(2).permutation(48)])
+    out2, _ = _run_double(gpu, w, x[perm], pos[perm], 16, wt, wi)
+    assert rel_l2(out2 - x[perm], out[perm] - x[perm]) < 1e-2
