@@ -1,0 +1,259 @@
+"""Benchmark of one selective-upsampling step on one MI355X.
+
+A step is one pass of the whole hot path over one synthetic input batch:
+score (spatial + temporal + fuse) -> top-K select -> gather + 2x upsample ->
+double-stream MMDiT block on the compacted sequence -> scatter, at the
+FLUX-shaped 1024^2 workload (hidden 3072, 24x128 heads, 512 text tokens,
+64x64 high-res latent, keep ratio 0.3 -> k = 1229, S = 1741), bf16 storage
+with fp32 accumulation.  All inputs are resident in HBM before timing; the
+joint log-sum-exp the scorer consumes is produced once beforehand (it is the
+previous step's attention by-product) and timed separately.
+
+Prints one JSON line.  Usage: python bench.py [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "ms per selective DiT block step + attn MFMA util + score/select HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+# ---------------------------------------------------------------------------
+# Algorithmic work (what the step must read, write and compute).
+
+def block_flops(S: int, D: int, F: int | None = None) -> dict:
+    """FLOPs of one double-stream block on S rows (MLP hidden F, default 4D)."""
+    F = 4 * D if F is None else F
+    gemm = 2 * S * D * (3 * D + D + F + F)       # QKV, O, MLP in, MLP out
+    attn = 4 * S * S * D                          # Q K^T and P V, non-causal
+    return {"gemm": gemm, "attention": attn, "total": gemm + attn}
+
+
+def dense_model_flops(tokens: int, D: int = 3072, blocks: int = 57) -> float:
+    """24 D^2 S + 4 S^2 D per block (F = 4D), summed over the blocks."""
+    return blocks * (24 * D * D * tokens + 4 * tokens * tokens * D)
+
+
+def stage_bytes(w, e: int = 2) -> dict:
+    """Algorithmic HBM bytes per stage (canvas updated in place)."""
+    N, D, Df, L, R, k, H = w.N, w.D, w.Df, w.L, w.R, w.k, w.H
+    S = L + R + k
+    score = N * D * e + L * D * e + 4 * H * N + 2 * N * Df * e + 12 * N
+    select = 4 * N + 4 * k
+    gather = ((L + R) * D * e + k * D * e + w.N_lr * D * e + 4 * k          # reads
+              + S * D * e + (N - k) * D * e + 12 * k)                       # writes
+    scatter = 2 * k * D * e + 4 * k
+    return {"score": score, "select": select, "gather_upsample": gather, "scatter": scatter}
+
+
+# ---------------------------------------------------------------------------
+
+def _cpu_baseline(w, host, row_lse, wt, wi):
+    """Time the oracle (fp64 NumPy, untuned) on one full step of the same workload."""
+    import numpy as np
+    import oracle
+    from synth import generator as G
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    t0 = time.perf_counter()
+    s, _, _ = oracle.score(host["latent_q"], host["text_k"], row_lse, host["feat_t"], host["feat_prev"], w.alpha)
+    idx = oracle.select_topk(s, w.k)
+    compact, pos, canvas = oracle.gather_upsample(host["lowres"], host["highres_prev"],
+                                                  np.concatenate([host["text"], host["ref"]]), idx, w.H_lr, w.W_lr)
+    pos_all = np.concatenate([G.prefix_positions(w), pos])
+    out, _ = oracle.double_block(compact, pos_all, w.L, wt, wi, w.H)
+    oracle.scatter(out, idx, w.LR, canvas)
+    dt = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [threads])
+    except Exception:  # pragma: no cover
+        pass
+    return {"value": round(dt * 1e3, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
+            "sample": f"one full step (score, select, gather/upsample, double block, scatter) of {w.name} "
+                      f"in fp64 NumPy on the host; {os.cpu_count()} CPUs visible"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2608_17995_amd as avits
+    from paper_2608_17995_amd.step import SelectiveStep, StepShape
+    from synth import configs as C
+    from synth import generator as G
+
+    torch.cuda.set_device(0)
+    avits.load()
+    w = C.FLUX_1024
+    dt = torch.bfloat16
+
+    def cuda(a):
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dt).cuda()
+
+    t_gen = time.perf_counter()
+    si = G.score_inputs(w)
+    lay = G.layout_inputs(w, si["feat_t"])
+    wt, wi = G.double_stream_weights(w, 0, 0), G.double_stream_weights(w, 0, 1)
+    t_gen = time.perf_counter() - t_gen
+
+    q, kt, fp = cuda(si["latent_q"]), cuda(si["text_k"]), cuda(si["feat_prev"])
+    k_all = cuda(np.concatenate([si["text_k"], si["ref_k"], si["latent_k"]]))
+    high = cuda(lay["highres_prev"])       # = feat_t (hidden states); updated in place each step
+    low, text = cuda(lay["lowres"]), cuda(np.concatenate([lay["text"], lay["ref"]]))
+    bw = avits.BlockWeights(avits.BLOCK_DOUBLE, txt={k: cuda(v) for k, v in wt.items()},
+                            img={k: cuda(v) for k, v in wi.items()})
+    shape = StepShape(N=w.N, H_lr=w.H_lr, W_lr=w.W_lr, L=w.L, R=w.R, k=w.k, D=w.D, H=w.H, D_f=w.Df,
+                      mlp_hidden=w.mlp_ratio * w.D)
+    step = SelectiveStep(shape, bw, torch.from_numpy(G.prefix_positions(w)).cuda(), dt, alpha=w.alpha)
+    lse = torch.empty(w.H, w.N, device="cuda")
+    row_lse_host = None
+
+    # Setup: the joint log-sum-exp over [text; image] keys (timed on its own).
+    avits.avits_joint_lse(q, k_all, lse)
+    torch.cuda.synchronize()
+    row_lse_host = lse.double().cpu().numpy()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(5):
+        avits.avits_joint_lse(q, k_all, lse)
+    ev[1].record()
+    torch.cuda.synchronize()
+    joint_lse_ms = ev[0].elapsed_time(ev[1]) / 5
+
+    stages = ("score", "select", "gather_upsample", "block", "scatter")
+
+    def run_step(events=None):
+        def mark(i):
+            if events is not None:
+                events[i].record()
+        mark(0)
+        step.score(q, kt, lse, high, fp)
+        mark(1)
+        step.select()
+        mark(2)
+        step.gather(low, high, text)
+        mark(3)
+        step.block()
+        mark(4)
+        step.scatter(high)
+        mark(5)
+
+    for _ in range(args.warmup):
+        run_step()
+    torch.cuda.synchronize()
+
+    # Timed region: K steps, stage events on the stream and library launch timing.
+    step_events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    avits.avits_timing_reset()
+    avits.avits_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        run_step(step_events[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    avits.avits_timing_enable(False)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+
+    stage_ms = {s: 0.0 for s in stages}
+    for evs in step_events:
+        for j, s in enumerate(stages):
+            stage_ms[s] += evs[j].elapsed_time(evs[j + 1]) / args.steps
+    fam = {}
+    for f in ("score_spatial", "score_temporal", "score_finalize", "select", "gather_upsample", "scatter",
+              "ln_mod", "gemm", "qk_rope", "attention"):
+        tot, n = avits.avits_timing_read(f)
+        fam[f] = {"ms_per_step": round(tot / args.steps, 4), "launches_per_step": n / args.steps,
+                  "avg_launch_us": round(1e3 * tot / max(n, 1), 2)}
+
+    S, D, F = w.S, w.D, w.mlp_ratio * w.D
+    fl = block_flops(S, D, F)
+    by = stage_bytes(w)
+    gemm_tot_ms, gemm_n = avits.avits_timing_read("gemm")
+    gemm_per_launch_flops = fl["gemm"] * args.steps / gemm_n
+    gemm_avg_s = gemm_tot_ms / gemm_n / 1e3
+    gemm_tflops = gemm_per_launch_flops / gemm_avg_s / 1e12
+    attn_ms, attn_n = avits.avits_timing_read("attention")
+    attn_tflops = fl["attention"] / (attn_ms / attn_n / 1e3) / 1e12   # one launch per step
+
+    def gbs(nbytes, ms):
+        return round(nbytes / (ms / 1e3) / 1e9, 1) if ms > 0 else None
+
+    result = {
+        "metric": METRIC,
+        "value": round(ms_per_step, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "hidden": D, "heads": w.H, "head_dim": w.d, "text_tokens": w.L,
+                   "lowres_grid": [w.H_lr, w.W_lr], "highres_grid": [w.H_hr, w.W_hr], "keep_ratio": w.rho,
+                   "k": w.k, "seq_len": S, "alpha": w.alpha, "upsample": "nearest"},
+        "roofline": {
+            "kernel": "gemm_bf16_kernel",
+            "bound": "mfma",
+            "achieved": round(gemm_tflops, 1),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+            "flops_per_launch": int(gemm_per_launch_flops),
+            "avg_launch_us": round(gemm_avg_s * 1e6, 2),
+        },
+        "stages_ms": {s: round(v, 4) for s, v in stage_ms.items()},
+        "launch_families": fam,
+        "attention": {"tflops": round(attn_tflops, 1), "mfma_frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                      "flops": fl["attention"]},
+        "block": {"ms": round(stage_ms["block"], 4), "flops": fl["total"],
+                  "tflops": round(fl["total"] / (stage_ms["block"] / 1e3) / 1e12, 1),
+                  "mfma_frac": round(fl["total"] / (stage_ms["block"] / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
+        "hbm_gbs": {s: gbs(by[s], stage_ms[s]) for s in ("score", "select", "gather_upsample", "scatter")},
+        "hbm_frac": {s: (round(gbs(by[s], stage_ms[s]) / PEAK_HBM_GBS, 4) if stage_ms[s] > 0 else None)
+                     for s in ("score", "select", "gather_upsample", "scatter")},
+        "algorithmic_bytes": by,
+        "tokens_per_s": round(S / (ms_per_step / 1e3), 1),
+        "canvas_tokens_per_s": round(w.N / (ms_per_step / 1e3), 1),
+        "joint_lse_ms_untimed_setup": round(joint_lse_ms, 4),
+        "input_generation_s": round(t_gen, 1),
+    }
+    if not args.no_cpu_baseline:
+        host = dict(si)
+        host.update(lay)
+        result["cpu_baseline"] = _cpu_baseline(w, host, row_lse_host, wt, wi)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -204,6 +204,21 @@ int avits_scatter(const void* out, const int32_t* idx, int64_t k, int64_t row_of
 int avits_joint_lse(const void* q, const void* k_all, int64_t N, int64_t Nk,
                     int32_t H, int32_t d, int dtype, float* lse, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Launch timing (instrumentation for benchmarks; not part of the method).
+ * While enabled, every kernel the library enqueues is bracketed by a pair of
+ * HIP events on the caller's stream.  avits_timing_read() waits for the
+ * recorded events and returns the accumulated time and launch count of one
+ * launch family: "score_spatial", "score_temporal", "score_finalize",
+ * "select", "gather_upsample", "scatter", "ln_mod", "gemm", "qk_rope",
+ * "attention", "joint_lse".  Unknown family -> AVITS_ERR_INVALID_ARG.
+ * avits_timing_reset() waits for pending events and zeroes every total.
+ * Not thread-safe: use from one host thread.
+ * ---------------------------------------------------------------------- */
+int avits_timing_enable(int on);
+void avits_timing_reset(void);
+int avits_timing_read(const char* family, double* total_ms, int64_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

@@ -14,4 +14,5 @@ from ._binding import (  # noqa: F401
     avits_select_workspace_bytes, avits_select,
     avits_gather_upsample, avits_scatter, avits_joint_lse,
     avits_block_workspace_bytes, avits_block_forward, BlockWeights,
+    avits_timing_enable, avits_timing_reset, avits_timing_read,
 )

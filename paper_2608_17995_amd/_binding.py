@@ -53,6 +53,10 @@ _SIGS = {
     "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, ctypes.c_int, _c_void_p, _c_void_p]),
     "avits_joint_lse": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i32, _i32, ctypes.c_int, _c_void_p,
                                        _c_void_p]),
+    "avits_timing_enable": (ctypes.c_int, [ctypes.c_int]),
+    "avits_timing_reset": (None, []),
+    "avits_timing_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(_i64)]),
 }
 
 EXPORTS = tuple(_SIGS)
@@ -207,6 +211,21 @@ class BlockWeights:
             self.c.mlp_hidden = single["w_out"].shape[1] - D
             for name, _ in _Single._fields_:
                 setattr(self.c.single, name, _dev(single[name], f"single.{name}"))
+
+
+def avits_timing_enable(on: bool = True):
+    _check(load().avits_timing_enable(1 if on else 0))
+
+
+def avits_timing_reset():
+    load().avits_timing_reset()
+
+
+def avits_timing_read(family: str):
+    """(total milliseconds, launches) recorded for one launch family."""
+    ms, n = ctypes.c_double(), _i64()
+    _check(load().avits_timing_read(family.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
 
 
 def avits_block_workspace_bytes(kind: int, S: int, H: int, d: int, mlp_hidden: int, dtype: int) -> int:

@@ -255,6 +255,7 @@ void launch_dh(const AttnArgs& a, int dtype, hipStream_t s) {
 
 int launch_attention(const AttnArgs& a, int dtype, hipStream_t s) {
   if (a.Sq == 0) return AVITS_OK;
+  TimedLaunch timed(a.vt ? "attention" : "joint_lse", s);
   if (a.d == 128) launch_dh<128>(a, dtype, s);
   else launch_dh<64>(a, dtype, s);
   return launch_status("attention");

@@ -176,10 +176,12 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
   if (dbl) {
     const void* ma = n_txt ? w->txt.mod : w->img.mod;
     const void* mb = n_img ? w->img.mod : w->txt.mod;
+    TimedLaunch timed("ln_mod", s);
     hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, n_txt, mod_row(ma, 0), mod_row(ma, 1),
                        mod_row(mb, 0), mod_row(mb, 1));
   } else {
     const void* mm = w->single.mod;
+    TimedLaunch timed("ln_mod", s);
     hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, S, mod_row(mm, 0), mod_row(mm, 1),
                        mod_row(mm, 0), mod_row(mm, 1));
   }
@@ -230,6 +232,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
       na = S;
     }
     const dim3 grid(unsigned(ceil_div64(S, 64)), unsigned(H));
+    TimedLaunch timed("qk_rope", s);
     if (d == 128)
       hipLaunchKernelGGL((qk_rope_relayout_kernel<T, 128>), grid, blk, 0, s, qkv, 3 * D, pos, S, H, na, gqa, gka,
                          gqb, gkb, reinterpret_cast<T*>(ws.q), reinterpret_cast<T*>(ws.k),
@@ -282,6 +285,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
   {
     const void* ma = n_txt ? w->txt.mod : w->img.mod;
     const void* mb = n_img ? w->img.mod : w->txt.mod;
+    TimedLaunch timed("ln_mod", s);
     hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, xmid, h, S, D, n_txt, mod_row(ma, 3), mod_row(ma, 4),
                        mod_row(mb, 3), mod_row(mb, 4));
   }

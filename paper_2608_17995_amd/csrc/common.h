@@ -85,10 +85,25 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) { return __builtin_b
 
 }  // namespace avits
 
-// Host-side error plumbing (abi.cpp).
+// Host-side error plumbing and launch timing (abi.hip).
 namespace avits {
 int set_error(int code, const char* fmt, ...);
 int launch_status(const char* what);
+
+// Brackets the launches made during its lifetime with timing events when
+// timing is enabled (avits_timing_enable); a no-op otherwise.
+class TimedLaunch {
+ public:
+  TimedLaunch(const char* family, hipStream_t stream);
+  ~TimedLaunch();
+  TimedLaunch(const TimedLaunch&) = delete;
+  TimedLaunch& operator=(const TimedLaunch&) = delete;
+
+ private:
+  int family_;
+  hipStream_t stream_;
+  hipEvent_t start_ = nullptr;
+};
 }  // namespace avits
 
 #define AVITS_REQUIRE(cond, ...)                                            \

@@ -201,6 +201,7 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s) {
   int64_t tiles = 0;
   for (int i = 0; i < a.nprob; ++i) tiles += ceil_div64(a.p[i].M, bm) * tn;
   if (tiles == 0) return AVITS_OK;
+  TimedLaunch timed("gemm", s);
   if (dtype == AVITS_BF16)
     hipLaunchKernelGGL(gemm_bf16_kernel, dim3(unsigned(tiles)), dim3(256), 0, s, a);
   else

@@ -141,6 +141,7 @@ extern "C" int avits_gather_upsample(const void* lowres, const void* highres_pre
   const dim3 grid(unsigned(ceil_div(jobs, kRowsPerBlock))), block(kWave * kRowsPerBlock);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int alias = canvas == highres_prev;
+  TimedLaunch timed("gather_upsample", s);
   if (dtype == AVITS_F32)
     hipLaunchKernelGGL(gather_upsample_kernel<float>, grid, block, 0, s, (const float*)lowres,
                        (const float*)highres_prev, (const float*)prefix, idx, k, H_lr, W_lr, n_prefix, D,
@@ -164,6 +165,7 @@ extern "C" int avits_scatter(const void* out, const int32_t* idx, int64_t k, int
   AVITS_REQUIRE(out && idx && canvas, "scatter: null pointer");
   const dim3 grid(unsigned(ceil_div(k, kRowsPerBlock))), block(kWave * kRowsPerBlock);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  TimedLaunch timed("scatter", s);
   if (dtype == AVITS_F32)
     hipLaunchKernelGGL(scatter_kernel<float>, grid, block, 0, s, (const float*)out, idx, k, row_offset, D,
                        (float*)canvas);

@@ -287,6 +287,8 @@ extern "C" int avits_score(const void* latent_q, const void* text_k, const float
   hipStream_t s = static_cast<hipStream_t>(stream);
 
   const int n = int(N), l = int(L);
+  {
+  TimedLaunch timed("score_spatial", s);
   if (dtype == AVITS_BF16) {
     const dim3 grid(unsigned((N + kSpRows - 1) / kSpRows), unsigned(H));
     if (d == 128)
@@ -304,14 +306,19 @@ extern "C" int avits_score(const void* latent_q, const void* text_k, const float
       hipLaunchKernelGGL(spatial_f32_kernel<64>, grid, dim3(128), 0, s, (const float*)latent_q,
                          (const float*)text_k, row_lse, n, l, H, ws.part);
   }
+  }
   const int tblocks = int(std::min<int64_t>(kTmpBlocks, (N + 3) / 4));
+  {
+  TimedLaunch timed("score_temporal", s);
   if (dtype == AVITS_BF16)
     hipLaunchKernelGGL(temporal_kernel<bf16_t>, dim3(tblocks), dim3(256), 0, s, (const bf16_t*)feat_t,
                        (const bf16_t*)feat_prev, ws.part, N, H, D_f, a_dst, v_dst, ws.mm);
   else
     hipLaunchKernelGGL(temporal_kernel<float>, dim3(tblocks), dim3(256), 0, s, (const float*)feat_t,
                        (const float*)feat_prev, ws.part, N, H, D_f, a_dst, v_dst, ws.mm);
+  }
   const int fblocks = int(std::min<int64_t>(256, (N + 255) / 256));
+  TimedLaunch timed("score_finalize", s);
   hipLaunchKernelGGL(finalize_kernel, dim3(fblocks), dim3(256), 0, s, a_dst, v_dst, ws.mm, tblocks, N, alpha, eps,
                      scores);
   return launch_status("score");

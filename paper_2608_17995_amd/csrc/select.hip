@@ -126,6 +126,7 @@ extern "C" int avits_select(const float* scores, int64_t N, int64_t k, int32_t* 
   AVITS_REQUIRE(k >= 0 && k <= N, "select: k=%lld outside [0, N=%lld]", (long long)k, (long long)N);
   if (k == 0) return AVITS_OK;
   AVITS_REQUIRE(scores && idx, "select: null scores/idx");
+  TimedLaunch timed("select", static_cast<hipStream_t>(stream));
   hipLaunchKernelGGL(radix_select_kernel, dim3(1), dim3(kThreads), 0, static_cast<hipStream_t>(stream), scores,
                      int(N), int(k), idx);
   return launch_status("select");
