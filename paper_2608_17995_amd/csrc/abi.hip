@@ -31,8 +31,9 @@ int launch_status(const char* what) {
 // HIP events on its stream; avits_timing_read() waits for them and adds the
 // elapsed times to per-family totals.  Single-threaded use only.
 static const char* const kFamilies[] = {"score_spatial", "score_temporal", "score_finalize", "select",
-                                        "gather_upsample", "scatter", "ln_mod", "gemm", "qk_rope",
-                                        "attention", "joint_lse"};
+                                        "gather_upsample", "scatter", "ln_mod", "gemm_qkv", "gemm_o",
+                                        "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
+                                        "qk_rope", "attention", "joint_lse"};
 constexpr int kNumFamilies = sizeof(kFamilies) / sizeof(kFamilies[0]);
 
 struct Pending {
@@ -106,12 +107,23 @@ extern "C" void avits_timing_reset(void) {
 }
 
 extern "C" int avits_timing_read(const char* family, double* total_ms, int64_t* launches) {
-  const int f = family ? avits::family_index(family) : -1;
-  if (f < 0) return avits::set_error(AVITS_ERR_INVALID_ARG, "timing_read: unknown launch family '%s'",
-                                     family ? family : "(null)");
+  // "gemm" sums every GEMM family.
+  const bool all_gemm = family && strcmp(family, "gemm") == 0;
+  const int f = family && !all_gemm ? avits::family_index(family) : -1;
+  if (f < 0 && !all_gemm)
+    return avits::set_error(AVITS_ERR_INVALID_ARG, "timing_read: unknown launch family '%s'",
+                            family ? family : "(null)");
   avits::drain();
-  if (total_ms) *total_ms = avits::g_ms[f];
-  if (launches) *launches = avits::g_launches[f];
+  double ms = 0.0;
+  int64_t n = 0;
+  for (int i = 0; i < avits::kNumFamilies; ++i) {
+    if (all_gemm ? strncmp(avits::kFamilies[i], "gemm_", 5) == 0 : i == f) {
+      ms += avits::g_ms[i];
+      n += avits::g_launches[i];
+    }
+  }
+  if (total_ms) *total_ms = ms;
+  if (launches) *launches = n;
   return AVITS_OK;
 }
 

@@ -2,175 +2,196 @@
 // Section 3.3.1, Eqs. joint_qk and dit_attn), and its LSE-only form.
 //
 // bf16: one 256-thread workgroup per (128 query rows, head), 32 rows per
-// wave.  Key tiles of 64 rows and the matching V^T tile are staged in padded
-// LDS.  Both products run on v_mfma_f32_16x16x32_bf16 in transposed form:
-//   S^T = K Q^T   -> each lane holds 4 keys x 1 query row (row = lane % 16),
-//   O^T = V^T P^T -> each lane holds 4 head-dim values of the same row,
-// so the online-softmax statistics of a row never leave its lane group, and
-// the probabilities produced by the first product are, register for
-// register, the B operand of the second (the contraction order over keys is
-// the same permutation on both operands).  Softmax runs in the log2 domain
-// with fp32 statistics.
+// wave, two workgroups per CU.  Key tiles of 64 rows and the matching V^T
+// tile are prefetched into registers one tile ahead and staged in padded LDS.
+// Both products run on v_mfma_f32_32x32x16_bf16 in transposed form:
+//   S^T = K Q^T   -> each lane holds 16 keys x 1 query row (row = lane % 32),
+//   O^T = V^T P^T -> each lane holds 16 head-dim values of the same row,
+// so a row's online-softmax statistics live in two lanes (l, l ^ 32), and the
+// probabilities produced by the first product are, register for register,
+// the B operand of the second (the contraction over keys uses the same key
+// permutation on both operands).  Softmax runs in the log2 domain with fp32
+// statistics.
 // fp32: one thread per query row on the VALU (exactness path).
 #include "kernels.h"
 
 namespace avits {
 namespace {
 
-constexpr int kRows = 128;       // query rows per workgroup
+constexpr int kRows = 128;        // query rows per workgroup (4 waves x 32)
 constexpr int kKT = kAttnKeyTile; // keys per tile
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Lane l of a 32x32 MFMA output tile holds row 8*(r/4) + 4*(l/32) + r%4 of
+// column l%32 in register r.  With S^T = K Q^T the column is the query row
+// and the row is the key, so key(r, h) = 8*(r/4) + 4*h + r%4 (h = l/32).
 template <int DH, bool WITH_V>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(const AttnArgs a) {
-  constexpr int kC = DH / 32;       // head-dim chunks of 32
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
+  constexpr int kC = DH / 16;       // 16-wide head-dim chunks (MFMA k)
   constexpr int kKL = DH + 8;       // padded K row (elements)
-  constexpr int kVL = kKT + 8;      // padded V^T row (elements)
+  constexpr int kVL = kKT + 4;      // padded V^T row: 34-word stride keeps 32 rows of 8-byte reads conflict-free
+  constexpr int kKP = kKT * DH / 8 / 256;  // 16-byte K pieces per thread per tile
+  constexpr int kVP = DH * kKT / 8 / 256;  // 16-byte V^T pieces per thread per tile
   __shared__ __attribute__((aligned(16))) bf16_t Ks[kKT * kKL];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[WITH_V ? DH * kVL : 8];
 
   const int h = blockIdx.y;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  const int g = lane / 16, r16 = lane % 16;
-  const int64_t row_base = int64_t(blockIdx.x) * kRows + wave * 32;
+  const int l32 = lane % 32, hi = lane / 32;
+  const int64_t row = int64_t(blockIdx.x) * kRows + wave * 32 + l32;
   const bf16_t* Q = static_cast<const bf16_t*>(a.q);
   const bf16_t* K = static_cast<const bf16_t*>(a.k);
   const bf16_t* VT = static_cast<const bf16_t*>(a.vt);
 
-  bf16x8 qf[2][kC];
+  // Q^T fragments (B operand): lane holds head-dim 16c + 8hi .. +7 of its row.
+  bf16x8 qf[kC];
+  {
+    const bf16_t* src = Q + std::min<int64_t>(row, a.Sq - 1) * a.q_tok + h * a.q_head + 8 * hi;
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    const int64_t row = row_base + 16 * rt + r16;
-    const bf16_t* src = Q + row * a.q_tok + h * a.q_head + 8 * g;
-#pragma unroll
-    for (int c = 0; c < kC; ++c) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (row < a.Sq) v = *reinterpret_cast<const u32x4*>(src + 32 * c);
-      qf[rt][c] = as_bf16x8(v);
-    }
+    for (int c = 0; c < kC; ++c) qf[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + 16 * c));
   }
   const float scale2 = kLog2e * rsqrtf(float(DH));
-  float mrow[2] = {-INFINITY, -INFINITY};
-  float lrow[2] = {0.f, 0.f};
-  f32x4 oacc[2][WITH_V ? DH / 16 : 1];
+  float mrow = -INFINITY, lrow = 0.f;
+  f32x16 oacc[WITH_V ? DH / 32 : 1];
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt)
+  for (int dt = 0; dt < (WITH_V ? DH / 32 : 1); ++dt)
 #pragma unroll
-    for (int dt = 0; dt < (WITH_V ? DH / 16 : 1); ++dt) oacc[rt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
 
-  for (int64_t k0 = 0; k0 < a.Sk; k0 += kKT) {
-    __syncthreads();
-    for (int p = tid; p < kKT * DH / 8; p += 256) {
-      const int key = p / (DH / 8), col = (p % (DH / 8)) * 8;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (k0 + key < a.Sk) v = *reinterpret_cast<const u32x4*>(K + (k0 + key) * a.k_tok + h * a.k_head + col);
-      *reinterpret_cast<u32x4*>(&Ks[key * kKL + col]) = v;
+  // Register prefetch of the next K / V^T tile.
+  u32x4 kreg[kKP], vreg[WITH_V ? kVP : 1];
+  auto load_tile = [&](int64_t k0) {
+#pragma unroll
+    for (int j = 0; j < kKP; ++j) {
+      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
+      const int64_t kr = std::min<int64_t>(k0 + key, a.Sk - 1);
+      kreg[j] = *reinterpret_cast<const u32x4*>(K + kr * a.k_tok + h * a.k_head + col);
     }
     if constexpr (WITH_V) {
       const bf16_t* vsrc = VT + int64_t(h) * DH * a.ldvt + k0;
-      for (int p = tid; p < DH * kKT / 8; p += 256) {
-        const int dv = p / (kKT / 8), kc = (p % (kKT / 8)) * 8;
-        *reinterpret_cast<u32x4*>(&Vs[dv * kVL + kc]) =
-            *reinterpret_cast<const u32x4*>(vsrc + int64_t(dv) * a.ldvt + kc);
+#pragma unroll
+      for (int j = 0; j < kVP; ++j) {
+        const int p = tid + 256 * j, dv = p / (kKT / 8), kc = (p % (kKT / 8)) * 8;
+        vreg[j] = *reinterpret_cast<const u32x4*>(vsrc + int64_t(dv) * a.ldvt + kc);
+        // Keys past the end (the row padding up to ldvt) may hold anything:
+        // zero them so that 0-probability keys contribute exactly 0.
+        const int64_t key0 = k0 + kc;
+        if (key0 + 8 > a.Sk) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int64_t kk = key0 + 2 * e;
+            vreg[j][e] = (kk < a.Sk ? vreg[j][e] & 0xffffu : 0u) | (kk + 1 < a.Sk ? vreg[j][e] & 0xffff0000u : 0u);
+          }
+        }
       }
     }
-    __syncthreads();
-
-    // Logits: s[rt][t][i] = q_row . k_(16t + 4g + i), log2-scaled.
-    f32x4 s[2][kKT / 16];
+  };
+  auto store_tile = [&]() {
 #pragma unroll
-    for (int t = 0; t < kKT / 16; ++t) {
-      bf16x8 kf[kC];
-#pragma unroll
-      for (int c = 0; c < kC; ++c)
-        kf[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(&Ks[(16 * t + r16) * kKL + 32 * c + 8 * g]));
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < kC; ++c) acc = mfma16x16x32(kf[c], qf[rt][c], acc);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const bool valid = k0 + 16 * t + 4 * g + i < a.Sk;
-          acc[i] = valid ? acc[i] * scale2 : -INFINITY;
-        }
-        s[rt][t] = acc;
-      }
-    }
-    // Online softmax per row (the row's four lane groups share statistics).
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      float mx = -INFINITY;
-#pragma unroll
-      for (int t = 0; t < kKT / 16; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[rt][t][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      const float mnew = fmaxf(mrow[rt], mx);
-      const float corr = exp2f(mrow[rt] - mnew);
-      mrow[rt] = mnew;
-      float ls = 0.f;
-#pragma unroll
-      for (int t = 0; t < kKT / 16; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float e = exp2f(s[rt][t][i] - mnew);
-          s[rt][t][i] = e;
-          ls += e;
-        }
-      lrow[rt] = lrow[rt] * corr + ls;
-      if constexpr (WITH_V) {
-#pragma unroll
-        for (int dt = 0; dt < DH / 16; ++dt) oacc[rt][dt] *= corr;
-      }
+    for (int j = 0; j < kKP; ++j) {
+      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
+      *reinterpret_cast<u32x4*>(&Ks[key * kKL + col]) = kreg[j];
     }
     if constexpr (WITH_V) {
-      // P^T operand for key chunk c2: keys {32c2 + 4g + i} then {32c2 + 16 + 4g + i}.
-      bf16x8 pf[2][2];
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
+      for (int j = 0; j < kVP; ++j) {
+        const int p = tid + 256 * j, dv = p / (kKT / 8), kc = (p % (kKT / 8)) * 8;
+        *reinterpret_cast<u32x4*>(&Vs[dv * kVL + kc]) = vreg[j];
+      }
+    }
+  };
+
+  load_tile(0);
+  for (int64_t k0 = 0; k0 < a.Sk; k0 += kKT) {
+    __syncthreads();  // previous tile fully consumed
+    store_tile();
+    __syncthreads();
+    if (k0 + kKT < a.Sk) load_tile(k0 + kKT);
+
+    // Logits of the 64-key tile: two 32-key sub-tiles, log2-scaled.
+    f32x16 s[kKT / 32];
 #pragma unroll
-        for (int c2 = 0; c2 < 2; ++c2) {
-          const f32x4 lo = s[rt][2 * c2], hi = s[rt][2 * c2 + 1];
-          u32x4 v = {pack_bf2(lo[0], lo[1]), pack_bf2(lo[2], lo[3]), pack_bf2(hi[0], hi[1]), pack_bf2(hi[2], hi[3])};
-          pf[rt][c2] = as_bf16x8(v);
-        }
+    for (int t = 0; t < kKT / 32; ++t) {
+      f32x16 acc;
 #pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) {
+      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
-        for (int c2 = 0; c2 < 2; ++c2) {
-          const bf16_t* vr = &Vs[(16 * dt + r16) * kVL + 32 * c2 + 4 * g];
+      for (int c = 0; c < kC; ++c) {
+        const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(&Ks[(32 * t + l32) * kKL + 16 * c + 8 * hi]));
+        acc = mfma32(kf, qf[c], acc);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
+        acc[r] = key < a.Sk ? acc[r] * scale2 : -INFINITY;
+      }
+      s[t] = acc;
+    }
+    // Online softmax: a row lives in lanes l32 and l32 + 32.
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < kKT / 32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float mnew = fmaxf(mrow, mx);
+    const float corr = exp2f(mrow - mnew);
+    mrow = mnew;
+    float ls = 0.f;
+#pragma unroll
+    for (int t = 0; t < kKT / 32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = exp2f(s[t][r] - mnew);
+        s[t][r] = e;
+        ls += e;
+      }
+    lrow = lrow * corr + ls;
+    if constexpr (WITH_V) {
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt) oacc[dt] *= corr;
+      // P^T operand for 16-key chunk c (keys 16c .. 16c + 15 of the tile):
+      // registers 8(c%2) .. 8(c%2) + 7 of sub-tile c/2 hold keys
+      // 16c + 4hi + {0..3} and 16c + 8 + 4hi + {0..3}.
+#pragma unroll
+      for (int c = 0; c < kKT / 16; ++c) {
+        const f32x16& st = s[c / 2];
+        const int b = 8 * (c % 2);
+        const u32x4 pv = {pack_bf2(st[b + 0], st[b + 1]), pack_bf2(st[b + 2], st[b + 3]),
+                          pack_bf2(st[b + 4], st[b + 5]), pack_bf2(st[b + 6], st[b + 7])};
+        const bf16x8 pf = as_bf16x8(pv);
+#pragma unroll
+        for (int dt = 0; dt < DH / 32; ++dt) {
+          const bf16_t* vr = &Vs[(32 * dt + l32) * kVL + 16 * c + 4 * hi];
           const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(vr + 16);
-          const u32x4 v = {lo[0], lo[1], hi[0], hi[1]};
-          const bf16x8 vf = as_bf16x8(v);
-#pragma unroll
-          for (int rt = 0; rt < 2; ++rt) oacc[rt][dt] = mfma16x16x32(vf, pf[rt][c2], oacc[rt][dt]);
+          const u32x2 up = *reinterpret_cast<const u32x2*>(vr + 8);
+          const u32x4 vv = {lo[0], lo[1], up[0], up[1]};
+          oacc[dt] = mfma32(as_bf16x8(vv), pf, oacc[dt]);
         }
       }
     }
   }
 
+  float l = lrow + __shfl_xor(lrow, 32, kWave);
+  if (row >= a.Sq) return;
+  if (a.lse && hi == 0) a.lse[int64_t(h) * a.Sq + row] = (mrow + log2f(l)) * kLn2;
+  if constexpr (WITH_V) {
+    // oacc[dt][r] = O[row][32 dt + 8(r/4) + 4hi + r%4].
+    const float inv = 1.f / l;
+    bf16_t* dst = static_cast<bf16_t*>(a.o) + row * a.ldo + int64_t(h) * DH + 4 * hi;
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    float l = lrow[rt];
-    l += __shfl_xor(l, 16, kWave);
-    l += __shfl_xor(l, 32, kWave);
-    const int64_t row = row_base + 16 * rt + r16;
-    if (row >= a.Sq) continue;
-    if (a.lse && g == 0) a.lse[int64_t(h) * a.Sq + row] = (mrow[rt] + log2f(l)) * kLn2;
-    if constexpr (WITH_V) {
-      const float inv = 1.f / l;
-      bf16_t* dst = static_cast<bf16_t*>(a.o) + row * a.ldo + int64_t(h) * DH + 4 * g;
+    for (int dt = 0; dt < DH / 32; ++dt)
 #pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) {
-        const f32x4 o = oacc[rt][dt];
-        const u32x2 w = {pack_bf2(o[0] * inv, o[1] * inv), pack_bf2(o[2] * inv, o[3] * inv)};
-        *reinterpret_cast<u32x2*>(dst + 16 * dt) = w;
+      for (int q = 0; q < 4; ++q) {
+        const f32x16& o = oacc[dt];
+        const u32x2 w = {pack_bf2(o[4 * q] * inv, o[4 * q + 1] * inv), pack_bf2(o[4 * q + 2] * inv, o[4 * q + 3] * inv)};
+        *reinterpret_cast<u32x2*>(dst + 32 * dt + 8 * q) = w;
       }
-    }
   }
 }
 

@@ -3,18 +3,18 @@
 // Launch sequence (double-stream; each GEMM is one grouped launch covering
 // the text rows with the text weights and the image rows with the image
 // weights):
-//   ln_mod(x, shift1, scale1) -> h
-//   h W_qkv^T + b                       -> qkv          [S, 3D]
-//   qk_rope_relayout(qkv)               -> q, k [H, S, d] (RMSNorm * g, RoPE at pos),
-//                                          v^T [H, d, S padded to 64]
-//   attention(q, k, v^T)                -> o [S, D], lse [H, S]
-//   x + gate1 (o W_o^T + b)             -> x_mid        (fused epilogue)
-//   ln_mod(x_mid, shift2, scale2)       -> h
-//   GELU(h W_1^T + b)                   -> m [S, F]     (fused epilogue)
-//   x_mid + gate2 (m W_2^T + b)         -> x_out        (fused epilogue)
-// Single-stream: ln_mod -> one GEMM whose epilogue writes q|k|v to qkv and
+//   ln_mod(x, shift1, scale1)             -> h                 [S, D]
+//   h W_qkv^T + b                         -> qk [S, 2D] (q | k, token-major)
+//                                            v^T [H, d, S_pad] (transposed epilogue)
+//   qk_norm_rope(qk) in place             -> RMSNorm * g, RoPE at pos
+//   attention(q, k, v^T)                  -> o [S, D], lse [H, S]
+//   x + gate1 (o W_o^T + b)               -> x_mid             (fused epilogue)
+//   ln_mod(x_mid, shift2, scale2)         -> h
+//   GELU(h W_1^T + b)                     -> m [S, F]          (fused epilogue)
+//   x_mid + gate2 (m W_2^T + b)           -> x_out             (fused epilogue)
+// Single-stream: ln_mod -> one GEMM whose epilogue writes q | k, v^T, and
 // GELU(m) beside the attention output (cat = [o, GELU(m)], [S, D + F]) ->
-// relayout -> attention into cat -> x + gate (cat W_out^T + b).
+// qk_norm_rope -> attention into cat -> x + gate (cat W_out^T + b).
 #include "kernels.h"
 
 namespace avits {
@@ -22,9 +22,12 @@ namespace {
 
 constexpr float kLnEps = 1e-6f, kRmsEps = 1e-6f;
 constexpr float kLog2Theta = 13.287712379549449f;  // log2(10000)
+constexpr int kLnMaxChunks = 8;                    // bf16 rows up to 64 * 8 * 8 = 4096 elements in registers
 
 // h = LN(x) (1 + scale) + shift, one wavefront per row; rows [0, n_a) use
-// (shift_a, scale_a), the rest (shift_b, scale_b).
+// (shift_a, scale_a), the rest (shift_b, scale_b).  bf16 rows of up to 4096
+// elements are held in registers (one read, one write); other rows take the
+// generic three-pass form.
 template <typename T>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, T* __restrict__ h, int64_t S,
                                                      int64_t D, int64_t n_a, const T* __restrict__ shift_a,
@@ -34,6 +37,59 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, T*
   const int64_t row = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave;
   if (row >= S) return;
   const T* xr = x + row * D;
+  const T* sh = row < n_a ? shift_a : shift_b;
+  const T* sc = row < n_a ? scale_a : scale_b;
+  T* hr = h + row * D;
+  if constexpr (sizeof(T) == 2) {
+    const int64_t nchunk = D / 8;
+    if (D % 8 == 0 && nchunk <= int64_t(kWave) * kLnMaxChunks) {
+      u32x4 v[kLnMaxChunks];
+      float s = 0.f;
+#pragma unroll
+      for (int c = 0; c < kLnMaxChunks; ++c) {
+        const int64_t idx = lane + kWave * c;
+        if (idx < nchunk) {
+          v[c] = reinterpret_cast<const u32x4*>(xr)[idx];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) s += __uint_as_float(v[c][e] << 16) + __uint_as_float(v[c][e] & 0xffff0000u);
+        }
+      }
+      const float mean = wave_sum(s) / float(D);
+      float q = 0.f;
+#pragma unroll
+      for (int c = 0; c < kLnMaxChunks; ++c) {
+        const int64_t idx = lane + kWave * c;
+        if (idx < nchunk) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float a = __uint_as_float(v[c][e] << 16) - mean, b = __uint_as_float(v[c][e] & 0xffff0000u) - mean;
+            q = fmaf(a, a, fmaf(b, b, q));
+          }
+        }
+      }
+      const float rstd = rsqrtf(wave_sum(q) / float(D) + kLnEps);
+#pragma unroll
+      for (int c = 0; c < kLnMaxChunks; ++c) {
+        const int64_t idx = lane + kWave * c;
+        if (idx < nchunk) {
+          const u32x4 g = reinterpret_cast<const u32x4*>(sc)[idx];
+          const u32x4 t = reinterpret_cast<const u32x4*>(sh)[idx];
+          u32x4 o;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float a = (__uint_as_float(v[c][e] << 16) - mean) * rstd * (1.f + __uint_as_float(g[e] << 16)) +
+                            __uint_as_float(t[e] << 16);
+            const float b = (__uint_as_float(v[c][e] & 0xffff0000u) - mean) * rstd *
+                                (1.f + __uint_as_float(g[e] & 0xffff0000u)) +
+                            __uint_as_float(t[e] & 0xffff0000u);
+            o[e] = pack_bf2(a, b);
+          }
+          reinterpret_cast<u32x4*>(hr)[idx] = o;
+        }
+      }
+      return;
+    }
+  }
   float s = 0.f;
   for (int64_t c = lane; c < D; c += kWave) s += ld(xr, c);
   const float mean = wave_sum(s) / float(D);
@@ -43,81 +99,79 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, T*
     v = fmaf(t, t, v);
   }
   const float rstd = rsqrtf(wave_sum(v) / float(D) + kLnEps);
-  const T* sh = row < n_a ? shift_a : shift_b;
-  const T* sc = row < n_a ? scale_a : scale_b;
-  T* hr = h + row * D;
   for (int64_t c = lane; c < D; c += kWave) st(hr, c, (ld(xr, c) - mean) * rstd * (1.f + ld(sc, c)) + ld(sh, c));
 }
 
-// RMSNorm + RoPE of q and k, and the per-head transpose of v.
-// Workgroup: 64 sequence rows x one head.  Rows [0, n_a) use the gains of
-// stream a.  q, k: [H, S, d]; vt: [H, d, ldvt], zero beyond S.
+// In-place RMSNorm (times the gain) and RoPE of q and k in qk [S, 2D]
+// (q | k, head-major within each).  Each lane owns 8 consecutive elements
+// (4 rotation pairs) of one head, so a d-wide head spans d/8 lanes and the
+// RMS reduction stays inside that lane group.  Rows [0, n_a) use the gains
+// of stream a.  One wavefront walks the 2H heads of a row, 64*8/d heads at a
+// time.
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void qk_rope_relayout_kernel(
-    const T* __restrict__ qkv, int64_t ld_qkv, const int32_t* __restrict__ pos, int64_t S, int H, int64_t n_a,
-    const T* __restrict__ gq_a, const T* __restrict__ gk_a, const T* __restrict__ gq_b,
-    const T* __restrict__ gk_b, T* __restrict__ q, T* __restrict__ k, T* __restrict__ vt, int64_t ldvt) {
-  constexpr int kPairs = DH / 2;
-  __shared__ float vs[64][DH + 1];
-  const int h = blockIdx.y;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int64_t row0 = int64_t(blockIdx.x) * 64;
-  const int64_t D = int64_t(H) * DH;
-
-  // Pair m = lane (d = 128) or lane < 32 (d = 64): axis and in-axis index.
-  const int m = lane;
-  const bool live = m < kPairs;
-  constexpr int p0 = DH / 16, p1 = 7 * DH / 32;  // pairs per axis: (p0, p1, p1)
-  const int axis = m < p0 ? 0 : (m < p0 + p1 ? 1 : 2);
-  const int mi = axis == 0 ? m : (axis == 1 ? m - p0 : m - p0 - p1);
-  const int na = axis == 0 ? 2 * p0 : 2 * p1;  // axis width in dims
-  const float freq = exp2f(-2.f * float(mi) / float(na) * kLog2Theta);
-
-  for (int r = wave; r < 64; r += 4) {
-    const int64_t row = row0 + r;
-    if (row >= S) break;
-    const T* src = qkv + row * ld_qkv + int64_t(h) * DH;
-    const float ang = float(pos[3 * row + axis]) * freq;
-    float sn, cs;
-    sincosf(ang, &sn, &cs);
-    const bool a = row < n_a;
+__global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ qk, const int32_t* __restrict__ pos,
+                                                           int64_t S, int H, int64_t n_a, const T* __restrict__ gq_a,
+                                                           const T* __restrict__ gk_a, const T* __restrict__ gq_b,
+                                                           const T* __restrict__ gk_b) {
+  constexpr int kLanesPerHead = DH / 8;
+  constexpr int kHeadsPerPass = kWave / kLanesPerHead;
+  constexpr int p0 = DH / 16, p1 = 7 * DH / 32;  // rotation pairs per axis: (p0, p1, p1)
+  const int lane = threadIdx.x % kWave;
+  const int64_t row = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave;
+  if (row >= S) return;
+  const int sub = lane % kLanesPerHead;           // position of the lane inside its head
+  const int hoff = lane / kLanesPerHead;          // head slot within a pass
+  const bool a_rows = row < n_a;
+  // Angles of this lane's four pairs m = 4 sub + j.
+  float cs[4], sn[4];
+  const int32_t pr[3] = {pos[3 * row], pos[3 * row + 1], pos[3 * row + 2]};
 #pragma unroll
-    for (int which = 0; which < 2; ++which) {
-      const T* x = src + which * D;
-      const T* gain = which == 0 ? (a ? gq_a : gq_b) : (a ? gk_a : gk_b);
-      const float x0 = live ? ld(x, 2 * m) : 0.f, x1 = live ? ld(x, 2 * m + 1) : 0.f;
-      const float ms = wave_sum(x0 * x0 + x1 * x1) / float(DH);
-      const float r_ = rsqrtf(ms + kRmsEps);
-      if (live) {
-        const float y0 = x0 * r_ * ld(gain, 2 * m), y1 = x1 * r_ * ld(gain, 2 * m + 1);
-        T* dst = (which == 0 ? q : k) + (int64_t(h) * S + row) * DH + 2 * m;
-        st(dst, 0, y0 * cs - y1 * sn);
-        st(dst, 1, y0 * sn + y1 * cs);
+  for (int j = 0; j < 4; ++j) {
+    const int m = 4 * sub + j;
+    const int axis = m < p0 ? 0 : (m < p0 + p1 ? 1 : 2);
+    const int mi = axis == 0 ? m : (axis == 1 ? m - p0 : m - p0 - p1);
+    const int na = axis == 0 ? 2 * p0 : 2 * p1;
+    const float freq = exp2f(-2.f * float(mi) / float(na) * kLog2Theta);
+    sincosf(float(pr[axis]) * freq, &sn[j], &cs[j]);
+  }
+  T* base = qk + row * (2 * int64_t(H) * DH);
+  for (int h0 = 0; h0 < 2 * H; h0 += kHeadsPerPass) {
+    const int head = h0 + hoff;                  // 0..H-1 query heads, H..2H-1 key heads
+    const bool live = head < 2 * H;
+    const T* gain = head < H ? (a_rows ? gq_a : gq_b) : (a_rows ? gk_a : gk_b);
+    T* p = base + int64_t(live ? head : 0) * DH + 8 * sub;
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = live ? ld(p, e) : 0.f;
+    float ss = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
+#pragma unroll
+    for (int o = 1; o < kLanesPerHead; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+    const float r = rsqrtf(ss / float(DH) + kRmsEps);
+    if (live) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float y0 = x[2 * j] * r * ld(gain, 8 * sub + 2 * j);
+        const float y1 = x[2 * j + 1] * r * ld(gain, 8 * sub + 2 * j + 1);
+        x[2 * j] = y0 * cs[j] - y1 * sn[j];
+        x[2 * j + 1] = y0 * sn[j] + y1 * cs[j];
       }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) st(p, e, x[e]);
     }
-  }
-  // v^T through LDS: read rows coalesced, write keys coalesced.
-  for (int p = threadIdx.x; p < 64 * DH; p += 256) {
-    const int r = p / DH, c = p % DH;
-    const int64_t row = row0 + r;
-    vs[r][c] = row < S ? ld(qkv + row * ld_qkv + 2 * D + int64_t(h) * DH, c) : 0.f;
-  }
-  __syncthreads();
-  for (int p = threadIdx.x; p < 64 * DH; p += 256) {
-    const int c = p / 64, r = p % 64;
-    if (row0 + r < ldvt) st(vt + (int64_t(h) * DH + c) * ldvt + row0, r, vs[r][c]);
   }
 }
 
 struct BlockWs {
-  char* h;
-  char* qkv;
-  char* q;
-  char* k;
-  char* vt;
+  char* h;      // [S, D]
+  char* qk;     // [S, 2D]
+  char* vt;     // [H, d, ldvt]
   char* o;      // double: [S, D]; single: cat [S, D + F]
   char* xmid;   // double only
   char* mlp;    // double only: [S, F]
+  float* partial;  // split-K partial sums of the N = D projections
+  size_t partial_bytes;
   int64_t ldvt;
   size_t bytes;
 };
@@ -127,23 +181,23 @@ BlockWs block_ws_layout(char* base, int kind, int64_t S, int64_t H, int64_t d, i
   const int64_t D = H * d;
   w.ldvt = ceil_div64(std::max<int64_t>(S, 1), kAttnKeyTile) * kAttnKeyTile;
   size_t off = 0;
-  auto take = [&](int64_t elems) {
+  auto take = [&](size_t bytes) {
     char* p = base ? base + off : nullptr;
-    off += align_up(size_t(elems) * size_t(esz), 256);
+    off += align_up(bytes, 256);
     return p;
   };
-  w.h = take(S * D);
-  w.qkv = take(S * 3 * D);
-  w.q = take(H * S * d);
-  w.k = take(H * S * d);
-  w.vt = take(H * d * w.ldvt);
+  w.h = take(size_t(S * D * esz));
+  w.qk = take(size_t(S * 2 * D * esz));
+  w.vt = take(size_t(H * d * w.ldvt * esz));
   if (kind == AVITS_BLOCK_DOUBLE) {
-    w.o = take(S * D);
-    w.xmid = take(S * D);
-    w.mlp = take(S * F);
+    w.o = take(size_t(S * D * esz));
+    w.xmid = take(size_t(S * D * esz));
+    w.mlp = take(size_t(S * F * esz));
   } else {
-    w.o = take(S * (D + F));
+    w.o = take(size_t(S * (D + F) * esz));
   }
+  w.partial_bytes = gemm_partial_reserve(S, D);
+  w.partial = reinterpret_cast<float*>(take(w.partial_bytes));
   w.bytes = off;
   return w;
 }
@@ -153,11 +207,11 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
               const avits_block_weights* w, int H, int d, int dtype, float* lse_out, const BlockWs& ws,
               hipStream_t s) {
   const int64_t S = n_txt + n_img, D = int64_t(H) * d, F = w->mlp_hidden;
-  const int64_t esz = sizeof(T);
   const bool dbl = w->kind == AVITS_BLOCK_DOUBLE;
   const T* x = static_cast<const T*>(x_in);
   T* h = reinterpret_cast<T*>(ws.h);
-  T* qkv = reinterpret_cast<T*>(ws.qkv);
+  T* qk = reinterpret_cast<T*>(ws.qk);
+  T* vt = reinterpret_cast<T*>(ws.vt);
   const dim3 rows_grid(unsigned(ceil_div64(S, 4))), blk(256);
   int rc;
 
@@ -170,86 +224,85 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
     for (auto& t : st2)
       if (t.rows > 0) streams[nst++] = t;
   }
+  // Weights of the text rows and of the image rows (an empty stream borrows
+  // the other's pointers; they are never read for it).
+  const avits_double_stream_weights& wa = n_txt ? w->txt : w->img;
+  const avits_double_stream_weights& wb = n_img ? w->img : w->txt;
   auto mod_row = [&](const void* mod, int r) { return static_cast<const T*>(mod) + r * D; };
 
   // 1. modulated layer norm.
-  if (dbl) {
-    const void* ma = n_txt ? w->txt.mod : w->img.mod;
-    const void* mb = n_img ? w->img.mod : w->txt.mod;
+  {
     TimedLaunch timed("ln_mod", s);
-    hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, n_txt, mod_row(ma, 0), mod_row(ma, 1),
-                       mod_row(mb, 0), mod_row(mb, 1));
-  } else {
-    const void* mm = w->single.mod;
-    TimedLaunch timed("ln_mod", s);
-    hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, S, mod_row(mm, 0), mod_row(mm, 1),
-                       mod_row(mm, 0), mod_row(mm, 1));
+    if (dbl)
+      hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, n_txt, mod_row(wa.mod, 0),
+                         mod_row(wa.mod, 1), mod_row(wb.mod, 0), mod_row(wb.mod, 1));
+    else
+      hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, S, mod_row(w->single.mod, 0),
+                         mod_row(w->single.mod, 1), mod_row(w->single.mod, 0), mod_row(w->single.mod, 1));
+    if ((rc = launch_status("block ln_mod")) != AVITS_OK) return rc;
   }
-  if ((rc = launch_status("block ln_mod")) != AVITS_OK) return rc;
 
-  // 2. QKV projection (+ the single block's MLP input, GELU'd beside o).
+  // 2. QKV projection: q | k token-major, v transposed per head
+  //    (+ the single block's MLP input, GELU'd beside o).
   {
     GemmArgs g{};
     g.K = D;
+    g.n_split = 2 * D;
+    g.n_split2 = 3 * D;
+    g.mode0 = EPI_STORE;
+    g.mode1 = EPI_STORE_T;
+    g.mode2 = EPI_GELU;
     if (dbl) {
       g.N = 3 * D;
-      g.n_split = g.N;
-      g.mode0 = g.mode1 = EPI_STORE;
       for (int i = 0; i < nst; ++i) {
         GemmProblem& p = g.p[i];
-        p.A = h + streams[i].r0 * D; p.lda = D;
+        const int64_t r0 = streams[i].r0;
+        p.A = h + r0 * D; p.lda = D;
         p.W = streams[i].dw->w_qkv; p.bias = streams[i].dw->b_qkv; p.M = streams[i].rows;
-        p.out0 = qkv + streams[i].r0 * 3 * D; p.ld0 = 3 * D;
+        p.out0 = qk + r0 * 2 * D; p.ld0 = 2 * D;
+        p.out1 = vt + r0; p.ld1 = ws.ldvt;
       }
       g.nprob = nst;
     } else {
       g.N = 3 * D + F;
-      g.n_split = 3 * D;
-      g.mode0 = EPI_STORE;
-      g.mode1 = EPI_GELU;
       GemmProblem& p = g.p[0];
       p.A = h; p.lda = D; p.W = w->single.w_in; p.bias = w->single.b_in; p.M = S;
-      p.out0 = qkv; p.ld0 = 3 * D;
-      p.out1 = reinterpret_cast<T*>(ws.o) + D; p.ld1 = D + F;
+      p.out0 = qk; p.ld0 = 2 * D;
+      p.out1 = vt; p.ld1 = ws.ldvt;
+      p.out2 = reinterpret_cast<T*>(ws.o) + D; p.ld2 = D + F;
       g.nprob = 1;
     }
-    if ((rc = launch_gemm(g, dtype, s)) != AVITS_OK) return rc;
+    if ((rc = launch_gemm(g, dtype, s, dbl ? "gemm_qkv" : "gemm_single_in", ws.partial, ws.partial_bytes)) != AVITS_OK)
+      return rc;
   }
 
-  // 3. q/k RMSNorm + RoPE, v transpose.
+  // 3. q/k RMSNorm + RoPE in place.
   {
     const T *gqa, *gka, *gqb, *gkb;
     int64_t na;
     if (dbl) {
-      const avits_double_stream_weights& ta = n_txt ? w->txt : w->img;
-      const avits_double_stream_weights& tb = n_img ? w->img : w->txt;
-      gqa = static_cast<const T*>(ta.g_q); gka = static_cast<const T*>(ta.g_k);
-      gqb = static_cast<const T*>(tb.g_q); gkb = static_cast<const T*>(tb.g_k);
+      gqa = static_cast<const T*>(wa.g_q); gka = static_cast<const T*>(wa.g_k);
+      gqb = static_cast<const T*>(wb.g_q); gkb = static_cast<const T*>(wb.g_k);
       na = n_txt;
     } else {
       gqa = gqb = static_cast<const T*>(w->single.g_q);
       gka = gkb = static_cast<const T*>(w->single.g_k);
       na = S;
     }
-    const dim3 grid(unsigned(ceil_div64(S, 64)), unsigned(H));
     TimedLaunch timed("qk_rope", s);
     if (d == 128)
-      hipLaunchKernelGGL((qk_rope_relayout_kernel<T, 128>), grid, blk, 0, s, qkv, 3 * D, pos, S, H, na, gqa, gka,
-                         gqb, gkb, reinterpret_cast<T*>(ws.q), reinterpret_cast<T*>(ws.k),
-                         reinterpret_cast<T*>(ws.vt), ws.ldvt);
+      hipLaunchKernelGGL((qk_norm_rope_kernel<T, 128>), rows_grid, blk, 0, s, qk, pos, S, H, na, gqa, gka, gqb, gkb);
     else
-      hipLaunchKernelGGL((qk_rope_relayout_kernel<T, 64>), grid, blk, 0, s, qkv, 3 * D, pos, S, H, na, gqa, gka,
-                         gqb, gkb, reinterpret_cast<T*>(ws.q), reinterpret_cast<T*>(ws.k),
-                         reinterpret_cast<T*>(ws.vt), ws.ldvt);
-    if ((rc = launch_status("block qk_rope_relayout")) != AVITS_OK) return rc;
+      hipLaunchKernelGGL((qk_norm_rope_kernel<T, 64>), rows_grid, blk, 0, s, qk, pos, S, H, na, gqa, gka, gqb, gkb);
+    if ((rc = launch_status("block qk_norm_rope")) != AVITS_OK) return rc;
   }
 
   // 4. joint attention over all S rows.
   {
     AttnArgs a{};
-    a.q = ws.q; a.q_tok = d; a.q_head = S * d;
-    a.k = ws.k; a.k_tok = d; a.k_head = S * d;
-    a.vt = ws.vt; a.ldvt = ws.ldvt;
+    a.q = qk; a.q_tok = 2 * D; a.q_head = d;
+    a.k = qk + D; a.k_tok = 2 * D; a.k_head = d;
+    a.vt = vt; a.ldvt = ws.ldvt;
     a.o = ws.o; a.ldo = dbl ? D : D + F;
     a.lse = lse_out;
     a.Sq = S; a.Sk = S; a.H = H; a.d = d;
@@ -259,18 +312,18 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
   T* out = static_cast<T*>(x_out);
   if (!dbl) {
     GemmArgs g{};
-    g.N = D; g.K = D + F; g.n_split = g.N; g.mode0 = g.mode1 = EPI_RESID_GATE; g.nprob = 1;
+    g.N = D; g.K = D + F; g.n_split = g.n_split2 = g.N; g.mode0 = EPI_RESID_GATE; g.nprob = 1;
     GemmProblem& p = g.p[0];
     p.A = ws.o; p.lda = D + F; p.W = w->single.w_out; p.bias = w->single.b_out; p.M = S;
     p.out0 = out; p.ld0 = D; p.resid = x; p.ldr = D; p.gate = mod_row(w->single.mod, 2);
-    return launch_gemm(g, dtype, s);
+    return launch_gemm(g, dtype, s, "gemm_single_out", ws.partial, ws.partial_bytes);
   }
 
   // 5. output projection + gated residual.
   T* xmid = reinterpret_cast<T*>(ws.xmid);
   {
     GemmArgs g{};
-    g.N = D; g.K = D; g.n_split = g.N; g.mode0 = g.mode1 = EPI_RESID_GATE; g.nprob = nst;
+    g.N = D; g.K = D; g.n_split = g.n_split2 = g.N; g.mode0 = EPI_RESID_GATE; g.nprob = nst;
     for (int i = 0; i < nst; ++i) {
       GemmProblem& p = g.p[i];
       const int64_t r0 = streams[i].r0;
@@ -279,34 +332,32 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
       p.out0 = xmid + r0 * D; p.ld0 = D; p.resid = x + r0 * D; p.ldr = D;
       p.gate = mod_row(streams[i].dw->mod, 2);
     }
-    if ((rc = launch_gemm(g, dtype, s)) != AVITS_OK) return rc;
+    if ((rc = launch_gemm(g, dtype, s, "gemm_o", ws.partial, ws.partial_bytes)) != AVITS_OK) return rc;
   }
   // 6. second modulated layer norm.
   {
-    const void* ma = n_txt ? w->txt.mod : w->img.mod;
-    const void* mb = n_img ? w->img.mod : w->txt.mod;
     TimedLaunch timed("ln_mod", s);
-    hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, xmid, h, S, D, n_txt, mod_row(ma, 3), mod_row(ma, 4),
-                       mod_row(mb, 3), mod_row(mb, 4));
+    hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, xmid, h, S, D, n_txt, mod_row(wa.mod, 3),
+                       mod_row(wa.mod, 4), mod_row(wb.mod, 3), mod_row(wb.mod, 4));
+    if ((rc = launch_status("block ln_mod2")) != AVITS_OK) return rc;
   }
-  if ((rc = launch_status("block ln_mod2")) != AVITS_OK) return rc;
   // 7. MLP in + GELU.
   T* mlp = reinterpret_cast<T*>(ws.mlp);
   {
     GemmArgs g{};
-    g.N = F; g.K = D; g.n_split = g.N; g.mode0 = g.mode1 = EPI_GELU; g.nprob = nst;
+    g.N = F; g.K = D; g.n_split = g.n_split2 = g.N; g.mode0 = EPI_GELU; g.nprob = nst;
     for (int i = 0; i < nst; ++i) {
       GemmProblem& p = g.p[i];
       const int64_t r0 = streams[i].r0;
       p.A = h + r0 * D; p.lda = D; p.W = streams[i].dw->w_mlp1; p.bias = streams[i].dw->b_mlp1;
       p.M = streams[i].rows; p.out0 = mlp + r0 * F; p.ld0 = F;
     }
-    if ((rc = launch_gemm(g, dtype, s)) != AVITS_OK) return rc;
+    if ((rc = launch_gemm(g, dtype, s, "gemm_mlp_in", ws.partial, ws.partial_bytes)) != AVITS_OK) return rc;
   }
   // 8. MLP out + gated residual.
   {
     GemmArgs g{};
-    g.N = D; g.K = F; g.n_split = g.N; g.mode0 = g.mode1 = EPI_RESID_GATE; g.nprob = nst;
+    g.N = D; g.K = F; g.n_split = g.n_split2 = g.N; g.mode0 = EPI_RESID_GATE; g.nprob = nst;
     for (int i = 0; i < nst; ++i) {
       GemmProblem& p = g.p[i];
       const int64_t r0 = streams[i].r0;
@@ -314,9 +365,8 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
       p.M = streams[i].rows; p.out0 = out + r0 * D; p.ld0 = D; p.resid = xmid + r0 * D; p.ldr = D;
       p.gate = mod_row(streams[i].dw->mod, 5);
     }
-    if ((rc = launch_gemm(g, dtype, s)) != AVITS_OK) return rc;
+    if ((rc = launch_gemm(g, dtype, s, "gemm_mlp_out", ws.partial, ws.partial_bytes)) != AVITS_OK) return rc;
   }
-  (void)esz;
   return AVITS_OK;
 }
 
@@ -350,8 +400,8 @@ extern "C" int avits_block_forward(const void* x_in, void* x_out, const int32_t*
     return set_error(AVITS_ERR_UNSUPPORTED, "block_forward: dtype %d unsupported", dtype);
   AVITS_REQUIRE(w->kind == AVITS_BLOCK_DOUBLE || w->kind == AVITS_BLOCK_SINGLE, "block_forward: bad kind %d",
                 w->kind);
-  AVITS_REQUIRE(w->mlp_hidden >= 64 && w->mlp_hidden % 64 == 0, "block_forward: mlp_hidden=%d must be a positive multiple of 64",
-                w->mlp_hidden);
+  AVITS_REQUIRE(w->mlp_hidden >= 64 && w->mlp_hidden % 64 == 0,
+                "block_forward: mlp_hidden=%d must be a positive multiple of 64", w->mlp_hidden);
   const int64_t S = n_txt + n_img;
   AVITS_REQUIRE(S <= INT32_MAX, "block_forward: S=%lld too large", (long long)S);
   if (S == 0) return AVITS_OK;

@@ -1,26 +1,46 @@
 // GEMMs of the MMDiT block (QKV, output projection, MLP), with the bias,
 // GELU and gated-residual epilogues fused.
 //
-// bf16: 128x128 output tile per 256-thread workgroup, k-tiles of 64 staged
-// through padded LDS rows (conflict-free 16-byte fragment reads), each wave a
-// 64x64 quadrant of 4x4 v_mfma_f32_16x16x32_bf16 tiles.  The MFMA computes
-// C^T = W A^T so that each lane ends up owning four consecutive output
-// columns of one row: the epilogue stores 8 contiguous bytes per lane.
-// fp32: 64x64 tiles on the VALU (the fp32 path exists for exactness checks).
+// bf16 path (MFMA):
+//  - Macro tile 256 x BN (BN in {256, 192, 128}) x 64, one 512-thread
+//    workgroup of 8 waves (2 x 4, or 4 x 2 for BN = 192), each wave a
+//    128 x 64 (64 x 96) block of v_mfma_f32_32x32x16_bf16 tiles; two
+//    waves per SIMD hide each other's LDS and barrier waits.
+//  - The MFMA computes C^T = W A^T, so each lane owns groups of four
+//    consecutive output columns of one row (8-byte stores in the epilogue).
+//  - k-tiles are staged global -> registers -> LDS with two register stages
+//    and two LDS buffers, one barrier per k-tile: while tile t is
+//    multiplied, tile t+1 waits in registers and tile t+2 is in flight.  LDS rows are 128 bytes (64 bf16) with the 16-byte chunk index
+//    XOR-swizzled by (row / 2) mod 8, which makes both the staging writes and
+//    the 16-byte fragment reads of 16 consecutive rows bank-conflict free.
+//  - Small-N GEMMs (the N = D projections) are split along K when the tile
+//    grid would leave most of the 256 CUs idle: each split writes fp32
+//    partials and a reduce kernel sums them in split order (deterministic)
+//    and applies the epilogue.
+// fp32 path: 64x64 tiles on the VALU (the exactness path).
+#include <stdio.h>
+#include <stdlib.h>
+
 #include "kernels.h"
 
 namespace avits {
 namespace {
 
-constexpr int kBM = 128, kBN = 128, kBK = 64;
-constexpr int kLdsRow = kBK + 8;  // padded row, bf16 elements
+constexpr int kBM = 256, kBK = 64;
+constexpr int kCUs = 256;
 
 __device__ __forceinline__ float gelu_tanh(float x) {
   const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
   return 0.5f * x * (1.f + tanhf(u));
 }
 
-// Epilogue for four consecutive columns n..n+3 of row m (n % 4 == 0, n < N).
+__device__ __forceinline__ f32x16 mfma32x32x16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Epilogue for four consecutive columns n..n+3 of row m of problem p (the
+// four columns never straddle a region boundary: region starts are
+// multiples of 4).
 template <typename T>
 __device__ __forceinline__ void epilogue4(const GemmArgs& a, const GemmProblem& p, int64_t m, int64_t n,
                                           float v0, float v1, float v2, float v3) {
@@ -30,11 +50,16 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, const GemmProblem& 
 #pragma unroll
     for (int r = 0; r < 4; ++r) v[r] += ld(b, n + r);
   }
-  const bool first = n < a.n_split;
-  const int mode = first ? a.mode0 : a.mode1;
-  T* out = static_cast<T*>(first ? p.out0 : p.out1);
-  const int64_t col = first ? n : n - a.n_split;
-  const int64_t ldo = first ? p.ld0 : p.ld1;
+  int mode;
+  T* out;
+  int64_t col, ldo;
+  if (n < a.n_split) {
+    mode = a.mode0; out = static_cast<T*>(p.out0); col = n; ldo = p.ld0;
+  } else if (n < a.n_split2) {
+    mode = a.mode1; out = static_cast<T*>(p.out1); col = n - a.n_split; ldo = p.ld1;
+  } else {
+    mode = a.mode2; out = static_cast<T*>(p.out2); col = n - a.n_split2; ldo = p.ld2;
+  }
   if (mode == EPI_GELU) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) v[r] = gelu_tanh(v[r]);
@@ -43,6 +68,10 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, const GemmProblem& 
     const T* gt = static_cast<const T*>(p.gate);
 #pragma unroll
     for (int r = 0; r < 4; ++r) v[r] = ld(res, m * p.ldr + col + r) + ld(gt, n + r) * v[r];
+  } else if (mode == EPI_STORE_T) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) st(out, (col + r) * ldo + m, v[r]);
+    return;
   }
   T* dst = out + m * ldo + col;
   if constexpr (sizeof(T) == 2) {
@@ -53,101 +82,189 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, const GemmProblem& 
   }
 }
 
-// Map the flat workgroup id onto (problem, tile row, tile col).
-__device__ __forceinline__ bool map_tile(const GemmArgs& a, int bm, int bn, int& prob, int64_t& m0, int64_t& n0) {
+// Flat workgroup id -> (problem, tile origin, k split).  Tiles of one problem
+// come first; within a problem, consecutive ids walk down the rows of one
+// column block so neighbouring workgroups share the weight tile.
+__device__ __forceinline__ bool map_tile(const GemmArgs& a, int bm, int bn, int splits, int& prob, int64_t& m0,
+                                         int64_t& n0, int& ks) {
   const int64_t tn = (a.N + bn - 1) / bn;
   int64_t bid = blockIdx.x;
-  const int64_t t0 = ((a.p[0].M + bm - 1) / bm) * tn;
+  ks = int(bid % splits);
+  bid /= splits;
+  const int64_t tm0 = (a.p[0].M + bm - 1) / bm;
+  const int64_t t0 = tm0 * tn;
   prob = 0;
+  int64_t tm = tm0;
   if (bid >= t0) {
     bid -= t0;
     prob = 1;
     if (a.nprob < 2) return false;
+    tm = (a.p[1].M + bm - 1) / bm;
   }
-  m0 = (bid / tn) * bm;
-  n0 = (bid % tn) * bn;
-  return m0 < a.p[prob].M;
+  if (tm == 0) return false;
+  m0 = (bid % tm) * bm;
+  n0 = (bid / tm) * bn;
+  return m0 < a.p[prob].M && n0 < a.N;
 }
 
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(const GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t As[kBM * kLdsRow];
-  __shared__ __attribute__((aligned(16))) bf16_t Ws[kBN * kLdsRow];
-  int prob;
+// Swizzled 16-byte chunk slot of (row, chunk) in a 128-byte LDS row.
+__device__ __forceinline__ int swz(int row, int chunk) { return row * 8 + (chunk ^ ((row >> 1) & 7)); }
+
+template <int BN, int WAVES_M, int WAVES_N>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(const GemmArgs a,
+                                                                           float* __restrict__ partial, int splits) {
+  constexpr int NT = 64 * WAVES_M * WAVES_N;
+  constexpr int WM = kBM / WAVES_M, WN = BN / WAVES_N;
+  constexpr int TM = WM / 32, TN = WN / 32;  // 32x32 MFMA tiles per wave
+  constexpr int CA = kBM * 8 / NT;           // 16-byte A chunks staged per thread per k-tile
+  constexpr int CW = BN * 8 / NT;
+  constexpr int RS = NT / 8;                 // rows between a thread's chunks
+  static_assert(WM % 32 == 0 && WN % 32 == 0 && (BN * 8) % NT == 0 && RS % 16 == 0, "tile shape");
+  __shared__ u32x4 lds[2][(kBM + BN) * 8];
+
+  int prob, ks;
   int64_t m0, n0;
-  if (!map_tile(a, kBM, kBN, prob, m0, n0)) return;
+  if (!map_tile(a, kBM, BN, splits, prob, m0, n0, ks)) return;
   const GemmProblem& p = a.p[prob];
   const bf16_t* A = static_cast<const bf16_t*>(p.A);
   const bf16_t* W = static_cast<const bf16_t*>(p.W);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  const int g = lane / 16, r16 = lane % 16;
-  const int wm = wave / 2, wn = wave % 2;
+  const int l32 = lane % 32, hi = lane / 32;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
-  // Global -> register staging: 4 16-byte pieces of each operand per thread.
-  u32x4 ra[4], rw[4];
-  auto load_tile = [&](int64_t k0) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int piece = tid + 256 * j;
-      const int row = piece / 8, kc = (piece % 8) * 8;
-      const int64_t m = m0 + row, n = n0 + row;
-      u32x4 z = {0u, 0u, 0u, 0u};
-      ra[j] = m < p.M ? *reinterpret_cast<const u32x4*>(A + m * p.lda + k0 + kc) : z;
-      rw[j] = n < a.N ? *reinterpret_cast<const u32x4*>(W + n * a.K + k0 + kc) : z;
-    }
-  };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int piece = tid + 256 * j;
-      const int row = piece / 8, kc = (piece % 8) * 8;
-      *reinterpret_cast<u32x4*>(&As[row * kLdsRow + kc]) = ra[j];
-      *reinterpret_cast<u32x4*>(&Ws[row * kLdsRow + kc]) = rw[j];
-    }
-  };
+  const int64_t nk = a.K / kBK;
+  const int64_t kt0 = nk * ks / splits, kt1 = nk * (ks + 1) / splits;
 
-  f32x4 acc[4][4];
+  // Staging: thread t moves 16-byte chunk (t % 8) of rows t / 8 + RS j, so all
+  // of its chunks share one column offset and one swizzle (RS j / 2 = 0 mod 8).
+  // Rows past the end re-read the last valid row (no branch around the load)
+  // and are zeroed by a select, so every load is unconditional.
+  const int row_t = tid / 8, kc_t = tid % 8;
+  const int slot_t = row_t * 8 + (kc_t ^ ((row_t >> 1) & 7));
+  const bf16_t* a_ptr[CA];
+  const bf16_t* w_ptr[CW];
+  uint32_t a_valid = 0, w_valid = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  load_tile(0);
-  store_tile();
-  __syncthreads();
-  for (int64_t k0 = 0; k0 < a.K; k0 += kBK) {
-    const bool more = k0 + kBK < a.K;
-    if (more) load_tile(k0 + kBK);
-#pragma unroll
-    for (int c = 0; c < kBK / 32; ++c) {
-      bf16x8 af[4], wf[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = as_bf16x8(*reinterpret_cast<const u32x4*>(&As[(wm * 64 + 16 * i + r16) * kLdsRow + 32 * c + 8 * g]));
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        wf[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(&Ws[(wn * 64 + 16 * j + r16) * kLdsRow + 32 * c + 8 * g]));
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(wf[j], af[i], acc[i][j]);
-    }
-    __syncthreads();
-    if (more) {
-      store_tile();
-      __syncthreads();
-    }
+  for (int j = 0; j < CA; ++j) {
+    const int64_t m = m0 + row_t + RS * j;
+    a_valid |= uint32_t(m < p.M) << j;
+    a_ptr[j] = A + std::min<int64_t>(m, p.M - 1) * p.lda + kc_t * 8;
   }
-  // acc[i][j][r] = C[m0 + wm*64 + 16i + r16][n0 + wn*64 + 16j + 4g + r].
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t m = m0 + wm * 64 + 16 * i + r16;
+  for (int j = 0; j < CW; ++j) {
+    const int64_t n = n0 + row_t + RS * j;
+    w_valid |= uint32_t(n < a.N) << j;
+    w_ptr[j] = W + std::min<int64_t>(n, a.N - 1) * a.K + kc_t * 8;
+  }
+  struct Stage {
+    u32x4 a[CA], w[CW];
+  };
+  auto load_tile = [&](Stage& st, int64_t kt) {
+    const int64_t off = kt * kBK;
+#pragma unroll
+    for (int j = 0; j < CA; ++j) st.a[j] = *reinterpret_cast<const u32x4*>(a_ptr[j] + off);
+#pragma unroll
+    for (int j = 0; j < CW; ++j) st.w[j] = *reinterpret_cast<const u32x4*>(w_ptr[j] + off);
+  };
+  auto store_tile = [&](const Stage& st, int buf) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < CA; ++j) lds[buf][slot_t + RS * 8 * j] = (a_valid >> j) & 1u ? st.a[j] : z;
+#pragma unroll
+    for (int j = 0; j < CW; ++j) lds[buf][kBM * 8 + slot_t + RS * 8 * j] = (w_valid >> j) & 1u ? st.w[j] : z;
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  auto compute = [&](int buf) {
+    const u32x4* L = lds[buf];
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      const int chunk = 2 * kk + hi;
+      bf16x8 af[TM], wf[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[i] = as_bf16x8(L[swz(wm * WM + 32 * i + l32, chunk)]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) wf[j] = as_bf16x8(L[kBM * 8 + swz(wn * WN + 32 * j + l32, chunk)]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(wf[j], af[i], acc[i][j]);
+    }
+  };
+
+  // Software pipeline, two register stages: while k-tile t is multiplied
+  // from LDS, tile t + 1 (loaded one iteration earlier) is stored to the
+  // other LDS buffer and tile t + 2 is in flight from memory.
+  Stage s0, s1;
+  const int64_t n_t = kt1 - kt0;
+  if (n_t > 0) {
+    load_tile(s0, kt0);
+    if (n_t > 1) load_tile(s1, kt0 + 1);
+    store_tile(s0, 0);
+  }
+  __syncthreads();
+  for (int64_t t = 0; t < n_t; t += 2) {
+    // even step: compute buffer 0; s1 holds tile t + 1.
+    if (t + 2 < n_t) load_tile(s0, kt0 + t + 2);
+    compute(0);
+    if (t + 1 < n_t) store_tile(s1, 1);
+    __syncthreads();
+    if (t + 1 >= n_t) break;
+    // odd step: compute buffer 1; s0 holds tile t + 2.
+    if (t + 3 < n_t) load_tile(s1, kt0 + t + 3);
+    compute(1);
+    if (t + 2 < n_t) store_tile(s0, 0);
+    __syncthreads();
+  }
+
+  // acc[i][j][4q + r] = C[m0 + wm*WM + 32i + l32][n0 + wn*WN + 32j + 8q + 4hi + r].
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int64_t m = m0 + wm * WM + 32 * i + l32;
     if (m >= p.M) continue;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t n = n0 + wn * 64 + 16 * j + 4 * g;
-      if (n < a.N) epilogue4<bf16_t>(a, p, m, n, acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t n = n0 + wn * WN + 32 * j + 8 * q + 4 * hi;
+        if (n >= a.N) continue;
+        const f32x16& c = acc[i][j];
+        if (splits == 1) {
+          epilogue4<bf16_t>(a, p, m, n, c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
+        } else {
+          const int64_t grow = (prob == 0 ? 0 : a.p[0].M) + m;
+          const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+          float* dst = partial + (int64_t(ks) * rows + grow) * a.N + n;
+          *reinterpret_cast<float4*>(dst) = make_float4(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
+        }
+      }
     }
   }
+}
+
+// Sum the split-K partials in split order and apply the epilogue.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmArgs a, const float* __restrict__ partial,
+                                                            int splits) {
+  const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+  const int64_t groups = a.N / 4;
+  const int64_t g = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (g >= rows * groups) return;
+  const int64_t grow = g / groups, n = (g % groups) * 4;
+  float4 s = *reinterpret_cast<const float4*>(partial + grow * a.N + n);
+  for (int k = 1; k < splits; ++k) {
+    const float4 t = *reinterpret_cast<const float4*>(partial + (int64_t(k) * rows + grow) * a.N + n);
+    s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
+  }
+  const int prob = grow < a.p[0].M ? 0 : 1;
+  const int64_t m = prob == 0 ? grow : grow - a.p[0].M;
+  epilogue4<bf16_t>(a, a.p[prob], m, n, s.x, s.y, s.z, s.w);
 }
 
 // fp32 VALU GEMM: 64x64 tile, 16x16 threads, 4x4 outputs per thread.
@@ -155,9 +272,9 @@ constexpr int kFB = 64, kFK = 16;
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmArgs a) {
   __shared__ float As[kFK][kFB + 4];
   __shared__ float Ws[kFK][kFB + 4];
-  int prob;
+  int prob, ks;
   int64_t m0, n0;
-  if (!map_tile(a, kFB, kFB, prob, m0, n0)) return;
+  if (!map_tile(a, kFB, kFB, 1, prob, m0, n0, ks)) return;
   const GemmProblem& p = a.p[prob];
   const float* A = static_cast<const float*>(p.A);
   const float* W = static_cast<const float*>(p.W);
@@ -193,19 +310,86 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmArgs a) {
   }
 }
 
+int64_t tiles_of(const GemmArgs& a, int bm, int bn) {
+  int64_t t = 0;
+  for (int i = 0; i < a.nprob; ++i) t += ceil_div64(a.p[i].M, bm) * ceil_div64(a.N, bn);
+  return t;
+}
+
 }  // namespace
 
-int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s) {
-  const int bm = dtype == AVITS_BF16 ? kBM : kFB, bn = bm;
-  const int64_t tn = ceil_div64(a.N, bn);
-  int64_t tiles = 0;
-  for (int i = 0; i < a.nprob; ++i) tiles += ceil_div64(a.p[i].M, bm) * tn;
-  if (tiles == 0) return AVITS_OK;
-  TimedLaunch timed("gemm", s);
-  if (dtype == AVITS_BF16)
-    hipLaunchKernelGGL(gemm_bf16_kernel, dim3(unsigned(tiles)), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(gemm_f32_kernel, dim3(unsigned(tiles)), dim3(256), 0, s, a);
+GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes) {
+  GemmPlan pl;
+  if (dtype != AVITS_BF16) {
+    pl.bn = kFB;
+    pl.tiles = tiles_of(a, kFB, kFB);
+    return pl;
+  }
+  // Score every (column tile, K split) pair: busy fraction of the last wave
+  // of work units on the 256 CUs, times a per-tile factor (larger tiles move
+  // less L2 data per FLOP; measured on MI355X at the FLUX block shapes), times
+  // a factor for the extra fp32 partial traffic of a split.
+  const int cands[3] = {256, 192, 128};
+  const double eff[3] = {1.0, 0.97, 0.85};
+  const int64_t nk = a.K / kBK;
+  const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+  double best = -1.0;
+  for (int c = 0; c < 3; ++c) {
+    const int64_t t = tiles_of(a, kBM, cands[c]);
+    if (t == 0) continue;
+    for (int sp = 1; sp <= 4; ++sp) {
+      if (sp > 1 && (nk / sp < 4 || size_t(sp) * size_t(rows) * size_t(a.N) * sizeof(float) > partial_bytes)) break;
+      const int64_t units = t * sp;
+      const double fill = double(units) / double(ceil_div64(units, kCUs) * kCUs);
+      const double score = fill * eff[c] * (sp > 1 ? 0.95 : 1.0);
+      if (score > best + 1e-9) {
+        best = score;
+        pl.bn = cands[c];
+        pl.tiles = t;
+        pl.splits = sp;
+      }
+    }
+  }
+  // Tuning override "BN,SPLITS" (e.g. AVITS_GEMM_TILE=256,3).
+  if (const char* env = getenv("AVITS_GEMM_TILE")) {
+    int bn = 0, sp = 0;
+    if (sscanf(env, "%d,%d", &bn, &sp) == 2 && (bn == 256 || bn == 192 || bn == 128) && sp >= 1 && sp <= 4) {
+      pl.bn = bn;
+      pl.splits = sp;
+      pl.tiles = tiles_of(a, kBM, bn);
+    }
+  }
+  return pl;
+}
+
+size_t gemm_partial_bytes(const GemmArgs& a, const GemmPlan& pl) {
+  if (pl.splits <= 1) return 0;
+  const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+  return size_t(pl.splits) * size_t(rows) * size_t(a.N) * sizeof(float);
+}
+
+int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family, float* partial,
+                size_t partial_bytes) {
+  GemmPlan pl = plan_gemm(a, dtype, partial ? partial_bytes : 0);
+  if (pl.tiles == 0) return AVITS_OK;
+  if (pl.splits > 1 && (!partial || partial_bytes < gemm_partial_bytes(a, pl))) pl.splits = 1;
+  TimedLaunch timed(family, s);
+  if (dtype == AVITS_BF16) {
+    const dim3 grid(unsigned(pl.tiles * pl.splits));
+    switch (pl.bn) {
+      case 256: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+      case 192: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+      default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+    }
+    if (pl.splits > 1) {
+      const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+      const int64_t work = rows * (a.N / 4);
+      hipLaunchKernelGGL(splitk_reduce_kernel, dim3(unsigned(ceil_div64(work, 256))), dim3(256), 0, s, a,
+                         (const float*)partial, pl.splits);
+    }
+  } else {
+    hipLaunchKernelGGL(gemm_f32_kernel, dim3(unsigned(pl.tiles)), dim3(256), 0, s, a);
+  }
   return launch_status("gemm");
 }
 

@@ -15,21 +15,25 @@ enum EpiMode : int {
   EPI_STORE = 0,       // out = C
   EPI_GELU = 1,        // out = GELU_tanh(C)
   EPI_RESID_GATE = 2,  // out = resid + gate[n] * C
+  EPI_STORE_T = 3,     // out[col * ld + m] = C (transposed store)
 };
 
+// Output columns are split into up to three regions, [0, n_split),
+// [n_split, n_split2) and [n_split2, N); region r writes out_r with row
+// stride ld_r at column (n - region start) and applies mode_r.
 struct GemmProblem {
   const void* A;       // [M, lda]
   int64_t lda;
   const void* W;       // [N, K]
   const void* bias;    // [N] or null
   int64_t M;
-  // Output columns n < n_split go to out0 (row stride ld0, column n),
-  // the others to out1 (row stride ld1, column n - n_split).
   void* out0;
   int64_t ld0;
   void* out1;
   int64_t ld1;
-  const void* resid;   // EPI_RESID_GATE: [M, ldr], same columns as out0
+  void* out2;
+  int64_t ld2;
+  const void* resid;   // EPI_RESID_GATE: [M, ldr], same columns as the region
   int64_t ldr;
   const void* gate;    // EPI_RESID_GATE: [N]
 };
@@ -38,18 +42,33 @@ struct GemmArgs {
   GemmProblem p[2];
   int nprob;
   int64_t N, K;
-  int64_t n_split;     // >= N when the output is not split
-  int mode0, mode1;
+  int64_t n_split, n_split2;  // region starts; >= N when unused
+  int mode0, mode1, mode2;
 };
 
-int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s);
+struct GemmPlan {
+  int bn = 0;          // column tile
+  int splits = 1;      // K splits (fp32 partials + reduce when > 1)
+  int64_t tiles = 0;   // output tiles
+};
+GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes);
+size_t gemm_partial_bytes(const GemmArgs& a, const GemmPlan& pl);
+// `partial` is scratch for split-K partial sums; when it is null or smaller
+// than the plan needs, the GEMM runs unsplit.
+// `family` names the timing family of the launch (see avits_timing_read).
+int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family, float* partial = nullptr,
+                size_t partial_bytes = 0);
+
+// Bytes of split-K scratch the block reserves: up to 4 splits of an [S, D] fp32 output.
+inline size_t gemm_partial_reserve(int64_t S, int64_t D) { return size_t(4) * size_t(S) * size_t(D) * sizeof(float); }
 
 // ----------------------------------------------------------------------------
 // Flash attention over one sequence, all heads.  q/k are addressed as
 // base + token * tok_stride + head * head_stride (elements); v is given
 // transposed per head, vt[h][c][key] with row stride ldvt >= Sk rounded up to
-// the key tile (the padding must hold finite values); o is [Sq, H*d] with row
-// stride ldo.  Without v (vt == null) only the log-sum-exp is produced.
+// the key tile (the padding keys are read but masked, whatever they hold);
+// o is [Sq, H*d] with row stride ldo.  Without v (vt == null) only the
+// log-sum-exp is produced.
 struct AttnArgs {
   const void* q;
   int64_t q_tok, q_head;

@@ -49,31 +49,79 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
   return before + incl - v;
 }
 
+// Up to kRegKeys keys per thread stay in registers (N <= 16384); larger N
+// re-reads the scores (L2-resident) on every pass.
+constexpr int kRegKeys = 16;
+
+// Calls f(j, i, key) for every element i = tid + kThreads * j < N.
+template <bool IN_REGS, typename F>
+__device__ __forceinline__ void for_each_key(const uint32_t (&keys)[IN_REGS ? kRegKeys : 1],
+                                             const float* __restrict__ scores, int N, F&& f) {
+  if constexpr (IN_REGS) {
+#pragma unroll
+    for (int j = 0; j < kRegKeys; ++j) {
+      const int i = threadIdx.x + kThreads * j;
+      if (i < N) f(i, keys[j]);
+    }
+  } else {
+    for (int i = threadIdx.x; i < N; i += kThreads) f(i, order_key(scores[i]));
+  }
+}
+
+template <bool IN_REGS>
 __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __restrict__ scores, int N, int k,
                                                                 int32_t* __restrict__ idx) {
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t hist[kWaves][256];   // per-wave histograms: atomics contend only inside a wave
+  __shared__ uint32_t tot_s[256], suf_s[256];
   __shared__ uint32_t wsum[kWaves];
   __shared__ uint32_t s_digit, s_above;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+
+  uint32_t keys[IN_REGS ? kRegKeys : 1] = {};
+  if constexpr (IN_REGS) {
+#pragma unroll
+    for (int j = 0; j < kRegKeys; ++j) {
+      const int i = tid + kThreads * j;
+      keys[j] = i < N ? order_key(scores[i]) : 0u;
+    }
+  }
 
   uint32_t prefix = 0u, mask = 0u;
-  uint32_t remaining = uint32_t(k);  // rank of T among the current candidates
+  uint32_t remaining = uint32_t(k);  // rank of the k-th largest among the current candidates
   for (int shift = 24; shift >= 0; shift -= 8) {
-    if (tid < 256) hist[tid] = 0u;
+    for (int b = tid; b < kWaves * 256; b += kThreads) (&hist[0][0])[b] = 0u;
     __syncthreads();
-    for (int i = tid; i < N; i += kThreads) {
-      const uint32_t key = order_key(scores[i]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    for_each_key<IN_REGS>(keys, scores, N, [&](int, uint32_t key) {
+      if ((key & mask) == prefix) atomicAdd(&hist[wave][(key >> shift) & 255u], 1u);
+    });
+    __syncthreads();
+    // Waves 0..3 own digits 64w .. 64w + 63: the count per digit and its
+    // suffix sum inside the wave (shuffle scan from the high lanes down).
+    if (wave < 4) {
+      const int b = 64 * wave + lane;
+      uint32_t c = 0u;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) c += hist[w][b];
+      uint32_t suf = c;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t t = __shfl_down(suf, o, kWave);
+        if (lane + o < kWave) suf += t;
+      }
+      tot_s[b] = c;
+      suf_s[b] = suf;
+      if (lane == 0) wsum[wave] = suf;  // this wave's 64 digits in total
     }
     __syncthreads();
-    // Suffix sums over digits: above[b] = candidates with digit > b.
-    if (tid < 256) {
-      // Count of candidates whose digit is strictly greater than this bin.
-      uint32_t above = 0u;
-      for (int b = 255; b > tid; --b) above += hist[b];
-      const uint32_t here = hist[tid];
-      if (above < remaining && above + here >= remaining) {
-        s_digit = uint32_t(tid);
+    // The selected digit b has (candidates above b) < remaining <= (candidates at or above b).
+    if (wave < 4) {
+      const int b = 64 * wave + lane;
+      uint32_t higher = 0u;
+      for (int w = wave + 1; w < 4; ++w) higher += wsum[w];
+      const uint32_t c = tot_s[b];
+      const uint32_t above = suf_s[b] - c + higher;
+      if (above < remaining && above + c >= remaining) {
+        s_digit = uint32_t(b);
         s_above = above;
       }
     }
@@ -83,14 +131,14 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
     remaining -= s_above;
     __syncthreads();
   }
-  // T = prefix; `remaining` elements equal to T are still needed.
+  // T = prefix; `remaining` elements equal to T are still needed.  Emit in
+  // index order, one 1024-element chunk per block-wide scan.
   const uint32_t T = prefix, need = remaining;
   uint32_t eq_before = 0u, out_before = 0u;
-  for (int base = 0; base < N; base += kThreads) {
-    const int i = base + tid;
+  const int nchunks = (N + kThreads - 1) / kThreads;
+  auto emit_chunk = [&](int i, uint32_t key) {
     uint32_t gt = 0u, eq = 0u;
     if (i < N) {
-      const uint32_t key = order_key(scores[i]);
       gt = key > T;
       eq = key == T;
     }
@@ -105,6 +153,16 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
     if (sel && at < uint32_t(k)) idx[at] = i;
     out_before += gt_tot + min(eq_tot, eq_quota);
     eq_before += eq_tot;
+  };
+  if constexpr (IN_REGS) {
+#pragma unroll
+    for (int j = 0; j < kRegKeys; ++j)
+      if (j < nchunks) emit_chunk(tid + kThreads * j, keys[j]);
+  } else {
+    for (int j = 0; j < nchunks; ++j) {
+      const int i = tid + kThreads * j;
+      emit_chunk(i, i < N ? order_key(scores[i]) : 0u);
+    }
   }
 }
 
@@ -126,8 +184,11 @@ extern "C" int avits_select(const float* scores, int64_t N, int64_t k, int32_t* 
   AVITS_REQUIRE(k >= 0 && k <= N, "select: k=%lld outside [0, N=%lld]", (long long)k, (long long)N);
   if (k == 0) return AVITS_OK;
   AVITS_REQUIRE(scores && idx, "select: null scores/idx");
-  TimedLaunch timed("select", static_cast<hipStream_t>(stream));
-  hipLaunchKernelGGL(radix_select_kernel, dim3(1), dim3(kThreads), 0, static_cast<hipStream_t>(stream), scores,
-                     int(N), int(k), idx);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  TimedLaunch timed("select", s);
+  if (N <= int64_t(kThreads) * kRegKeys)
+    hipLaunchKernelGGL(radix_select_kernel<true>, dim3(1), dim3(kThreads), 0, s, scores, int(N), int(k), idx);
+  else
+    hipLaunchKernelGGL(radix_select_kernel<false>, dim3(1), dim3(kThreads), 0, s, scores, int(N), int(k), idx);
   return launch_status("select");
 }
