@@ -83,6 +83,40 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, 
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Workgroup barrier for LDS producer/consumer hand-offs: waits for this
+// wave's own LDS operations (lgkmcnt) and meets the other waves, but leaves
+// its global loads in flight.  __syncthreads() also carries a release fence,
+// which drains every outstanding global load at each barrier; a software
+// pipeline that keeps the next tiles' loads in flight across the barrier
+// needs this narrower form.  The memory clobber keeps the compiler from
+// moving LDS accesses across it.
+// Raw (untyped, stride 0) buffer resource for the bytes [base, base + bytes):
+// loads at offsets >= bytes return zeros.
+__device__ __forceinline__ u32x4 buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  return u32x4{uint32_t(b), uint32_t(b >> 32) & 0xffffu, bytes, 0x00020000u};
+}
+
+// 16-byte buffer load whose completion the caller waits for explicitly with
+// vm_wait<N>() followed by vm_ready() on the destination (the compiler does
+// not track the load, so it neither drains nor reorders around it).
+__device__ __forceinline__ void buffer_load16(u32x4& dst, const u32x4& rsrc, uint32_t voff) {
+  asm volatile("buffer_load_dwordx4 %0, %1, %2, 0 offen" : "=v"(dst) : "v"(voff), "s"(rsrc) : "memory");
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Marks a register as (re)defined here, so no use of it moves above the
+// preceding vm_wait.
+__device__ __forceinline__ void vm_ready(u32x4& v) { asm volatile("" : "+v"(v)); }
+
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 }  // namespace avits
 
 // Host-side error plumbing and launch timing (abi.hip).

@@ -82,13 +82,24 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, const GemmProblem& 
   }
 }
 
-// Flat workgroup id -> (problem, tile origin, k split).  Tiles of one problem
-// come first; within a problem, consecutive ids walk down the rows of one
-// column block so neighbouring workgroups share the weight tile.
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own
+// L2).  Renumber them so that XCD x runs a contiguous range of logical ids:
+// neighbouring logical tiles share weight / activation tiles in one L2.
+__device__ __forceinline__ int64_t xcd_logical_id(int64_t bid, int64_t grid) {
+  constexpr int kXcds = 8;
+  const int64_t per = grid / kXcds, rem = grid % kXcds;
+  const int64_t x = bid % kXcds, i = bid / kXcds;
+  return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
+}
+
+// Logical id -> (problem, tile origin, k split).  Tiles of one problem come
+// first; within a problem, consecutive ids walk down the rows of one column
+// block so neighbouring workgroups share the weight tile; the k splits of a
+// tile are adjacent.
 __device__ __forceinline__ bool map_tile(const GemmArgs& a, int bm, int bn, int splits, int& prob, int64_t& m0,
                                          int64_t& n0, int& ks) {
   const int64_t tn = (a.N + bn - 1) / bn;
-  int64_t bid = blockIdx.x;
+  int64_t bid = xcd_logical_id(blockIdx.x, gridDim.x);
   ks = int(bid % splits);
   bid /= splits;
   const int64_t tm0 = (a.p[0].M + bm - 1) / bm;
@@ -110,7 +121,7 @@ __device__ __forceinline__ bool map_tile(const GemmArgs& a, int bm, int bn, int 
 // Swizzled 16-byte chunk slot of (row, chunk) in a 128-byte LDS row.
 __device__ __forceinline__ int swz(int row, int chunk) { return row * 8 + (chunk ^ ((row >> 1) & 7)); }
 
-template <int BN, int WAVES_M, int WAVES_N>
+template <int BN, int WAVES_M, int WAVES_N, int STAGES>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(const GemmArgs a,
                                                                            float* __restrict__ partial, int splits) {
   constexpr int NT = 64 * WAVES_M * WAVES_N;
@@ -137,41 +148,43 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(const
 
   // Staging: thread t moves 16-byte chunk (t % 8) of rows t / 8 + RS j, so all
   // of its chunks share one column offset and one swizzle (RS j / 2 = 0 mod 8).
-  // Rows past the end re-read the last valid row (no branch around the load)
-  // and are zeroed by a select, so every load is unconditional.
+  // Loads are raw buffer loads with loop-invariant per-thread offsets; the
+  // k-advance moves the scalar resource base.  The resource covers only the
+  // rows that exist, so the range check returns zeros past the end of A or W.
+  constexpr int LPT = CA + CW;  // loads per thread per k-tile
   const int row_t = tid / 8, kc_t = tid % 8;
   const int slot_t = row_t * 8 + (kc_t ^ ((row_t >> 1) & 7));
-  const bf16_t* a_ptr[CA];
-  const bf16_t* w_ptr[CW];
-  uint32_t a_valid = 0, w_valid = 0;
+  uint32_t a_off[CA], w_off[CW];
 #pragma unroll
-  for (int j = 0; j < CA; ++j) {
-    const int64_t m = m0 + row_t + RS * j;
-    a_valid |= uint32_t(m < p.M) << j;
-    a_ptr[j] = A + std::min<int64_t>(m, p.M - 1) * p.lda + kc_t * 8;
-  }
+  for (int j = 0; j < CA; ++j) a_off[j] = uint32_t(((row_t + RS * j) * p.lda + kc_t * 8) * 2);
 #pragma unroll
-  for (int j = 0; j < CW; ++j) {
-    const int64_t n = n0 + row_t + RS * j;
-    w_valid |= uint32_t(n < a.N) << j;
-    w_ptr[j] = W + std::min<int64_t>(n, a.N - 1) * a.K + kc_t * 8;
-  }
+  for (int j = 0; j < CW; ++j) w_off[j] = uint32_t(((row_t + RS * j) * a.K + kc_t * 8) * 2);
+  const char* a_base = reinterpret_cast<const char*>(A + m0 * p.lda);
+  const char* w_base = reinterpret_cast<const char*>(W + n0 * a.K);
+  const int64_t a_bytes = (p.M - m0) * p.lda * 2, w_bytes = (a.N - n0) * a.K * 2;
   struct Stage {
     u32x4 a[CA], w[CW];
   };
   auto load_tile = [&](Stage& st, int64_t kt) {
-    const int64_t off = kt * kBK;
+    const int64_t koff = kt * kBK * 2;
+    const u32x4 ra = buffer_rsrc(a_base + koff, uint32_t(a_bytes - koff));
+    const u32x4 rw = buffer_rsrc(w_base + koff, uint32_t(w_bytes - koff));
 #pragma unroll
-    for (int j = 0; j < CA; ++j) st.a[j] = *reinterpret_cast<const u32x4*>(a_ptr[j] + off);
+    for (int j = 0; j < CA; ++j) buffer_load16(st.a[j], ra, a_off[j]);
 #pragma unroll
-    for (int j = 0; j < CW; ++j) st.w[j] = *reinterpret_cast<const u32x4*>(w_ptr[j] + off);
+    for (int j = 0; j < CW; ++j) buffer_load16(st.w[j], rw, w_off[j]);
+  };
+  auto ready = [&](Stage& st) {
+#pragma unroll
+    for (int j = 0; j < CA; ++j) vm_ready(st.a[j]);
+#pragma unroll
+    for (int j = 0; j < CW; ++j) vm_ready(st.w[j]);
   };
   auto store_tile = [&](const Stage& st, int buf) {
-    const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-    for (int j = 0; j < CA; ++j) lds[buf][slot_t + RS * 8 * j] = (a_valid >> j) & 1u ? st.a[j] : z;
+    for (int j = 0; j < CA; ++j) lds[buf][slot_t + RS * 8 * j] = st.a[j];
 #pragma unroll
-    for (int j = 0; j < CW; ++j) lds[buf][kBM * 8 + slot_t + RS * 8 * j] = (w_valid >> j) & 1u ? st.w[j] : z;
+    for (int j = 0; j < CW; ++j) lds[buf][kBM * 8 + slot_t + RS * 8 * j] = st.w[j];
   };
 
   f32x16 acc[TM][TN];
@@ -182,46 +195,96 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(const
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // Fragments are double-buffered across the 16-wide k steps: the LDS reads
+  // of step kk + 1 are in flight while the MFMAs of step kk run, so a wave
+  // rarely stalls on LDS latency.
   auto compute = [&](int buf) {
     const u32x4* L = lds[buf];
+    bf16x8 af[2][TM], wf[2][TN];
+    auto read = [&](int kk, int slot) {
+      const int chunk = 2 * kk + hi;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[slot][i] = as_bf16x8(L[swz(wm * WM + 32 * i + l32, chunk)]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) wf[slot][j] = as_bf16x8(L[kBM * 8 + swz(wn * WN + 32 * j + l32, chunk)]);
+    };
+    read(0, 0);
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
-      const int chunk = 2 * kk + hi;
-      bf16x8 af[TM], wf[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) af[i] = as_bf16x8(L[swz(wm * WM + 32 * i + l32, chunk)]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) wf[j] = as_bf16x8(L[kBM * 8 + swz(wn * WN + 32 * j + l32, chunk)]);
+      if (kk + 1 < kBK / 16) read(kk + 1, (kk + 1) & 1);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(wf[j], af[i], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(wf[kk & 1][j], af[kk & 1][i], acc[i][j]);
     }
   };
 
-  // Software pipeline, two register stages: while k-tile t is multiplied
-  // from LDS, tile t + 1 (loaded one iteration earlier) is stored to the
-  // other LDS buffer and tile t + 2 is in flight from memory.
-  Stage s0, s1;
   const int64_t n_t = kt1 - kt0;
-  if (n_t > 0) {
-    load_tile(s0, kt0);
-    if (n_t > 1) load_tile(s1, kt0 + 1);
-    store_tile(s0, 0);
-  }
-  __syncthreads();
-  for (int64_t t = 0; t < n_t; t += 2) {
-    // even step: compute buffer 0; s1 holds tile t + 1.
-    if (t + 2 < n_t) load_tile(s0, kt0 + t + 2);
-    compute(0);
-    if (t + 1 < n_t) store_tile(s1, 1);
-    __syncthreads();
-    if (t + 1 >= n_t) break;
-    // odd step: compute buffer 1; s0 holds tile t + 2.
-    if (t + 3 < n_t) load_tile(s1, kt0 + t + 3);
-    compute(1);
-    if (t + 2 < n_t) store_tile(s0, 0);
-    __syncthreads();
+  if constexpr (STAGES == 2) {
+    // Software pipeline, two register stages and two LDS buffers: while
+    // k-tile t is multiplied from LDS, tile t + 1 (loaded one step earlier)
+    // is stored to the other buffer and tile t + 2 is in flight.  Loads
+    // complete in issue order, so "the older stage is ready" is
+    // vmcnt <= LPT while the newer stage is in flight, else vmcnt == 0.
+    Stage s0, s1;
+    if (n_t > 0) {
+      load_tile(s0, kt0);
+      if (n_t > 1) {
+        load_tile(s1, kt0 + 1);
+        vm_wait<LPT>();
+      } else {
+        vm_wait<0>();
+      }
+      ready(s0);
+      store_tile(s0, 0);
+    }
+    lds_barrier();
+    for (int64_t t = 0; t < n_t; t += 2) {
+      // even step: compute buffer 0; s1 holds tile t + 1.
+      const bool next2 = t + 2 < n_t;
+      if (next2) load_tile(s0, kt0 + t + 2);
+      compute(0);
+      if (t + 1 < n_t) {
+        if (next2) vm_wait<LPT>(); else vm_wait<0>();
+        ready(s1);
+        store_tile(s1, 1);
+      }
+      lds_barrier();
+      if (t + 1 >= n_t) break;
+      // odd step: compute buffer 1; s0 holds tile t + 2.
+      const bool next3 = t + 3 < n_t;
+      if (next3) load_tile(s1, kt0 + t + 3);
+      compute(1);
+      if (next2) {
+        if (next3) vm_wait<LPT>(); else vm_wait<0>();
+        ready(s0);
+        store_tile(s0, 0);
+      }
+      lds_barrier();
+    }
+  } else {
+    // One register stage, two LDS buffers: tile t + 1 is in flight while
+    // tile t is multiplied.
+    Stage st;
+    if (n_t > 0) {
+      load_tile(st, kt0);
+      vm_wait<0>();
+      ready(st);
+      store_tile(st, 0);
+    }
+    lds_barrier();
+    for (int64_t t = 0; t < n_t; ++t) {
+      const int buf = int(t & 1);
+      const bool next = t + 1 < n_t;
+      if (next) load_tile(st, kt0 + t + 1);
+      compute(buf);
+      if (next) {
+        vm_wait<0>();
+        ready(st);
+        store_tile(st, buf ^ 1);
+      }
+      lds_barrier();
+    }
   }
 
   // acc[i][j][4q + r] = C[m0 + wm*WM + 32i + l32][n0 + wn*WN + 32j + 8q + 4hi + r].
@@ -350,12 +413,18 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes) {
       }
     }
   }
-  // Tuning override "BN,SPLITS" (e.g. AVITS_GEMM_TILE=256,3).
+  pl.waves = 8;
+  pl.stages = pl.bn == 256 ? 1 : 2;  // two stages do not fit the 256-wide tile's registers
+  // Tuning override "BN,SPLITS[,WAVES[,STAGES]]" (e.g. AVITS_GEMM_TILE=256,3,8,1).
   if (const char* env = getenv("AVITS_GEMM_TILE")) {
-    int bn = 0, sp = 0;
-    if (sscanf(env, "%d,%d", &bn, &sp) == 2 && (bn == 256 || bn == 192 || bn == 128) && sp >= 1 && sp <= 4) {
+    int bn = 0, sp = 0, wv = 8, stg = 2;
+    const int got = sscanf(env, "%d,%d,%d,%d", &bn, &sp, &wv, &stg);
+    if (got >= 2 && (bn == 256 || bn == 192 || bn == 128) && sp >= 1 && sp <= 4 &&
+        (wv == 8 || (wv == 4 && bn == 256)) && (stg == 1 || stg == 2)) {
       pl.bn = bn;
       pl.splits = sp;
+      pl.waves = wv;
+      pl.stages = wv == 4 ? 1 : stg;
       pl.tiles = tiles_of(a, kBM, bn);
     }
   }
@@ -376,10 +445,14 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
   TimedLaunch timed(family, s);
   if (dtype == AVITS_BF16) {
     const dim3 grid(unsigned(pl.tiles * pl.splits));
-    switch (pl.bn) {
-      case 256: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
-      case 192: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
-      default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+    switch (pl.bn * 100 + pl.waves * 10 + pl.stages) {
+      case 25641: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 2, 1>), grid, dim3(256), 0, s, a, partial, pl.splits); break;
+      case 25681: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+      case 25682: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+      case 19281: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+      case 19282: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+      case 12881: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+      default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
     }
     if (pl.splits > 1) {
       const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
