@@ -185,7 +185,7 @@ def main(argv=None):
         for j, s in enumerate(stages):
             stage_ms[s] += evs[j].elapsed_time(evs[j + 1]) / args.steps
     fam = {}
-    for f in ("score_spatial", "score_temporal", "score_finalize", "select", "gather_upsample", "scatter",
+    for f in ("score_spatial", "score_combine", "score_finalize", "select", "gather_upsample", "scatter",
               "ln_mod", "gemm", "qk_rope", "attention"):
         tot, n = avits.avits_timing_read(f)
         fam[f] = {"ms_per_step": round(tot / args.steps, 4), "launches_per_step": n / args.steps,

@@ -209,7 +209,7 @@ int avits_joint_lse(const void* q, const void* k_all, int64_t N, int64_t Nk,
  * While enabled, every kernel the library enqueues is bracketed by a pair of
  * HIP events on the caller's stream.  avits_timing_read() waits for the
  * recorded events and returns the accumulated time and launch count of one
- * launch family: "score_spatial", "score_temporal", "score_finalize",
+ * launch family: "score_spatial", "score_combine", "score_finalize",
  * "select", "gather_upsample", "scatter", "ln_mod", "gemm_qkv", "gemm_o",
  * "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
  * "qk_rope", "attention", "joint_lse"; "gemm" returns the sum of the six

@@ -30,7 +30,7 @@ int launch_status(const char* what) {
 // Launch timing: when enabled, every internal launch is bracketed by a pair of
 // HIP events on its stream; avits_timing_read() waits for them and adds the
 // elapsed times to per-family totals.  Single-threaded use only.
-static const char* const kFamilies[] = {"score_spatial", "score_temporal", "score_finalize", "select",
+static const char* const kFamilies[] = {"score_spatial", "score_combine", "score_finalize", "select",
                                         "gather_upsample", "scatter", "ln_mod", "gemm_qkv", "gemm_o",
                                         "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
                                         "qk_rope", "attention", "joint_lse"};

@@ -13,13 +13,14 @@
 // permutation on both operands).  Softmax runs in the log2 domain with fp32
 // statistics.
 // fp32: one thread per query row on the VALU (exactness path).
+#include <stdlib.h>
+
 #include "kernels.h"
 
 namespace avits {
 namespace {
 
 constexpr int kRows = 128;        // query rows per workgroup (4 waves x 32)
-constexpr int kKT = kAttnKeyTile; // keys per tile
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -30,15 +31,17 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
 // Lane l of a 32x32 MFMA output tile holds row 8*(r/4) + 4*(l/32) + r%4 of
 // column l%32 in register r.  With S^T = K Q^T the column is the query row
 // and the row is the key, so key(r, h) = 8*(r/4) + 4*h + r%4 (h = l/32).
-template <int DH, bool WITH_V>
+template <int DH, bool WITH_V, int KT>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
+  constexpr int kKT = KT;           // keys per tile (32 or 64)
   constexpr int kC = DH / 16;       // 16-wide head-dim chunks (MFMA k)
   constexpr int kKL = DH + 8;       // padded K row (elements)
-  constexpr int kVL = kKT + 4;      // padded V^T row: 34-word stride keeps 32 rows of 8-byte reads conflict-free
+  constexpr int kVL = kKT + 4;      // padded V^T row: 2 mod 4 words keeps 32 rows of 8-byte reads conflict-free
   constexpr int kKP = kKT * DH / 8 / 256;  // 16-byte K pieces per thread per tile
   constexpr int kVP = DH * kKT / 8 / 256;  // 16-byte V^T pieces per thread per tile
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[kKT * kKL];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[WITH_V ? DH * kVL : 8];
+  // Two LDS buffers: tile t + 1 is stored while tile t is consumed.
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][kKT * kKL];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][WITH_V ? DH * kVL : 8];
 
   const int h = blockIdx.y;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
@@ -91,29 +94,31 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
       }
     }
   };
-  auto store_tile = [&]() {
+  auto store_tile = [&](int buf) {
 #pragma unroll
     for (int j = 0; j < kKP; ++j) {
       const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
-      *reinterpret_cast<u32x4*>(&Ks[key * kKL + col]) = kreg[j];
+      *reinterpret_cast<u32x4*>(&Ks[buf][key * kKL + col]) = kreg[j];
     }
     if constexpr (WITH_V) {
 #pragma unroll
       for (int j = 0; j < kVP; ++j) {
         const int p = tid + 256 * j, dv = p / (kKT / 8), kc = (p % (kKT / 8)) * 8;
-        *reinterpret_cast<u32x4*>(&Vs[dv * kVL + kc]) = vreg[j];
+        *reinterpret_cast<u32x4*>(&Vs[buf][dv * kVL + kc]) = vreg[j];
       }
     }
   };
 
   load_tile(0);
-  for (int64_t k0 = 0; k0 < a.Sk; k0 += kKT) {
-    __syncthreads();  // previous tile fully consumed
-    store_tile();
-    __syncthreads();
-    if (k0 + kKT < a.Sk) load_tile(k0 + kKT);
+  store_tile(0);
+  lds_barrier();
+  int buf = 0;
+  for (int64_t k0 = 0; k0 < a.Sk; k0 += kKT, buf ^= 1) {
+    const bool more = k0 + kKT < a.Sk;
+    if (more) load_tile(k0 + kKT);
 
-    // Logits of the 64-key tile: two 32-key sub-tiles, log2-scaled.
+    // Raw logits of the tile: KT/32 sub-tiles of 32 keys.  Keys past the end
+    // (last tile only) are set to -inf.
     f32x16 s[kKT / 32];
 #pragma unroll
     for (int t = 0; t < kKT / 32; ++t) {
@@ -122,39 +127,52 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
       for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
       for (int c = 0; c < kC; ++c) {
-        const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(&Ks[(32 * t + l32) * kKL + 16 * c + 8 * hi]));
+        const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(&Ks[buf][(32 * t + l32) * kKL + 16 * c + 8 * hi]));
         acc = mfma32(kf, qf[c], acc);
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
-        acc[r] = key < a.Sk ? acc[r] * scale2 : -INFINITY;
       }
       s[t] = acc;
     }
-    // Online softmax: a row lives in lanes l32 and l32 + 32.
+    if (k0 + kKT > a.Sk) {
+#pragma unroll
+      for (int t = 0; t < kKT / 32; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
+          if (key >= a.Sk) s[t][r] = -INFINITY;
+        }
+    }
+    // Online softmax in the log2 domain; a row lives in lanes l32 and l32 + 32.
+    // The running max is raised only when the tile max exceeds it by more
+    // than 8 (a factor 256), so most tiles skip the rescale of the output
+    // accumulators; exponents stay <= 2^8, exact in the fp32 sums and
+    // representable in bf16.
     float mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < kKT / 32; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float mnew = fmaxf(mrow, mx);
-    const float corr = exp2f(mrow - mnew);
-    mrow = mnew;
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale2;
+    const bool raise = mx > mrow + 8.f;
+    float corr = 1.f;
+    if (raise) {
+      corr = exp2f(mrow - mx);
+      mrow = mx;
+    }
     float ls = 0.f;
 #pragma unroll
     for (int t = 0; t < kKT / 32; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = exp2f(s[t][r] - mnew);
+        const float e = exp2f(fmaf(s[t][r], scale2, -mrow));
         s[t][r] = e;
         ls += e;
       }
     lrow = lrow * corr + ls;
     if constexpr (WITH_V) {
+      if (__any(raise)) {
 #pragma unroll
-      for (int dt = 0; dt < DH / 32; ++dt) oacc[dt] *= corr;
+        for (int dt = 0; dt < DH / 32; ++dt) oacc[dt] *= corr;
+      }
       // P^T operand for 16-key chunk c (keys 16c .. 16c + 15 of the tile):
       // registers 8(c%2) .. 8(c%2) + 7 of sub-tile c/2 hold keys
       // 16c + 4hi + {0..3} and 16c + 8 + 4hi + {0..3}.
@@ -167,7 +185,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
         const bf16x8 pf = as_bf16x8(pv);
 #pragma unroll
         for (int dt = 0; dt < DH / 32; ++dt) {
-          const bf16_t* vr = &Vs[(32 * dt + l32) * kVL + 16 * c + 4 * hi];
+          const bf16_t* vr = &Vs[buf][(32 * dt + l32) * kVL + 16 * c + 4 * hi];
           const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
           const u32x2 up = *reinterpret_cast<const u32x2*>(vr + 8);
           const u32x4 vv = {lo[0], lo[1], up[0], up[1]};
@@ -175,6 +193,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
         }
       }
     }
+    if (more) store_tile(buf ^ 1);
+    lds_barrier();
   }
 
   float l = lrow + __shfl_xor(lrow, 32, kWave);
@@ -258,13 +278,22 @@ __global__ __launch_bounds__(kFRows) void attn_f32_kernel(const AttnArgs a) {
   }
 }
 
+// Key tile: 64 keys when V is used, 32 keys otherwise; AVITS_ATTN_KT
+// (32 or 64) overrides it for tuning.
 template <int DH>
 void launch_dh(const AttnArgs& a, int dtype, hipStream_t s) {
   const bool with_v = a.vt != nullptr;
   if (dtype == AVITS_BF16) {
+    int kt = 64;
+    if (const char* env = getenv("AVITS_ATTN_KT")) kt = atoi(env) == 32 ? 32 : 64;
     const dim3 grid(unsigned(ceil_div64(a.Sq, kRows)), unsigned(a.H));
-    if (with_v) hipLaunchKernelGGL((attn_bf16_kernel<DH, true>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<DH, false>), grid, dim3(256), 0, s, a);
+    if (with_v) {
+      if (kt == 32) hipLaunchKernelGGL((attn_bf16_kernel<DH, true, 32>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<DH, true, 64>), grid, dim3(256), 0, s, a);
+    } else {
+      if (kt == 32) hipLaunchKernelGGL((attn_bf16_kernel<DH, false, 32>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<DH, false, 64>), grid, dim3(256), 0, s, a);
+    }
   } else {
     const dim3 grid(unsigned(ceil_div64(a.Sq, kFRows)), unsigned(a.H));
     if (with_v) hipLaunchKernelGGL((attn_f32_kernel<DH, true>), grid, dim3(kFRows), 0, s, a);

@@ -43,13 +43,22 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, T*
   if constexpr (sizeof(T) == 2) {
     const int64_t nchunk = D / 8;
     if (D % 8 == 0 && nchunk <= int64_t(kWave) * kLnMaxChunks) {
-      u32x4 v[kLnMaxChunks];
-      float s = 0.f;
+      // All loads (row, scale, shift) are issued before the reductions.
+      u32x4 v[kLnMaxChunks], g[kLnMaxChunks], t[kLnMaxChunks];
 #pragma unroll
       for (int c = 0; c < kLnMaxChunks; ++c) {
         const int64_t idx = lane + kWave * c;
         if (idx < nchunk) {
           v[c] = reinterpret_cast<const u32x4*>(xr)[idx];
+          g[c] = reinterpret_cast<const u32x4*>(sc)[idx];
+          t[c] = reinterpret_cast<const u32x4*>(sh)[idx];
+        }
+      }
+      float s = 0.f;
+#pragma unroll
+      for (int c = 0; c < kLnMaxChunks; ++c) {
+        const int64_t idx = lane + kWave * c;
+        if (idx < nchunk) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) s += __uint_as_float(v[c][e] << 16) + __uint_as_float(v[c][e] & 0xffff0000u);
         }
@@ -72,16 +81,14 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, T*
       for (int c = 0; c < kLnMaxChunks; ++c) {
         const int64_t idx = lane + kWave * c;
         if (idx < nchunk) {
-          const u32x4 g = reinterpret_cast<const u32x4*>(sc)[idx];
-          const u32x4 t = reinterpret_cast<const u32x4*>(sh)[idx];
           u32x4 o;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float a = (__uint_as_float(v[c][e] << 16) - mean) * rstd * (1.f + __uint_as_float(g[e] << 16)) +
-                            __uint_as_float(t[e] << 16);
+            const float a = (__uint_as_float(v[c][e] << 16) - mean) * rstd * (1.f + __uint_as_float(g[c][e] << 16)) +
+                            __uint_as_float(t[c][e] << 16);
             const float b = (__uint_as_float(v[c][e] & 0xffff0000u) - mean) * rstd *
-                                (1.f + __uint_as_float(g[e] & 0xffff0000u)) +
-                            __uint_as_float(t[e] & 0xffff0000u);
+                                (1.f + __uint_as_float(g[c][e] & 0xffff0000u)) +
+                            __uint_as_float(t[c][e] & 0xffff0000u);
             o[e] = pack_bf2(a, b);
           }
           reinterpret_cast<u32x4*>(hr)[idx] = o;
@@ -100,6 +107,28 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, T*
   }
   const float rstd = rsqrtf(wave_sum(v) / float(D) + kLnEps);
   for (int64_t c = lane; c < D; c += kWave) st(hr, c, (ld(xr, c) - mean) * rstd * (1.f + ld(sc, c)) + ld(sh, c));
+}
+
+// Eight consecutive elements (16 bytes of bf16, 32 of fp32) to / from fp32.
+__device__ __forceinline__ void load8(const bf16_t* p, int64_t off, float (&x)[8]) {
+  const u32x4 v = *reinterpret_cast<const u32x4*>(p + off);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[2 * e] = __uint_as_float(v[e] << 16);
+    x[2 * e + 1] = __uint_as_float(v[e] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float* p, int64_t off, float (&x)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p + off), b = *reinterpret_cast<const float4*>(p + off + 4);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+__device__ __forceinline__ void store8(bf16_t* p, const float (&x)[8]) {
+  *reinterpret_cast<u32x4*>(p) =
+      u32x4{pack_bf2(x[0], x[1]), pack_bf2(x[2], x[3]), pack_bf2(x[4], x[5]), pack_bf2(x[6], x[7])};
+}
+__device__ __forceinline__ void store8(float* p, const float (&x)[8]) {
+  *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
 }
 
 // In-place RMSNorm (times the gain) and RoPE of q and k in qk [S, 2D]
@@ -135,31 +164,31 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ qk, c
     sincosf(float(pr[axis]) * freq, &sn[j], &cs[j]);
   }
   T* base = qk + row * (2 * int64_t(H) * DH);
+  // Both gain vectors of this lane's 8 elements, loaded once per row.
+  float gq[8], gk[8];
+  load8(a_rows ? gq_a : gq_b, 8 * sub, gq);
+  load8(a_rows ? gk_a : gk_b, 8 * sub, gk);
   for (int h0 = 0; h0 < 2 * H; h0 += kHeadsPerPass) {
     const int head = h0 + hoff;                  // 0..H-1 query heads, H..2H-1 key heads
     const bool live = head < 2 * H;
-    const T* gain = head < H ? (a_rows ? gq_a : gq_b) : (a_rows ? gk_a : gk_b);
     T* p = base + int64_t(live ? head : 0) * DH + 8 * sub;
     float x[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = live ? ld(p, e) : 0.f;
+    load8(p, 0, x);
     float ss = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
 #pragma unroll
     for (int o = 1; o < kLanesPerHead; o <<= 1) ss += __shfl_xor(ss, o, kWave);
     const float r = rsqrtf(ss / float(DH) + kRmsEps);
-    if (live) {
+    const float* g = head < H ? gq : gk;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float y0 = x[2 * j] * r * ld(gain, 8 * sub + 2 * j);
-        const float y1 = x[2 * j + 1] * r * ld(gain, 8 * sub + 2 * j + 1);
-        x[2 * j] = y0 * cs[j] - y1 * sn[j];
-        x[2 * j + 1] = y0 * sn[j] + y1 * cs[j];
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) st(p, e, x[e]);
+    for (int j = 0; j < 4; ++j) {
+      const float y0 = x[2 * j] * r * g[2 * j];
+      const float y1 = x[2 * j + 1] * r * g[2 * j + 1];
+      x[2 * j] = y0 * cs[j] - y1 * sn[j];
+      x[2 * j + 1] = y0 * sn[j] + y1 * cs[j];
     }
+    if (live) store8(p, x);
   }
 }
 

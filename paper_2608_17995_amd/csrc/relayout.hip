@@ -12,13 +12,22 @@ namespace {
 
 constexpr int kRowsPerBlock = 4;  // one wavefront per row job
 
-// Copy `bytes` (multiple of 16) from src to dst with the 64 lanes of a wave.
+// Copy `bytes` (multiple of 16) from src to dst with the 64 lanes of a wave,
+// four 16-byte chunks per lane in flight at a time.
 __device__ __forceinline__ void wave_copy_row(const char* __restrict__ src, char* __restrict__ dst,
                                               int64_t bytes, int lane) {
   const u32x4* s = reinterpret_cast<const u32x4*>(src);
   u32x4* d = reinterpret_cast<u32x4*>(dst);
   const int64_t n = bytes / 16;
-  for (int64_t i = lane; i < n; i += kWave) d[i] = s[i];
+  int64_t i = lane;
+  for (; i + 3 * kWave < n; i += 4 * kWave) {
+    const u32x4 a = s[i], b = s[i + kWave], c = s[i + 2 * kWave], e = s[i + 3 * kWave];
+    d[i] = a;
+    d[i + kWave] = b;
+    d[i + 2 * kWave] = c;
+    d[i + 3 * kWave] = e;
+  }
+  for (; i < n; i += kWave) d[i] = s[i];
 }
 
 // First position in the ascending idx[0..k) not below p.

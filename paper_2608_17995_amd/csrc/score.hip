@@ -2,14 +2,15 @@
 // joint).
 //
 // Three launches on the caller's stream:
-//  1. spatial partials P[h, i] = sum_{j<L} exp(q_ih . k_jh / sqrt(d) - lse[h, i]).
-//     bf16: one workgroup per (128 image rows, head); text keys staged through
-//     LDS in 64-key tiles; q.k^T on v_mfma_f32_16x16x32_bf16 computed as
-//     K Q^T so that each lane owns one query row and four keys, which keeps
-//     the exp-and-sum in registers.  fp32: the same tiling on the VALU.
-//  2. per row i: A_i = mean_h P[h, i], V_i = sum_c (f_t - f_prev)^2 / (2 D_f)
-//     (one wavefront per row, streaming both feature rows), plus one min/max
-//     partial of A and V per workgroup.
+//  1. per (head h, image row i): the spatial partial
+//       P[h, i] = sum_{j<L} exp(q_ih . k_jh / sqrt(d) - lse[h, i])
+//     and, for bf16, the temporal partial over the head's channel slice
+//       Q[h, i] = sum_{c in slice h} (f_t[i, c] - f_prev[i, c])^2
+//     in one fused kernel (MFMA q.k^T with the feature stream overlapped);
+//     fp32 runs the spatial partials on the VALU.
+//  2. combine: A_i = mean_h P[h, i], V_i = sum_h Q[h, i] / (2 D_f) (fp32: the
+//     variance is streamed here), plus one min/max partial of A and V per
+//     workgroup.
 //  3. finalize: every workgroup reduces the same partials in the same order
 //     (deterministic global min/max) and writes S for its slice of rows.
 #include "common.h"
@@ -23,82 +24,147 @@ constexpr int kTmpBlocks = 512;  // max workgroups of the temporal pass
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
-// 1. spatial partials, bf16 MFMA.
+// 1. bf16: spatial partials on MFMA fused with the temporal partials.
+//
+// Workgroup = (128 image rows, head h), 4 waves x 32 rows.  Spatial part:
+// S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (lane = one query row, 16 keys per
+// 32-key sub-tile), text-key tiles of 64 staged in LDS with the next tile
+// prefetched into registers; exp2(logit - lse) summed per row.
+// Temporal part: the workgroup streams channel slice [h D_f / H, (h+1) D_f / H)
+// of both feature rows of its 128 rows, so the 2 N D_f-element stream is spread
+// over every workgroup and overlaps the MFMA work; per-(head, row) partial sums
+// of squared differences go to part_v.
 template <int DH>
-__global__ __launch_bounds__(256) void spatial_bf16_kernel(const bf16_t* __restrict__ q,
-                                                           const bf16_t* __restrict__ ktxt,
-                                                           const float* __restrict__ lse, int N, int L,
-                                                           int H, float* __restrict__ part) {
-  constexpr int kChunks = DH / 32;      // 32-wide slices of the head dim
-  constexpr int kLds = DH + 8;          // padded LDS row (bf16 elements)
+__global__ __launch_bounds__(256) void spatial_temporal_bf16_kernel(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ ktxt, const float* __restrict__ lse,
+    const bf16_t* __restrict__ ft, const bf16_t* __restrict__ fp, int N, int L, int H, int64_t Df,
+    float* __restrict__ part_a, float* __restrict__ part_v) {
+  constexpr int kC = DH / 16;                 // 16-wide head-dim chunks (MFMA k)
+  constexpr int kLds = DH + 8;                // padded LDS row (bf16 elements)
+  constexpr int kKP = kSpKeys * DH / 8 / 256; // 16-byte K pieces per thread per tile
   __shared__ __attribute__((aligned(16))) bf16_t ks[kSpKeys * kLds];
 
   const int h = blockIdx.y;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int g = lane / 16, r16 = lane % 16;
-  const int row_base = blockIdx.x * kSpRows + wave * 32;
-  const int64_t qstride = int64_t(H) * DH;  // elements between consecutive tokens
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int l32 = lane % 32, hi = lane / 32;
+  const int wrow0 = blockIdx.x * kSpRows + wave * 32;  // this wave's 32 rows
+  const int row = wrow0 + l32;
+  const int64_t qstride = int64_t(H) * DH;
 
-  // Query fragments (B operand): lane holds row r16 of each 16-row tile,
-  // head-dim elements 32c + 8g .. 32c + 8g + 7.
-  bf16x8 qf[2][kChunks];
-  float lse2[2];
+  // ---- temporal slice (issued first: its loads overlap the MFMA work) ----
+  const int64_t c0 = Df * h / H, c1 = Df * (h + 1) / H;
+  const int64_t nch = (c1 - c0) / 8;  // 16-byte chunks per row in the slice
+  const bool vec = (c0 % 8 == 0) && ((c1 - c0) % 8 == 0) && nch > 0 && nch <= 64 && (64 % nch == 0);
+  if (vec) {
+    const int rpi = int(64 / nch);               // rows per 64-lane instruction
+    const int r_in = lane / int(nch), cc = lane % int(nch);
+    for (int r0 = 0; r0 < 32; r0 += rpi) {
+      const int rr = wrow0 + r0 + r_in;
+      float acc = 0.f;
+      if (rr < N) {
+        const u32x4 x = *reinterpret_cast<const u32x4*>(ft + int64_t(rr) * Df + c0 + 8 * cc);
+        const u32x4 y = *reinterpret_cast<const u32x4*>(fp + int64_t(rr) * Df + c0 + 8 * cc);
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    const int row = row_base + rt * 16 + r16;
-    const bool ok = row < N;
-    const bf16_t* src = q + int64_t(row) * qstride + int64_t(h) * DH + 8 * g;
-#pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (ok) v = *reinterpret_cast<const u32x4*>(src + 32 * c);
-      qf[rt][c] = as_bf16x8(v);
+        for (int e = 0; e < 4; ++e) {
+          const float d0 = __uint_as_float(x[e] << 16) - __uint_as_float(y[e] << 16);
+          const float d1 = __uint_as_float(x[e] & 0xffff0000u) - __uint_as_float(y[e] & 0xffff0000u);
+          acc = fmaf(d0, d0, fmaf(d1, d1, acc));
+        }
+      }
+      for (int o = 1; o < nch; o <<= 1) acc += __shfl_xor(acc, o, kWave);
+      if (cc == 0 && rr < N) part_v[int64_t(h) * N + rr] = acc;
     }
-    lse2[rt] = ok ? lse[int64_t(h) * N + row] * kLog2e : 0.f;
+  } else {
+    for (int r = 0; r < 32; ++r) {
+      const int rr = wrow0 + r;
+      if (rr >= N) break;
+      float acc = 0.f;
+      for (int64_t c = c0 + lane; c < c1; c += kWave) {
+        const float d0 = bf2f(ft[int64_t(rr) * Df + c]) - bf2f(fp[int64_t(rr) * Df + c]);
+        acc = fmaf(d0, d0, acc);
+      }
+      acc = wave_sum(acc);
+      if (lane == 0) part_v[int64_t(h) * N + rr] = acc;
+    }
   }
-  const float scale2 = kLog2e * rsqrtf(float(DH));
-  float acc_sum[2] = {0.f, 0.f};
 
+  // ---- spatial: Q^T fragments (B operand), lane = row l32, dims 16c + 8hi .. +7 ----
+  bf16x8 qf[kC];
+  {
+    const bf16_t* src = q + int64_t(min(row, N - 1)) * qstride + int64_t(h) * DH + 8 * hi;
+#pragma unroll
+    for (int c = 0; c < kC; ++c) qf[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + 16 * c));
+  }
+  const float lse2 = row < N ? lse[int64_t(h) * N + row] * kLog2e : 0.f;
+  const float scale2 = kLog2e * rsqrtf(float(DH));
+  float psum = 0.f;
+
+  u32x4 kreg[kKP];
+  auto load_k = [&](int k0) {
+#pragma unroll
+    for (int j = 0; j < kKP; ++j) {
+      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
+      const int kr = min(k0 + key, L - 1);
+      kreg[j] = *reinterpret_cast<const u32x4*>(ktxt + (int64_t(kr) * H + h) * DH + col);
+    }
+  };
+  load_k(0);
   for (int k0 = 0; k0 < L; k0 += kSpKeys) {
     __syncthreads();
-    // Stage 64 keys x DH into LDS (16-byte pieces), zero beyond L.
-    constexpr int kPieces = kSpKeys * DH / 8;
-    for (int p = threadIdx.x; p < kPieces; p += 256) {
-      const int key = p / (DH / 8), col = (p % (DH / 8)) * 8;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (k0 + key < L) v = *reinterpret_cast<const u32x4*>(ktxt + (int64_t(k0 + key) * H + h) * DH + col);
-      *reinterpret_cast<u32x4*>(&ks[key * kLds + col]) = v;
+#pragma unroll
+    for (int j = 0; j < kKP; ++j) {
+      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
+      *reinterpret_cast<u32x4*>(&ks[key * kLds + col]) = kreg[j];
     }
     __syncthreads();
+    if (k0 + kSpKeys < L) load_k(k0 + kSpKeys);
 #pragma unroll
-    for (int t = 0; t < kSpKeys / 16; ++t) {
-      bf16x8 kf[kChunks];
+    for (int t = 0; t < kSpKeys / 32; ++t) {
+      f32x16 acc;
 #pragma unroll
-      for (int c = 0; c < kChunks; ++c)
-        kf[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(&ks[(16 * t + r16) * kLds + 32 * c + 8 * g]));
+      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        f32x4 s = {0.f, 0.f, 0.f, 0.f};
+      for (int c = 0; c < kC; ++c) {
+        const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(&ks[(32 * t + l32) * kLds + 16 * c + 8 * hi]));
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], acc, 0, 0, 0);
+      }
+      // acc[r] = logit of key 32t + 8(r/4) + 4hi + r%4 against this lane's row.
 #pragma unroll
-        for (int c = 0; c < kChunks; ++c) s = mfma16x16x32(kf[c], qf[rt][c], s);
-        // s[i] = logit of key 16t + 4g + i against this lane's row.
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = k0 + 16 * t + 4 * g + i;
-          const float e = exp2f(s[i] * scale2 - lse2[rt]);
-          acc_sum[rt] += key < L ? e : 0.f;
-        }
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
+        const float e = exp2f(acc[r] * scale2 - lse2);
+        psum += key < L ? e : 0.f;
       }
     }
   }
-#pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    float v = acc_sum[rt];
-    v += __shfl_xor(v, 16, kWave);
-    v += __shfl_xor(v, 32, kWave);
-    const int row = row_base + rt * 16 + r16;
-    if (g == 0 && row < N) part[int64_t(h) * N + row] = v;
+  psum += __shfl_xor(psum, 32, kWave);
+  if (hi == 0 && row < N) part_a[int64_t(h) * N + row] = psum;
+}
+
+// 1b. bf16: per row, A = mean_h part_a, V = sum_h part_v / (2 D_f); one
+// min/max partial of A and V per 64-row workgroup.
+__global__ __launch_bounds__(64) void combine_kernel(const float* __restrict__ part_a,
+                                                     const float* __restrict__ part_v, int64_t N, int H, int64_t Df,
+                                                     float* __restrict__ a_out, float* __restrict__ v_out,
+                                                     float4* __restrict__ mm) {
+  const int64_t i = int64_t(blockIdx.x) * kWave + threadIdx.x;
+  float amin = INFINITY, amax = -INFINITY, vmin = INFINITY, vmax = -INFINITY;
+  if (i < N) {
+    float sa = 0.f, sv = 0.f;
+#pragma unroll 8
+    for (int h = 0; h < H; ++h) {
+      sa += part_a[int64_t(h) * N + i];
+      sv += part_v[int64_t(h) * N + i];
+    }
+    const float A = sa / float(H), V = sv / (2.f * float(Df));
+    a_out[i] = A;
+    v_out[i] = V;
+    amin = amax = A;
+    vmin = vmax = V;
   }
+  amin = wave_min(amin); amax = wave_max(amax);
+  vmin = wave_min(vmin); vmax = wave_max(vmax);
+  if (threadIdx.x == 0) mm[blockIdx.x] = make_float4(amin, amax, vmin, vmax);
 }
 
 // 1'. spatial partials, fp32 on the VALU: one thread per image row.
@@ -136,7 +202,7 @@ __global__ __launch_bounds__(128) void spatial_f32_kernel(const float* __restric
 }
 
 // ---------------------------------------------------------------------------
-// 2. temporal variance and head-mean of the spatial partials.
+// 2'. fp32: temporal variance and head-mean of the spatial partials.
 template <typename T>
 __global__ __launch_bounds__(256) void temporal_kernel(const T* __restrict__ ft, const T* __restrict__ fp,
                                                        const float* __restrict__ part, int64_t N, int H,
@@ -237,10 +303,11 @@ __global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct ScoreWs {
-  float* part;  // [H, N]
+  float* part;  // [H, N] spatial partials
+  float* part_v;  // [H, N] temporal partials (bf16 path)
   float* a;     // [N]
   float* v;     // [N]
-  float4* mm;   // [kTmpBlocks]
+  float4* mm;   // min/max partials, one per combine workgroup
   size_t bytes;
 };
 
@@ -248,9 +315,11 @@ ScoreWs score_ws_layout(char* base, int64_t N, int32_t H) {
   ScoreWs w;
   size_t off = 0;
   w.part = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * size_t(N) * H);
+  w.part_v = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * size_t(N) * H);
   w.a = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * size_t(N));
   w.v = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * size_t(N));
-  w.mm = reinterpret_cast<float4*>(base + off); off += align256(sizeof(float4) * kTmpBlocks);
+  w.mm = reinterpret_cast<float4*>(base + off);
+  off += align256(sizeof(float4) * size_t(std::max<int64_t>(kTmpBlocks, (N + kWave - 1) / kWave)));
   w.bytes = off;
   return w;
 }
@@ -287,39 +356,43 @@ extern "C" int avits_score(const void* latent_q, const void* text_k, const float
   hipStream_t s = static_cast<hipStream_t>(stream);
 
   const int n = int(N), l = int(L);
-  {
-  TimedLaunch timed("score_spatial", s);
+  int nmm;
   if (dtype == AVITS_BF16) {
-    const dim3 grid(unsigned((N + kSpRows - 1) / kSpRows), unsigned(H));
-    if (d == 128)
-      hipLaunchKernelGGL(spatial_bf16_kernel<128>, grid, dim3(256), 0, s, (const bf16_t*)latent_q,
-                         (const bf16_t*)text_k, row_lse, n, l, H, ws.part);
-    else
-      hipLaunchKernelGGL(spatial_bf16_kernel<64>, grid, dim3(256), 0, s, (const bf16_t*)latent_q,
-                         (const bf16_t*)text_k, row_lse, n, l, H, ws.part);
+    {
+      TimedLaunch timed("score_spatial", s);
+      const dim3 grid(unsigned((N + kSpRows - 1) / kSpRows), unsigned(H));
+      if (d == 128)
+        hipLaunchKernelGGL(spatial_temporal_bf16_kernel<128>, grid, dim3(256), 0, s, (const bf16_t*)latent_q,
+                           (const bf16_t*)text_k, row_lse, (const bf16_t*)feat_t, (const bf16_t*)feat_prev, n, l, H,
+                           D_f, ws.part, ws.part_v);
+      else
+        hipLaunchKernelGGL(spatial_temporal_bf16_kernel<64>, grid, dim3(256), 0, s, (const bf16_t*)latent_q,
+                           (const bf16_t*)text_k, row_lse, (const bf16_t*)feat_t, (const bf16_t*)feat_prev, n, l, H,
+                           D_f, ws.part, ws.part_v);
+    }
+    nmm = int((N + kWave - 1) / kWave);
+    TimedLaunch timed("score_combine", s);
+    hipLaunchKernelGGL(combine_kernel, dim3(nmm), dim3(kWave), 0, s, ws.part, ws.part_v, N, H, D_f, a_dst, v_dst,
+                       ws.mm);
   } else {
-    const dim3 grid(unsigned((N + 127) / 128), unsigned(H));
-    if (d == 128)
-      hipLaunchKernelGGL(spatial_f32_kernel<128>, grid, dim3(128), 0, s, (const float*)latent_q,
-                         (const float*)text_k, row_lse, n, l, H, ws.part);
-    else
-      hipLaunchKernelGGL(spatial_f32_kernel<64>, grid, dim3(128), 0, s, (const float*)latent_q,
-                         (const float*)text_k, row_lse, n, l, H, ws.part);
-  }
-  }
-  const int tblocks = int(std::min<int64_t>(kTmpBlocks, (N + 3) / 4));
-  {
-  TimedLaunch timed("score_temporal", s);
-  if (dtype == AVITS_BF16)
-    hipLaunchKernelGGL(temporal_kernel<bf16_t>, dim3(tblocks), dim3(256), 0, s, (const bf16_t*)feat_t,
-                       (const bf16_t*)feat_prev, ws.part, N, H, D_f, a_dst, v_dst, ws.mm);
-  else
-    hipLaunchKernelGGL(temporal_kernel<float>, dim3(tblocks), dim3(256), 0, s, (const float*)feat_t,
+    {
+      TimedLaunch timed("score_spatial", s);
+      const dim3 grid(unsigned((N + 127) / 128), unsigned(H));
+      if (d == 128)
+        hipLaunchKernelGGL(spatial_f32_kernel<128>, grid, dim3(128), 0, s, (const float*)latent_q,
+                           (const float*)text_k, row_lse, n, l, H, ws.part);
+      else
+        hipLaunchKernelGGL(spatial_f32_kernel<64>, grid, dim3(128), 0, s, (const float*)latent_q,
+                           (const float*)text_k, row_lse, n, l, H, ws.part);
+    }
+    nmm = int(std::min<int64_t>(kTmpBlocks, (N + 3) / 4));
+    TimedLaunch timed("score_combine", s);
+    hipLaunchKernelGGL(temporal_kernel<float>, dim3(nmm), dim3(256), 0, s, (const float*)feat_t,
                        (const float*)feat_prev, ws.part, N, H, D_f, a_dst, v_dst, ws.mm);
   }
   const int fblocks = int(std::min<int64_t>(256, (N + 255) / 256));
   TimedLaunch timed("score_finalize", s);
-  hipLaunchKernelGGL(finalize_kernel, dim3(fblocks), dim3(256), 0, s, a_dst, v_dst, ws.mm, tblocks, N, alpha, eps,
+  hipLaunchKernelGGL(finalize_kernel, dim3(fblocks), dim3(256), 0, s, a_dst, v_dst, ws.mm, nmm, N, alpha, eps,
                      scores);
   return launch_status("score");
 }
