@@ -28,6 +28,37 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 
+# HBM traffic of the dominant kernel, measured with the FETCH_SIZE and
+# WRITE_SIZE counters (each in its own profiler pass) and scaled by what the
+# same counters read for a plain copy of known size.  It is reported only while
+# the GEMM sources hash to what they were when the counters were taken.
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_bf16_flux1024_hbm_traffic.md")
+GEMM_SOURCES = ("gemm.hip", "kernels.h", "common.h")
+
+
+def gemm_sources_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_17995_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic() -> dict | None:
+    """{'bytes_per_launch': ..., ...} from the committed counter summary, or
+    None when there is none or the GEMM sources changed since it was taken."""
+    try:
+        with open(TRAFFIC_PROFILE) as fh:
+            for line in fh:
+                if line.startswith("traffic_json: "):
+                    rec = json.loads(line[len("traffic_json: "):])
+                    return rec if rec.get("sources_sha256") == gemm_sources_sha256() else None
+    except OSError:
+        return None
+    return None
+
+
 # ---------------------------------------------------------------------------
 # Algorithmic work (what the step must read, write and compute).
 
@@ -42,6 +73,19 @@ def block_flops(S: int, D: int, F: int | None = None) -> dict:
 def dense_model_flops(tokens: int, D: int = 3072, blocks: int = 57) -> float:
     """24 D^2 S + 4 S^2 D per block (F = 4D), summed over the blocks."""
     return blocks * (24 * D * D * tokens + 4 * tokens * tokens * D)
+
+
+def gemm_min_bytes(S: int, D: int, F: int, e: int = 2) -> int:
+    """Compulsory HBM bytes of the four GEMM launches of one double-stream
+    block (both streams): each operand read once, each output written once.
+    QKV: x_mod, W_qkv -> qkv; O: attn, W_o, residual -> x; MLP in: x_mod, W_1
+    -> h; MLP out: h, W_2, residual -> x.  Biases and gates are negligible."""
+    w = 2 * (3 * D * D + D * D + D * F + F * D)           # two streams' weights
+    act = S * D + S * 3 * D                               # QKV
+    act += S * D + 2 * S * D                              # O (in, resid, out)
+    act += S * D + S * F                                  # MLP in
+    act += S * F + 2 * S * D                              # MLP out (in, resid, out)
+    return e * (w + act)
 
 
 def stage_bytes(w, e: int = 2) -> dict:
@@ -93,6 +137,9 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 512 MiB device-to-device copy (a kernel of known traffic, the "
+                         "reference for scaling FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args(argv)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -109,6 +156,18 @@ def main(argv=None):
 
     torch.cuda.set_device(0)
     avits.load()
+    copy_ms = None
+    if args.copy_calibration:
+        src = torch.empty(256 * 1024 * 1024, dtype=torch.int16, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        copy_ms = e0.elapsed_time(e1)
+        del src, dst
     w = C.FLUX_1024
     dt = torch.bfloat16
 
@@ -167,18 +226,29 @@ def main(argv=None):
         run_step()
     torch.cuda.synchronize()
 
-    # Timed region: K steps, stage events on the stream and library launch timing.
+    # Timed region 1: K steps, nothing but the step's own launches -> value.
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run_step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+
+    # Timed region 2: the same K steps with stage events on the stream and the
+    # library's own HIP events around every internal launch -> per-stage and
+    # per-kernel times, the roofline of the dominant kernel.
     step_events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
     avits.avits_timing_reset()
     avits.avits_timing_enable(True)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
+    t2 = time.perf_counter()
     for i in range(args.steps):
         run_step(step_events[i])
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    t3 = time.perf_counter()
     avits.avits_timing_enable(False)
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ms_instrumented = (t3 - t2) * 1e3 / args.steps
 
     stage_ms = {s: 0.0 for s in stages}
     for evs in step_events:
@@ -186,7 +256,7 @@ def main(argv=None):
             stage_ms[s] += evs[j].elapsed_time(evs[j + 1]) / args.steps
     fam = {}
     for f in ("score_spatial", "score_combine", "score_finalize", "select", "gather_upsample", "scatter",
-              "ln_mod", "gemm", "qk_rope", "attention"):
+              "ln_mod", "gemm", "splitk_reduce", "qk_rope", "attention"):
         tot, n = avits.avits_timing_read(f)
         fam[f] = {"ms_per_step": round(tot / args.steps, 4), "launches_per_step": n / args.steps,
                   "avg_launch_us": round(1e3 * tot / max(n, 1), 2)}
@@ -194,10 +264,12 @@ def main(argv=None):
     S, D, F = w.S, w.D, w.mlp_ratio * w.D
     fl = block_flops(S, D, F)
     by = stage_bytes(w)
+    gemm_bytes = gemm_min_bytes(S, D, F)
     gemm_tot_ms, gemm_n = avits.avits_timing_read("gemm")
     gemm_per_launch_flops = fl["gemm"] * args.steps / gemm_n
     gemm_avg_s = gemm_tot_ms / gemm_n / 1e3
     gemm_tflops = gemm_per_launch_flops / gemm_avg_s / 1e12
+    traffic = measured_traffic()
     attn_ms, attn_n = avits.avits_timing_read("attention")
     attn_tflops = fl["attention"] / (attn_ms / attn_n / 1e3) / 1e12   # one launch per step
 
@@ -212,6 +284,7 @@ def main(argv=None):
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step_instrumented": round(ms_instrumented, 4),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -227,7 +300,9 @@ def main(argv=None):
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": None if traffic is None else traffic["bytes_per_launch"],
+            "traffic_unit": "bytes per launch (HBM, counter-measured)",
+            "algorithmic_bytes_per_launch": int(gemm_bytes * args.steps / gemm_n),
             "flops_per_launch": int(gemm_per_launch_flops),
             "avg_launch_us": round(gemm_avg_s * 1e6, 2),
         },
@@ -246,6 +321,7 @@ def main(argv=None):
         "canvas_tokens_per_s": round(w.N / (ms_per_step / 1e3), 1),
         "joint_lse_ms_untimed_setup": round(joint_lse_ms, 4),
         "input_generation_s": round(t_gen, 1),
+        "copy_calibration_ms": None if copy_ms is None else round(copy_ms, 4),
     }
     if not args.no_cpu_baseline:
         host = dict(si)

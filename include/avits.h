@@ -212,8 +212,9 @@ int avits_joint_lse(const void* q, const void* k_all, int64_t N, int64_t Nk,
  * launch family: "score_spatial", "score_combine", "score_finalize",
  * "select", "gather_upsample", "scatter", "ln_mod", "gemm_qkv", "gemm_o",
  * "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
- * "qk_rope", "attention", "joint_lse"; "gemm" returns the sum of the six
- * GEMM families.  Unknown family -> AVITS_ERR_INVALID_ARG.
+ * "splitk_reduce", "qk_rope", "attention", "joint_lse"; "gemm" returns the
+ * sum of the six GEMM families (the GEMM kernels alone: the split-K
+ * reduction that follows a split launch is "splitk_reduce").  Unknown family -> AVITS_ERR_INVALID_ARG.
  * avits_timing_reset() waits for pending events and zeroes every total.
  * Not thread-safe: use from one host thread.
  * ---------------------------------------------------------------------- */

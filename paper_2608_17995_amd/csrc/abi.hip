@@ -33,7 +33,7 @@ int launch_status(const char* what) {
 static const char* const kFamilies[] = {"score_spatial", "score_combine", "score_finalize", "select",
                                         "gather_upsample", "scatter", "ln_mod", "gemm_qkv", "gemm_o",
                                         "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
-                                        "qk_rope", "attention", "joint_lse"};
+                                        "splitk_reduce", "qk_rope", "attention", "joint_lse"};
 constexpr int kNumFamilies = sizeof(kFamilies) / sizeof(kFamilies[0]);
 
 struct Pending {

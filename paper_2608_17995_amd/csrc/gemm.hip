@@ -415,16 +415,16 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes) {
   }
   pl.waves = 8;
   pl.stages = pl.bn == 256 ? 1 : 2;  // two stages do not fit the 256-wide tile's registers
-  // Tuning override "BN,SPLITS[,WAVES[,STAGES]]" (e.g. AVITS_GEMM_TILE=256,3,8,1).
+  // Tuning override "BN,SPLITS[,8[,STAGES]]" (e.g. AVITS_GEMM_TILE=256,3,8,1).
   if (const char* env = getenv("AVITS_GEMM_TILE")) {
     int bn = 0, sp = 0, wv = 8, stg = 2;
     const int got = sscanf(env, "%d,%d,%d,%d", &bn, &sp, &wv, &stg);
-    if (got >= 2 && (bn == 256 || bn == 192 || bn == 128) && sp >= 1 && sp <= 4 &&
-        (wv == 8 || (wv == 4 && bn == 256)) && (stg == 1 || stg == 2)) {
+    if (got >= 2 && (bn == 256 || bn == 192 || bn == 128) && sp >= 1 && sp <= 4 && wv == 8 &&
+        (stg == 1 || stg == 2)) {
       pl.bn = bn;
       pl.splits = sp;
       pl.waves = wv;
-      pl.stages = wv == 4 ? 1 : stg;
+      pl.stages = stg;
       pl.tiles = tiles_of(a, kBM, bn);
     }
   }
@@ -442,11 +442,11 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
   GemmPlan pl = plan_gemm(a, dtype, partial ? partial_bytes : 0);
   if (pl.tiles == 0) return AVITS_OK;
   if (pl.splits > 1 && (!partial || partial_bytes < gemm_partial_bytes(a, pl))) pl.splits = 1;
-  TimedLaunch timed(family, s);
   if (dtype == AVITS_BF16) {
     const dim3 grid(unsigned(pl.tiles * pl.splits));
+    {
+    TimedLaunch timed(family, s);  // the GEMM kernel alone; the reduce is its own family
     switch (pl.bn * 100 + pl.waves * 10 + pl.stages) {
-      case 25641: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 2, 1>), grid, dim3(256), 0, s, a, partial, pl.splits); break;
       case 25681: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 25682: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 19281: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
@@ -454,13 +454,16 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
       case 12881: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
     }
+    }
     if (pl.splits > 1) {
+      TimedLaunch timed_reduce("splitk_reduce", s);
       const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
       const int64_t work = rows * (a.N / 4);
       hipLaunchKernelGGL(splitk_reduce_kernel, dim3(unsigned(ceil_div64(work, 256))), dim3(256), 0, s, a,
                          (const float*)partial, pl.splits);
     }
   } else {
+    TimedLaunch timed(family, s);
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(unsigned(pl.tiles)), dim3(256), 0, s, a);
   }
   return launch_status("gemm");

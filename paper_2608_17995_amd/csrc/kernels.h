@@ -49,7 +49,7 @@ struct GemmArgs {
 struct GemmPlan {
   int bn = 0;          // column tile
   int splits = 1;      // K splits (fp32 partials + reduce when > 1)
-  int waves = 8;       // waves per workgroup (4: 128 x 128 wave tiles, BN = 256 only)
+  int waves = 8;       // waves per workgroup
   int stages = 2;      // register staging depth of the k-tile pipeline (1 or 2)
   int64_t tiles = 0;   // output tiles
 };

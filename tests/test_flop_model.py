@@ -41,3 +41,22 @@ def test_stage_bytes_flux_1024():
     assert abs(b["score"] / 1e6 - 79.1) < 0.1
     assert abs(b["gather_upsample"] / 1e6 - 45.3) < 0.1
     assert abs(b["scatter"] / 1e6 - 15.1) < 0.1
+
+
+def test_gemm_compulsory_bytes():
+    # both streams' weights (2 x 36864 x 3072 bf16) plus each activation read or written once
+    b = bench.gemm_min_bytes(1741, 3072, 12288)
+    weights = 2 * 2 * (3 + 1 + 4 + 4) * 3072 * 3072
+    acts = 2 * 1741 * ((4 + 3 + 1 + 2) * 3072 + 2 * 12288)   # QKV, O, MLP in, MLP out
+    assert b == weights + acts
+    assert abs(b / 4 / 1e6 - 161.38) < 0.01
+
+
+def test_traffic_record_tracks_gemm_sources(monkeypatch, tmp_path):
+    rec = bench.measured_traffic()
+    if rec is not None:   # recorded for exactly the current GEMM sources
+        assert rec["sources_sha256"] == bench.gemm_sources_sha256() and rec["bytes_per_launch"] > 0
+    stale = tmp_path / "t.md"
+    stale.write_text('traffic_json: {"sources_sha256": "0", "bytes_per_launch": 1}\n')
+    monkeypatch.setattr(bench, "TRAFFIC_PROFILE", str(stale))
+    assert bench.measured_traffic() is None
