@@ -187,6 +187,28 @@ int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos,
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_block_qk — the first stage of a block alone (the attention probe of
+ * Section 3.3.1: the queries and keys whose joint softmax defines the
+ * image-to-text attention mass of Eq. spatial): for each row,
+ *   h = LN(x)(1 + scale1) + shift1;  q = h W_q^T + b_q;  k = h W_k^T + b_k;
+ *   q, k = RMSNorm_d(.) * g;  RoPE(q, k) at pos
+ * exactly as avits_block_forward computes them (W_q, W_k = the first 2D
+ * output rows of W_qkv, or of W_in for the single kind; stream weights per
+ * row as there).
+ * x_in [S, D], pos [S, 3] int32; q_out, k_out [S, D] = [S, H, d] (distinct,
+ * not aliasing x_in), which is the layout avits_score and avits_joint_lse
+ * take: the image queries are q_out + n_txt * D, the text keys k_out, the
+ * joint key set k_out itself.  workspace >= avits_block_qk_workspace_bytes(S,
+ * H, d, dtype) bytes (S*D elements).  S == 0 is a no-op.  Other arguments
+ * and errors as avits_block_forward.
+ * ---------------------------------------------------------------------- */
+size_t avits_block_qk_workspace_bytes(int64_t S, int32_t H, int32_t d, int dtype);
+int avits_block_qk(const void* x_in, const int32_t* pos, int64_t n_txt, int64_t n_img,
+                   const avits_block_weights* w, int32_t H, int32_t d, int dtype,
+                   void* q_out, void* k_out, void* workspace, size_t workspace_bytes,
+                   void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_scatter — Stage-3 re-layout: canvas[idx[j]] = out[row_offset + j]
  * for j < k.  out [row_offset + k, D], idx [k] int32 (unique, < rows of
  * canvas), canvas [*, D].  k == 0 enqueues nothing.
@@ -214,7 +236,8 @@ int avits_joint_lse(const void* q, const void* k_all, int64_t N, int64_t Nk,
  * "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
  * "splitk_reduce", "qk_rope", "attention", "joint_lse"; "gemm" returns the
  * sum of the six GEMM families (the GEMM kernels alone: the split-K
- * reduction that follows a split launch is "splitk_reduce").  Unknown family -> AVITS_ERR_INVALID_ARG.
+ * reduction that follows a split launch is "splitk_reduce").  Unknown
+ * family -> AVITS_ERR_INVALID_ARG.
  * avits_timing_reset() waits for pending events and zeroes every total.
  * Not thread-safe: use from one host thread.
  * ---------------------------------------------------------------------- */

@@ -166,6 +166,35 @@ def double_block(x, pos, n_txt: int, w_txt: dict, w_img: dict, H: int, rows=None
     return out, lse
 
 
+def block_qk(x, pos, n_txt: int, w_txt: dict | None, w_img: dict | None, H: int, single: dict | None = None):
+    """Normalised, rotated queries and keys of a block's first stage.
+
+    These are the q and k whose joint softmax the block's attention takes
+    (Section 3.3.1, Eq. joint_qk) and from which Eq. spatial reads the
+    image-to-text attention mass: per row, h = LN(x)(1 + scale1) + shift1,
+    q = RMSNorm(h W_q^T + b_q) * g_q, k likewise, both rotated at pos.  For a
+    double block rows [0, n_txt) use w_txt and the rest w_img; with ``single``
+    given, every row uses the single-block weights (W_q, W_k = the first 2D
+    rows of W_in).  Returns (q, k), each [S, H, d].
+    """
+    x = _f64(x)
+    S, D = x.shape
+    d = D // H
+    ang = rope_angles(pos, d)
+    q = np.empty((S, H, d))
+    k = np.empty((S, H, d))
+    parts = ((0, S, single, "w_in", "b_in"),) if single is not None else \
+        ((0, n_txt, w_txt, "w_qkv", "b_qkv"), (n_txt, S, w_img, "w_qkv", "b_qkv"))
+    for lo, hi, w, wn, bn in parts:
+        if hi <= lo:
+            continue
+        mod, W, b = _f64(w["mod"]), _f64(w[wn]), _f64(w[bn])
+        h = _modulate(x[lo:hi], mod[0], mod[1])
+        q[lo:hi] = rms_norm((h @ W[:D].T + b[:D]).reshape(-1, H, d), w["g_q"])
+        k[lo:hi] = rms_norm((h @ W[D:2 * D].T + b[D:2 * D]).reshape(-1, H, d), w["g_k"])
+    return apply_rope(q, ang), apply_rope(k, ang)
+
+
 def single_block(x, pos, w: dict, H: int, rows=None):
     """Single-stream block on x [S, D]; ``rows`` as in double_block."""
     x = _f64(x)

@@ -50,6 +50,9 @@ _SIGS = {
     "avits_block_forward": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _i64,
                                            ctypes.POINTER(_BlockWeights), _i32, _i32, ctypes.c_int, _c_void_p,
                                            _c_void_p, _size, _c_void_p]),
+    "avits_block_qk_workspace_bytes": (_size, [_i64, _i32, _i32, ctypes.c_int]),
+    "avits_block_qk": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, ctypes.POINTER(_BlockWeights), _i32, _i32,
+                                      ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, ctypes.c_int, _c_void_p, _c_void_p]),
     "avits_joint_lse": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i32, _i32, ctypes.c_int, _c_void_p,
                                        _c_void_p]),
@@ -244,3 +247,20 @@ def avits_block_forward(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H
         _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), n_txt, n_img,
         ctypes.byref(weights.c), H, d, code, _dev(lse_out, "lse_out", torch.float32), wsp, wsb, _stream(stream)))
     return x_out
+
+
+def avits_block_qk_workspace_bytes(S: int, H: int, d: int, dtype: int) -> int:
+    return load().avits_block_qk_workspace_bytes(S, H, d, dtype)
+
+
+def avits_block_qk(x_in, pos, n_txt, n_img, weights: BlockWeights, H, q_out, k_out, workspace=None, stream=None):
+    """q_out, k_out [S, D] (or [S, H, d]): the block's normalised, rotated queries and keys."""
+    import torch
+    S, D = x_in.shape
+    d = D // H
+    code = _dtype_code(x_in)
+    ws, wsp, wsb = _workspace(workspace, avits_block_qk_workspace_bytes(S, H, d, code), x_in.device)
+    _check(load().avits_block_qk(
+        _dev(x_in, "x_in"), _dev(pos, "pos", torch.int32), n_txt, n_img, ctypes.byref(weights.c), H, d, code,
+        _dev(q_out, "q_out", x_in.dtype), _dev(k_out, "k_out", x_in.dtype), wsp, wsb, _stream(stream)))
+    return q_out, k_out

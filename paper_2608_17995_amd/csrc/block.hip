@@ -131,14 +131,16 @@ __device__ __forceinline__ void store8(float* p, const float (&x)[8]) {
   *reinterpret_cast<float4*>(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
 }
 
-// In-place RMSNorm (times the gain) and RoPE of q and k in qk [S, 2D]
-// (q | k, head-major within each).  Each lane owns 8 consecutive elements
+// In-place RMSNorm (times the gain) and RoPE of q [S, ld] and k [S, ld]
+// (head-major within a row: the block passes q | k of one [S, 2D] buffer,
+// ld = 2D; the probe passes two [S, D] arrays, ld = D).  Each lane owns 8 consecutive elements
 // (4 rotation pairs) of one head, so a d-wide head spans d/8 lanes and the
 // RMS reduction stays inside that lane group.  Rows [0, n_a) use the gains
 // of stream a.  One wavefront walks the 2H heads of a row, 64*8/d heads at a
 // time.
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ qk, const int32_t* __restrict__ pos,
+__global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ q, T* __restrict__ k, int64_t ld,
+                                                           const int32_t* __restrict__ pos,
                                                            int64_t S, int H, int64_t n_a, const T* __restrict__ gq_a,
                                                            const T* __restrict__ gk_a, const T* __restrict__ gq_b,
                                                            const T* __restrict__ gk_b) {
@@ -163,7 +165,8 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ qk, c
     const float freq = exp2f(-2.f * float(mi) / float(na) * kLog2Theta);
     sincosf(float(pr[axis]) * freq, &sn[j], &cs[j]);
   }
-  T* base = qk + row * (2 * int64_t(H) * DH);
+  T* const qrow = q + row * ld;
+  T* const krow = k + row * ld;
   // Both gain vectors of this lane's 8 elements, loaded once per row.
   float gq[8], gk[8];
   load8(a_rows ? gq_a : gq_b, 8 * sub, gq);
@@ -171,7 +174,8 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ qk, c
   for (int h0 = 0; h0 < 2 * H; h0 += kHeadsPerPass) {
     const int head = h0 + hoff;                  // 0..H-1 query heads, H..2H-1 key heads
     const bool live = head < 2 * H;
-    T* p = base + int64_t(live ? head : 0) * DH + 8 * sub;
+    const int hh = live ? head : 0;
+    T* p = (hh < H ? qrow + int64_t(hh) * DH : krow + int64_t(hh - H) * DH) + 8 * sub;
     float x[8];
     load8(p, 0, x);
     float ss = 0.f;
@@ -231,6 +235,100 @@ BlockWs block_ws_layout(char* base, int kind, int64_t S, int64_t H, int64_t d, i
   return w;
 }
 
+// Per-stream views of a block call: (row offset, row count, weights).
+struct Stream { int64_t r0, rows; const avits_double_stream_weights* dw; };
+
+template <typename T>
+const T* mod_row(const void* mod, int r, int64_t D) { return static_cast<const T*>(mod) + r * D; }
+
+// h = LN(x)(1 + scale) + shift with the modulation rows (r_shift, r_scale) of
+// each stream (the single kind has one set for every row).
+template <typename T>
+int launch_ln_mod(const T* x, T* h, int64_t S, int64_t D, int64_t n_txt, const avits_block_weights* w, int r_shift,
+                  hipStream_t s) {
+  const dim3 rows_grid(unsigned(ceil_div64(S, 4))), blk(256);
+  TimedLaunch timed("ln_mod", s);
+  if (w->kind == AVITS_BLOCK_DOUBLE) {
+    const avits_double_stream_weights& wa = n_txt ? w->txt : w->img;
+    const avits_double_stream_weights& wb = n_txt < S ? w->img : w->txt;
+    hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, n_txt, mod_row<T>(wa.mod, r_shift, D),
+                       mod_row<T>(wa.mod, r_shift + 1, D), mod_row<T>(wb.mod, r_shift, D),
+                       mod_row<T>(wb.mod, r_shift + 1, D));
+  } else {
+    const void* m = w->single.mod;
+    hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, S, mod_row<T>(m, 0, D),
+                       mod_row<T>(m, 1, D), mod_row<T>(m, 0, D), mod_row<T>(m, 1, D));
+  }
+  return launch_status("block ln_mod");
+}
+
+// RMSNorm * g and RoPE of q and k in place, with each stream's gains.
+template <typename T>
+int launch_qk_norm_rope(T* q, T* k, int64_t ld, const int32_t* pos, int64_t S, int64_t n_txt, int H, int d,
+                        const avits_block_weights* w, hipStream_t s) {
+  const T *gqa, *gka, *gqb, *gkb;
+  int64_t na;
+  if (w->kind == AVITS_BLOCK_DOUBLE) {
+    const avits_double_stream_weights& wa = n_txt ? w->txt : w->img;
+    const avits_double_stream_weights& wb = n_txt < S ? w->img : w->txt;
+    gqa = static_cast<const T*>(wa.g_q); gka = static_cast<const T*>(wa.g_k);
+    gqb = static_cast<const T*>(wb.g_q); gkb = static_cast<const T*>(wb.g_k);
+    na = n_txt;
+  } else {
+    gqa = gqb = static_cast<const T*>(w->single.g_q);
+    gka = gkb = static_cast<const T*>(w->single.g_k);
+    na = S;
+  }
+  const dim3 rows_grid(unsigned(ceil_div64(S, 4))), blk(256);
+  TimedLaunch timed("qk_rope", s);
+  if (d == 128)
+    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 128>), rows_grid, blk, 0, s, q, k, ld, pos, S, H, na, gqa, gka, gqb,
+                       gkb);
+  else
+    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 64>), rows_grid, blk, 0, s, q, k, ld, pos, S, H, na, gqa, gka, gqb,
+                       gkb);
+  return launch_status("block qk_norm_rope");
+}
+
+// The block's first stage alone: LN + modulation, the q and k projections,
+// RMSNorm and RoPE, written to q_out [S, D] and k_out [S, D].
+template <typename T>
+int run_block_qk(const void* x_in, const int32_t* pos, int64_t n_txt, int64_t n_img, const avits_block_weights* w,
+                 int H, int d, int dtype, void* q_out, void* k_out, void* h_ws, hipStream_t s) {
+  const int64_t S = n_txt + n_img, D = int64_t(H) * d;
+  T* h = static_cast<T*>(h_ws);
+  T* q = static_cast<T*>(q_out);
+  T* k = static_cast<T*>(k_out);
+  int rc;
+  if ((rc = launch_ln_mod<T>(static_cast<const T*>(x_in), h, S, D, n_txt, w, 0, s)) != AVITS_OK) return rc;
+  GemmArgs g{};
+  g.N = 2 * D;          // the first 2D output rows of W_qkv (or W_in): q then k
+  g.K = D;
+  g.n_split = D;
+  g.n_split2 = 2 * D;
+  g.mode0 = EPI_STORE;
+  g.mode1 = EPI_STORE;
+  if (w->kind == AVITS_BLOCK_DOUBLE) {
+    const Stream st2[2] = {{0, n_txt, &w->txt}, {n_txt, n_img, &w->img}};
+    for (const Stream& t : st2) {
+      if (t.rows == 0) continue;
+      GemmProblem& p = g.p[g.nprob++];
+      p.A = h + t.r0 * D; p.lda = D; p.W = t.dw->w_qkv; p.bias = t.dw->b_qkv; p.M = t.rows;
+      p.out0 = q + t.r0 * D; p.ld0 = D;
+      p.out1 = k + t.r0 * D; p.ld1 = D;
+    }
+  } else {
+    GemmProblem& p = g.p[g.nprob++];
+    p.A = h; p.lda = D; p.W = w->single.w_in; p.bias = w->single.b_in; p.M = S;
+    p.out0 = q; p.ld0 = D;
+    p.out1 = k; p.ld1 = D;
+  }
+  if ((rc = launch_gemm(g, dtype, s, w->kind == AVITS_BLOCK_DOUBLE ? "gemm_qkv" : "gemm_single_in", nullptr, 0)) !=
+      AVITS_OK)
+    return rc;
+  return launch_qk_norm_rope<T>(q, k, D, pos, S, n_txt, H, d, w, s);
+}
+
 template <typename T>
 int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, int64_t n_img,
               const avits_block_weights* w, int H, int d, int dtype, float* lse_out, const BlockWs& ws,
@@ -241,35 +339,20 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
   T* h = reinterpret_cast<T*>(ws.h);
   T* qk = reinterpret_cast<T*>(ws.qk);
   T* vt = reinterpret_cast<T*>(ws.vt);
-  const dim3 rows_grid(unsigned(ceil_div64(S, 4))), blk(256);
   int rc;
 
-  // Per-stream views: (row offset, row count, weights) for up to two streams.
-  struct Stream { int64_t r0, rows; const avits_double_stream_weights* dw; };
-  Stream st2[2] = {{0, n_txt, &w->txt}, {n_txt, n_img, &w->img}};
+  // The non-empty streams (double kind).
+  const Stream st2[2] = {{0, n_txt, &w->txt}, {n_txt, n_img, &w->img}};
   int nst = 0;
   Stream streams[2];
   if (dbl) {
-    for (auto& t : st2)
+    for (const Stream& t : st2)
       if (t.rows > 0) streams[nst++] = t;
   }
-  // Weights of the text rows and of the image rows (an empty stream borrows
-  // the other's pointers; they are never read for it).
-  const avits_double_stream_weights& wa = n_txt ? w->txt : w->img;
-  const avits_double_stream_weights& wb = n_img ? w->img : w->txt;
   auto mod_row = [&](const void* mod, int r) { return static_cast<const T*>(mod) + r * D; };
 
   // 1. modulated layer norm.
-  {
-    TimedLaunch timed("ln_mod", s);
-    if (dbl)
-      hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, n_txt, mod_row(wa.mod, 0),
-                         mod_row(wa.mod, 1), mod_row(wb.mod, 0), mod_row(wb.mod, 1));
-    else
-      hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, S, mod_row(w->single.mod, 0),
-                         mod_row(w->single.mod, 1), mod_row(w->single.mod, 0), mod_row(w->single.mod, 1));
-    if ((rc = launch_status("block ln_mod")) != AVITS_OK) return rc;
-  }
+  if ((rc = launch_ln_mod<T>(x, h, S, D, n_txt, w, 0, s)) != AVITS_OK) return rc;
 
   // 2. QKV projection: q | k token-major, v transposed per head
   //    (+ the single block's MLP input, GELU'd beside o).
@@ -306,25 +389,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
   }
 
   // 3. q/k RMSNorm + RoPE in place.
-  {
-    const T *gqa, *gka, *gqb, *gkb;
-    int64_t na;
-    if (dbl) {
-      gqa = static_cast<const T*>(wa.g_q); gka = static_cast<const T*>(wa.g_k);
-      gqb = static_cast<const T*>(wb.g_q); gkb = static_cast<const T*>(wb.g_k);
-      na = n_txt;
-    } else {
-      gqa = gqb = static_cast<const T*>(w->single.g_q);
-      gka = gkb = static_cast<const T*>(w->single.g_k);
-      na = S;
-    }
-    TimedLaunch timed("qk_rope", s);
-    if (d == 128)
-      hipLaunchKernelGGL((qk_norm_rope_kernel<T, 128>), rows_grid, blk, 0, s, qk, pos, S, H, na, gqa, gka, gqb, gkb);
-    else
-      hipLaunchKernelGGL((qk_norm_rope_kernel<T, 64>), rows_grid, blk, 0, s, qk, pos, S, H, na, gqa, gka, gqb, gkb);
-    if ((rc = launch_status("block qk_norm_rope")) != AVITS_OK) return rc;
-  }
+  if ((rc = launch_qk_norm_rope<T>(qk, qk + D, 2 * D, pos, S, n_txt, H, d, w, s)) != AVITS_OK) return rc;
 
   // 4. joint attention over all S rows.
   {
@@ -364,12 +429,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
     if ((rc = launch_gemm(g, dtype, s, "gemm_o", ws.partial, ws.partial_bytes)) != AVITS_OK) return rc;
   }
   // 6. second modulated layer norm.
-  {
-    TimedLaunch timed("ln_mod", s);
-    hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, xmid, h, S, D, n_txt, mod_row(wa.mod, 3),
-                       mod_row(wa.mod, 4), mod_row(wb.mod, 3), mod_row(wb.mod, 4));
-    if ((rc = launch_status("block ln_mod2")) != AVITS_OK) return rc;
-  }
+  if ((rc = launch_ln_mod<T>(xmid, h, S, D, n_txt, w, 3, s)) != AVITS_OK) return rc;
   // 7. MLP in + GELU.
   T* mlp = reinterpret_cast<T*>(ws.mlp);
   {
@@ -417,33 +477,70 @@ extern "C" size_t avits_block_workspace_bytes(int32_t kind, int64_t S, int32_t H
   return block_ws_layout(nullptr, kind, S, H, d, mlp_hidden, dtype == AVITS_F32 ? 4 : 2).bytes;
 }
 
-extern "C" int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt,
-                                   int64_t n_img, const avits_block_weights* w, int32_t H, int32_t d, int dtype,
-                                   float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
-  AVITS_REQUIRE(w, "block_forward: null weights");
-  AVITS_REQUIRE(n_txt >= 0 && n_img >= 0, "block_forward: n_txt=%lld n_img=%lld must be >= 0", (long long)n_txt,
+namespace avits {
+namespace {
+// Host-side checks shared by avits_block_forward and avits_block_qk; returns
+// AVITS_OK or the error code (with the message set).
+int check_block_args(const char* fn, const void* x_in, const int32_t* pos, int64_t n_txt, int64_t n_img,
+                     const avits_block_weights* w, int32_t H, int32_t d, int dtype) {
+  AVITS_REQUIRE(w, "%s: null weights", fn);
+  AVITS_REQUIRE(n_txt >= 0 && n_img >= 0, "%s: n_txt=%lld n_img=%lld must be >= 0", fn, (long long)n_txt,
                 (long long)n_img);
-  AVITS_REQUIRE(H >= 1, "block_forward: H=%d < 1", H);
-  if (d != 64 && d != 128) return set_error(AVITS_ERR_UNSUPPORTED, "block_forward: head dim %d (need 64 or 128)", d);
+  AVITS_REQUIRE(H >= 1, "%s: H=%d < 1", fn, H);
+  if (d != 64 && d != 128) return set_error(AVITS_ERR_UNSUPPORTED, "%s: head dim %d (need 64 or 128)", fn, d);
   if (dtype != AVITS_F32 && dtype != AVITS_BF16)
-    return set_error(AVITS_ERR_UNSUPPORTED, "block_forward: dtype %d unsupported", dtype);
-  AVITS_REQUIRE(w->kind == AVITS_BLOCK_DOUBLE || w->kind == AVITS_BLOCK_SINGLE, "block_forward: bad kind %d",
-                w->kind);
+    return set_error(AVITS_ERR_UNSUPPORTED, "%s: dtype %d unsupported", fn, dtype);
+  AVITS_REQUIRE(w->kind == AVITS_BLOCK_DOUBLE || w->kind == AVITS_BLOCK_SINGLE, "%s: bad kind %d", fn, w->kind);
   AVITS_REQUIRE(w->mlp_hidden >= 64 && w->mlp_hidden % 64 == 0,
-                "block_forward: mlp_hidden=%d must be a positive multiple of 64", w->mlp_hidden);
+                "%s: mlp_hidden=%d must be a positive multiple of 64", fn, w->mlp_hidden);
   const int64_t S = n_txt + n_img;
-  AVITS_REQUIRE(S <= INT32_MAX, "block_forward: S=%lld too large", (long long)S);
+  AVITS_REQUIRE(S <= INT32_MAX, "%s: S=%lld too large", fn, (long long)S);
   if (S == 0) return AVITS_OK;
-  AVITS_REQUIRE(x_in && x_out && pos, "block_forward: null x_in/x_out/pos");
-  AVITS_REQUIRE(x_in != x_out, "block_forward: x_out must not alias x_in");
+  AVITS_REQUIRE(x_in && pos, "%s: null x_in/pos", fn);
   if (w->kind == AVITS_BLOCK_DOUBLE) {
-    AVITS_REQUIRE(n_txt == 0 || all_set(w->txt), "block_forward: missing text-stream weight");
-    AVITS_REQUIRE(n_img == 0 || all_set(w->img), "block_forward: missing image-stream weight");
+    AVITS_REQUIRE(n_txt == 0 || all_set(w->txt), "%s: missing text-stream weight", fn);
+    AVITS_REQUIRE(n_img == 0 || all_set(w->img), "%s: missing image-stream weight", fn);
   } else {
     const avits_single_weights& sw = w->single;
     AVITS_REQUIRE(sw.mod && sw.w_in && sw.b_in && sw.g_q && sw.g_k && sw.w_out && sw.b_out,
-                  "block_forward: missing single-block weight");
+                  "%s: missing single-block weight", fn);
   }
+  return AVITS_OK;
+}
+}  // namespace
+}  // namespace avits
+
+extern "C" size_t avits_block_qk_workspace_bytes(int64_t S, int32_t H, int32_t d, int dtype) {
+  if (S < 0 || H < 1 || d < 1 || (dtype != AVITS_F32 && dtype != AVITS_BF16)) return 0;
+  return align_up(size_t(S) * size_t(H) * size_t(d) * (dtype == AVITS_F32 ? 4 : 2), 256);
+}
+
+extern "C" int avits_block_qk(const void* x_in, const int32_t* pos, int64_t n_txt, int64_t n_img,
+                              const avits_block_weights* w, int32_t H, int32_t d, int dtype, void* q_out, void* k_out,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_block_args("block_qk", x_in, pos, n_txt, n_img, w, H, d, dtype);
+  if (rc != AVITS_OK) return rc;
+  const int64_t S = n_txt + n_img;
+  if (S == 0) return AVITS_OK;
+  AVITS_REQUIRE(q_out && k_out && q_out != k_out, "block_qk: q_out and k_out must be distinct non-null buffers");
+  const size_t need = avits_block_qk_workspace_bytes(S, H, d, dtype);
+  if (!workspace || workspace_bytes < need)
+    return set_error(AVITS_ERR_WORKSPACE, "block_qk: workspace of %zu bytes, need %zu", workspace_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dtype == AVITS_BF16)
+    return run_block_qk<bf16_t>(x_in, pos, n_txt, n_img, w, H, d, dtype, q_out, k_out, workspace, s);
+  return run_block_qk<float>(x_in, pos, n_txt, n_img, w, H, d, dtype, q_out, k_out, workspace, s);
+}
+
+extern "C" int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt,
+                                   int64_t n_img, const avits_block_weights* w, int32_t H, int32_t d, int dtype,
+                                   float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_block_args("block_forward", x_in, pos, n_txt, n_img, w, H, d, dtype);
+  if (rc != AVITS_OK) return rc;
+  const int64_t S = n_txt + n_img;
+  if (S == 0) return AVITS_OK;
+  AVITS_REQUIRE(x_out, "block_forward: null x_out");
+  AVITS_REQUIRE(x_in != x_out, "block_forward: x_out must not alias x_in");
   const int64_t esz = dtype == AVITS_F32 ? 4 : 2;
   const BlockWs need = block_ws_layout(nullptr, w->kind, S, H, d, w->mlp_hidden, esz);
   if (!workspace || workspace_bytes < need.bytes)

@@ -87,3 +87,96 @@ class SelectiveStep:
         self.gather(lowres, highres_prev, prefix, stream)
         self.block(stream)
         self.scatter(highres_prev, stream)
+
+
+class StackStep:
+    """One denoising step of a selective block stack (Section 3.2 Stage 2 over
+    the whole backbone, the importance taken from its first double block):
+
+      probe    double block 0's first stage on [prefix; X_prev] -> q, k
+      lse      joint log-sum-exp of the image queries over [prefix; image] keys
+      score    spatial (text mass) + temporal (X_prev vs X_prev2) -> S
+      select   top-k of S
+      gather   compact = [prefix; X_prev[idx]], canvas = X_prev on idx, else up(lowres)
+      blocks   the double blocks, then the single blocks, on the compacted rows
+      scatter  canvas[idx] = last block's image rows  -> X_new
+
+    Buffers are allocated once; run() enqueues library calls only.  The
+    prefix rows ([text; ref]) use the text weights for the text rows and the
+    image weights for the reference rows, as in the block.  ``on_block(i, x_in,
+    x_out)``, if given, is called after block i is enqueued (for inspection).
+    """
+
+    def __init__(self, shape: StepShape, doubles: list, singles: list, prefix_pos, dtype, device="cuda",
+                 alpha=0.5, eps=1e-8, mode=B.UP_NEAREST):
+        import torch
+        s = shape
+        if not doubles:
+            raise ValueError("the probe needs at least one double block")
+        self.shape, self.doubles, self.singles = s, list(doubles), list(singles)
+        self.alpha, self.eps, self.mode = alpha, eps, mode
+        f32, i32 = torch.float32, torch.int32
+        d = s.D // s.H
+        code = B.BF16 if dtype == torch.bfloat16 else B.F32
+        LR = s.L + s.R
+        self.q_prefix = torch.empty(max(LR, 1), s.D, dtype=dtype, device=device)
+        self.q_img = torch.empty(s.N, s.D, dtype=dtype, device=device)
+        self.k_all = torch.empty(LR + s.N, s.D, dtype=dtype, device=device)
+        self.lse = torch.empty(s.H, s.N, dtype=f32, device=device)
+        self.prefix_pos = torch.as_tensor(prefix_pos, dtype=i32).to(device)
+        r = torch.arange(s.N, dtype=i32, device=device)
+        W_hr = 2 * s.W_lr
+        self.img_pos = torch.stack([torch.zeros_like(r), r // W_hr, r % W_hr], dim=1).contiguous()
+        self.scores = torch.empty(s.N, dtype=f32, device=device)
+        self.a_raw = torch.empty(s.N, dtype=f32, device=device)
+        self.v_raw = torch.empty(s.N, dtype=f32, device=device)
+        self.idx = torch.empty(s.k, dtype=i32, device=device)
+        self.compact = torch.empty(s.S, s.D, dtype=dtype, device=device)
+        self.pos = torch.empty(s.S, 3, dtype=i32, device=device)
+        self.pos[:LR].copy_(self.prefix_pos)
+        self.x = [torch.empty(s.S, s.D, dtype=dtype, device=device) for _ in range(2)]
+        self.ws_score = torch.empty(max(B.avits_score_workspace_bytes(s.N, s.H), 1), dtype=torch.uint8, device=device)
+        self.ws_select = torch.empty(max(B.avits_select_workspace_bytes(s.N), 1), dtype=torch.uint8, device=device)
+        need = max(B.avits_block_qk_workspace_bytes(max(LR, s.N), s.H, d, code),
+                   B.avits_block_workspace_bytes(B.BLOCK_DOUBLE, s.S, s.H, d, s.mlp_hidden, code),
+                   B.avits_block_workspace_bytes(B.BLOCK_SINGLE, s.S, s.H, d, s.mlp_hidden, code) if singles else 0)
+        self.ws_block = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+        self.out = None
+
+    def probe(self, x_prev, prefix, stream=None):
+        s = self.shape
+        LR = s.L + s.R
+        w0 = self.doubles[0]
+        if LR:
+            B.avits_block_qk(prefix, self.prefix_pos, s.L, s.R, w0, s.H, self.q_prefix[:LR], self.k_all[:LR],
+                             self.ws_block, stream)
+        B.avits_block_qk(x_prev, self.img_pos, 0, s.N, w0, s.H, self.q_img, self.k_all[LR:], self.ws_block, stream)
+        d = s.D // s.H
+        B.avits_joint_lse(self.q_img.view(s.N, s.H, d), self.k_all.view(LR + s.N, s.H, d), self.lse, stream)
+
+    def run(self, x_prev, x_prev2, lowres, prefix, canvas, stream=None, on_block=None):
+        """X_new (written to ``canvas``, which must not alias x_prev) from X_prev and X_prev2."""
+        s = self.shape
+        LR = s.L + s.R
+        d = s.D // s.H
+        if canvas.data_ptr() == x_prev.data_ptr():
+            raise ValueError("canvas must not alias x_prev: X_prev is the next step's X_prev2")
+        self.probe(x_prev, prefix, stream)
+        B.avits_score(self.q_img.view(s.N, s.H, d), self.k_all[:s.L].view(s.L, s.H, d), self.lse, x_prev, x_prev2,
+                      self.alpha, self.eps, self.scores, self.a_raw, self.v_raw, self.ws_score, stream)
+        if s.k:
+            B.avits_select(self.scores, s.k, self.idx, self.ws_select, stream)
+        B.avits_gather_upsample(lowres, x_prev, prefix if LR else None, self.idx, s.H_lr, s.W_lr, self.compact,
+                                self.pos[LR:], canvas, self.mode, stream)
+        cur = self.compact
+        blocks = self.doubles + self.singles
+        for i, w in enumerate(blocks):
+            nxt = self.x[i % 2]
+            B.avits_block_forward(cur, nxt, self.pos, s.L, s.R + s.k, w, s.H, None, self.ws_block, stream)
+            if on_block is not None:
+                on_block(i, cur, nxt)
+            cur = nxt
+        self.out = cur
+        if s.k:
+            B.avits_scatter(cur, self.idx, LR, canvas, stream)
+        return canvas

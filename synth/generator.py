@@ -36,11 +36,21 @@ def rng(seed: int, tensor_id: int) -> np.random.Generator:
     return np.random.default_rng([seed, tensor_id])
 
 
+def _bf16_rne_u32(x32: np.ndarray) -> np.ndarray:
+    """float32 bits rounded to bf16 (RNE), left in the low 16 bits of uint32
+    (computed in place on one temporary: weights run to 10^8 elements)."""
+    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32)
+    r = u >> np.uint32(16)
+    r &= np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
+    return r
+
+
 def to_bf16_bits(x32: np.ndarray) -> np.ndarray:
     """uint16 bit patterns of float32 values rounded to bf16 (RNE)."""
-    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32)
-    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
-    return r.astype(np.uint16)
+    return _bf16_rne_u32(x32).astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -53,7 +63,9 @@ def round_to(x: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "f32":
         return x32
     if dtype == "bf16":
-        return bf16_bits_to_f32(to_bf16_bits(x32))
+        r = _bf16_rne_u32(x32)
+        r <<= np.uint32(16)
+        return r.view(np.float32)
     raise ValueError(dtype)
 
 

@@ -128,3 +128,27 @@ def test_block_validation(lib):
     assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
     assert lib.avits_block_workspace_bytes(1, 10, 1, 64, 256, 1) > 0
     assert lib.avits_block_workspace_bytes(3, 10, 1, 64, 256, 1) == 0
+
+
+def test_block_qk_validation(lib):
+    import ctypes
+    w = _binding._BlockWeights()
+    w.kind, w.mlp_hidden = 0, 256
+    f = lib.avits_block_qk
+    ws = lib.avits_block_qk_workspace_bytes(10, 2, 64, 1)
+    assert ws >= 10 * 128 * 2 and lib.avits_block_qk_workspace_bytes(10, 2, 64, 0) >= 10 * 128 * 4
+    assert lib.avits_block_qk_workspace_bytes(10, 0, 64, 1) == 0
+    q, k = FAKE + 4096, FAKE + 8192
+    assert f(FAKE, FAKE, 5, 5, None, 2, 64, 1, q, k, FAKE, ws, None) == INVALID                 # null weights
+    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, FAKE, ws, None) == INVALID      # missing weights
+    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 96, 1, q, k, FAKE, ws, None) == UNSUPPORTED
+    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 3, q, k, FAKE, ws, None) == UNSUPPORTED
+    assert f(FAKE, FAKE, 0, 0, ctypes.byref(w), 2, 64, 1, None, None, None, 0, None) == 0     # S == 0
+    for part in ("txt", "img"):
+        for name, _ in _binding._DoubleStream._fields_:
+            setattr(getattr(w, part), name, FAKE)
+    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, q, FAKE, ws, None) == INVALID      # q aliases k
+    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, None, k, FAKE, ws, None) == INVALID
+    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, FAKE, ws - 1, None) == WORKSPACE
+    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, None, ws, None) == WORKSPACE
+    assert b"block_qk" in lib.avits_last_error()

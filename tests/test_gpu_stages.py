@@ -241,3 +241,50 @@ def test_block_relayout_equivariance(gpu):
     perm = np.concatenate([np.arange(16), 16 + np.random.default_rng(2).permutation(48)])
     out2, _ = _run_double(gpu, w, x[perm], pos[perm], 16, wt, wi)
     assert rel_l2(out2 - x[perm], out[perm] - x[perm]) < 1e-2
+
+
+def _run_block_qk(gpu, w, x, pos, n_txt, bw):
+    t_x = dev(x, w.dtype)
+    q = torch.empty_like(t_x)
+    k = torch.empty_like(t_x)
+    gpu.avits_block_qk(t_x, dev(pos), n_txt, x.shape[0] - n_txt, bw, w.H, q, k)
+    torch.cuda.synchronize()
+    return host(q), host(k)
+
+
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+def test_block_qk_probe(gpu, w):
+    n_txt, n_img = w.L, w.R + w.k
+    x, pos = _block_inputs(w, n_txt, n_img, seed=5)
+    wt, wi = G.double_stream_weights(w, 0, 0), G.double_stream_weights(w, 0, 1)
+    bw = gpu.BlockWeights(gpu.BLOCK_DOUBLE, txt=double_weights_dev(wt, w.dtype), img=double_weights_dev(wi, w.dtype))
+    q, k = _run_block_qk(gpu, w, x, pos, n_txt, bw)
+    rq, rk = oracle.block_qk(x, pos, n_txt, wt, wi, w.H)
+    assert_close(q, rq.reshape(len(x), -1), w.dtype, "probe q")
+    assert_close(k, rk.reshape(len(x), -1), w.dtype, "probe k")
+    # The probe's q and k give the block's own attention normaliser.
+    _, lse = _run_double(gpu, w, x, pos, n_txt, wt, wi)
+    assert_close(lse, oracle.joint_lse(rq, rk), w.dtype, "block lse vs probe")
+
+
+@pytest.mark.parametrize("n_txt,n_img", [(40, 0), (0, 77), (1, 1), (129, 130)])
+def test_block_qk_probe_degenerate_streams(gpu, n_txt, n_img):
+    w = C.TINY_BF16
+    x, pos = _block_inputs(w, n_txt, n_img, seed=7 + n_txt)
+    wt, wi = G.double_stream_weights(w, 0, 0), G.double_stream_weights(w, 0, 1)
+    bw = gpu.BlockWeights(gpu.BLOCK_DOUBLE, txt=double_weights_dev(wt, w.dtype), img=double_weights_dev(wi, w.dtype))
+    q, k = _run_block_qk(gpu, w, x, pos, n_txt, bw)
+    rq, rk = oracle.block_qk(x, pos, n_txt, wt, wi, w.H)
+    assert_close(q, rq.reshape(len(x), -1), "bf16", "probe q")
+    assert_close(k, rk.reshape(len(x), -1), "bf16", "probe k")
+
+
+@pytest.mark.parametrize("w", [C.TINY_F32, C.TINY_BF16], ids=["f32", "bf16"])
+def test_block_qk_probe_single(gpu, w):
+    x, pos = _block_inputs(w, w.L, w.k, seed=11)
+    ws = G.single_block_weights(w, 0)
+    bw = gpu.BlockWeights(gpu.BLOCK_SINGLE, single=double_weights_dev(ws, w.dtype))
+    q, k = _run_block_qk(gpu, w, x, pos, w.L, bw)
+    rq, rk = oracle.block_qk(x, pos, 0, None, None, w.H, single=ws)
+    assert_close(q, rq.reshape(len(x), -1), w.dtype, "probe q")
+    assert_close(k, rk.reshape(len(x), -1), w.dtype, "probe k")

@@ -285,3 +285,49 @@ def test_single_block_zero_gate_identity():
     ws["mod"][2] = 0.0
     out, _ = oracle.single_block(x, pos, ws, 2)
     np.testing.assert_array_equal(out, x.astype(np.float64))
+
+
+def _brute_qk(x, pos, n_txt, wt, wi, H, wname="w_qkv", bname="b_qkv"):
+    """Per-row scalar statement of the block's first stage: LN + modulation,
+    the q / k projections, RMSNorm and complex-number RoPE."""
+    S, D = len(x), len(x[0])
+    d = D // H
+    Q, K = [], []
+    for i in range(S):
+        w = wt if i < n_txt else wi
+        mod = w["mod"]
+        h = [a * (1 + s) + t for a, s, t in zip(_vec_ln(x[i]), mod[1], mod[0])]
+        t = _matvec(w[wname][:2 * D], w[bname][:2 * D], h)
+        Q.append([v for hq in _heads(t[:D], H, d) for v in _rope_head(_rms(hq, w["g_q"]), pos[i], d)])
+        K.append([v for hk in _heads(t[D:], H, d) for v in _rope_head(_rms(hk, w["g_k"]), pos[i], d)])
+    return np.array(Q).reshape(S, H, d), np.array(K).reshape(S, H, d)
+
+
+def test_block_qk_matches_scalar_bruteforce():
+    x, pos = _tiny_inputs()
+    wt = generator.double_stream_weights(_TINY, 0, 0)
+    wi = generator.double_stream_weights(_TINY, 0, 1)
+    q, k = oracle.block_qk(x, pos, 2, wt, wi, 2)
+    rq, rk = _brute_qk(x.astype(float).tolist(), pos.tolist(), 2, _lists(wt), _lists(wi), 2)
+    np.testing.assert_allclose(q, rq, atol=1e-12)
+    np.testing.assert_allclose(k, rk, atol=1e-12)
+    ws = generator.single_block_weights(_TINY, 0)
+    q, k = oracle.block_qk(x, pos, 0, None, None, 2, single=ws)
+    rq, rk = _brute_qk(x.astype(float).tolist(), pos.tolist(), 0, _lists(ws), _lists(ws), 2, "w_in", "b_in")
+    np.testing.assert_allclose(q, rq, atol=1e-12)
+    np.testing.assert_allclose(k, rk, atol=1e-12)
+
+
+def test_block_qk_softmax_normaliser_is_the_blocks():
+    # The probe's queries and keys give exactly the block's attention LSE, and
+    # with every position zero the rotation drops out (pure RMSNorm * g rows).
+    w = _TINY.replace(D=128, H=2, d=64, mlp_ratio=4)
+    x = generator.block_input(w, 9)
+    pos = np.stack([np.zeros(9), np.arange(9) % 3, np.arange(9) // 3], axis=1).astype(np.int32)
+    wt, wi = generator.double_stream_weights(w, 0, 0), generator.double_stream_weights(w, 0, 1)
+    q, k = oracle.block_qk(x, pos, 4, wt, wi, 2)
+    _, lse = oracle.double_block(x, pos, 4, wt, wi, 2)
+    np.testing.assert_allclose(oracle.joint_lse(q, k), lse, atol=1e-12)
+    q0, _ = oracle.block_qk(x, np.zeros_like(pos), 4, wt, wi, 2)
+    g = np.stack([np.asarray(wt["g_q"], float)] * 4 + [np.asarray(wi["g_q"], float)] * 5)[:, None, :]
+    np.testing.assert_allclose(np.sqrt(((q0 / g) ** 2).mean(-1)), np.ones((9, 2)), atol=1e-6)
