@@ -142,6 +142,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
         }
     }
     // Online softmax in the log2 domain; a row lives in lanes l32 and l32 + 32.
+    // exp2 is the hardware instruction (about 1 ulp; results below 2^-126
+    // flush to zero, far below what a sum of at least one term of size 1 can
+    // register).
     // The running max is raised only when the tile max exceeds it by more
     // than 8 (a factor 256), so most tiles skip the rescale of the output
     // accumulators; exponents stay <= 2^8, exact in the fp32 sums and
@@ -155,7 +158,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
     const bool raise = mx > mrow + 8.f;
     float corr = 1.f;
     if (raise) {
-      corr = exp2f(mrow - mx);
+      corr = __builtin_amdgcn_exp2f(mrow - mx);
       mrow = mx;
     }
     float ls = 0.f;
@@ -163,7 +166,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
     for (int t = 0; t < kKT / 32; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = exp2f(fmaf(s[t][r], scale2, -mrow));
+        const float e = __builtin_amdgcn_exp2f(fmaf(s[t][r], scale2, -mrow));
         s[t][r] = e;
         ls += e;
       }

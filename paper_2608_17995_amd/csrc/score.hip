@@ -11,8 +11,8 @@
 //  2. combine: A_i = mean_h P[h, i], V_i = sum_h Q[h, i] / (2 D_f) (fp32: the
 //     variance is streamed here), plus one min/max partial of A and V per
 //     workgroup.
-//  3. finalize: every workgroup reduces the same partials in the same order
-//     (deterministic global min/max) and writes S for its slice of rows.
+//  3. finalize: every workgroup reduces the same partials (min and max are
+//     exact in any order) and writes S for its slice of rows.
 #include "common.h"
 
 namespace avits {
@@ -28,21 +28,24 @@ constexpr float kLog2e = 1.4426950408889634f;
 //
 // Workgroup = (128 image rows, head h), 4 waves x 32 rows.  Spatial part:
 // S^T = K Q^T on v_mfma_f32_32x32x16_bf16 (lane = one query row, 16 keys per
-// 32-key sub-tile), text-key tiles of 64 staged in LDS with the next tile
-// prefetched into registers; exp2(logit - lse) summed per row.
+// 32-key sub-tile), text-key tiles of 64 double-buffered in LDS with the next
+// tile prefetched into registers (one barrier per tile); exp2(logit - lse)
+// summed per row.
 // Temporal part: the workgroup streams channel slice [h D_f / H, (h+1) D_f / H)
-// of both feature rows of its 128 rows, so the 2 N D_f-element stream is spread
-// over every workgroup and overlaps the MFMA work; per-(head, row) partial sums
-// of squared differences go to part_v.
+// of both feature rows of its 128 rows, one (row, 16-byte chunk) pair per lane
+// per key tile, software-pipelined: the pair consumed in tile t was loaded
+// during tile t - 1, so the 2 N D_f-element stream is in flight while the
+// MFMAs run; per-(head, row) partial sums of squared differences go to
+// part_v.
 template <int DH>
-__global__ __launch_bounds__(256) void spatial_temporal_bf16_kernel(
+__global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ ktxt, const float* __restrict__ lse,
     const bf16_t* __restrict__ ft, const bf16_t* __restrict__ fp, int N, int L, int H, int64_t Df,
     float* __restrict__ part_a, float* __restrict__ part_v) {
   constexpr int kC = DH / 16;                 // 16-wide head-dim chunks (MFMA k)
   constexpr int kLds = DH + 8;                // padded LDS row (bf16 elements)
   constexpr int kKP = kSpKeys * DH / 8 / 256; // 16-byte K pieces per thread per tile
-  __shared__ __attribute__((aligned(16))) bf16_t ks[kSpKeys * kLds];
+  __shared__ __attribute__((aligned(16))) bf16_t ks[2][kSpKeys * kLds];
 
   const int h = blockIdx.y;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
@@ -51,30 +54,142 @@ __global__ __launch_bounds__(256) void spatial_temporal_bf16_kernel(
   const int row = wrow0 + l32;
   const int64_t qstride = int64_t(H) * DH;
 
-  // ---- temporal slice (issued first: its loads overlap the MFMA work) ----
+  // ---- temporal slice: lane pairs j = 0 .. npairs - 1 cover row
+  // wrow0 + j rpi + lane / nch, chunk lane % nch (rpi = 64 / nch rows per
+  // instruction). ----
   const int64_t c0 = Df * h / H, c1 = Df * (h + 1) / H;
   const int64_t nch = (c1 - c0) / 8;  // 16-byte chunks per row in the slice
   const bool vec = (c0 % 8 == 0) && ((c1 - c0) % 8 == 0) && nch > 0 && nch <= 64 && (64 % nch == 0);
-  if (vec) {
-    const int rpi = int(64 / nch);               // rows per 64-lane instruction
-    const int r_in = lane / int(nch), cc = lane % int(nch);
-    for (int r0 = 0; r0 < 32; r0 += rpi) {
-      const int rr = wrow0 + r0 + r_in;
-      float acc = 0.f;
-      if (rr < N) {
-        const u32x4 x = *reinterpret_cast<const u32x4*>(ft + int64_t(rr) * Df + c0 + 8 * cc);
-        const u32x4 y = *reinterpret_cast<const u32x4*>(fp + int64_t(rr) * Df + c0 + 8 * cc);
+  const int rpi = vec ? int(64 / nch) : 1;
+  const int npairs = vec ? int(32 / rpi) : 0;
+  const int r_in = vec ? lane / int(nch) : 0, cc = vec ? lane % int(nch) : 0;
+  auto issue_pair = [&](int j, u32x4& x, u32x4& y) {
+    x = u32x4{0u, 0u, 0u, 0u};
+    y = x;
+    const int rr = wrow0 + j * rpi + r_in;
+    if (j < npairs && rr < N) {
+      x = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ft + int64_t(rr) * Df + c0 + 8 * cc));
+      y = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(fp + int64_t(rr) * Df + c0 + 8 * cc));
+    }
+  };
+  auto consume_pair = [&](int j, const u32x4& x, const u32x4& y) {
+    if (j >= npairs) return;  // uniform across the wave
+    float acc = 0.f;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float d0 = __uint_as_float(x[e] << 16) - __uint_as_float(y[e] << 16);
-          const float d1 = __uint_as_float(x[e] & 0xffff0000u) - __uint_as_float(y[e] & 0xffff0000u);
-          acc = fmaf(d0, d0, fmaf(d1, d1, acc));
+    for (int e = 0; e < 4; ++e) {
+      const float d0 = __uint_as_float(x[e] << 16) - __uint_as_float(y[e] << 16);
+      const float d1 = __uint_as_float(x[e] & 0xffff0000u) - __uint_as_float(y[e] & 0xffff0000u);
+      acc = fmaf(d0, d0, fmaf(d1, d1, acc));
+    }
+    for (int o = 1; o < nch; o <<= 1) acc += __shfl_xor(acc, o, kWave);
+    const int rr = wrow0 + j * rpi + r_in;
+    if (cc == 0 && rr < N) part_v[int64_t(h) * N + rr] = acc;
+  };
+  u32x4 cx, cy, nx, ny;  // pair in flight for this tile, pair for the next
+  issue_pair(0, cx, cy);
+
+  // ---- spatial: Q^T fragments (B operand), lane = row l32, dims 16c + 8hi .. +7 ----
+  bf16x8 qf[kC];
+  {
+    const bf16_t* src = q + int64_t(min(row, N - 1)) * qstride + int64_t(h) * DH + 8 * hi;
+#pragma unroll
+    for (int c = 0; c < kC; ++c)
+      qf[c] = as_bf16x8(__builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + 16 * c)));
+  }
+  const float lse2 = row < N ? lse[int64_t(h) * N + row] * kLog2e : 0.f;
+  const float scale2 = kLog2e * rsqrtf(float(DH));
+  float psum = 0.f;
+
+  // Text keys: tile t + 2 is loaded into registers while tile t is
+  // multiplied and stored to LDS at the end of tile t + 1 (two LDS buffers,
+  // two register sets, one barrier per tile), so a key load has two tiles of
+  // work to arrive in.
+  auto load_k = [&](u32x4 (&kr)[kKP], int k0) {
+#pragma unroll
+    for (int j = 0; j < kKP; ++j) {
+      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
+      const int krow = min(k0 + key, L - 1);
+      kr[j] = *reinterpret_cast<const u32x4*>(ktxt + (int64_t(krow) * H + h) * DH + col);
+    }
+  };
+  auto store_k = [&](const u32x4 (&kr)[kKP], int buf) {
+#pragma unroll
+    for (int j = 0; j < kKP; ++j) {
+      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
+      *reinterpret_cast<u32x4*>(&ks[buf][key * kLds + col]) = kr[j];
+    }
+  };
+  int jt = 0;  // key tiles done = temporal pairs consumed
+  // One key tile from ks[buf] at k0; knext1 holds tile k0 + 64 (in flight),
+  // knext2 receives tile k0 + 128.
+  auto tile = [&](int buf, int k0, u32x4 (&knext2)[kKP], const u32x4 (&knext1)[kKP]) {
+    if (k0 + 2 * kSpKeys < L) load_k(knext2, k0 + 2 * kSpKeys);
+    issue_pair(jt + 1, nx, ny);
+    const bool full = k0 + kSpKeys <= L;
+#pragma unroll
+    for (int t = 0; t < kSpKeys / 32; ++t) {
+      f32x16 acc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+      for (int c = 0; c < kC; ++c) {
+        const bf16x8 kf =
+            as_bf16x8(*reinterpret_cast<const u32x4*>(&ks[buf][(32 * t + l32) * kLds + 16 * c + 8 * hi]));
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], acc, 0, 0, 0);
+      }
+      // acc[r] = logit of key 32t + 8(r/4) + 4hi + r%4 against this lane's
+      // row.  exp2 is the hardware instruction (about 1 ulp; terms below
+      // 2^-126 flush to zero); only the last tile masks keys past L.
+      if (full) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) psum += __builtin_amdgcn_exp2f(fmaf(acc[r], scale2, -lse2));
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
+          const float e = __builtin_amdgcn_exp2f(fmaf(acc[r], scale2, -lse2));
+          psum += key < L ? e : 0.f;
         }
       }
-      for (int o = 1; o < nch; o <<= 1) acc += __shfl_xor(acc, o, kWave);
-      if (cc == 0 && rr < N) part_v[int64_t(h) * N + rr] = acc;
     }
-  } else {
+    consume_pair(jt, cx, cy);
+    cx = nx;
+    cy = ny;
+    ++jt;
+    // The other buffer was last read one tile ago, before the barrier that
+    // ended that tile, so it can be refilled now.
+    if (k0 + kSpKeys < L) store_k(knext1, buf ^ 1);
+    __syncthreads();
+  };
+  u32x4 ka[kKP], kb[kKP];
+  load_k(ka, 0);
+  if (kSpKeys < L) load_k(kb, kSpKeys);
+  store_k(ka, 0);
+  __syncthreads();
+  for (int k0 = 0; k0 < L; k0 += 2 * kSpKeys) {
+    tile(0, k0, ka, kb);
+    if (k0 + kSpKeys >= L) break;
+    tile(1, k0 + kSpKeys, kb, ka);
+  }
+  psum += __shfl_xor(psum, 32, kWave);
+  if (hi == 0 && row < N) part_a[int64_t(h) * N + row] = psum;
+  // Pairs left when the slice has more pairs than there are key tiles
+  // (cx, cy hold pair jt, in flight): issued in batches so their loads
+  // overlap instead of waiting one after another.
+  constexpr int kBatch = 8;
+  while (jt < npairs) {
+    u32x4 bx[kBatch], by[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) issue_pair(jt + 1 + u, bx[u], by[u]);
+    consume_pair(jt, cx, cy);
+#pragma unroll
+    for (int u = 0; u < kBatch - 1; ++u) consume_pair(jt + 1 + u, bx[u], by[u]);
+    cx = bx[kBatch - 1];
+    cy = by[kBatch - 1];
+    jt += kBatch;
+  }
+
+  if (!vec) {
     for (int r = 0; r < 32; ++r) {
       const int rr = wrow0 + r;
       if (rr >= N) break;
@@ -87,62 +202,13 @@ __global__ __launch_bounds__(256) void spatial_temporal_bf16_kernel(
       if (lane == 0) part_v[int64_t(h) * N + rr] = acc;
     }
   }
-
-  // ---- spatial: Q^T fragments (B operand), lane = row l32, dims 16c + 8hi .. +7 ----
-  bf16x8 qf[kC];
-  {
-    const bf16_t* src = q + int64_t(min(row, N - 1)) * qstride + int64_t(h) * DH + 8 * hi;
-#pragma unroll
-    for (int c = 0; c < kC; ++c) qf[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + 16 * c));
-  }
-  const float lse2 = row < N ? lse[int64_t(h) * N + row] * kLog2e : 0.f;
-  const float scale2 = kLog2e * rsqrtf(float(DH));
-  float psum = 0.f;
-
-  u32x4 kreg[kKP];
-  auto load_k = [&](int k0) {
-#pragma unroll
-    for (int j = 0; j < kKP; ++j) {
-      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
-      const int kr = min(k0 + key, L - 1);
-      kreg[j] = *reinterpret_cast<const u32x4*>(ktxt + (int64_t(kr) * H + h) * DH + col);
-    }
-  };
-  load_k(0);
-  for (int k0 = 0; k0 < L; k0 += kSpKeys) {
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kKP; ++j) {
-      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
-      *reinterpret_cast<u32x4*>(&ks[key * kLds + col]) = kreg[j];
-    }
-    __syncthreads();
-    if (k0 + kSpKeys < L) load_k(k0 + kSpKeys);
-#pragma unroll
-    for (int t = 0; t < kSpKeys / 32; ++t) {
-      f32x16 acc;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-#pragma unroll
-      for (int c = 0; c < kC; ++c) {
-        const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(&ks[(32 * t + l32) * kLds + 16 * c + 8 * hi]));
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], acc, 0, 0, 0);
-      }
-      // acc[r] = logit of key 32t + 8(r/4) + 4hi + r%4 against this lane's row.
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
-        const float e = exp2f(acc[r] * scale2 - lse2);
-        psum += key < L ? e : 0.f;
-      }
-    }
-  }
-  psum += __shfl_xor(psum, 32, kWave);
-  if (hi == 0 && row < N) part_a[int64_t(h) * N + row] = psum;
 }
 
-// 1b. bf16: per row, A = mean_h part_a, V = sum_h part_v / (2 D_f); one
-// min/max partial of A and V per 64-row workgroup.
+// 1b. bf16: per row, A = mean_h part_a, V = sum_h part_v / (2 D_f), with
+// every head's load in flight at once; one min/max partial of A and V per
+// 64-row workgroup.
+constexpr int kCombineHeads = 32;  // heads summed with every load issued up front
+
 __global__ __launch_bounds__(64) void combine_kernel(const float* __restrict__ part_a,
                                                      const float* __restrict__ part_v, int64_t N, int H, int64_t Df,
                                                      float* __restrict__ a_out, float* __restrict__ v_out,
@@ -151,10 +217,23 @@ __global__ __launch_bounds__(64) void combine_kernel(const float* __restrict__ p
   float amin = INFINITY, amax = -INFINITY, vmin = INFINITY, vmax = -INFINITY;
   if (i < N) {
     float sa = 0.f, sv = 0.f;
-#pragma unroll 8
-    for (int h = 0; h < H; ++h) {
-      sa += part_a[int64_t(h) * N + i];
-      sv += part_v[int64_t(h) * N + i];
+    if (H <= kCombineHeads) {
+      float pa[kCombineHeads], pv[kCombineHeads];
+#pragma unroll
+      for (int h = 0; h < kCombineHeads; ++h) {
+        pa[h] = h < H ? part_a[int64_t(h) * N + i] : 0.f;
+        pv[h] = h < H ? part_v[int64_t(h) * N + i] : 0.f;
+      }
+#pragma unroll
+      for (int h = 0; h < kCombineHeads; ++h) {
+        sa += pa[h];
+        sv += pv[h];
+      }
+    } else {
+      for (int h = 0; h < H; ++h) {
+        sa += part_a[int64_t(h) * N + i];
+        sv += part_v[int64_t(h) * N + i];
+      }
     }
     const float A = sa / float(H), V = sv / (2.f * float(Df));
     a_out[i] = A;
