@@ -131,6 +131,40 @@ def _cpu_baseline(w, host, row_lse, wt, wi):
                       f"in fp64 NumPy on the host; {os.cpu_count()} CPUs visible"}
 
 
+def _select_sweep(avits, torch, reps: int = 10) -> list:
+    """Top-k selection beyond the step's N: k = 0.3 N of N scores drawn as
+    u^(1/4) (u uniform; the top exponent bits coincide, as for min-max
+    normalised scores).  Above 16384 scores the selection makes six streaming
+    passes over them (four digit histograms, count, emit); `hbm_gbs` counts
+    those reads plus the 4k-byte index write."""
+    out = []
+    for lg in (14, 20, 22, 24, 26):
+        N = 1 << lg
+        k = int(0.3 * N + 0.5)
+        g = torch.Generator(device="cuda")
+        g.manual_seed(lg)
+        s = torch.rand(N, device="cuda", generator=g) ** 0.25
+        idx = torch.empty(k, dtype=torch.int32, device="cuda")
+        ws = torch.empty(max(avits.avits_select_workspace_bytes(N), 1), dtype=torch.uint8, device="cuda")
+        for _ in range(2):
+            avits.avits_select(s, k, idx, workspace=ws)
+        torch.cuda.synchronize()
+        avits.avits_timing_reset()
+        avits.avits_timing_enable(True)
+        for _ in range(reps):
+            avits.avits_select(s, k, idx, workspace=ws)
+        torch.cuda.synchronize()
+        avits.avits_timing_enable(False)
+        ms, n = avits.avits_timing_read("select")
+        t = ms / n / 1e3
+        passes = 1 if N <= 16384 else 6
+        gbs = (passes * 4 * N + 4 * k) / t / 1e9
+        out.append({"N": N, "k": k, "us": round(t * 1e6, 1), "passes": passes, "hbm_gbs": round(gbs, 1),
+                    "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)})
+        del s, idx, ws
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -323,6 +357,7 @@ def main(argv=None):
         "input_generation_s": round(t_gen, 1),
         "copy_calibration_ms": None if copy_ms is None else round(copy_ms, 4),
     }
+    result["select_sweep"] = _select_sweep(avits, torch)
     if not args.no_cpu_baseline:
         host = dict(si)
         host.update(lay)

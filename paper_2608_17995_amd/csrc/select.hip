@@ -9,9 +9,10 @@
 // indices win), so the output is ascending and independent of atomic order:
 // the only atomics are histogram increments, whose sums are order-free.
 //
-// One 1024-thread workgroup does the whole selection: at the sizes of a
-// resolution transition (N = 4096 .. 16384 scores, 16-64 KiB) the cost is
-// latency, not bandwidth; the scores stay in L2 between passes.
+// Up to N = 16384 one 1024-thread workgroup does the whole selection: at the
+// sizes of a resolution transition (N = 4096 .. 16384 scores, 16-64 KiB) the
+// cost is latency, not bandwidth, and the keys stay in registers between
+// passes.  Larger N runs the same passes grid-wide (below).
 #include "common.h"
 
 namespace avits {
@@ -25,6 +26,12 @@ __device__ __forceinline__ uint32_t order_key(float f) {
   if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;  // NaN ranks lowest
   if (u == 0x80000000u) u = 0u;                     // -0.0 == +0.0
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) v += __shfl_xor(v, o, kWave);
+  return v;
 }
 
 // Exclusive prefix sum over the workgroup; returns the total in *total.
@@ -49,26 +56,19 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
   return before + incl - v;
 }
 
-// Up to kRegKeys keys per thread stay in registers (N <= 16384); larger N
-// re-reads the scores (L2-resident) on every pass.
+// kRegKeys keys per thread stay in registers: N <= 16384.
 constexpr int kRegKeys = 16;
 
-// Calls f(j, i, key) for every element i = tid + kThreads * j < N.
-template <bool IN_REGS, typename F>
-__device__ __forceinline__ void for_each_key(const uint32_t (&keys)[IN_REGS ? kRegKeys : 1],
-                                             const float* __restrict__ scores, int N, F&& f) {
-  if constexpr (IN_REGS) {
+// Calls f(i, key) for every element i = tid + kThreads * j < N.
+template <typename F>
+__device__ __forceinline__ void for_each_key(const uint32_t (&keys)[kRegKeys], int N, F&& f) {
 #pragma unroll
-    for (int j = 0; j < kRegKeys; ++j) {
-      const int i = threadIdx.x + kThreads * j;
-      if (i < N) f(i, keys[j]);
-    }
-  } else {
-    for (int i = threadIdx.x; i < N; i += kThreads) f(i, order_key(scores[i]));
+  for (int j = 0; j < kRegKeys; ++j) {
+    const int i = threadIdx.x + kThreads * j;
+    if (i < N) f(i, keys[j]);
   }
 }
 
-template <bool IN_REGS>
 __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __restrict__ scores, int N, int k,
                                                                 int32_t* __restrict__ idx) {
   __shared__ uint32_t hist[kWaves][256];   // per-wave histograms: atomics contend only inside a wave
@@ -77,13 +77,11 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
   __shared__ uint32_t s_digit, s_above;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
 
-  uint32_t keys[IN_REGS ? kRegKeys : 1] = {};
-  if constexpr (IN_REGS) {
+  uint32_t keys[kRegKeys];
 #pragma unroll
-    for (int j = 0; j < kRegKeys; ++j) {
-      const int i = tid + kThreads * j;
-      keys[j] = i < N ? order_key(scores[i]) : 0u;
-    }
+  for (int j = 0; j < kRegKeys; ++j) {
+    const int i = tid + kThreads * j;
+    keys[j] = i < N ? order_key(scores[i]) : 0u;
   }
 
   uint32_t prefix = 0u, mask = 0u;
@@ -91,7 +89,7 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int b = tid; b < kWaves * 256; b += kThreads) (&hist[0][0])[b] = 0u;
     __syncthreads();
-    for_each_key<IN_REGS>(keys, scores, N, [&](int, uint32_t key) {
+    for_each_key(keys, N, [&](int, uint32_t key) {
       if ((key & mask) == prefix) atomicAdd(&hist[wave][(key >> shift) & 255u], 1u);
     });
     __syncthreads();
@@ -154,17 +152,310 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
     out_before += gt_tot + min(eq_tot, eq_quota);
     eq_before += eq_tot;
   };
-  if constexpr (IN_REGS) {
 #pragma unroll
-    for (int j = 0; j < kRegKeys; ++j)
-      if (j < nchunks) emit_chunk(tid + kThreads * j, keys[j]);
+  for (int j = 0; j < kRegKeys; ++j)
+    if (j < nchunks) emit_chunk(tid + kThreads * j, keys[j]);
+}
+
+// ---------------------------------------------------------------------------
+// Grid-wide radix select for N above what one workgroup holds in registers:
+// the same four digit passes and index-order emission, spread over the GPU.
+//   init            state: prefix 0, need k, histograms zeroed
+//   4 x hist, scan  every workgroup histograms the current digit of the keys
+//                   that match the prefix (LDS, then one atomic per bin: the
+//                   sums are order-free); one workgroup picks the digit
+//   count           per 4096-element chunk: keys > T and keys == T
+//   offsets         one workgroup scans the chunk counts in index order:
+//                   each chunk's output offset and its quota of keys == T
+//   emit            each chunk writes its selected indices in index order
+// Scores are read with 16-byte loads; every pass streams them once.
+constexpr int kGT = 256;               // threads per workgroup of the grid passes
+constexpr int kGWaves = kGT / kWave;
+constexpr int kHistBlocks = 2048;      // histogram workgroups (grid-stride)
+constexpr int kChunk = 16 * kGT;       // elements per count / emit workgroup (16 per thread)
+
+struct SelState {
+  uint32_t prefix;                     // digits chosen so far, in place
+  uint32_t need;                       // rank of the k-th largest among keys matching the prefix
+  uint32_t pad[62];
+  uint32_t hist[4][256];               // global digit histograms, one per pass
+};
+
+__global__ __launch_bounds__(kGT) void select_init_kernel(SelState* __restrict__ st, uint32_t k) {
+  for (int b = threadIdx.x; b < 4 * 256; b += kGT) (&st->hist[0][0])[b] = 0u;
+  if (threadIdx.x == 0) {
+    st->prefix = 0u;
+    st->need = k;
+  }
+}
+
+// Keys of elements i0 .. i0 + 3; live[e] is false past the end of the scores.
+__device__ __forceinline__ void load_keys4(const float* __restrict__ scores, int64_t N, int64_t i0, uint32_t (&key)[4],
+                                           bool (&live)[4]) {
+  if (i0 + 3 < N && (reinterpret_cast<uintptr_t>(scores + i0) & 15) == 0) {
+    const float4 v = *reinterpret_cast<const float4*>(scores + i0);
+    key[0] = order_key(v.x); key[1] = order_key(v.y); key[2] = order_key(v.z); key[3] = order_key(v.w);
+    live[0] = live[1] = live[2] = live[3] = true;
   } else {
-    for (int j = 0; j < nchunks; ++j) {
-      const int i = tid + kThreads * j;
-      emit_chunk(i, i < N ? order_key(scores[i]) : 0u);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      live[e] = i0 + e < N;
+      key[e] = live[e] ? order_key(scores[i0 + e]) : 0u;
     }
   }
 }
+
+constexpr int kSubHist = 4;  // LDS histogram copies per wave (lane % 4): spreads atomics on one bin
+
+__global__ __launch_bounds__(kGT) void select_hist_kernel(const float* __restrict__ scores, int64_t N, int pass,
+                                                          SelState* __restrict__ st) {
+  __shared__ uint32_t hs[kGWaves * kSubHist][256];
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  uint32_t* h = hs[wave * kSubHist + (lane & (kSubHist - 1))];
+  for (int b = tid; b < kGWaves * kSubHist * 256; b += kGT) (&hs[0][0])[b] = 0u;
+  __syncthreads();
+  const int shift = 24 - 8 * pass;
+  const uint32_t mask = pass ? 0xffffffffu << (32 - 8 * pass) : 0u;
+  const uint32_t prefix = st->prefix & mask;
+  // The top digit of similar scores coincides (one exponent covers most of a
+  // min-max-normalised score range), so in the first pass a wave adds its two
+  // most frequent-looking digits with one atomic each (ballot) before the
+  // remaining lanes add one by one; later passes, whose digits are spread,
+  // aggregate only one (which also bounds the cost of heavily tied scores).
+  const int rounds = pass == 0 ? 2 : 1;
+  auto count = [&](uint32_t key, bool ok) {
+    bool pending = ok && (key & mask) == prefix;
+    const uint32_t digit = (key >> shift) & 255u;
+    for (int it = 0; it < rounds; ++it) {
+      const uint64_t act = __ballot(pending);
+      if (act == 0) break;
+      const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
+      const uint32_t d0 = __shfl(digit, leader, kWave);
+      const uint64_t same = __ballot(pending && digit == d0);
+      if (lane == leader) atomicAdd(&h[d0], uint32_t(__popcll(same)));
+      pending = pending && digit != d0;
+    }
+    if (pending) atomicAdd(&h[digit], 1u);
+  };
+  const int64_t groups = (N + 3) / 4;
+  for (int64_t g = int64_t(blockIdx.x) * kGT + tid; g - tid < groups; g += int64_t(gridDim.x) * kGT) {
+    uint32_t key[4];
+    bool live[4];
+    load_keys4(scores, N, 4 * g, key, live);  // past the end: live = false
+#pragma unroll
+    for (int e = 0; e < 4; ++e) count(key[e], live[e]);
+  }
+  __syncthreads();
+  for (int b = tid; b < 256; b += kGT) {
+    uint32_t c = 0u;
+#pragma unroll
+    for (int w = 0; w < kGWaves * kSubHist; ++w) c += hs[w][b];
+    if (c) atomicAdd(&st->hist[pass][b], c);
+  }
+}
+
+// One workgroup: the digit b of this pass with (matching keys above b) <
+// need <= (matching keys at or above b).
+__global__ __launch_bounds__(256) void select_scan_kernel(int pass, SelState* __restrict__ st) {
+  __shared__ uint32_t wsum[4];
+  const int b = threadIdx.x, wave = b / kWave, lane = b % kWave;
+  const uint32_t c = st->hist[pass][b];
+  uint32_t suf = c;  // suffix sum inside the wave, high lanes down
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t t = __shfl_down(suf, o, kWave);
+    if (lane + o < kWave) suf += t;
+  }
+  if (lane == 0) wsum[wave] = suf;
+  __syncthreads();
+  uint32_t higher = 0u;
+  for (int w = wave + 1; w < 4; ++w) higher += wsum[w];
+  const uint32_t above = suf - c + higher, need = st->need;
+  __syncthreads();
+  if (above < need && above + c >= need) {
+    st->prefix |= uint32_t(b) << (24 - 8 * pass);
+    st->need = need - above;
+  }
+}
+
+// Sixteen consecutive elements of thread t of chunk `chunk`: t * 16 ..
+__device__ __forceinline__ void chunk_keys(const float* __restrict__ scores, int64_t N, int64_t i0, uint32_t (&key)[16],
+                                           bool (&live)[16]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint32_t k4[4];
+    bool l4[4];
+    load_keys4(scores, N, i0 + 4 * q, k4, l4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      key[4 * q + e] = k4[e];
+      live[4 * q + e] = l4[e];
+    }
+  }
+}
+
+// Exclusive scan over a kGT-thread workgroup; *total gets the sum.
+__device__ __forceinline__ uint32_t grid_block_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  uint32_t incl = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t t = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += t;
+  }
+  __syncthreads();
+  if (lane == kWave - 1) wsum[wave] = incl;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < kGWaves; ++w) {
+    before += w < wave ? wsum[w] : 0u;
+    all += wsum[w];
+  }
+  *total = all;
+  return before + incl - v;
+}
+
+__global__ __launch_bounds__(kGT) void select_count_kernel(const float* __restrict__ scores, int64_t N,
+                                                           const SelState* __restrict__ st,
+                                                           uint32_t* __restrict__ cnt) {
+  __shared__ uint32_t wsum[kGWaves];
+  const uint32_t T = st->prefix;
+  const int64_t i0 = int64_t(blockIdx.x) * kChunk + 16 * threadIdx.x;
+  uint32_t key[16];
+  bool live[16];
+  chunk_keys(scores, N, i0, key, live);
+  uint32_t packed = 0u;  // keys > T in the high 16 bits, keys == T in the low
+#pragma unroll
+  for (int e = 0; e < 16; ++e) packed += live[e] ? ((key[e] > T) << 16) | uint32_t(key[e] == T) : 0u;
+  uint32_t tot;
+  grid_block_scan(packed, wsum, &tot);
+  if (threadIdx.x == 0) {
+    cnt[2 * blockIdx.x] = tot >> 16;
+    cnt[2 * blockIdx.x + 1] = tot & 0xffffu;
+  }
+}
+
+// One workgroup of 1024 threads walks the chunks in index order, four
+// consecutive chunks per thread per step (two 16-byte loads), with two
+// block-wide scans per step: every chunk's quota of keys == T (the first
+// `need` of them in index order) and its output offset.
+__global__ __launch_bounds__(kThreads) void select_offsets_kernel(const uint32_t* __restrict__ cnt, int nchunks,
+                                                                  const SelState* __restrict__ st,
+                                                                  uint32_t* __restrict__ off) {
+  constexpr int kPer = 4;
+  __shared__ uint32_t wsum[kWaves];
+  const uint32_t need = st->need;
+  uint32_t eq_before = 0u, out_before = 0u;
+  for (int c0 = 0; c0 < nchunks; c0 += kThreads * kPer) {
+    const int cb = c0 + kPer * threadIdx.x;
+    uint32_t gt[kPer], eq[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      gt[j] = cb + j < nchunks ? cnt[2 * (cb + j)] : 0u;
+      eq[j] = cb + j < nchunks ? cnt[2 * (cb + j) + 1] : 0u;
+    }
+    const uint32_t eq_run = eq[0] + eq[1] + eq[2] + eq[3];
+    uint32_t eq_tot;
+    uint32_t eb = eq_before + block_exclusive_scan(eq_run, wsum, &eq_tot);
+    uint32_t take[kPer], sel_run = 0u;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      take[j] = eb < need ? min(eq[j], need - eb) : 0u;
+      eb += eq[j];
+      sel_run += gt[j] + take[j];
+    }
+    uint32_t sel_tot;
+    uint32_t ob = out_before + block_exclusive_scan(sel_run, wsum, &sel_tot);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      if (cb + j < nchunks) {
+        off[2 * (cb + j)] = ob;
+        off[2 * (cb + j) + 1] = take[j];
+      }
+      ob += gt[j] + take[j];
+    }
+    eq_before += eq_tot;
+    out_before += sel_tot;
+  }
+}
+
+// Chunk = 4 waves x 4 rounds x 256 consecutive elements (4 per lane, one
+// 16-byte load).  Counts per wave first (keys stay in registers), a 4-entry
+// scan in LDS, then each round ranks its lanes with a wave scan, so
+// neighbouring lanes store neighbouring output positions.
+__global__ __launch_bounds__(kGT) void select_emit_kernel(const float* __restrict__ scores, int64_t N,
+                                                          const SelState* __restrict__ st,
+                                                          const uint32_t* __restrict__ off, int64_t k,
+                                                          int32_t* __restrict__ idx) {
+  constexpr int kRounds = kChunk / kGT / 4;  // 4
+  __shared__ uint32_t wcnt[kGWaves];
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const uint32_t T = st->prefix;
+  const int64_t w0 = int64_t(blockIdx.x) * kChunk + int64_t(wave) * kRounds * 4 * kWave;
+  uint32_t key[kRounds][4];
+  bool live[kRounds][4];
+  uint32_t packed = 0u;  // keys > T in the high 16 bits, keys == T in the low
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    load_keys4(scores, N, w0 + 4 * (r * kWave + lane), key[r], live[r]);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) packed += live[r][e] ? ((key[r][e] > T) << 16) | uint32_t(key[r][e] == T) : 0u;
+  }
+  packed = wave_sum_u32(packed);
+  if (lane == 0) wcnt[wave] = packed;
+  __syncthreads();
+  uint32_t before = 0u;  // this chunk's keys before this wave, packed
+  for (int w = 0; w < wave; ++w) before += wcnt[w];
+  uint32_t gt_b = before >> 16, eq_b = before & 0xffffu;
+  const uint32_t base = off[2 * blockIdx.x], take = off[2 * blockIdx.x + 1];
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    uint32_t mine = 0u;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) mine += live[r][e] ? ((key[r][e] > T) << 16) | uint32_t(key[r][e] == T) : 0u;
+    uint32_t incl = mine;  // wave inclusive scan of the packed counts
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const uint32_t t = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += t;
+    }
+    const uint32_t ex = incl - mine, all = __shfl(incl, kWave - 1, kWave);
+    uint32_t g = gt_b + (ex >> 16), q = eq_b + (ex & 0xffffu);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool gt = live[r][e] && key[r][e] > T, eq = live[r][e] && key[r][e] == T;
+      const bool sel = gt || (eq && q < take);
+      const uint32_t at = base + g + min(q, take);
+      if (sel && at < uint64_t(k)) idx[at] = int32_t(w0 + 4 * (r * kWave + lane) + e);
+      g += gt;
+      q += eq;
+    }
+    gt_b += all >> 16;
+    eq_b += all & 0xffffu;
+  }
+}
+
+inline size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+struct SelWs {
+  SelState* st;
+  uint32_t* cnt;  // [nchunks][2]
+  uint32_t* off;  // [nchunks][2]
+  size_t bytes;
+};
+SelWs select_ws_layout(char* base, int64_t N) {
+  SelWs w{};
+  const int64_t nchunks = (N + kChunk - 1) / kChunk;
+  size_t o = 0;
+  w.st = reinterpret_cast<SelState*>(base + o); o += align256(sizeof(SelState));
+  w.cnt = reinterpret_cast<uint32_t*>(base + o); o += align256(size_t(nchunks) * 8);
+  w.off = reinterpret_cast<uint32_t*>(base + o); o += align256(size_t(nchunks) * 8);
+  w.bytes = o;
+  return w;
+}
+
+constexpr int64_t kOneBlockMax = int64_t(kThreads) * kRegKeys;  // 16384: one workgroup, keys in registers
 
 }  // namespace
 }  // namespace avits
@@ -172,23 +463,37 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
 using namespace avits;
 
 extern "C" size_t avits_select_workspace_bytes(int64_t N) {
-  (void)N;
-  return 0;
+  if (N <= kOneBlockMax) return 0;
+  return select_ws_layout(nullptr, N).bytes;
 }
 
 extern "C" int avits_select(const float* scores, int64_t N, int64_t k, int32_t* idx, void* workspace,
                             size_t workspace_bytes, void* stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   AVITS_REQUIRE(N >= 1 && N <= INT32_MAX, "select: N=%lld outside [1, 2^31)", (long long)N);
   AVITS_REQUIRE(k >= 0 && k <= N, "select: k=%lld outside [0, N=%lld]", (long long)k, (long long)N);
   if (k == 0) return AVITS_OK;
   AVITS_REQUIRE(scores && idx, "select: null scores/idx");
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (N <= kOneBlockMax) {
+    TimedLaunch timed("select", s);
+    hipLaunchKernelGGL(radix_select_kernel, dim3(1), dim3(kThreads), 0, s, scores, int(N), int(k), idx);
+    return launch_status("select");
+  }
+  const SelWs need = select_ws_layout(nullptr, N);
+  if (!workspace || workspace_bytes < need.bytes)
+    return set_error(AVITS_ERR_WORKSPACE, "select: workspace of %zu bytes, need %zu for N=%lld", workspace_bytes,
+                     need.bytes, (long long)N);
+  const SelWs ws = select_ws_layout(static_cast<char*>(workspace), N);
+  const int nchunks = int((N + kChunk - 1) / kChunk);
+  const int hblocks = int(std::min<int64_t>(kHistBlocks, (N + 4 * kGT * 8 - 1) / (4 * kGT * 8)));
   TimedLaunch timed("select", s);
-  if (N <= int64_t(kThreads) * kRegKeys)
-    hipLaunchKernelGGL(radix_select_kernel<true>, dim3(1), dim3(kThreads), 0, s, scores, int(N), int(k), idx);
-  else
-    hipLaunchKernelGGL(radix_select_kernel<false>, dim3(1), dim3(kThreads), 0, s, scores, int(N), int(k), idx);
+  hipLaunchKernelGGL(select_init_kernel, dim3(1), dim3(kGT), 0, s, ws.st, uint32_t(k));
+  for (int pass = 0; pass < 4; ++pass) {
+    hipLaunchKernelGGL(select_hist_kernel, dim3(hblocks), dim3(kGT), 0, s, scores, N, pass, ws.st);
+    hipLaunchKernelGGL(select_scan_kernel, dim3(1), dim3(256), 0, s, pass, ws.st);
+  }
+  hipLaunchKernelGGL(select_count_kernel, dim3(nchunks), dim3(kGT), 0, s, scores, N, ws.st, ws.cnt);
+  hipLaunchKernelGGL(select_offsets_kernel, dim3(1), dim3(kThreads), 0, s, ws.cnt, nchunks, ws.st, ws.off);
+  hipLaunchKernelGGL(select_emit_kernel, dim3(nchunks), dim3(kGT), 0, s, scores, N, ws.st, ws.off, k, idx);
   return launch_status("select");
 }

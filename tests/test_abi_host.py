@@ -55,6 +55,10 @@ def test_select_validation(lib):
     assert lib.avits_select(None, 10, 0, None, None, 0, None) == 0            # k == 0: no-op
     assert lib.avits_select(None, 10, 3, None, None, 0, None) == INVALID      # null pointers
     assert lib.avits_select_workspace_bytes(4096) == 0
+    need = lib.avits_select_workspace_bytes(20000)              # grid-wide path: state + chunk counts
+    assert need > 0
+    assert lib.avits_select(FAKE, 20000, 5, FAKE, None, need, None) == WORKSPACE
+    assert lib.avits_select(FAKE, 20000, 5, FAKE, FAKE, need - 1, None) == WORKSPACE
 
 
 def _score(lib, **kw):

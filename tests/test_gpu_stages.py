@@ -109,6 +109,57 @@ def test_select_special_values_and_k0(gpu):
     assert raw[0] == -7
 
 
+# Above 16384 scores the selection runs grid-wide (histogram passes over many
+# workgroups, chunked index-order emission).
+@pytest.mark.parametrize("n,k", [(16385, 1), (16385, 16385), (65573, 19672), (1 << 20, 314573),
+                                 (3_000_017, 900_005)])
+def test_select_grid_random(gpu, n, k):
+    g = np.random.default_rng(n + k)
+    s = g.standard_normal(n).astype(np.float32)
+    got, raw = _select(gpu, s, k)
+    np.testing.assert_array_equal(got, oracle.select_topk(s, k))
+    # Min-max-normalised scores share their top bits (one exponent for most
+    # of [0.5, 1)): the histogram's concentrated-digit path.
+    u = g.random(n).astype(np.float32) ** 0.25
+    got, _ = _select(gpu, u, k)
+    np.testing.assert_array_equal(got, oracle.select_topk(u, k))
+
+
+@pytest.mark.parametrize("n,k,levels", [(100_003, 30_001, 8), (1 << 20, 524_288, 2), (70_000, 69_999, 1),
+                                        (200_000, 123, 3)])
+def test_select_grid_ties_lowest_index(gpu, n, k, levels):
+    s = G.quantised_scores(n, n, levels)
+    got, _ = _select(gpu, s, k)
+    np.testing.assert_array_equal(got, oracle.select_topk(s, k))
+
+
+def test_select_grid_special_values(gpu):
+    n = 50_000
+    g = np.random.default_rng(5)
+    s = g.standard_normal(n).astype(np.float32)
+    specials = np.array([np.nan, -0.0, 0.0, -np.inf, np.inf], dtype=np.float32)
+    pos = g.integers(0, n, 5000)
+    s[pos] = specials[g.integers(0, len(specials), 5000)]
+    for k in (1, 37, 20_000, n - 3, n):
+        buf = torch.full((n + 8,), -7, dtype=torch.int32, device="cuda")
+        gpu.avits_select(torch.from_numpy(s).cuda(), k, buf[:k])
+        torch.cuda.synchronize()
+        raw = host(buf)
+        np.testing.assert_array_equal(raw[:k], oracle.select_topk(s, k))
+        assert np.all(raw[k:] == -7)  # nothing written past k
+
+
+def test_select_grid_workspace(gpu):
+    assert gpu.avits_select_workspace_bytes(16384) == 0
+    assert gpu.avits_select_workspace_bytes(16385) > 0
+    s = torch.rand(40_000, device="cuda")
+    idx = torch.empty(10, dtype=torch.int32, device="cuda")
+    small = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(gpu.AvitsError) as e:
+        gpu.avits_select(s, 10, idx, workspace=small)
+    assert e.value.code == -3
+
+
 def _gather(gpu, w, k, mode, alias, seed=0):
     lay = G.layout_inputs(w)
     idx = G.random_selection(w, k, seed)
