@@ -381,7 +381,7 @@ int64_t tiles_of(const GemmArgs& a, int bm, int bn) {
 
 }  // namespace
 
-GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes) {
+GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const char* family) {
   GemmPlan pl;
   if (dtype != AVITS_BF16) {
     pl.bn = kFB;
@@ -415,8 +415,16 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes) {
   }
   pl.waves = 8;
   pl.stages = pl.bn == 256 ? 1 : 2;  // two stages do not fit the 256-wide tile's registers
-  // Tuning override "BN,SPLITS[,8[,STAGES]]" (e.g. AVITS_GEMM_TILE=256,3,8,1).
-  if (const char* env = getenv("AVITS_GEMM_TILE")) {
+  // Tuning override "BN,SPLITS[,8[,STAGES]]" (e.g. AVITS_GEMM_TILE=256,3,8,1),
+  // for one launch family with AVITS_GEMM_TILE_<family> (e.g. _gemm_o).
+  const char* env = nullptr;
+  if (family) {
+    char name[64];
+    snprintf(name, sizeof(name), "AVITS_GEMM_TILE_%s", family);
+    env = getenv(name);
+  }
+  if (!env) env = getenv("AVITS_GEMM_TILE");
+  if (env) {
     int bn = 0, sp = 0, wv = 8, stg = 2;
     const int got = sscanf(env, "%d,%d,%d,%d", &bn, &sp, &wv, &stg);
     if (got >= 2 && (bn == 256 || bn == 192 || bn == 128) && sp >= 1 && sp <= 4 && wv == 8 &&
@@ -439,7 +447,7 @@ size_t gemm_partial_bytes(const GemmArgs& a, const GemmPlan& pl) {
 
 int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family, float* partial,
                 size_t partial_bytes) {
-  GemmPlan pl = plan_gemm(a, dtype, partial ? partial_bytes : 0);
+  GemmPlan pl = plan_gemm(a, dtype, partial ? partial_bytes : 0, family);
   if (pl.tiles == 0) return AVITS_OK;
   if (pl.splits > 1 && (!partial || partial_bytes < gemm_partial_bytes(a, pl))) pl.splits = 1;
   if (dtype == AVITS_BF16) {

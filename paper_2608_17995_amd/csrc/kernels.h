@@ -53,7 +53,7 @@ struct GemmPlan {
   int stages = 2;      // register staging depth of the k-tile pipeline (1 or 2)
   int64_t tiles = 0;   // output tiles
 };
-GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes);
+GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const char* family = nullptr);
 size_t gemm_partial_bytes(const GemmArgs& a, const GemmPlan& pl);
 // `partial` is scratch for split-K partial sums; when it is null or smaller
 // than the plan needs, the GEMM runs unsplit.
