@@ -131,6 +131,41 @@ def _cpu_baseline(w, host, row_lse, wt, wi):
                       f"in fp64 NumPy on the host; {os.cpu_count()} CPUs visible"}
 
 
+def _fused_scoring(avits, torch, w, q, k_all, kt, feat_t, feat_prev, lse, reps: int = 10) -> dict:
+    """The scoring stage with the text mass taken inside the joint-softmax
+    pass (avits_joint_attention_stats + avits_score_from_mass) beside the
+    form the step uses (joint LSE, then the query/key scorer).  Both pairs run
+    on the step's inputs; times are per call, from the library's events."""
+    N, H = w.N, w.H
+    mass = torch.empty(H, N, device="cuda")
+    snaps = torch.stack([feat_prev, feat_t])
+    s1, s2 = torch.empty(N, device="cuda"), torch.empty(N, device="cuda")
+    ws = torch.empty(avits.avits_score_workspace_bytes(N, H), dtype=torch.uint8, device="cuda")
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    out = {
+        "stats_pass_us": timed(lambda: avits.avits_joint_attention_stats(q, k_all, w.L, mass, lse=lse)),
+        "score_from_mass_us": timed(lambda: avits.avits_score_from_mass(mass, 1, snaps, w.alpha, w.eps_minmax, s1,
+                                                                        workspace=ws)),
+        "joint_lse_us": timed(lambda: avits.avits_joint_lse(q, k_all, lse)),
+        "score_us": timed(lambda: avits.avits_score(q, kt, lse, feat_t, feat_prev, w.alpha, w.eps_minmax, s2,
+                                                    workspace=ws)),
+    }
+    out = {k: round(v, 2) for k, v in out.items()}
+    out["max_abs_score_diff"] = float((s1 - s2).abs().max().item())
+    return out
+
+
 def _select_sweep(avits, torch, reps: int = 10) -> list:
     """Top-k selection beyond the step's N: k = 0.3 N of N scores drawn as
     u^(1/4) (u uniform; the top exponent bits coincide, as for min-max
@@ -357,6 +392,7 @@ def main(argv=None):
         "input_generation_s": round(t_gen, 1),
         "copy_calibration_ms": None if copy_ms is None else round(copy_ms, 4),
     }
+    result["fused_scoring"] = _fused_scoring(avits, torch, w, q, k_all, kt, high, fp, lse)
     result["select_sweep"] = _select_sweep(avits, torch)
     if not args.no_cpu_baseline:
         host = dict(si)

@@ -227,6 +227,43 @@ int avits_joint_lse(const void* q, const void* k_all, int64_t N, int64_t Nk,
                     int32_t H, int32_t d, int dtype, float* lse, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_joint_attention_stats — the joint softmax statistics of each image
+ * query in one pass over the joint key set (Eq. dit_attn), with the
+ * image-to-text attention mass of Eq. spatial per head tracked inside the
+ * online softmax under the same running maximum:
+ *   lse[h, i]   = log sum_{j < Nk} exp(q_ih . k_jh / sqrt(d))      (natural log)
+ *   mass[h, i] (+)= sum_{j < L} exp(q_ih . k_jh / sqrt(d) - lse[h, i])
+ * The first L rows of k_all are the text keys.  With accumulate != 0 the
+ * mass is added to what `mass` holds, so the probes of several blocks or
+ * steps sum into one buffer (the aggregation over selected blocks and
+ * steps of Section 3.3.1; avits_score_from_mass divides by their count).
+ * q [N, H, d], k_all [Nk, H, d] (dtype); lse [H, N] fp32 or NULL; mass
+ * [H, N] fp32.  Requires N, Nk, H >= 1, 0 <= L <= Nk, d in {64, 128}.
+ * ---------------------------------------------------------------------- */
+int avits_joint_attention_stats(const void* q, const void* k_all, int64_t N, int64_t Nk,
+                                int64_t L, int32_t H, int32_t d, int dtype, float* lse,
+                                float* mass, int accumulate, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_score_from_mass — the fused importance score from precomputed
+ * attention masses (Eq. spatial, aggregated) and N_T feature snapshots
+ * (Eqs. zbar and step_var for general N_T):
+ *   A_i = (1 / (H count)) sum_h mass[h, i]
+ *   V_i = (1 / D_f) sum_c sum_k (z_k[i, c] - zbar[i, c])^2 / (N_T - 1)
+ *   S_i = alpha (A_i - min A) / (max A - min A + eps)
+ *       + (1 - alpha) (V_i - min V) / (max V - min V + eps)
+ * mass [H, N] fp32 (the sum of `count` probes); snapshots [N_T, N, D_f]
+ * (dtype), consecutive steps; scores, a_raw, v_raw as avits_score.
+ * workspace >= avits_score_workspace_bytes(N, H).  Requires n_t >= 2,
+ * count >= 1.  With one probe and n_t = 2 it computes what avits_score
+ * computes, from the mass instead of the query/key recomputation.
+ * ---------------------------------------------------------------------- */
+int avits_score_from_mass(const float* mass, int32_t H, int32_t count, const void* snapshots,
+                          int32_t n_t, int64_t N, int64_t D_f, float alpha, float eps,
+                          int dtype, float* scores, float* a_raw, float* v_raw,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Launch timing (instrumentation for benchmarks; not part of the method).
  * While enabled, every kernel the library enqueues is bracketed by a pair of
  * HIP events on the caller's stream.  avits_timing_read() waits for the
@@ -234,7 +271,8 @@ int avits_joint_lse(const void* q, const void* k_all, int64_t N, int64_t Nk,
  * launch family: "score_spatial", "score_combine", "score_finalize",
  * "select", "gather_upsample", "scatter", "ln_mod", "gemm_qkv", "gemm_o",
  * "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
- * "splitk_reduce", "qk_rope", "attention", "joint_lse"; "gemm" returns the
+ * "splitk_reduce", "qk_rope", "attention", "joint_lse" (also the
+ * statistics pass of avits_joint_attention_stats); "gemm" returns the
  * sum of the six GEMM families (the GEMM kernels alone: the split-K
  * reduction that follows a split launch is "splitk_reduce").  Unknown
  * family -> AVITS_ERR_INVALID_ARG.

@@ -15,7 +15,7 @@ invariants; none is marked unpinned.
 """
 from .importance import (  # noqa: F401
     spatial_importance, spatial_importance_bruteforce, joint_lse, step_variance,
-    minmax_normalise, joint_score, score,
+    minmax_normalise, joint_score, score, text_attention_mass, score_from_mass,
 )
 from .selection import select_topk  # noqa: F401
 from .relayout import (  # noqa: F401

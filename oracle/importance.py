@@ -77,6 +77,27 @@ def spatial_importance_bruteforce(q, k_all, L: int):
     return acc / H
 
 
+def text_attention_mass(q, k_all, L: int, row_chunk: int = 1024):
+    """Per-head image-to-text attention mass (Eq. spatial before the head
+    mean, with the softmax of Eq. dit_attn over the joint key set).
+
+    mass[h, i] = sum_{j < L} softmax_j(q_ih . k_jh / sqrt(d)), the softmax
+    taken over every row of ``k_all`` (text keys first).  q: [N, H, d];
+    k_all: [Nk, H, d].  Returns [H, N] fp64.
+    """
+    q, k_all = _f64(q), _f64(k_all)
+    N, H, d = q.shape
+    out = np.empty((H, N))
+    scale = 1.0 / np.sqrt(d)
+    for h in range(H):
+        kh = k_all[:, h, :]
+        for r0 in range(0, N, row_chunk):
+            p = (q[r0:r0 + row_chunk, h, :] @ kh.T) * scale
+            e = np.exp(p - p.max(axis=1, keepdims=True))
+            out[h, r0:r0 + row_chunk] = e[:, :L].sum(axis=1) / e.sum(axis=1)
+    return out
+
+
 def step_variance(snapshots):
     """Temporal importance V_i (Section 3.3.2, Eqs. zbar and step_var).
 
@@ -117,5 +138,19 @@ def score(latent_q, text_k, row_lse, feat_t, feat_prev, alpha: float, eps: float
     """
     a = spatial_importance(latent_q, text_k, row_lse)
     v = step_variance(np.stack([_f64(feat_prev), _f64(feat_t)]))
+    s = joint_score(a, v, alpha, eps)
+    return s.astype(np.float32), a, v
+
+
+def score_from_mass(mass_sum, count: int, snapshots, alpha: float, eps: float = 1e-8):
+    """The scoring stage from aggregated attention masses: (S fp32, A, V).
+
+    mass_sum: [H, N], the sum of ``count`` per-head text masses (probes of
+    several blocks or steps, Section 3.3.1); A is their mean over heads and
+    probes.  snapshots: [N_T, N, D_f] for the step variance (Section 3.3.2).
+    """
+    mass_sum = _f64(mass_sum)
+    a = mass_sum.sum(axis=0) / (mass_sum.shape[0] * count)
+    v = step_variance(snapshots)
     s = joint_score(a, v, alpha, eps)
     return s.astype(np.float32), a, v

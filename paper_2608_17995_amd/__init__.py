@@ -15,5 +15,6 @@ from ._binding import (  # noqa: F401
     avits_gather_upsample, avits_scatter, avits_joint_lse,
     avits_block_workspace_bytes, avits_block_forward, BlockWeights,
     avits_block_qk_workspace_bytes, avits_block_qk,
+    avits_joint_attention_stats, avits_score_from_mass,
     avits_timing_enable, avits_timing_reset, avits_timing_read,
 )

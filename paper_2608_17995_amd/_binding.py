@@ -56,6 +56,11 @@ _SIGS = {
     "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, ctypes.c_int, _c_void_p, _c_void_p]),
     "avits_joint_lse": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i32, _i32, ctypes.c_int, _c_void_p,
                                        _c_void_p]),
+    "avits_joint_attention_stats": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, _i32, _i32, ctypes.c_int,
+                                                   _c_void_p, _c_void_p, ctypes.c_int, _c_void_p]),
+    "avits_score_from_mass": (ctypes.c_int, [_c_void_p, _i32, _i32, _c_void_p, _i32, _i64, _i64, _f32, _f32,
+                                             ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _size,
+                                             _c_void_p]),
     "avits_timing_enable": (ctypes.c_int, [ctypes.c_int]),
     "avits_timing_reset": (None, []),
     "avits_timing_read": (ctypes.c_int, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
@@ -264,3 +269,27 @@ def avits_block_qk(x_in, pos, n_txt, n_img, weights: BlockWeights, H, q_out, k_o
         _dev(x_in, "x_in"), _dev(pos, "pos", torch.int32), n_txt, n_img, ctypes.byref(weights.c), H, d, code,
         _dev(q_out, "q_out", x_in.dtype), _dev(k_out, "k_out", x_in.dtype), wsp, wsb, _stream(stream)))
     return q_out, k_out
+
+
+def avits_joint_attention_stats(q, k_all, L, mass, lse=None, accumulate=False, stream=None):
+    """q [N, H, d], k_all [Nk, H, d] (text keys first); mass [H, N] fp32 (added to when accumulate)."""
+    import torch
+    N, H, d = q.shape
+    _check(load().avits_joint_attention_stats(
+        _dev(q, "q"), _dev(k_all, "k_all", q.dtype), N, k_all.shape[0], L, H, d, _dtype_code(q),
+        _dev(lse, "lse", torch.float32), _dev(mass, "mass", torch.float32), 1 if accumulate else 0, _stream(stream)))
+    return mass
+
+
+def avits_score_from_mass(mass, count, snapshots, alpha, eps, scores, a_raw=None, v_raw=None, workspace=None,
+                          stream=None):
+    """mass [H, N] fp32 (sum of `count` probes); snapshots [N_T, N, D_f]."""
+    import torch
+    H, N = mass.shape
+    n_t, _, Df = snapshots.shape
+    ws, wsp, wsb = _workspace(workspace, avits_score_workspace_bytes(N, H), mass.device)
+    _check(load().avits_score_from_mass(
+        _dev(mass, "mass", torch.float32), H, count, _dev(snapshots, "snapshots"), n_t, N, Df, alpha, eps,
+        _dtype_code(snapshots), _dev(scores, "scores", torch.float32), _dev(a_raw, "a_raw", torch.float32),
+        _dev(v_raw, "v_raw", torch.float32), wsp, wsb, _stream(stream)))
+    return scores

@@ -60,6 +60,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   }
   const float scale2 = kLog2e * rsqrtf(float(DH));
   float mrow = -INFINITY, lrow = 0.f;
+  float trow = 0.f;  // the part of lrow from keys < a.mass_keys (when a.mass is set)
   f32x16 oacc[WITH_V ? DH / 32 : 1];
 #pragma unroll
   for (int dt = 0; dt < (WITH_V ? DH / 32 : 1); ++dt)
@@ -171,6 +172,20 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
         ls += e;
       }
     lrow = lrow * corr + ls;
+    if (a.mass && k0 < a.mass_keys) {
+      float ts = ls;  // whole tile below mass_keys, else only its leading keys
+      if (k0 + kKT > a.mass_keys) {
+        ts = 0.f;
+#pragma unroll
+        for (int t = 0; t < kKT / 32; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int64_t key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
+            ts += key < a.mass_keys ? s[t][r] : 0.f;
+          }
+      }
+      trow = trow * corr + ts;
+    }
     if constexpr (WITH_V) {
       if (__any(raise)) {
 #pragma unroll
@@ -201,8 +216,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   }
 
   float l = lrow + __shfl_xor(lrow, 32, kWave);
+  const float tm = trow + __shfl_xor(trow, 32, kWave);
   if (row >= a.Sq) return;
   if (a.lse && hi == 0) a.lse[int64_t(h) * a.Sq + row] = (mrow + log2f(l)) * kLn2;
+  if (a.mass && hi == 0) {
+    float* dst = a.mass + int64_t(h) * a.Sq + row;
+    *dst = (a.mass_accumulate ? *dst : 0.f) + tm / l;
+  }
   if constexpr (WITH_V) {
     // oacc[dt][r] = O[row][32 dt + 8(r/4) + 4hi + r%4].
     const float inv = 1.f / l;
@@ -236,7 +256,7 @@ __global__ __launch_bounds__(kFRows) void attn_f32_kernel(const AttnArgs a) {
 #pragma unroll
   for (int c = 0; c < (WITH_V ? DH : 1); ++c) o[c] = 0.f;
   const float scale = rsqrtf(float(DH));
-  float m = -INFINITY, l = 0.f;
+  float m = -INFINITY, l = 0.f, tl = 0.f;  // tl: the part of l from keys < a.mass_keys
   for (int64_t k0 = 0; k0 < a.Sk; k0 += kFKT) {
     __syncthreads();
     for (int p = threadIdx.x; p < kFKT * DH; p += kFRows) {
@@ -259,6 +279,7 @@ __global__ __launch_bounds__(kFRows) void attn_f32_kernel(const AttnArgs a) {
     const float corr = expf(m - mx);
     m = mx;
     l *= corr;
+    tl *= corr;
     if constexpr (WITH_V) {
 #pragma unroll
       for (int c = 0; c < DH; ++c) o[c] *= corr;
@@ -266,6 +287,7 @@ __global__ __launch_bounds__(kFRows) void attn_f32_kernel(const AttnArgs a) {
     for (int j = 0; j < nk; ++j) {
       const float e = expf(s[j] - m);
       l += e;
+      tl += k0 + j < a.mass_keys ? e : 0.f;
       if constexpr (WITH_V) {
 #pragma unroll
         for (int c = 0; c < DH; ++c) o[c] = fmaf(e, Vs[j * DH + c], o[c]);
@@ -274,6 +296,10 @@ __global__ __launch_bounds__(kFRows) void attn_f32_kernel(const AttnArgs a) {
   }
   if (!ok) return;
   if (a.lse) a.lse[int64_t(h) * a.Sq + row] = m + logf(l);
+  if (a.mass) {
+    float* dst = a.mass + int64_t(h) * a.Sq + row;
+    *dst = (a.mass_accumulate ? *dst : 0.f) + tl / l;
+  }
   if constexpr (WITH_V) {
     float* dst = static_cast<float*>(a.o) + row * a.ldo + int64_t(h) * DH;
 #pragma unroll
@@ -334,6 +360,36 @@ extern "C" int avits_joint_lse(const void* q, const void* k_all, int64_t N, int6
   a.k_tok = int64_t(H) * d;
   a.k_head = d;
   a.lse = lse;
+  a.Sq = N;
+  a.Sk = Nk;
+  a.H = H;
+  a.d = d;
+  return launch_attention(a, dtype, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int avits_joint_attention_stats(const void* q, const void* k_all, int64_t N, int64_t Nk, int64_t L,
+                                           int32_t H, int32_t d, int dtype, float* lse, float* mass, int accumulate,
+                                           void* stream) {
+  AVITS_REQUIRE(N >= 1 && Nk >= 1 && H >= 1, "joint_attention_stats: N=%lld Nk=%lld H=%d must be >= 1",
+                (long long)N, (long long)Nk, H);
+  AVITS_REQUIRE(L >= 0 && L <= Nk, "joint_attention_stats: L=%lld outside [0, Nk=%lld]", (long long)L,
+                (long long)Nk);
+  if (d != 64 && d != 128)
+    return set_error(AVITS_ERR_UNSUPPORTED, "joint_attention_stats: head dim %d (need 64 or 128)", d);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "joint_attention_stats: dtype %d unsupported", dtype);
+  AVITS_REQUIRE(q && k_all && mass, "joint_attention_stats: null q/k_all/mass");
+  AttnArgs a{};
+  a.q = q;
+  a.q_tok = int64_t(H) * d;
+  a.q_head = d;
+  a.k = k_all;
+  a.k_tok = int64_t(H) * d;
+  a.k_head = d;
+  a.lse = lse;
+  a.mass = mass;
+  a.mass_keys = L;
+  a.mass_accumulate = accumulate != 0;
   a.Sq = N;
   a.Sk = Nk;
   a.H = H;

@@ -81,6 +81,9 @@ struct AttnArgs {
   void* o;             // [Sq, ldo] or null
   int64_t ldo;
   float* lse;          // [H, Sq] or null
+  float* mass;         // [H, Sq] or null: softmax mass of keys [0, mass_keys) (the text keys)
+  int64_t mass_keys;
+  int mass_accumulate; // add to `mass` instead of overwriting it
   int64_t Sq, Sk;
   int H, d;
 };

@@ -350,6 +350,93 @@ __global__ __launch_bounds__(256) void temporal_kernel(const T* __restrict__ ft,
 }
 
 // ---------------------------------------------------------------------------
+// 2''. From precomputed attention masses and N_T snapshots: A_i = sum_h
+// mass[h, i] * inv (inv = 1 / (H * count) averages heads and the `count`
+// accumulated probes), V_i = (1 / D_f) sum_c var_k(z[k, i, c]) with the
+// unbiased variance over the N_T snapshots, formed from the deviations
+// d_k = z_k - z_0 (sum d and sum d^2 in fp32; the shift keeps the sums small
+// for slowly changing features).  One wave per row; per-workgroup min/max
+// partials as temporal_kernel.
+template <typename T>
+__global__ __launch_bounds__(256) void mass_temporal_kernel(const float* __restrict__ mass, int H, float inv,
+                                                            const T* __restrict__ z, int n_t, int64_t N, int64_t Df,
+                                                            float* __restrict__ a_out, float* __restrict__ v_out,
+                                                            float4* __restrict__ mm) {
+  __shared__ float4 red[4];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int64_t wstep = int64_t(gridDim.x) * 4;
+  const int64_t plane = N * Df;  // elements per snapshot
+  const float nt = float(n_t), inv_nm1 = 1.f / float(n_t - 1);
+  float amin = INFINITY, amax = -INFINITY, vmin = INFINITY, vmax = -INFINITY;
+  constexpr int kVec = 16 / sizeof(T);
+  const bool vec = (Df % kVec) == 0;
+  for (int64_t i = int64_t(blockIdx.x) * 4 + wave; i < N; i += wstep) {
+    const T* z0 = z + i * Df;
+    float acc = 0.f;
+    if (vec) {
+      for (int64_t c = lane; c < Df / kVec; c += kWave) {
+        float base[kVec], s1[kVec], s2[kVec];
+        const u32x4 b = reinterpret_cast<const u32x4*>(z0)[c];
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) {
+          if constexpr (sizeof(T) == 2) base[e] = __uint_as_float(e % 2 ? b[e / 2] & 0xffff0000u : b[e / 2] << 16);
+          else base[e] = __uint_as_float(b[e]);
+          s1[e] = 0.f;
+          s2[e] = 0.f;
+        }
+        for (int k = 1; k < n_t; ++k) {
+          const u32x4 v = reinterpret_cast<const u32x4*>(z0 + int64_t(k) * plane)[c];
+#pragma unroll
+          for (int e = 0; e < kVec; ++e) {
+            float x;
+            if constexpr (sizeof(T) == 2) x = __uint_as_float(e % 2 ? v[e / 2] & 0xffff0000u : v[e / 2] << 16);
+            else x = __uint_as_float(v[e]);
+            const float d = x - base[e];
+            s1[e] += d;
+            s2[e] = fmaf(d, d, s2[e]);
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) acc += (s2[e] - s1[e] * s1[e] / nt) * inv_nm1;
+      }
+    } else {
+      for (int64_t c = lane; c < Df; c += kWave) {
+        const float b0 = ld(z0, c);
+        float s1 = 0.f, s2 = 0.f;
+        for (int k = 1; k < n_t; ++k) {
+          const float d = ld(z0 + int64_t(k) * plane, c) - b0;
+          s1 += d;
+          s2 = fmaf(d, d, s2);
+        }
+        acc += (s2 - s1 * s1 / nt) * inv_nm1;
+      }
+    }
+    acc = wave_sum(acc);
+    float ah = 0.f;
+    for (int h = lane; h < H; h += kWave) ah += mass[int64_t(h) * N + i];
+    ah = wave_sum(ah);
+    const float A = ah * inv;
+    const float V = acc / float(Df);
+    if (lane == 0) {
+      a_out[i] = A;
+      v_out[i] = V;
+    }
+    amin = fminf(amin, A); amax = fmaxf(amax, A);
+    vmin = fminf(vmin, V); vmax = fmaxf(vmax, V);
+  }
+  if (lane == 0) red[wave] = make_float4(amin, amax, vmin, vmax);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float4 r = red[0];
+    for (int w = 1; w < 4; ++w) {
+      r.x = fminf(r.x, red[w].x); r.y = fmaxf(r.y, red[w].y);
+      r.z = fminf(r.z, red[w].z); r.w = fmaxf(r.w, red[w].w);
+    }
+    mm[blockIdx.x] = r;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // 3. global min/max and the fused score.
 __global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__ a, const float* __restrict__ v,
                                                        const float4* __restrict__ mm, int n_mm, int64_t N,
@@ -474,4 +561,43 @@ extern "C" int avits_score(const void* latent_q, const void* text_k, const float
   hipLaunchKernelGGL(finalize_kernel, dim3(fblocks), dim3(256), 0, s, a_dst, v_dst, ws.mm, nmm, N, alpha, eps,
                      scores);
   return launch_status("score");
+}
+
+extern "C" int avits_score_from_mass(const float* mass, int32_t H, int32_t count, const void* snapshots, int32_t n_t,
+                                     int64_t N, int64_t D_f, float alpha, float eps, int dtype, float* scores,
+                                     float* a_raw, float* v_raw, void* workspace, size_t workspace_bytes,
+                                     void* stream) {
+  AVITS_REQUIRE(N >= 1 && N <= INT32_MAX, "score_from_mass: N=%lld outside [1, 2^31)", (long long)N);
+  AVITS_REQUIRE(H >= 1 && count >= 1 && D_f >= 1, "score_from_mass: H=%d count=%d D_f=%lld must be >= 1", H, count,
+                (long long)D_f);
+  AVITS_REQUIRE(n_t >= 2, "score_from_mass: n_t=%d snapshots (need >= 2)", n_t);
+  AVITS_REQUIRE(alpha >= 0.f && alpha <= 1.f, "score_from_mass: alpha=%g outside [0, 1]", alpha);
+  AVITS_REQUIRE(eps >= 0.f, "score_from_mass: eps=%g < 0", eps);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "score_from_mass: dtype %d unsupported", dtype);
+  AVITS_REQUIRE(mass && snapshots && scores, "score_from_mass: null input/output pointer");
+  const ScoreWs need = score_ws_layout(nullptr, N, H);
+  if (!workspace || workspace_bytes < need.bytes)
+    return set_error(AVITS_ERR_WORKSPACE, "score_from_mass: workspace of %zu bytes, need %zu", workspace_bytes,
+                     need.bytes);
+  ScoreWs ws = score_ws_layout(static_cast<char*>(workspace), N, H);
+  float* a_dst = a_raw ? a_raw : ws.a;
+  float* v_dst = v_raw ? v_raw : ws.v;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int nmm = int(std::min<int64_t>(kTmpBlocks, (N + 3) / 4));
+  const float inv = 1.f / (float(H) * float(count));
+  {
+    TimedLaunch timed("score_combine", s);
+    if (dtype == AVITS_BF16)
+      hipLaunchKernelGGL(mass_temporal_kernel<bf16_t>, dim3(nmm), dim3(256), 0, s, mass, H, inv,
+                         (const bf16_t*)snapshots, n_t, N, D_f, a_dst, v_dst, ws.mm);
+    else
+      hipLaunchKernelGGL(mass_temporal_kernel<float>, dim3(nmm), dim3(256), 0, s, mass, H, inv,
+                         (const float*)snapshots, n_t, N, D_f, a_dst, v_dst, ws.mm);
+  }
+  const int fblocks = int(std::min<int64_t>(256, (N + 255) / 256));
+  TimedLaunch timed("score_finalize", s);
+  hipLaunchKernelGGL(finalize_kernel, dim3(fblocks), dim3(256), 0, s, a_dst, v_dst, ws.mm, nmm, N, alpha, eps,
+                     scores);
+  return launch_status("score_from_mass");
 }

@@ -156,3 +156,20 @@ def test_block_qk_validation(lib):
     assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, FAKE, ws - 1, None) == WORKSPACE
     assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, None, ws, None) == WORKSPACE
     assert b"block_qk" in lib.avits_last_error()
+
+
+def test_stats_and_mass_score_validation(lib):
+    f = lib.avits_joint_attention_stats
+    assert f(FAKE, FAKE, 0, 5, 2, 2, 64, 1, None, FAKE, 0, None) == INVALID        # N < 1
+    assert f(FAKE, FAKE, 5, 5, 6, 2, 64, 1, None, FAKE, 0, None) == INVALID        # L > Nk
+    assert f(FAKE, FAKE, 5, 5, -1, 2, 64, 1, None, FAKE, 0, None) == INVALID       # L < 0
+    assert f(FAKE, FAKE, 5, 5, 2, 2, 96, 1, None, FAKE, 0, None) == UNSUPPORTED    # head dim
+    assert f(FAKE, FAKE, 5, 5, 2, 2, 64, 1, None, None, 0, None) == INVALID        # mass required
+    g = lib.avits_score_from_mass
+    ws = lib.avits_score_workspace_bytes(16, 2)
+    assert g(FAKE, 2, 1, FAKE, 1, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # n_t < 2
+    assert g(FAKE, 2, 0, FAKE, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # count < 1
+    assert g(FAKE, 2, 1, FAKE, 2, 16, 8, 1.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # alpha
+    assert g(FAKE, 2, 1, FAKE, 2, 16, 8, 0.5, 1e-8, 9, FAKE, None, None, FAKE, ws, None) == UNSUPPORTED
+    assert g(FAKE, 2, 1, FAKE, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws - 1, None) == WORKSPACE
+    assert g(None, 2, 1, FAKE, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID

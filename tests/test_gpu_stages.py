@@ -339,3 +339,74 @@ def test_block_qk_probe_single(gpu, w):
     rq, rk = oracle.block_qk(x, pos, 0, None, None, w.H, single=ws)
     assert_close(q, rq.reshape(len(x), -1), w.dtype, "probe q")
     assert_close(k, rk.reshape(len(x), -1), w.dtype, "probe k")
+
+
+# ---------------------------------------------------------------------------
+# Text attention mass inside the statistics pass, and the score from it.
+
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+def test_joint_attention_stats(gpu, w):
+    si = G.score_inputs(w)
+    k_all = _k_all(si)
+    q, k = dev(si["latent_q"], w.dtype), dev(k_all, w.dtype)
+    lse = torch.empty(w.H, w.N, device="cuda")
+    mass = torch.full((w.H, w.N), 7.0, device="cuda")
+    gpu.avits_joint_attention_stats(q, k, w.L, mass, lse=lse)
+    torch.cuda.synchronize()
+    assert_close(host(lse), oracle.joint_lse(si["latent_q"], k_all), w.dtype, "lse")
+    ref = oracle.text_attention_mass(si["latent_q"], k_all, w.L)
+    assert_close(host(mass), ref, w.dtype, "text mass")
+    assert_close(host(mass).mean(axis=0), oracle.spatial_importance(si["latent_q"], si["text_k"],
+                                                                   oracle.joint_lse(si["latent_q"], k_all)),
+                 w.dtype, "head-mean mass = A")
+    # Accumulation over two probes; the limits L = 0 and L = Nk.
+    gpu.avits_joint_attention_stats(q, k, w.L, mass, accumulate=True)
+    torch.cuda.synchronize()
+    assert_close(host(mass), 2 * ref, w.dtype, "accumulated mass")
+    gpu.avits_joint_attention_stats(q, k, 0, mass)
+    gpu.avits_joint_attention_stats(q, k, k_all.shape[0], lse)  # lse buffer reused as a mass output
+    torch.cuda.synchronize()
+    assert np.all(host(mass) == 0.0)
+    np.testing.assert_allclose(host(lse), 1.0, atol=1e-5)
+
+
+@pytest.mark.parametrize("w", [C.TINY_F32, C.TINY_BF16, C.TINY_F32_RAGGED], ids=["f32", "bf16", "f32_ragged"])
+@pytest.mark.parametrize("n_t", [2, 3, 5])
+def test_score_from_mass(gpu, w, n_t):
+    si = G.score_inputs(w)
+    mass = oracle.text_attention_mass(si["latent_q"], _k_all(si), w.L).astype(np.float32)
+    g = np.random.default_rng(n_t)
+    snaps = [si["feat_prev"], si["feat_t"]]
+    while len(snaps) < n_t:
+        snaps.append(G.round_to(snaps[-1] + 0.1 * g.standard_normal(snaps[-1].shape), w.dtype))
+    snaps = np.stack(snaps)
+    s = torch.empty(w.N, device="cuda")
+    a = torch.empty(w.N, device="cuda")
+    v = torch.empty(w.N, device="cuda")
+    gpu.avits_score_from_mass(dev(2 * mass), 2, dev(snaps, w.dtype), w.alpha, w.eps_minmax, s, a_raw=a, v_raw=v)
+    torch.cuda.synchronize()
+    s_ref, a_ref, v_ref = oracle.score_from_mass(2 * mass.astype(np.float64), 2, snaps, w.alpha, w.eps_minmax)
+    assert_close(host(a), a_ref, w.dtype, "A")
+    assert_close(host(v), v_ref, w.dtype, "V")
+    assert_close(host(s), s_ref, w.dtype, "S")
+    assert np.abs(host(s) - s_ref).max() < 1e-4
+
+
+@pytest.mark.parametrize("w", [C.TINY_BF16, C.TINY_BF16_REF], ids=["bf16", "bf16_ref"])
+def test_fused_mass_score_matches_query_key_score(gpu, w):
+    # The statistics pass + score_from_mass and the LSE + query/key scorer are
+    # two GPU routes to the same scores.
+    si = G.score_inputs(w)
+    k_all = _k_all(si)
+    q = dev(si["latent_q"], w.dtype)
+    lse = torch.empty(w.H, w.N, device="cuda")
+    mass = torch.empty(w.H, w.N, device="cuda")
+    gpu.avits_joint_attention_stats(q, dev(k_all, w.dtype), w.L, mass, lse=lse)
+    s1 = torch.empty(w.N, device="cuda")
+    gpu.avits_score_from_mass(mass, 1, dev(np.stack([si["feat_prev"], si["feat_t"]]), w.dtype), w.alpha,
+                              w.eps_minmax, s1)
+    s2 = torch.empty(w.N, device="cuda")
+    gpu.avits_score(q, dev(si["text_k"], w.dtype), lse, dev(si["feat_t"], w.dtype), dev(si["feat_prev"], w.dtype),
+                    w.alpha, w.eps_minmax, s2)
+    torch.cuda.synchronize()
+    assert np.abs(host(s1) - host(s2)).max() < 1e-4

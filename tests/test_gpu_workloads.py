@@ -45,12 +45,14 @@ def run(gpu, request):
                          keep_lse=True)
     lse = torch.empty(w.H, w.N, device="cuda")
     gpu.avits_joint_lse(t["latent_q"], dev(k_all, w.dtype), lse)
+    mass = torch.empty(w.H, w.N, device="cuda")
+    gpu.avits_joint_attention_stats(t["latent_q"], dev(k_all, w.dtype), w.L, mass)
     step.score(t["latent_q"], t["text_k"], lse, high, t["feat_prev"])
     step.select()
     step.gather(dev(lay["lowres"], w.dtype), high, dev(prefix_np, w.dtype))
     torch.cuda.synchronize()
     out = {"w": w, "si": si, "lay": lay, "wt": wt, "wi": wi, "k_all": k_all, "prefix": prefix_np,
-           "lse": host(lse), "scores": step.scores.cpu().numpy(), "a": host(step.a_raw), "v": host(step.v_raw),
+           "lse": host(lse), "mass": host(mass), "scores": step.scores.cpu().numpy(), "a": host(step.a_raw), "v": host(step.v_raw),
            "idx": step.idx.cpu().numpy(), "compact": host(step.compact), "pos": step.pos.cpu().numpy(),
            "canvas_gather": host(canvas)}
     step.block()
@@ -69,6 +71,14 @@ def test_joint_lse_sampled(run):
     ref = oracle.joint_lse(run["si"]["latent_q"][rows], run["k_all"])
     assert np.abs(run["lse"][:, rows] - ref).max() < 2e-3
     assert_close(run["lse"][:, rows], ref, w.dtype, "joint_lse")
+
+
+def test_text_mass_sampled(run):
+    w = run["w"]
+    rows = np.unique(np.concatenate([np.arange(8), np.random.default_rng(1).integers(0, w.N, 56), [w.N - 1]]))
+    ref = oracle.text_attention_mass(run["si"]["latent_q"][rows], run["k_all"], w.L)
+    assert_close(run["mass"][:, rows], ref, w.dtype, "text mass")
+    assert np.abs(run["mass"][:, rows] - ref).max() < 2e-3
 
 
 def test_score(run):

@@ -164,3 +164,57 @@ def test_score_wrapper_composes_stages():
     an = (a - a.min()) / (a.max() - a.min() + 1e-8)
     vn = (v - v.min()) / (v.max() - v.min() + 1e-8)
     np.testing.assert_array_equal(s, (0.4 * an + 0.6 * vn).astype(np.float32))
+
+
+def _bruteforce_mass(q, k_all, L):
+    """Pure-Python per-head text mass: softmax over every key, sum of the first L."""
+    N, H, d = q.shape
+    out = np.zeros((H, N))
+    for i in range(N):
+        for h in range(H):
+            logits = [math.fsum(q[i, h, c] * k_all[j, h, c] for c in range(d)) / math.sqrt(d)
+                      for j in range(k_all.shape[0])]
+            m = max(logits)
+            e = [math.exp(x - m) for x in logits]
+            out[h, i] = math.fsum(e[:L]) / math.fsum(e)
+    return out
+
+
+@pytest.mark.parametrize("seed", [0, 5])
+def test_text_mass_matches_pure_python_and_limits(seed):
+    q, k_txt, k_rest = _tiny(seed, N=6, H=3, d=4, L=3, extra=5)
+    k_all = np.concatenate([k_txt, k_rest])
+    mass = oracle.text_attention_mass(q, k_all, 3)
+    np.testing.assert_allclose(mass, _bruteforce_mass(q, k_all, 3), atol=1e-12)
+    # Head mean is the spatial importance; L = 0 and L = Nk are the limits.
+    np.testing.assert_allclose(mass.mean(axis=0), _bruteforce_A(q, k_all, 3), atol=1e-12)
+    np.testing.assert_array_equal(oracle.text_attention_mass(q, k_all, 0), np.zeros((3, 6)))
+    np.testing.assert_allclose(oracle.text_attention_mass(q, k_all, 8), np.ones((3, 6)), atol=1e-15)
+    # Zero keys: every logit equal, so the mass is L / Nk exactly.
+    np.testing.assert_allclose(oracle.text_attention_mass(q, np.zeros_like(k_all), 3), np.full((3, 6), 3 / 8),
+                               atol=1e-15)
+
+
+def test_score_from_mass_aggregates_probes_and_snapshots():
+    g = np.random.default_rng(9)
+    H, N, Df = 4, 50, 12
+    m1, m2 = g.random((H, N)), g.random((H, N))
+    snaps = g.standard_normal((5, N, Df))
+    s, a, v = oracle.score_from_mass(m1 + m2, 2, snaps, 0.3, 1e-8)
+    # A: the plain average over heads and the two probes, element by element.
+    ref_a = np.array([math.fsum(list(m1[:, i]) + list(m2[:, i])) / (2 * H) for i in range(N)])
+    np.testing.assert_allclose(a, ref_a, atol=1e-14)
+    # V: the unbiased variance over the five steps, averaged over channels.
+    ref_v = np.array([statistics.fmean(statistics.variance(snaps[:, i, c]) for c in range(Df)) for i in range(N)])
+    np.testing.assert_allclose(v, ref_v, atol=1e-12)
+    np.testing.assert_array_equal(s, oracle.joint_score(ref_a, ref_v, 0.3, 1e-8).astype(np.float32))
+    # One probe and two snapshots: the same score as the query/key form.
+    q, k_txt, k_rest = _tiny(2, N=7, H=2, d=4, L=3, extra=6)
+    k_all = np.concatenate([k_txt, k_rest])
+    lse = oracle.joint_lse(q, k_all)
+    f0, f1 = g.standard_normal((7, 6)), g.standard_normal((7, 6))
+    s_qk, a_qk, v_qk = oracle.score(q, k_txt, lse, f1, f0, 0.5)
+    s_m, a_m, v_m = oracle.score_from_mass(oracle.text_attention_mass(q, k_all, 3), 1, np.stack([f0, f1]), 0.5)
+    np.testing.assert_allclose(a_m, a_qk, atol=1e-13)
+    np.testing.assert_allclose(v_m, v_qk, atol=1e-13)
+    np.testing.assert_allclose(s_m, s_qk, atol=1e-6)
