@@ -138,7 +138,7 @@ def _fused_scoring(avits, torch, w, q, k_all, kt, feat_t, feat_prev, lse, reps: 
     on the step's inputs; times are per call, from the library's events."""
     N, H = w.N, w.H
     mass = torch.empty(H, N, device="cuda")
-    snaps = torch.stack([feat_prev, feat_t])
+    snaps = [feat_prev, feat_t]
     s1, s2 = torch.empty(N, device="cuda"), torch.empty(N, device="cuda")
     ws = torch.empty(avits.avits_score_workspace_bytes(N, H), dtype=torch.uint8, device="cuda")
 

@@ -252,14 +252,14 @@ int avits_joint_attention_stats(const void* q, const void* k_all, int64_t N, int
  *   V_i = (1 / D_f) sum_c sum_k (z_k[i, c] - zbar[i, c])^2 / (N_T - 1)
  *   S_i = alpha (A_i - min A) / (max A - min A + eps)
  *       + (1 - alpha) (V_i - min V) / (max V - min V + eps)
- * mass [H, N] fp32 (the sum of `count` probes); snapshots [N_T, N, D_f]
- * (dtype), consecutive steps; scores, a_raw, v_raw as avits_score.
- * workspace >= avits_score_workspace_bytes(N, H).  Requires n_t >= 2,
- * count >= 1.  With one probe and n_t = 2 it computes what avits_score
+ * mass [H, N] fp32 (the sum of `count` probes); snapshots: a host array of
+ * n_t device pointers, snapshot k [N, D_f] (dtype), consecutive steps in
+ * order; scores, a_raw, v_raw as avits_score.  workspace >=
+ * avits_score_workspace_bytes(N, H).  Requires 2 <= n_t <= 16, count >= 1.  With one probe and n_t = 2 it computes what avits_score
  * computes, from the mass instead of the query/key recomputation.
  * ---------------------------------------------------------------------- */
-int avits_score_from_mass(const float* mass, int32_t H, int32_t count, const void* snapshots,
-                          int32_t n_t, int64_t N, int64_t D_f, float alpha, float eps,
+int avits_score_from_mass(const float* mass, int32_t H, int32_t count,
+                          const void* const* snapshots, int32_t n_t, int64_t N, int64_t D_f, float alpha, float eps,
                           int dtype, float* scores, float* a_raw, float* v_raw,
                           void* workspace, size_t workspace_bytes, void* stream);
 

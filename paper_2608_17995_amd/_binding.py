@@ -58,7 +58,8 @@ _SIGS = {
                                        _c_void_p]),
     "avits_joint_attention_stats": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, _i32, _i32, ctypes.c_int,
                                                    _c_void_p, _c_void_p, ctypes.c_int, _c_void_p]),
-    "avits_score_from_mass": (ctypes.c_int, [_c_void_p, _i32, _i32, _c_void_p, _i32, _i64, _i64, _f32, _f32,
+    "avits_score_from_mass": (ctypes.c_int, [_c_void_p, _i32, _i32, ctypes.POINTER(_c_void_p), _i32, _i64, _i64,
+                                             _f32, _f32,
                                              ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _size,
                                              _c_void_p]),
     "avits_timing_enable": (ctypes.c_int, [ctypes.c_int]),
@@ -283,13 +284,19 @@ def avits_joint_attention_stats(q, k_all, L, mass, lse=None, accumulate=False, s
 
 def avits_score_from_mass(mass, count, snapshots, alpha, eps, scores, a_raw=None, v_raw=None, workspace=None,
                           stream=None):
-    """mass [H, N] fp32 (sum of `count` probes); snapshots [N_T, N, D_f]."""
+    """mass [H, N] fp32 (sum of `count` probes); snapshots: N_T tensors [N, D_f], consecutive steps in order."""
     import torch
     H, N = mass.shape
-    n_t, _, Df = snapshots.shape
+    snaps = list(snapshots)
+    n_t = len(snaps)
+    Df = snaps[0].shape[-1]
+    for z in snaps:
+        if tuple(z.shape) != (N, Df) or z.dtype != snaps[0].dtype:
+            raise AvitsError(-1, "snapshots must all be [N, D_f] of one dtype")
+    ptrs = (_c_void_p * n_t)(*[_dev(z, "snapshot") for z in snaps])
     ws, wsp, wsb = _workspace(workspace, avits_score_workspace_bytes(N, H), mass.device)
     _check(load().avits_score_from_mass(
-        _dev(mass, "mass", torch.float32), H, count, _dev(snapshots, "snapshots"), n_t, N, Df, alpha, eps,
-        _dtype_code(snapshots), _dev(scores, "scores", torch.float32), _dev(a_raw, "a_raw", torch.float32),
-        _dev(v_raw, "v_raw", torch.float32), wsp, wsb, _stream(stream)))
+        _dev(mass, "mass", torch.float32), H, count, ptrs, n_t, N, Df, alpha, eps, _dtype_code(snaps[0]),
+        _dev(scores, "scores", torch.float32), _dev(a_raw, "a_raw", torch.float32), _dev(v_raw, "v_raw", torch.float32),
+        wsp, wsb, _stream(stream)))
     return scores

@@ -357,21 +357,25 @@ __global__ __launch_bounds__(256) void temporal_kernel(const T* __restrict__ ft,
 // d_k = z_k - z_0 (sum d and sum d^2 in fp32; the shift keeps the sums small
 // for slowly changing features).  One wave per row; per-workgroup min/max
 // partials as temporal_kernel.
+constexpr int kMaxSnapshots = 16;
+struct Snapshots {
+  const void* p[kMaxSnapshots];  // n_t device pointers, each [N, D_f]
+};
+
 template <typename T>
 __global__ __launch_bounds__(256) void mass_temporal_kernel(const float* __restrict__ mass, int H, float inv,
-                                                            const T* __restrict__ z, int n_t, int64_t N, int64_t Df,
+                                                            const Snapshots zs, int n_t, int64_t N, int64_t Df,
                                                             float* __restrict__ a_out, float* __restrict__ v_out,
                                                             float4* __restrict__ mm) {
   __shared__ float4 red[4];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int64_t wstep = int64_t(gridDim.x) * 4;
-  const int64_t plane = N * Df;  // elements per snapshot
   const float nt = float(n_t), inv_nm1 = 1.f / float(n_t - 1);
   float amin = INFINITY, amax = -INFINITY, vmin = INFINITY, vmax = -INFINITY;
   constexpr int kVec = 16 / sizeof(T);
   const bool vec = (Df % kVec) == 0;
   for (int64_t i = int64_t(blockIdx.x) * 4 + wave; i < N; i += wstep) {
-    const T* z0 = z + i * Df;
+    const T* z0 = static_cast<const T*>(zs.p[0]) + i * Df;
     float acc = 0.f;
     if (vec) {
       for (int64_t c = lane; c < Df / kVec; c += kWave) {
@@ -385,7 +389,7 @@ __global__ __launch_bounds__(256) void mass_temporal_kernel(const float* __restr
           s2[e] = 0.f;
         }
         for (int k = 1; k < n_t; ++k) {
-          const u32x4 v = reinterpret_cast<const u32x4*>(z0 + int64_t(k) * plane)[c];
+          const u32x4 v = reinterpret_cast<const u32x4*>(static_cast<const T*>(zs.p[k]) + i * Df)[c];
 #pragma unroll
           for (int e = 0; e < kVec; ++e) {
             float x;
@@ -404,7 +408,7 @@ __global__ __launch_bounds__(256) void mass_temporal_kernel(const float* __restr
         const float b0 = ld(z0, c);
         float s1 = 0.f, s2 = 0.f;
         for (int k = 1; k < n_t; ++k) {
-          const float d = ld(z0 + int64_t(k) * plane, c) - b0;
+          const float d = ld(static_cast<const T*>(zs.p[k]) + i * Df, c) - b0;
           s1 += d;
           s2 = fmaf(d, d, s2);
         }
@@ -563,19 +567,26 @@ extern "C" int avits_score(const void* latent_q, const void* text_k, const float
   return launch_status("score");
 }
 
-extern "C" int avits_score_from_mass(const float* mass, int32_t H, int32_t count, const void* snapshots, int32_t n_t,
+extern "C" int avits_score_from_mass(const float* mass, int32_t H, int32_t count, const void* const* snapshots,
+                                     int32_t n_t,
                                      int64_t N, int64_t D_f, float alpha, float eps, int dtype, float* scores,
                                      float* a_raw, float* v_raw, void* workspace, size_t workspace_bytes,
                                      void* stream) {
   AVITS_REQUIRE(N >= 1 && N <= INT32_MAX, "score_from_mass: N=%lld outside [1, 2^31)", (long long)N);
   AVITS_REQUIRE(H >= 1 && count >= 1 && D_f >= 1, "score_from_mass: H=%d count=%d D_f=%lld must be >= 1", H, count,
                 (long long)D_f);
-  AVITS_REQUIRE(n_t >= 2, "score_from_mass: n_t=%d snapshots (need >= 2)", n_t);
+  AVITS_REQUIRE(n_t >= 2 && n_t <= kMaxSnapshots, "score_from_mass: n_t=%d snapshots outside [2, %d]", n_t,
+                kMaxSnapshots);
   AVITS_REQUIRE(alpha >= 0.f && alpha <= 1.f, "score_from_mass: alpha=%g outside [0, 1]", alpha);
   AVITS_REQUIRE(eps >= 0.f, "score_from_mass: eps=%g < 0", eps);
   if (dtype != AVITS_F32 && dtype != AVITS_BF16)
     return set_error(AVITS_ERR_UNSUPPORTED, "score_from_mass: dtype %d unsupported", dtype);
   AVITS_REQUIRE(mass && snapshots && scores, "score_from_mass: null input/output pointer");
+  Snapshots zs{};
+  for (int k = 0; k < n_t; ++k) {
+    AVITS_REQUIRE(snapshots[k], "score_from_mass: snapshot %d is null", k);
+    zs.p[k] = snapshots[k];
+  }
   const ScoreWs need = score_ws_layout(nullptr, N, H);
   if (!workspace || workspace_bytes < need.bytes)
     return set_error(AVITS_ERR_WORKSPACE, "score_from_mass: workspace of %zu bytes, need %zu", workspace_bytes,
@@ -589,11 +600,11 @@ extern "C" int avits_score_from_mass(const float* mass, int32_t H, int32_t count
   {
     TimedLaunch timed("score_combine", s);
     if (dtype == AVITS_BF16)
-      hipLaunchKernelGGL(mass_temporal_kernel<bf16_t>, dim3(nmm), dim3(256), 0, s, mass, H, inv,
-                         (const bf16_t*)snapshots, n_t, N, D_f, a_dst, v_dst, ws.mm);
+      hipLaunchKernelGGL(mass_temporal_kernel<bf16_t>, dim3(nmm), dim3(256), 0, s, mass, H, inv, zs, n_t, N, D_f,
+                         a_dst, v_dst, ws.mm);
     else
-      hipLaunchKernelGGL(mass_temporal_kernel<float>, dim3(nmm), dim3(256), 0, s, mass, H, inv,
-                         (const float*)snapshots, n_t, N, D_f, a_dst, v_dst, ws.mm);
+      hipLaunchKernelGGL(mass_temporal_kernel<float>, dim3(nmm), dim3(256), 0, s, mass, H, inv, zs, n_t, N, D_f,
+                         a_dst, v_dst, ws.mm);
   }
   const int fblocks = int(std::min<int64_t>(256, (N + 255) / 256));
   TimedLaunch timed("score_finalize", s);

@@ -105,16 +105,27 @@ class StackStep:
     prefix rows ([text; ref]) use the text weights for the text rows and the
     image weights for the reference rows, as in the block.  ``on_block(i, x_in,
     x_out)``, if given, is called after block i is enqueued (for inspection).
+
+    ``fused=True`` takes the spatial importance from the joint-softmax pass
+    itself (avits_joint_attention_stats, the text mass tracked beside the
+    normaliser) and scores with avits_score_from_mass; ``probe_blocks`` lists
+    the double blocks whose first stages are probed, their masses averaged
+    (fused only; the default probes block 0).
     """
 
     def __init__(self, shape: StepShape, doubles: list, singles: list, prefix_pos, dtype, device="cuda",
-                 alpha=0.5, eps=1e-8, mode=B.UP_NEAREST):
+                 alpha=0.5, eps=1e-8, mode=B.UP_NEAREST, fused=False, probe_blocks=(0,)):
         import torch
         s = shape
         if not doubles:
             raise ValueError("the probe needs at least one double block")
         self.shape, self.doubles, self.singles = s, list(doubles), list(singles)
         self.alpha, self.eps, self.mode = alpha, eps, mode
+        self.fused, self.probe_blocks = fused, tuple(probe_blocks)
+        if not self.probe_blocks or any(b < 0 or b >= len(self.doubles) for b in self.probe_blocks):
+            raise ValueError("probe_blocks must name double blocks")
+        if not fused and self.probe_blocks != (0,):
+            raise ValueError("several probe blocks need fused=True")
         f32, i32 = torch.float32, torch.int32
         d = s.D // s.H
         code = B.BF16 if dtype == torch.bfloat16 else B.F32
@@ -123,6 +134,7 @@ class StackStep:
         self.q_img = torch.empty(s.N, s.D, dtype=dtype, device=device)
         self.k_all = torch.empty(LR + s.N, s.D, dtype=dtype, device=device)
         self.lse = torch.empty(s.H, s.N, dtype=f32, device=device)
+        self.mass = torch.empty(s.H, s.N, dtype=f32, device=device)
         self.prefix_pos = torch.as_tensor(prefix_pos, dtype=i32).to(device)
         r = torch.arange(s.N, dtype=i32, device=device)
         W_hr = 2 * s.W_lr
@@ -143,16 +155,27 @@ class StackStep:
         self.ws_block = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
         self.out = None
 
-    def probe(self, x_prev, prefix, stream=None):
+    def _qk(self, w, x_prev, prefix, stream):
         s = self.shape
         LR = s.L + s.R
-        w0 = self.doubles[0]
         if LR:
-            B.avits_block_qk(prefix, self.prefix_pos, s.L, s.R, w0, s.H, self.q_prefix[:LR], self.k_all[:LR],
+            B.avits_block_qk(prefix, self.prefix_pos, s.L, s.R, w, s.H, self.q_prefix[:LR], self.k_all[:LR],
                              self.ws_block, stream)
-        B.avits_block_qk(x_prev, self.img_pos, 0, s.N, w0, s.H, self.q_img, self.k_all[LR:], self.ws_block, stream)
+        B.avits_block_qk(x_prev, self.img_pos, 0, s.N, w, s.H, self.q_img, self.k_all[LR:], self.ws_block, stream)
+
+    def probe(self, x_prev, prefix, stream=None):
+        """The probe blocks' queries and keys, then the joint LSE (and, fused,
+        the text mass summed over the probe blocks)."""
+        s = self.shape
+        LR = s.L + s.R
         d = s.D // s.H
-        B.avits_joint_lse(self.q_img.view(s.N, s.H, d), self.k_all.view(LR + s.N, s.H, d), self.lse, stream)
+        q, k = self.q_img.view(s.N, s.H, d), self.k_all.view(LR + s.N, s.H, d)
+        for n, b in enumerate(self.probe_blocks):
+            self._qk(self.doubles[b], x_prev, prefix, stream)
+            if self.fused:
+                B.avits_joint_attention_stats(q, k, s.L, self.mass, lse=self.lse, accumulate=n > 0, stream=stream)
+            else:
+                B.avits_joint_lse(q, k, self.lse, stream)
 
     def run(self, x_prev, x_prev2, lowres, prefix, canvas, stream=None, on_block=None):
         """X_new (written to ``canvas``, which must not alias x_prev) from X_prev and X_prev2."""
@@ -162,8 +185,12 @@ class StackStep:
         if canvas.data_ptr() == x_prev.data_ptr():
             raise ValueError("canvas must not alias x_prev: X_prev is the next step's X_prev2")
         self.probe(x_prev, prefix, stream)
-        B.avits_score(self.q_img.view(s.N, s.H, d), self.k_all[:s.L].view(s.L, s.H, d), self.lse, x_prev, x_prev2,
-                      self.alpha, self.eps, self.scores, self.a_raw, self.v_raw, self.ws_score, stream)
+        if self.fused:
+            B.avits_score_from_mass(self.mass, len(self.probe_blocks), [x_prev2, x_prev], self.alpha, self.eps,
+                                    self.scores, self.a_raw, self.v_raw, self.ws_score, stream)
+        else:
+            B.avits_score(self.q_img.view(s.N, s.H, d), self.k_all[:s.L].view(s.L, s.H, d), self.lse, x_prev,
+                          x_prev2, self.alpha, self.eps, self.scores, self.a_raw, self.v_raw, self.ws_score, stream)
         if s.k:
             B.avits_select(self.scores, s.k, self.idx, self.ws_select, stream)
         B.avits_gather_upsample(lowres, x_prev, prefix if LR else None, self.idx, s.H_lr, s.W_lr, self.compact,

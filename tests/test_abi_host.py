@@ -165,11 +165,16 @@ def test_stats_and_mass_score_validation(lib):
     assert f(FAKE, FAKE, 5, 5, -1, 2, 64, 1, None, FAKE, 0, None) == INVALID       # L < 0
     assert f(FAKE, FAKE, 5, 5, 2, 2, 96, 1, None, FAKE, 0, None) == UNSUPPORTED    # head dim
     assert f(FAKE, FAKE, 5, 5, 2, 2, 64, 1, None, None, 0, None) == INVALID        # mass required
+    import ctypes
     g = lib.avits_score_from_mass
     ws = lib.avits_score_workspace_bytes(16, 2)
-    assert g(FAKE, 2, 1, FAKE, 1, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # n_t < 2
-    assert g(FAKE, 2, 0, FAKE, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # count < 1
-    assert g(FAKE, 2, 1, FAKE, 2, 16, 8, 1.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # alpha
-    assert g(FAKE, 2, 1, FAKE, 2, 16, 8, 0.5, 1e-8, 9, FAKE, None, None, FAKE, ws, None) == UNSUPPORTED
-    assert g(FAKE, 2, 1, FAKE, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws - 1, None) == WORKSPACE
-    assert g(None, 2, 1, FAKE, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID
+    two = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    assert g(FAKE, 2, 1, two, 1, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # n_t < 2
+    assert g(FAKE, 2, 1, two, 17, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # n_t > 16
+    assert g(FAKE, 2, 0, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # count < 1
+    assert g(FAKE, 2, 1, two, 2, 16, 8, 1.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # alpha
+    assert g(FAKE, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 9, FAKE, None, None, FAKE, ws, None) == UNSUPPORTED
+    assert g(FAKE, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws - 1, None) == WORKSPACE
+    assert g(None, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID
+    holes = (ctypes.c_void_p * 2)(FAKE, None)
+    assert g(FAKE, 2, 1, holes, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # null snapshot

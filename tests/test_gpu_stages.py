@@ -383,7 +383,8 @@ def test_score_from_mass(gpu, w, n_t):
     s = torch.empty(w.N, device="cuda")
     a = torch.empty(w.N, device="cuda")
     v = torch.empty(w.N, device="cuda")
-    gpu.avits_score_from_mass(dev(2 * mass), 2, dev(snaps, w.dtype), w.alpha, w.eps_minmax, s, a_raw=a, v_raw=v)
+    gpu.avits_score_from_mass(dev(2 * mass), 2, [dev(z, w.dtype) for z in snaps], w.alpha, w.eps_minmax, s,
+                              a_raw=a, v_raw=v)
     torch.cuda.synchronize()
     s_ref, a_ref, v_ref = oracle.score_from_mass(2 * mass.astype(np.float64), 2, snaps, w.alpha, w.eps_minmax)
     assert_close(host(a), a_ref, w.dtype, "A")
@@ -403,7 +404,7 @@ def test_fused_mass_score_matches_query_key_score(gpu, w):
     mass = torch.empty(w.H, w.N, device="cuda")
     gpu.avits_joint_attention_stats(q, dev(k_all, w.dtype), w.L, mass, lse=lse)
     s1 = torch.empty(w.N, device="cuda")
-    gpu.avits_score_from_mass(mass, 1, dev(np.stack([si["feat_prev"], si["feat_t"]]), w.dtype), w.alpha,
+    gpu.avits_score_from_mass(mass, 1, [dev(si["feat_prev"], w.dtype), dev(si["feat_t"], w.dtype)], w.alpha,
                               w.eps_minmax, s1)
     s2 = torch.empty(w.N, device="cuda")
     gpu.avits_score(q, dev(si["text_k"], w.dtype), lse, dev(si["feat_t"], w.dtype), dev(si["feat_prev"], w.dtype),
