@@ -20,6 +20,7 @@ from .importance import (  # noqa: F401
 from .selection import select_topk  # noqa: F401
 from .relayout import (  # noqa: F401
     upsample_nearest, upsample_bilinear, gather_upsample, scatter, selected_positions,
+    mixed_layout, gather_mixed, scatter_mixed,
 )
 from .block import (  # noqa: F401
     layer_norm, rms_norm, rope_angles, apply_rope, attention, gelu_tanh,

@@ -59,7 +59,11 @@ def rope_axes(d: int):
 
 
 def rope_angles(pos, d: int, theta: float = ROPE_THETA):
-    """Rotation angle of each adjacent pair: [S, d/2] for integer pos [S, 3]."""
+    """Rotation angle of each adjacent pair: [S, d/2] for pos [S, 3].
+
+    Positions are real: the grid's are integers, the low-res tokens of the
+    mixed-resolution Stage-2 sequence sit at half-integer block centres.
+    """
     pos = np.asarray(pos, dtype=np.float64)
     parts = []
     for a, n in enumerate(rope_axes(d)):

@@ -81,6 +81,12 @@ def keep_count(rho: float, n: int) -> int:
     return int(math.floor(rho * n + 0.5))
 
 
+def mixed_keep_count(rho: float, n_lr: int) -> int:
+    """Low-res tokens expanded in the mixed-resolution sequence: floor(rho M')
+    (Section 3.2, Stage 2), computed in fp64."""
+    return int(math.floor(rho * n_lr))
+
+
 # Tiny fp32 block: hidden 256, 4x64 heads, 32 text tokens, 16x16 -> 32x32.
 TINY_F32 = Workload("tiny_f32_d256", "f32", D=256, H=4, d=64, L=32, R=0,
                     H_lr=16, W_lr=16, rho=0.25, alpha=0.5, weight_std=None, seed=0)

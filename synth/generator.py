@@ -203,6 +203,13 @@ def random_selection(w: Workload, k: int, tid_offset: int = 0) -> np.ndarray:
     return np.sort(g.permutation(w.N)[:k]).astype(np.int32)
 
 
+def random_lowres_selection(w: Workload, k: int, tid_offset: int = 0) -> np.ndarray:
+    """k distinct low-res indices in ascending order (a stand-in selection at
+    the low-res granularity of the mixed-resolution sequence)."""
+    g = rng(w.seed, _TID["sel_perm"] + 50 + tid_offset)
+    return np.sort(g.permutation(w.N_lr)[:k]).astype(np.int32)
+
+
 def quantised_scores(seed: int, n: int, levels: int) -> np.ndarray:
     """fp32 scores with heavy duplicates: ``levels`` distinct values in [0, 1)."""
     g = rng(seed, _TID["scores_dup"])

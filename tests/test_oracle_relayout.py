@@ -80,3 +80,104 @@ def test_scatter_roundtrip():
     np.testing.assert_array_equal(c2[idx], out[5:])
     rest = np.setdiff1d(np.arange(64), idx)
     np.testing.assert_array_equal(c2[rest], canvas[rest])
+
+
+# ---------------------------------------------------------------------------
+# The mixed-resolution Stage-2 sequence (Section 3.2): selected low-res tokens
+# expanded to 2x2 children, the rest kept at low resolution.
+
+def _hr_index(pos_half, W_lr):
+    """High-res raster index of a child from its half-unit position."""
+    return (pos_half[:, 1] // 2) * (2 * W_lr) + pos_half[:, 2] // 2
+
+
+def test_mixed_worked_example():
+    # M' = 2x2, parents 1 = (0, 1) and 2 = (1, 0) selected; worked by hand.
+    # Children come parent by parent in (dr, dc) raster order at twice their
+    # high-res coordinate; kept parents 0 and 3 sit at their block centres
+    # (0.5, 0.5) and (2.5, 2.5), i.e. (1, 1) and (5, 5) in half units.
+    low = np.arange(8, dtype=float).reshape(4, 2)
+    pre = np.full((1, 2), -1.0)
+    compact, pos, children = oracle.gather_mixed(low, pre, [1, 2], 2, 2)
+    assert pos.tolist() == [[0, 0, 4], [0, 0, 6], [0, 2, 4], [0, 2, 6],
+                            [0, 4, 0], [0, 4, 2], [0, 6, 0], [0, 6, 2],
+                            [0, 1, 1], [0, 5, 5]]
+    assert children.tolist() == [2, 3, 6, 7, 8, 9, 12, 13]
+    want = [[-1, -1]] + [[2, 3]] * 4 + [[4, 5]] * 4 + [[0, 1], [6, 7]]
+    np.testing.assert_array_equal(compact, want)
+
+
+@pytest.mark.parametrize("mode,up", [("nearest", oracle.upsample_nearest), ("bilinear", oracle.upsample_bilinear)])
+def test_mixed_keep_all_is_the_upsampled_grid(mode, up):
+    # rho = 1: every token expanded; placing each row at the pixel its
+    # position names rebuilds the 2x upsampled grid, and the children are
+    # every high-res index.
+    H, W, D = 3, 5, 4
+    low = _grid(H, W, D, seed=11)
+    compact, pos, children = oracle.gather_mixed(low, None, np.arange(H * W), H, W, mode)
+    assert compact.shape == (4 * H * W, D)
+    assert (pos % 2 == 0).all()
+    q = _hr_index(pos, W)
+    assert sorted(q.tolist()) == list(range(4 * H * W))
+    grid = np.empty((4 * H * W, D))
+    grid[q] = compact
+    np.testing.assert_array_equal(grid, up(low, H, W))
+    np.testing.assert_array_equal(children, np.arange(4 * H * W))
+
+
+def test_mixed_keep_none_is_the_lowres_grid():
+    H, W, D = 4, 3, 2
+    low = _grid(H, W, D, seed=12)
+    pre = _grid(1, 3, D, seed=13)
+    compact, pos, children = oracle.gather_mixed(low, pre, np.zeros(0, np.int64), H, W)
+    np.testing.assert_array_equal(compact, np.concatenate([pre, low]))
+    assert children.shape == (0,)
+    # A kept token sits at the mean of its four children's positions.
+    _, pos_all, _ = oracle.gather_mixed(low, None, np.arange(H * W), H, W)
+    centres = pos_all.reshape(H * W, 4, 3).mean(axis=1)
+    np.testing.assert_array_equal(pos, centres)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_mixed_partition_and_roundtrip(seed):
+    g = np.random.default_rng(seed)
+    H, W, D = 5, 6, 3
+    Mp = H * W
+    k = int(g.integers(1, Mp))
+    idx = np.sort(g.permutation(Mp)[:k])
+    low = g.standard_normal((Mp, D))
+    pre = g.standard_normal((2, D))
+    compact, pos, children = oracle.gather_mixed(low, pre, idx, H, W)
+    assert compact.shape == (2 + 4 * k + Mp - k, D) and pos.shape == (4 * k + Mp - k, 3)
+    # Every low-res cell is covered once: by its four children or by itself.
+    cover = np.zeros((2 * H, 2 * W), dtype=int)
+    for (_, r2, c2) in pos:
+        if r2 % 2 == 0:
+            cover[r2 // 2, c2 // 2] += 1
+        else:
+            cover[(r2 - 1) // 2:(r2 + 3) // 2, (c2 - 1) // 2:(c2 + 3) // 2] += 1
+    assert (cover == 1).all()
+    assert len({tuple(p) for p in pos}) == len(pos)
+    assert (np.diff(children) > 0).all()
+    np.testing.assert_array_equal(np.sort(_hr_index(pos[:4 * k], W)), children)
+    # Identity blocks: the scatter sends every row back where it came from.
+    canvas0 = g.standard_normal((4 * Mp, D))
+    state0 = g.standard_normal((Mp, D))
+    canvas, state = oracle.scatter_mixed(compact, idx, 2, H, W, canvas0, state0)
+    up = oracle.upsample_nearest(low, H, W)
+    np.testing.assert_array_equal(canvas[children], up[children])
+    rest = np.setdiff1d(np.arange(4 * Mp), children)
+    np.testing.assert_array_equal(canvas[rest], canvas0[rest])
+    kept = np.setdiff1d(np.arange(Mp), idx)
+    np.testing.assert_array_equal(state[kept], low[kept])
+    np.testing.assert_array_equal(state[idx], state0[idx])
+    # Stage 3: expanding the kept tokens over that canvas gives the upsampled grid.
+    _, _, full = oracle.gather_upsample(state, canvas, None, children, H, W)
+    np.testing.assert_array_equal(full, up)
+
+
+def test_half_unit_positions_rotate_halfway():
+    # A token between two grid positions is rotated by the mean of their angles.
+    pos = np.array([[0, 3, 4], [0, 4, 5], [0, 3.5, 4.5]])
+    ang = oracle.rope_angles(pos, 64)
+    np.testing.assert_allclose(ang[2], (ang[0] + ang[1]) / 2, rtol=0, atol=1e-12)
