@@ -200,6 +200,77 @@ def _select_sweep(avits, torch, reps: int = 10) -> list:
     return out
 
 
+def _mixed_stage2(avits, torch, w, text, bw, reps: int = 10) -> dict:
+    """The paper's own Stage 2 at the same shape (Section 3.2): selection over
+    the M' low-res tokens, K = floor(rho M') expanded 2x2 and the rest kept at
+    low resolution in one mixed sequence; one double block on it.  Times the
+    transition (probe, text mass, score, select, gather_mixed), one step (the
+    block, half-unit RoPE) and the re-layout back (scatter_mixed)."""
+    import numpy as np
+    from paper_2608_17995_amd.step import MixedStage2
+    from synth import configs as C
+    from synth import generator as G
+    Mp = w.N_lr
+    K = C.mixed_keep_count(w.rho, Mp)
+    feat_t, feat_prev, _ = G.feature_pair(w.seed + 17, Mp, w.D, w.dtype)
+
+    def cuda(a):
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16).cuda()
+
+    z, z_prev = cuda(feat_t), cuda(feat_prev)
+    m = MixedStage2(w.H_lr, w.W_lr, w.L, w.R, K, w.D, w.H, w.mlp_ratio * w.D, [bw], [],
+                    G.prefix_positions(w), torch.bfloat16, alpha=w.alpha, eps=w.eps_minmax)
+    canvas = torch.empty(w.N, w.D, dtype=torch.bfloat16, device="cuda")
+    state = torch.empty_like(z)
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record()
+        for _ in range(reps):
+            fn()
+        e[1].record()
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / reps
+
+    t_trans = timed(lambda: m.transition(z, [z_prev, z], text))
+    x0 = m.x.clone()
+
+    def one_step():
+        m.x.copy_(x0)      # restart from the transition's sequence (copy timed separately below)
+        m.step()
+
+    t_copy = timed(lambda: m.x.copy_(x0))
+    t_step = timed(one_step) - t_copy
+    t_leave = timed(lambda: m.leave(canvas, state))
+    avits.avits_timing_reset()
+    avits.avits_timing_enable(True)
+    for _ in range(reps):
+        m.transition(z, [z_prev, z], text)
+        m.leave(canvas, state)
+    torch.cuda.synchronize()
+    avits.avits_timing_enable(False)
+    g_ms, g_n = avits.avits_timing_read("gather_mixed")
+    s_ms, s_n = avits.avits_timing_read("scatter_mixed")
+    e, D, S = 2, w.D, m.S
+    gather_bytes = (w.LR + Mp) * D * e + S * D * e + (S - w.LR) * 12 + 16 * K + 4 * K
+    scatter_bytes = 2 * (S - w.LR) * D * e + 4 * K
+    fl = block_flops(S, D, w.mlp_ratio * D)
+    g_us, s_us = 1e3 * g_ms / max(g_n, 1), 1e3 * s_ms / max(s_n, 1)
+    return {
+        "lowres_tokens": Mp, "K": K, "seq_len": S,
+        "seq_len_compacted_path": w.S,
+        "transition_ms": round(t_trans, 4), "block_step_ms": round(t_step, 4), "leave_ms": round(t_leave, 4),
+        "block_tflops": round(fl["total"] / (t_step / 1e3) / 1e12, 1),
+        "gather_mixed_us": round(g_us, 2), "scatter_mixed_us": round(s_us, 2),
+        "gather_mixed_gbs": round(gather_bytes / (g_us / 1e6) / 1e9, 1) if g_us > 0 else None,
+        "scatter_mixed_gbs": round(scatter_bytes / (s_us / 1e6) / 1e9, 1) if s_us > 0 else None,
+        "gather_mixed_bytes": gather_bytes, "scatter_mixed_bytes": scatter_bytes,
+    }
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -394,6 +465,7 @@ def main(argv=None):
     }
     result["fused_scoring"] = _fused_scoring(avits, torch, w, q, k_all, kt, high, fp, lse)
     result["select_sweep"] = _select_sweep(avits, torch)
+    result["mixed_stage2"] = _mixed_stage2(avits, torch, w, text, bw)
     if not args.no_cpu_baseline:
         host = dict(si)
         host.update(lay)

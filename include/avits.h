@@ -143,7 +143,10 @@ int avits_gather_upsample(const void* lowres, const void* highres_prev, const vo
  * single (shift, scale, gate).  Weights use the [out, in] layout.
  *
  * x_in, x_out [S, D] with S = n_txt + n_img, D = H*d (x_out must not alias
- * x_in); pos [S, 3] int32; lse_out [H, S] fp32 or NULL.  For the single kind
+ * x_in); pos [S, 3] int32, RoPE position = pos * pos_scale with pos_scale in
+ * (0, 1] (1: integer grid positions; 0.5: positions given in half units, as
+ * the mixed-resolution sequence of avits_gather_mixed has them); lse_out
+ * [H, S] fp32 or NULL.  For the single kind
  * n_txt only splits the count (both parts use the same weights).  S == 0 is a
  * no-op.  Requires d in {64, 128}; all weight pointers of the used kind
  * non-NULL.
@@ -181,7 +184,7 @@ typedef struct avits_block_weights {
 
 size_t avits_block_workspace_bytes(int32_t kind, int64_t S, int32_t H, int32_t d,
                                    int32_t mlp_hidden, int dtype);
-int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos,
+int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,
                         int64_t n_txt, int64_t n_img, const avits_block_weights* w,
                         int32_t H, int32_t d, int dtype, float* lse_out,
                         void* workspace, size_t workspace_bytes, void* stream);
@@ -203,7 +206,7 @@ int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos,
  * and errors as avits_block_forward.
  * ---------------------------------------------------------------------- */
 size_t avits_block_qk_workspace_bytes(int64_t S, int32_t H, int32_t d, int dtype);
-int avits_block_qk(const void* x_in, const int32_t* pos, int64_t n_txt, int64_t n_img,
+int avits_block_qk(const void* x_in, const int32_t* pos, float pos_scale, int64_t n_txt, int64_t n_img,
                    const avits_block_weights* w, int32_t H, int32_t d, int dtype,
                    void* q_out, void* k_out, void* workspace, size_t workspace_bytes,
                    void* stream);
@@ -215,6 +218,49 @@ int avits_block_qk(const void* x_in, const int32_t* pos, int64_t n_txt, int64_t 
  * ---------------------------------------------------------------------- */
 int avits_scatter(const void* out, const int32_t* idx, int64_t k, int64_t row_offset,
                   int64_t D, int dtype, void* canvas, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_gather_mixed — the mixed-resolution sequence of Stage 2 (Section
+ * 3.2): the tokens selected at low-res granularity are expanded to their four
+ * high-res children by 2x upsampling; the other M' - K low-res tokens stay in
+ * the sequence at low resolution.
+ *   compact rows [0, n_prefix)          = prefix
+ *   compact row n_prefix + 4j + 2dr + dc = up(lowres) at high-res pixel
+ *       (2r + dr, 2c + dc), (r, c) = divmod(idx[j], W_lr), dr, dc in {0, 1}
+ *   compact row n_prefix + 4K + m       = lowres[p_m], p_m the m-th
+ *       unselected low-res index in ascending order
+ * up() is nearest (the parent's row) or bilinear (as avits_gather_upsample).
+ * pos [4K + M' - K, 3] int32 is written for the rows after the prefix, in
+ * half units (twice the high-res coordinate, so a low-res token at its 2x2
+ * block centre stays integral): a child (0, 2(2r+dr), 2(2c+dc)); a kept
+ * token (0, 4r + 1, 4c + 1).  Run the block with pos_scale = 0.5 on these
+ * and with the prefix positions doubled.  children [4K] int32, if not NULL,
+ * receives the children's high-res raster indices in ascending order (the
+ * idx avits_gather_upsample and avits_scatter take for the Stage-3 full
+ * expansion).
+ * lowres [M', D] with M' = H_lr * W_lr; prefix [n_prefix, D] (may be NULL if
+ * n_prefix == 0); idx [K] int32, ascending and unique in [0, M') (as
+ * avits_select writes it; other contents give unspecified rows but no access
+ * outside the buffers); compact [n_prefix + 3K + M', D], not aliasing the
+ * inputs.  Requires D * elem_size % 16 == 0.  0 <= K <= M'.
+ * ---------------------------------------------------------------------- */
+int avits_gather_mixed(const void* lowres, const void* prefix, const int32_t* idx, int64_t k,
+                       int32_t H_lr, int32_t W_lr, int64_t n_prefix, int64_t D, int mode, int dtype,
+                       void* compact, int32_t* pos, int32_t* children, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_scatter_mixed — the inverse re-layout after the Stage-2 blocks: each
+ * expanded row goes to its high-res pixel, each kept row to its low-res slot.
+ *   canvas_hr[(2r+dr) * 2W_lr + 2c+dc] = out[row_offset + 4j + 2dr + dc]
+ *   state_lr[p_m]                       = out[row_offset + 4K + m]
+ * with the layout of avits_gather_mixed.  out [row_offset + 3K + M', D];
+ * canvas_hr [4M', D] (may be NULL if K == 0); state_lr [M', D] (may be NULL
+ * if K == M'; may alias the gather's lowres).  Other rows of canvas_hr and
+ * state_lr are left as they are.  idx and errors as avits_gather_mixed.
+ * ---------------------------------------------------------------------- */
+int avits_scatter_mixed(const void* out, const int32_t* idx, int64_t k, int32_t H_lr, int32_t W_lr,
+                        int64_t row_offset, int64_t D, int dtype, void* canvas_hr, void* state_lr,
+                        void* stream);
 
 /* ------------------------------------------------------------------------
  * avits_joint_lse — log-sum-exp of each image query's logits over the joint
@@ -272,7 +318,8 @@ int avits_score_from_mass(const float* mass, int32_t H, int32_t count,
  * "select", "gather_upsample", "scatter", "ln_mod", "gemm_qkv", "gemm_o",
  * "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
  * "splitk_reduce", "qk_rope", "attention", "joint_lse" (also the
- * statistics pass of avits_joint_attention_stats); "gemm" returns the
+ * statistics pass of avits_joint_attention_stats), "gather_mixed",
+ * "scatter_mixed"; "gemm" returns the
  * sum of the six GEMM families (the GEMM kernels alone: the split-K
  * reduction that follows a split launch is "splitk_reduce").  Unknown
  * family -> AVITS_ERR_INVALID_ARG.

@@ -47,13 +47,17 @@ _SIGS = {
                                              _i64, ctypes.c_int, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p,
                                              _c_void_p]),
     "avits_block_workspace_bytes": (_size, [_i32, _i64, _i32, _i32, _i32, ctypes.c_int]),
-    "avits_block_forward": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _i64,
+    "avits_block_forward": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _f32, _i64, _i64,
                                            ctypes.POINTER(_BlockWeights), _i32, _i32, ctypes.c_int, _c_void_p,
                                            _c_void_p, _size, _c_void_p]),
     "avits_block_qk_workspace_bytes": (_size, [_i64, _i32, _i32, ctypes.c_int]),
-    "avits_block_qk": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, ctypes.POINTER(_BlockWeights), _i32, _i32,
+    "avits_block_qk": (ctypes.c_int, [_c_void_p, _c_void_p, _f32, _i64, _i64, ctypes.POINTER(_BlockWeights), _i32, _i32,
                                       ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, ctypes.c_int, _c_void_p, _c_void_p]),
+    "avits_gather_mixed": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _i32, _i32, _i64, _i64,
+                                          ctypes.c_int, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _c_void_p]),
+    "avits_scatter_mixed": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i32, _i32, _i64, _i64, ctypes.c_int,
+                                           _c_void_p, _c_void_p, _c_void_p]),
     "avits_joint_lse": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i32, _i32, ctypes.c_int, _c_void_p,
                                        _c_void_p]),
     "avits_joint_attention_stats": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, _i32, _i32, ctypes.c_int,
@@ -191,6 +195,30 @@ def avits_scatter(out, idx, row_offset, canvas, stream=None):
     return canvas
 
 
+def avits_gather_mixed(lowres, prefix, idx, H_lr, W_lr, compact, pos, children=None, mode=UP_NEAREST,
+                       stream=None):
+    import torch
+    dt = lowres.dtype
+    n_prefix = 0 if prefix is None else prefix.shape[0]
+    k = 0 if idx is None else idx.shape[0]
+    _check(load().avits_gather_mixed(
+        _dev(lowres, "lowres"), _dev(prefix, "prefix", dt) if n_prefix else None,
+        _dev(idx, "idx", torch.int32) if k else None, k, H_lr, W_lr, n_prefix, lowres.shape[1], mode,
+        _dtype_code(lowres), _dev(compact, "compact", dt), _dev(pos, "pos", torch.int32),
+        _dev(children, "children", torch.int32), _stream(stream)))
+    return compact, pos, children
+
+
+def avits_scatter_mixed(out, idx, H_lr, W_lr, row_offset, canvas_hr, state_lr, stream=None):
+    import torch
+    dt = out.dtype
+    k = 0 if idx is None else idx.shape[0]
+    _check(load().avits_scatter_mixed(
+        _dev(out, "out"), _dev(idx, "idx", torch.int32) if k else None, k, H_lr, W_lr, row_offset, out.shape[1],
+        _dtype_code(out), _dev(canvas_hr, "canvas_hr", dt), _dev(state_lr, "state_lr", dt), _stream(stream)))
+    return canvas_hr, state_lr
+
+
 def avits_joint_lse(q, k_all, lse, stream=None):
     import torch
     N, H, d = q.shape
@@ -242,7 +270,7 @@ def avits_block_workspace_bytes(kind: int, S: int, H: int, d: int, mlp_hidden: i
 
 
 def avits_block_forward(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H, lse_out=None,
-                        workspace=None, stream=None):
+                        workspace=None, stream=None, pos_scale=1.0):
     import torch
     S, D = x_in.shape
     d = D // H
@@ -250,7 +278,7 @@ def avits_block_forward(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H
     ws, wsp, wsb = _workspace(
         workspace, avits_block_workspace_bytes(weights.kind, S, H, d, weights.c.mlp_hidden, code), x_in.device)
     _check(load().avits_block_forward(
-        _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), n_txt, n_img,
+        _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), pos_scale, n_txt, n_img,
         ctypes.byref(weights.c), H, d, code, _dev(lse_out, "lse_out", torch.float32), wsp, wsb, _stream(stream)))
     return x_out
 
@@ -259,7 +287,8 @@ def avits_block_qk_workspace_bytes(S: int, H: int, d: int, dtype: int) -> int:
     return load().avits_block_qk_workspace_bytes(S, H, d, dtype)
 
 
-def avits_block_qk(x_in, pos, n_txt, n_img, weights: BlockWeights, H, q_out, k_out, workspace=None, stream=None):
+def avits_block_qk(x_in, pos, n_txt, n_img, weights: BlockWeights, H, q_out, k_out, workspace=None, stream=None,
+                   pos_scale=1.0):
     """q_out, k_out [S, D] (or [S, H, d]): the block's normalised, rotated queries and keys."""
     import torch
     S, D = x_in.shape
@@ -267,7 +296,7 @@ def avits_block_qk(x_in, pos, n_txt, n_img, weights: BlockWeights, H, q_out, k_o
     code = _dtype_code(x_in)
     ws, wsp, wsb = _workspace(workspace, avits_block_qk_workspace_bytes(S, H, d, code), x_in.device)
     _check(load().avits_block_qk(
-        _dev(x_in, "x_in"), _dev(pos, "pos", torch.int32), n_txt, n_img, ctypes.byref(weights.c), H, d, code,
+        _dev(x_in, "x_in"), _dev(pos, "pos", torch.int32), pos_scale, n_txt, n_img, ctypes.byref(weights.c), H, d, code,
         _dev(q_out, "q_out", x_in.dtype), _dev(k_out, "k_out", x_in.dtype), wsp, wsb, _stream(stream)))
     return q_out, k_out
 

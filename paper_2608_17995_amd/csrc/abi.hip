@@ -33,7 +33,8 @@ int launch_status(const char* what) {
 static const char* const kFamilies[] = {"score_spatial", "score_combine", "score_finalize", "select",
                                         "gather_upsample", "scatter", "ln_mod", "gemm_qkv", "gemm_o",
                                         "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
-                                        "splitk_reduce", "qk_rope", "attention", "joint_lse"};
+                                        "splitk_reduce", "qk_rope", "attention", "joint_lse",
+                                        "gather_mixed", "scatter_mixed"};
 constexpr int kNumFamilies = sizeof(kFamilies) / sizeof(kFamilies[0]);
 
 struct Pending {

@@ -140,7 +140,7 @@ __device__ __forceinline__ void store8(float* p, const float (&x)[8]) {
 // time.
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ q, T* __restrict__ k, int64_t ld,
-                                                           const int32_t* __restrict__ pos,
+                                                           const int32_t* __restrict__ pos, float pos_scale,
                                                            int64_t S, int H, int64_t n_a, const T* __restrict__ gq_a,
                                                            const T* __restrict__ gk_a, const T* __restrict__ gq_b,
                                                            const T* __restrict__ gk_b) {
@@ -163,7 +163,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ q, T*
     const int mi = axis == 0 ? m : (axis == 1 ? m - p0 : m - p0 - p1);
     const int na = axis == 0 ? 2 * p0 : 2 * p1;
     const float freq = exp2f(-2.f * float(mi) / float(na) * kLog2Theta);
-    sincosf(float(pr[axis]) * freq, &sn[j], &cs[j]);
+    sincosf(float(pr[axis]) * pos_scale * freq, &sn[j], &cs[j]);
   }
   T* const qrow = q + row * ld;
   T* const krow = k + row * ld;
@@ -264,8 +264,8 @@ int launch_ln_mod(const T* x, T* h, int64_t S, int64_t D, int64_t n_txt, const a
 
 // RMSNorm * g and RoPE of q and k in place, with each stream's gains.
 template <typename T>
-int launch_qk_norm_rope(T* q, T* k, int64_t ld, const int32_t* pos, int64_t S, int64_t n_txt, int H, int d,
-                        const avits_block_weights* w, hipStream_t s) {
+int launch_qk_norm_rope(T* q, T* k, int64_t ld, const int32_t* pos, float pos_scale, int64_t S, int64_t n_txt, int H,
+                        int d, const avits_block_weights* w, hipStream_t s) {
   const T *gqa, *gka, *gqb, *gkb;
   int64_t na;
   if (w->kind == AVITS_BLOCK_DOUBLE) {
@@ -282,19 +282,20 @@ int launch_qk_norm_rope(T* q, T* k, int64_t ld, const int32_t* pos, int64_t S, i
   const dim3 rows_grid(unsigned(ceil_div64(S, 4))), blk(256);
   TimedLaunch timed("qk_rope", s);
   if (d == 128)
-    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 128>), rows_grid, blk, 0, s, q, k, ld, pos, S, H, na, gqa, gka, gqb,
-                       gkb);
+    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 128>), rows_grid, blk, 0, s, q, k, ld, pos, pos_scale, S, H, na, gqa,
+                       gka, gqb, gkb);
   else
-    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 64>), rows_grid, blk, 0, s, q, k, ld, pos, S, H, na, gqa, gka, gqb,
-                       gkb);
+    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 64>), rows_grid, blk, 0, s, q, k, ld, pos, pos_scale, S, H, na, gqa,
+                       gka, gqb, gkb);
   return launch_status("block qk_norm_rope");
 }
 
 // The block's first stage alone: LN + modulation, the q and k projections,
 // RMSNorm and RoPE, written to q_out [S, D] and k_out [S, D].
 template <typename T>
-int run_block_qk(const void* x_in, const int32_t* pos, int64_t n_txt, int64_t n_img, const avits_block_weights* w,
-                 int H, int d, int dtype, void* q_out, void* k_out, void* h_ws, hipStream_t s) {
+int run_block_qk(const void* x_in, const int32_t* pos, float pos_scale, int64_t n_txt, int64_t n_img,
+                 const avits_block_weights* w, int H, int d, int dtype, void* q_out, void* k_out, void* h_ws,
+                 hipStream_t s) {
   const int64_t S = n_txt + n_img, D = int64_t(H) * d;
   T* h = static_cast<T*>(h_ws);
   T* q = static_cast<T*>(q_out);
@@ -326,11 +327,11 @@ int run_block_qk(const void* x_in, const int32_t* pos, int64_t n_txt, int64_t n_
   if ((rc = launch_gemm(g, dtype, s, w->kind == AVITS_BLOCK_DOUBLE ? "gemm_qkv" : "gemm_single_in", nullptr, 0)) !=
       AVITS_OK)
     return rc;
-  return launch_qk_norm_rope<T>(q, k, D, pos, S, n_txt, H, d, w, s);
+  return launch_qk_norm_rope<T>(q, k, D, pos, pos_scale, S, n_txt, H, d, w, s);
 }
 
 template <typename T>
-int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, int64_t n_img,
+int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale, int64_t n_txt, int64_t n_img,
               const avits_block_weights* w, int H, int d, int dtype, float* lse_out, const BlockWs& ws,
               hipStream_t s) {
   const int64_t S = n_txt + n_img, D = int64_t(H) * d, F = w->mlp_hidden;
@@ -389,7 +390,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt, 
   }
 
   // 3. q/k RMSNorm + RoPE in place.
-  if ((rc = launch_qk_norm_rope<T>(qk, qk + D, 2 * D, pos, S, n_txt, H, d, w, s)) != AVITS_OK) return rc;
+  if ((rc = launch_qk_norm_rope<T>(qk, qk + D, 2 * D, pos, pos_scale, S, n_txt, H, d, w, s)) != AVITS_OK) return rc;
 
   // 4. joint attention over all S rows.
   {
@@ -481,12 +482,13 @@ namespace avits {
 namespace {
 // Host-side checks shared by avits_block_forward and avits_block_qk; returns
 // AVITS_OK or the error code (with the message set).
-int check_block_args(const char* fn, const void* x_in, const int32_t* pos, int64_t n_txt, int64_t n_img,
-                     const avits_block_weights* w, int32_t H, int32_t d, int dtype) {
+int check_block_args(const char* fn, const void* x_in, const int32_t* pos, float pos_scale, int64_t n_txt,
+                     int64_t n_img, const avits_block_weights* w, int32_t H, int32_t d, int dtype) {
   AVITS_REQUIRE(w, "%s: null weights", fn);
   AVITS_REQUIRE(n_txt >= 0 && n_img >= 0, "%s: n_txt=%lld n_img=%lld must be >= 0", fn, (long long)n_txt,
                 (long long)n_img);
   AVITS_REQUIRE(H >= 1, "%s: H=%d < 1", fn, H);
+  AVITS_REQUIRE(pos_scale > 0.f && pos_scale <= 1.f, "%s: pos_scale=%g outside (0, 1]", fn, pos_scale);
   if (d != 64 && d != 128) return set_error(AVITS_ERR_UNSUPPORTED, "%s: head dim %d (need 64 or 128)", fn, d);
   if (dtype != AVITS_F32 && dtype != AVITS_BF16)
     return set_error(AVITS_ERR_UNSUPPORTED, "%s: dtype %d unsupported", fn, dtype);
@@ -515,10 +517,10 @@ extern "C" size_t avits_block_qk_workspace_bytes(int64_t S, int32_t H, int32_t d
   return align_up(size_t(S) * size_t(H) * size_t(d) * (dtype == AVITS_F32 ? 4 : 2), 256);
 }
 
-extern "C" int avits_block_qk(const void* x_in, const int32_t* pos, int64_t n_txt, int64_t n_img,
+extern "C" int avits_block_qk(const void* x_in, const int32_t* pos, float pos_scale, int64_t n_txt, int64_t n_img,
                               const avits_block_weights* w, int32_t H, int32_t d, int dtype, void* q_out, void* k_out,
                               void* workspace, size_t workspace_bytes, void* stream) {
-  int rc = check_block_args("block_qk", x_in, pos, n_txt, n_img, w, H, d, dtype);
+  int rc = check_block_args("block_qk", x_in, pos, pos_scale, n_txt, n_img, w, H, d, dtype);
   if (rc != AVITS_OK) return rc;
   const int64_t S = n_txt + n_img;
   if (S == 0) return AVITS_OK;
@@ -528,14 +530,15 @@ extern "C" int avits_block_qk(const void* x_in, const int32_t* pos, int64_t n_tx
     return set_error(AVITS_ERR_WORKSPACE, "block_qk: workspace of %zu bytes, need %zu", workspace_bytes, need);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == AVITS_BF16)
-    return run_block_qk<bf16_t>(x_in, pos, n_txt, n_img, w, H, d, dtype, q_out, k_out, workspace, s);
-  return run_block_qk<float>(x_in, pos, n_txt, n_img, w, H, d, dtype, q_out, k_out, workspace, s);
+    return run_block_qk<bf16_t>(x_in, pos, pos_scale, n_txt, n_img, w, H, d, dtype, q_out, k_out, workspace, s);
+  return run_block_qk<float>(x_in, pos, pos_scale, n_txt, n_img, w, H, d, dtype, q_out, k_out, workspace, s);
 }
 
-extern "C" int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, int64_t n_txt,
-                                   int64_t n_img, const avits_block_weights* w, int32_t H, int32_t d, int dtype,
-                                   float* lse_out, void* workspace, size_t workspace_bytes, void* stream) {
-  int rc = check_block_args("block_forward", x_in, pos, n_txt, n_img, w, H, d, dtype);
+extern "C" int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,
+                                   int64_t n_txt, int64_t n_img, const avits_block_weights* w, int32_t H, int32_t d,
+                                   int dtype, float* lse_out, void* workspace, size_t workspace_bytes,
+                                   void* stream) {
+  int rc = check_block_args("block_forward", x_in, pos, pos_scale, n_txt, n_img, w, H, d, dtype);
   if (rc != AVITS_OK) return rc;
   const int64_t S = n_txt + n_img;
   if (S == 0) return AVITS_OK;
@@ -548,6 +551,7 @@ extern "C" int avits_block_forward(const void* x_in, void* x_out, const int32_t*
                      need.bytes);
   const BlockWs ws = block_ws_layout(static_cast<char*>(workspace), w->kind, S, H, d, w->mlp_hidden, esz);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (dtype == AVITS_BF16) return run_block<bf16_t>(x_in, x_out, pos, n_txt, n_img, w, H, d, dtype, lse_out, ws, s);
-  return run_block<float>(x_in, x_out, pos, n_txt, n_img, w, H, d, dtype, lse_out, ws, s);
+  if (dtype == AVITS_BF16)
+    return run_block<bf16_t>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, lse_out, ws, s);
+  return run_block<float>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, lse_out, ws, s);
 }

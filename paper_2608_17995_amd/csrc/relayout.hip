@@ -121,6 +121,122 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void scatter_kernel(
                 reinterpret_cast<char*>(canvas + int64_t(idx[j]) * D), D * int64_t(sizeof(T)), lane);
 }
 
+// ---------------------------------------------------------------------------
+// The mixed-resolution sequence of Stage 2 (Section 3.2): the K selected
+// low-res tokens are expanded to their four high-res children, the other
+// M' - K stay at low resolution, all in one sequence behind the prefix.
+// Rows: parent idx[j]'s children at 4j + 2 dr + dc (raster order inside the
+// 2x2 block), then the kept parents in ascending order.  Positions are in
+// half units (twice the high-res coordinate): a child (2r+dr, 2c+dc) sits at
+// (0, 2(2r+dr), 2(2c+dc)), a kept token at its block centre (0, 4r+1, 4c+1).
+//
+// One wave per low-res parent.  A selected parent's four rows are written
+// from one read of its low-res row (nearest) or interpolated per child
+// (bilinear); a kept parent is one row copy.  Row slots are derived from the
+// parent's rank in idx, and are bounds-checked so that an idx that is not
+// ascending and unique cannot write outside the buffers.
+
+// Copy one row of `bytes` (multiple of 16) to four destinations.
+__device__ __forceinline__ void wave_fan_row(const char* __restrict__ src, char* d0, char* d1, char* d2,
+                                             char* d3, int64_t bytes, int lane) {
+  const u32x4* s = reinterpret_cast<const u32x4*>(src);
+  const int64_t n = bytes / 16;
+  for (int64_t i = lane; i < n; i += kWave) {
+    const u32x4 v = s[i];
+    reinterpret_cast<u32x4*>(d0)[i] = v;
+    reinterpret_cast<u32x4*>(d1)[i] = v;
+    reinterpret_cast<u32x4*>(d2)[i] = v;
+    reinterpret_cast<u32x4*>(d3)[i] = v;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_mixed_kernel(
+    const T* __restrict__ lowres, const T* __restrict__ prefix, const int32_t* __restrict__ idx, int64_t k,
+    int H_lr, int W_lr, int64_t n_prefix, int64_t D, int mode, T* __restrict__ compact,
+    int32_t* __restrict__ pos, int32_t* __restrict__ children) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t job = int64_t(blockIdx.x) * kRowsPerBlock + threadIdx.x / kWave;
+  const int64_t Mp = int64_t(H_lr) * W_lr;
+  const int64_t row_bytes = D * int64_t(sizeof(T));
+  if (job < n_prefix) {
+    wave_copy_row(reinterpret_cast<const char*>(prefix + job * D),
+                  reinterpret_cast<char*>(compact + job * D), row_bytes, lane);
+    return;
+  }
+  const int64_t p = job - n_prefix;
+  if (p >= Mp) return;
+  const int r = int(p / W_lr), c = int(p % W_lr);
+  const int64_t at = lower_bound(idx, k, p);
+  T* body = compact + n_prefix * D;
+  if (at < k && idx[at] == p) {
+    const int W_hr = 2 * W_lr;
+    T* dst[4];
+    for (int ch = 0; ch < 4; ++ch) dst[ch] = body + (4 * at + ch) * D;
+    if (mode == AVITS_UP_NEAREST) {
+      wave_fan_row(reinterpret_cast<const char*>(lowres + p * D), reinterpret_cast<char*>(dst[0]),
+                   reinterpret_cast<char*>(dst[1]), reinterpret_cast<char*>(dst[2]),
+                   reinterpret_cast<char*>(dst[3]), row_bytes, lane);
+    } else {
+      for (int ch = 0; ch < 4; ++ch)
+        bilinear_row(lowres, dst[ch], int64_t(2 * r + (ch >> 1)) * W_hr + 2 * c + (ch & 1), H_lr, W_lr, D, lane);
+    }
+    if (lane < 4) {
+      const int dr = lane >> 1, dc = lane & 1;
+      int32_t* ps = pos + 3 * (4 * at + lane);
+      ps[0] = 0;
+      ps[1] = 2 * (2 * r + dr);
+      ps[2] = 2 * (2 * c + dc);
+      if (children) {
+        // Rank of child (2r+dr, 2c+dc) among all children in high-res raster
+        // order: the children of earlier low-res rows, then row 2r+dr's
+        // share of this row's selected parents, then the parents to the left.
+        const int64_t row0 = lower_bound(idx, k, int64_t(r) * W_lr);
+        const int64_t row1 = lower_bound(idx, k, int64_t(r + 1) * W_lr);
+        const int64_t rank = 4 * row0 + dr * 2 * (row1 - row0) + 2 * (at - row0) + dc;
+        if (rank >= 0 && rank < 4 * k) children[rank] = int32_t(int64_t(2 * r + dr) * W_hr + 2 * c + dc);
+      }
+    }
+    return;
+  }
+  const int64_t slot = p - at;  // kept parents before p
+  if (slot < 0 || slot >= Mp - k) return;
+  wave_copy_row(reinterpret_cast<const char*>(lowres + p * D),
+                reinterpret_cast<char*>(body + (4 * k + slot) * D), row_bytes, lane);
+  if (lane == 0) {
+    int32_t* ps = pos + 3 * (4 * k + slot);
+    ps[0] = 0;
+    ps[1] = 4 * r + 1;
+    ps[2] = 4 * c + 1;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kWave * kRowsPerBlock) void scatter_mixed_kernel(
+    const T* __restrict__ out, const int32_t* __restrict__ idx, int64_t k, int H_lr, int W_lr,
+    int64_t row_offset, int64_t D, T* __restrict__ canvas_hr, T* __restrict__ state_lr) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t p = int64_t(blockIdx.x) * kRowsPerBlock + threadIdx.x / kWave;
+  const int64_t Mp = int64_t(H_lr) * W_lr;
+  if (p >= Mp) return;
+  const int64_t row_bytes = D * int64_t(sizeof(T));
+  const int64_t at = lower_bound(idx, k, p);
+  const T* body = out + row_offset * D;
+  if (at < k && idx[at] == p) {
+    const int r = int(p / W_lr), c = int(p % W_lr), W_hr = 2 * W_lr;
+    for (int ch = 0; ch < 4; ++ch) {
+      const int64_t q = int64_t(2 * r + (ch >> 1)) * W_hr + 2 * c + (ch & 1);
+      wave_copy_row(reinterpret_cast<const char*>(body + (4 * at + ch) * D),
+                    reinterpret_cast<char*>(canvas_hr + q * D), row_bytes, lane);
+    }
+    return;
+  }
+  const int64_t slot = p - at;
+  if (slot < 0 || slot >= Mp - k) return;
+  wave_copy_row(reinterpret_cast<const char*>(body + (4 * k + slot) * D),
+                reinterpret_cast<char*>(state_lr + p * D), row_bytes, lane);
+}
+
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 }  // namespace
@@ -182,4 +298,61 @@ extern "C" int avits_scatter(const void* out, const int32_t* idx, int64_t k, int
     hipLaunchKernelGGL(scatter_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)out, idx, k, row_offset, D,
                        (bf16_t*)canvas);
   return launch_status("scatter");
+}
+
+extern "C" int avits_gather_mixed(const void* lowres, const void* prefix, const int32_t* idx, int64_t k,
+                                  int32_t H_lr, int32_t W_lr, int64_t n_prefix, int64_t D, int mode, int dtype,
+                                  void* compact, int32_t* pos, int32_t* children, void* stream) {
+  AVITS_REQUIRE(H_lr >= 1 && W_lr >= 1, "gather_mixed: H_lr=%d W_lr=%d must be >= 1", H_lr, W_lr);
+  const int64_t Mp = int64_t(H_lr) * W_lr;
+  AVITS_REQUIRE(k >= 0 && k <= Mp, "gather_mixed: k=%lld outside [0, M'=%lld]", (long long)k, (long long)Mp);
+  AVITS_REQUIRE(n_prefix >= 0, "gather_mixed: n_prefix=%lld < 0", (long long)n_prefix);
+  AVITS_REQUIRE(D >= 1, "gather_mixed: D=%lld < 1", (long long)D);
+  AVITS_REQUIRE(mode == AVITS_UP_NEAREST || mode == AVITS_UP_BILINEAR, "gather_mixed: bad mode %d", mode);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "gather_mixed: dtype %d unsupported", dtype);
+  const int64_t esz = dtype == AVITS_F32 ? 4 : 2;
+  AVITS_REQUIRE((D * esz) % 16 == 0, "gather_mixed: a row of D=%lld elements must be a multiple of 16 bytes", (long long)D);
+  AVITS_REQUIRE(lowres && compact && pos, "gather_mixed: null lowres/compact/pos");
+  AVITS_REQUIRE(n_prefix == 0 || prefix, "gather_mixed: null prefix with n_prefix=%lld", (long long)n_prefix);
+  AVITS_REQUIRE(k == 0 || idx, "gather_mixed: null idx with k=%lld", (long long)k);
+  const int64_t jobs = n_prefix + Mp;
+  const dim3 grid(unsigned(ceil_div(jobs, kRowsPerBlock))), block(kWave * kRowsPerBlock);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  TimedLaunch timed("gather_mixed", s);
+  if (dtype == AVITS_F32)
+    hipLaunchKernelGGL(gather_mixed_kernel<float>, grid, block, 0, s, (const float*)lowres, (const float*)prefix,
+                       idx, k, H_lr, W_lr, n_prefix, D, mode, (float*)compact, pos, children);
+  else
+    hipLaunchKernelGGL(gather_mixed_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)lowres,
+                       (const bf16_t*)prefix, idx, k, H_lr, W_lr, n_prefix, D, mode, (bf16_t*)compact, pos,
+                       children);
+  return launch_status("gather_mixed");
+}
+
+extern "C" int avits_scatter_mixed(const void* out, const int32_t* idx, int64_t k, int32_t H_lr, int32_t W_lr,
+                                   int64_t row_offset, int64_t D, int dtype, void* canvas_hr, void* state_lr,
+                                   void* stream) {
+  AVITS_REQUIRE(H_lr >= 1 && W_lr >= 1, "scatter_mixed: H_lr=%d W_lr=%d must be >= 1", H_lr, W_lr);
+  const int64_t Mp = int64_t(H_lr) * W_lr;
+  AVITS_REQUIRE(k >= 0 && k <= Mp, "scatter_mixed: k=%lld outside [0, M'=%lld]", (long long)k, (long long)Mp);
+  AVITS_REQUIRE(row_offset >= 0 && D >= 1, "scatter_mixed: bad row_offset=%lld D=%lld", (long long)row_offset,
+                (long long)D);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "scatter_mixed: dtype %d unsupported", dtype);
+  const int64_t esz = dtype == AVITS_F32 ? 4 : 2;
+  AVITS_REQUIRE((D * esz) % 16 == 0, "scatter_mixed: a row of D=%lld elements must be a multiple of 16 bytes", (long long)D);
+  AVITS_REQUIRE(out, "scatter_mixed: null out");
+  AVITS_REQUIRE(k == 0 || (idx && canvas_hr), "scatter_mixed: null idx/canvas_hr with k=%lld", (long long)k);
+  AVITS_REQUIRE(k == Mp || state_lr, "scatter_mixed: null state_lr with %lld kept tokens", (long long)(Mp - k));
+  const dim3 grid(unsigned(ceil_div(Mp, kRowsPerBlock))), block(kWave * kRowsPerBlock);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  TimedLaunch timed("scatter_mixed", s);
+  if (dtype == AVITS_F32)
+    hipLaunchKernelGGL(scatter_mixed_kernel<float>, grid, block, 0, s, (const float*)out, idx, k, H_lr, W_lr,
+                       row_offset, D, (float*)canvas_hr, (float*)state_lr);
+  else
+    hipLaunchKernelGGL(scatter_mixed_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)out, idx, k, H_lr, W_lr,
+                       row_offset, D, (bf16_t*)canvas_hr, (bf16_t*)state_lr);
+  return launch_status("scatter_mixed");
 }

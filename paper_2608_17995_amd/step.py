@@ -207,3 +207,109 @@ class StackStep:
         if s.k:
             B.avits_scatter(cur, self.idx, LR, canvas, stream)
         return canvas
+
+
+class MixedStage2:
+    """The paper's Stage 2 on one GPU (Section 3.2): score the M' low-res
+    tokens from Stage 1's signals, keep the top K = floor(rho M'), expand them
+    2x2 and keep the rest at low resolution in one mixed sequence, then run the
+    block stack on that sequence for each Stage-2 step, and finally send the
+    rows back (children to the high-res canvas, kept tokens to the low-res
+    state).
+
+      transition  probe (first stage of the probe double blocks on [prefix;
+                  Z_lr] at low-res grid positions) -> text mass -> score from
+                  the mass and the N_T low-res snapshots -> select K ->
+                  gather_mixed
+      step        the double blocks, then the single blocks, on the mixed
+                  sequence with half-unit positions (pos_scale 0.5)
+      leave       scatter_mixed into (canvas_hr, state_lr)
+
+    ``children`` holds the expanded tokens' high-res indices in ascending
+    order, the idx the Stage-3 expansion (avits_gather_upsample) takes.
+    Buffers are allocated once; the three calls enqueue library calls only.
+    """
+
+    def __init__(self, H_lr: int, W_lr: int, L: int, R: int, K: int, D: int, H: int, mlp_hidden: int,
+                 doubles: list, singles: list, prefix_pos, dtype, device="cuda", alpha=0.5, eps=1e-8,
+                 mode=B.UP_NEAREST, probe_blocks=(0,)):
+        import torch
+        if not doubles:
+            raise ValueError("the probe needs at least one double block")
+        Mp = H_lr * W_lr
+        if not 0 <= K <= Mp:
+            raise ValueError(f"K={K} outside [0, {Mp}]")
+        self.H_lr, self.W_lr, self.L, self.R, self.K, self.D, self.H = H_lr, W_lr, L, R, K, D, H
+        self.Mp, self.LR = Mp, L + R
+        self.S = self.LR + 4 * K + Mp - K
+        self.doubles, self.singles = list(doubles), list(singles)
+        self.alpha, self.eps, self.mode, self.probe_blocks = alpha, eps, mode, tuple(probe_blocks)
+        if not self.probe_blocks or any(b < 0 or b >= len(self.doubles) for b in self.probe_blocks):
+            raise ValueError("probe_blocks must name double blocks")
+        f32, i32 = torch.float32, torch.int32
+        d = D // H
+        code = B.BF16 if dtype == torch.bfloat16 else B.F32
+        LR = self.LR
+        prefix_pos = torch.as_tensor(prefix_pos, dtype=i32).to(device)
+        self.prefix_pos = prefix_pos
+        r = torch.arange(Mp, dtype=i32, device=device)
+        self.lr_pos = torch.stack([torch.zeros_like(r), r // W_lr, r % W_lr], dim=1).contiguous()
+        self.q_prefix = torch.empty(max(LR, 1), D, dtype=dtype, device=device)
+        self.q_img = torch.empty(Mp, D, dtype=dtype, device=device)
+        self.k_all = torch.empty(LR + Mp, D, dtype=dtype, device=device)
+        self.lse = torch.empty(H, Mp, dtype=f32, device=device)
+        self.mass = torch.empty(H, Mp, dtype=f32, device=device)
+        self.scores = torch.empty(Mp, dtype=f32, device=device)
+        self.idx = torch.empty(K, dtype=i32, device=device)
+        self.children = torch.empty(4 * K, dtype=i32, device=device)
+        self.x = torch.empty(self.S, D, dtype=dtype, device=device)
+        self.pos = torch.empty(self.S, 3, dtype=i32, device=device)
+        self.pos[:LR].copy_(2 * prefix_pos)     # half units
+        self.buf = [torch.empty(self.S, D, dtype=dtype, device=device) for _ in range(2)]
+        self.ws_score = torch.empty(max(B.avits_score_workspace_bytes(Mp, H), 1), dtype=torch.uint8, device=device)
+        self.ws_select = torch.empty(max(B.avits_select_workspace_bytes(Mp), 1), dtype=torch.uint8, device=device)
+        need = max(B.avits_block_qk_workspace_bytes(max(LR, Mp), H, d, code),
+                   B.avits_block_workspace_bytes(B.BLOCK_DOUBLE, self.S, H, d, mlp_hidden, code),
+                   B.avits_block_workspace_bytes(B.BLOCK_SINGLE, self.S, H, d, mlp_hidden, code) if singles else 0)
+        self.ws_block = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+
+    def transition(self, z_lr, snapshots, prefix, stream=None):
+        """Select and build the mixed sequence from the low-res latent z_lr
+        [M', D], Stage 1's N_T >= 2 low-res snapshots (oldest first) and the
+        prefix rows [L + R, D]."""
+        LR, Mp, H, D = self.LR, self.Mp, self.H, self.D
+        d = D // H
+        q, k = self.q_img.view(Mp, H, d), self.k_all.view(LR + Mp, H, d)
+        for n, b in enumerate(self.probe_blocks):
+            w = self.doubles[b]
+            if LR:
+                B.avits_block_qk(prefix, self.prefix_pos, self.L, self.R, w, H, self.q_prefix[:LR], self.k_all[:LR],
+                                 self.ws_block, stream)
+            B.avits_block_qk(z_lr, self.lr_pos, 0, Mp, w, H, self.q_img, self.k_all[LR:], self.ws_block, stream)
+            B.avits_joint_attention_stats(q, k, self.L, self.mass, lse=self.lse, accumulate=n > 0, stream=stream)
+        B.avits_score_from_mass(self.mass, len(self.probe_blocks), list(snapshots), self.alpha, self.eps,
+                                self.scores, workspace=self.ws_score, stream=stream)
+        if self.K:
+            B.avits_select(self.scores, self.K, self.idx, self.ws_select, stream)
+        B.avits_gather_mixed(z_lr, prefix if LR else None, self.idx if self.K else None, self.H_lr, self.W_lr,
+                             self.x, self.pos[LR:], self.children if self.K else None, self.mode, stream)
+
+    def step(self, stream=None, on_block=None):
+        """One pass of the block stack over the mixed sequence; the result
+        becomes the sequence the next step reads."""
+        cur = self.x
+        for i, w in enumerate(self.doubles + self.singles):
+            nxt = self.buf[i % 2]
+            B.avits_block_forward(cur, nxt, self.pos, self.L, self.S - self.L, w, self.H, None, self.ws_block,
+                                  stream, pos_scale=0.5)
+            if on_block is not None:
+                on_block(i, cur, nxt)
+            cur = nxt
+        self.x, self.buf[(len(self.doubles) + len(self.singles) - 1) % 2] = cur, self.x
+        return self.x
+
+    def leave(self, canvas_hr, state_lr, stream=None):
+        """Children rows to canvas_hr [4M', D], kept rows to state_lr [M', D]."""
+        B.avits_scatter_mixed(self.x, self.idx if self.K else None, self.H_lr, self.W_lr, self.LR,
+                              canvas_hr if self.K else None, state_lr if self.K < self.Mp else None, stream)
+        return canvas_hr, state_lr

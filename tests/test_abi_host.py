@@ -100,6 +100,27 @@ def test_gather_and_scatter_validation(lib):
     assert s(FAKE, FAKE, 3, 0, 64, 3, FAKE, None) == UNSUPPORTED
 
 
+def test_mixed_gather_and_scatter_validation(lib):
+    g = lib.avits_gather_mixed
+    # (lowres, prefix, idx, k, H_lr, W_lr, n_prefix, D, mode, dtype, compact, pos, children, stream)
+    assert g(FAKE, None, FAKE, 5, 2, 2, 0, 64, 0, 1, FAKE, FAKE, None, None) == INVALID    # k > M' = 4
+    assert g(FAKE, None, FAKE, 2, 0, 2, 0, 64, 0, 1, FAKE, FAKE, None, None) == INVALID    # H_lr
+    assert g(FAKE, None, FAKE, 2, 2, 2, 0, 64, 7, 1, FAKE, FAKE, None, None) == INVALID    # mode
+    assert g(FAKE, None, FAKE, 2, 2, 2, 0, 60, 0, 1, FAKE, FAKE, None, None) == INVALID    # 120-byte rows
+    assert g(FAKE, None, FAKE, 2, 2, 2, 3, 64, 0, 1, FAKE, FAKE, None, None) == INVALID    # null prefix
+    assert g(FAKE, None, None, 2, 2, 2, 0, 64, 0, 1, FAKE, FAKE, None, None) == INVALID    # null idx
+    assert g(FAKE, None, FAKE, 2, 2, 2, 0, 64, 0, 1, FAKE, None, None, None) == INVALID    # null pos
+    assert g(FAKE, None, FAKE, 2, 2, 2, 0, 64, 0, 4, FAKE, FAKE, None, None) == UNSUPPORTED
+    s = lib.avits_scatter_mixed
+    # (out, idx, k, H_lr, W_lr, row_offset, D, dtype, canvas_hr, state_lr, stream)
+    assert s(FAKE, FAKE, 5, 2, 2, 0, 64, 1, FAKE, FAKE, None) == INVALID      # k > M'
+    assert s(FAKE, FAKE, 2, 2, 2, -1, 64, 1, FAKE, FAKE, None) == INVALID     # row_offset
+    assert s(FAKE, FAKE, 2, 2, 2, 0, 64, 1, None, FAKE, None) == INVALID      # canvas needed
+    assert s(FAKE, FAKE, 2, 2, 2, 0, 64, 1, FAKE, None, None) == INVALID      # state needed
+    assert s(None, FAKE, 2, 2, 2, 0, 64, 1, FAKE, FAKE, None) == INVALID
+    assert s(FAKE, FAKE, 2, 2, 2, 0, 64, 2, FAKE, FAKE, None) == UNSUPPORTED
+
+
 def test_joint_lse_validation(lib):
     f = lib.avits_joint_lse
     assert f(FAKE, FAKE, 0, 5, 2, 64, 1, FAKE, None) == INVALID
@@ -115,21 +136,22 @@ def test_block_validation(lib):
     f = lib.avits_block_forward
     ws = lib.avits_block_workspace_bytes(0, 10, 1, 64, 256, 1)
     assert ws > 0
-    assert f(FAKE, FAKE + 64, FAKE, 5, 5, None, 1, 64, 1, None, FAKE, ws, None) == INVALID          # null weights
-    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID  # missing weights
-    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 80, 1, None, FAKE, ws, None) == UNSUPPORTED
-    assert f(FAKE, FAKE + 64, FAKE, -1, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
-    assert f(FAKE, FAKE, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID  # alias
-    assert f(FAKE, FAKE + 64, FAKE, 0, 0, ctypes.byref(w), 1, 64, 1, None, None, 0, None) == 0    # S == 0
+    assert f(FAKE, FAKE + 64, FAKE, 1.0, 5, 5, None, 1, 64, 1, None, FAKE, ws, None) == INVALID          # null weights
+    assert f(FAKE, FAKE + 64, FAKE, 1.0, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID  # missing weights
+    assert f(FAKE, FAKE + 64, FAKE, 0.0, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID  # pos_scale
+    assert f(FAKE, FAKE + 64, FAKE, 1.0, 5, 5, ctypes.byref(w), 1, 80, 1, None, FAKE, ws, None) == UNSUPPORTED
+    assert f(FAKE, FAKE + 64, FAKE, 1.0, -1, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
+    assert f(FAKE, FAKE, FAKE, 1.0, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID  # alias
+    assert f(FAKE, FAKE + 64, FAKE, 1.0, 0, 0, ctypes.byref(w), 1, 64, 1, None, None, 0, None) == 0    # S == 0
     for part in ("txt", "img"):
         for name, _ in _binding._DoubleStream._fields_:
             setattr(getattr(w, part), name, FAKE)
-    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws - 1, None) == WORKSPACE
-    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, None, ws, None) == WORKSPACE
+    assert f(FAKE, FAKE + 64, FAKE, 1.0, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws - 1, None) == WORKSPACE
+    assert f(FAKE, FAKE + 64, FAKE, 1.0, 5, 5, ctypes.byref(w), 1, 64, 1, None, None, ws, None) == WORKSPACE
     w.kind = 5
-    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
+    assert f(FAKE, FAKE + 64, FAKE, 1.0, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
     w.kind, w.mlp_hidden = 0, 100
-    assert f(FAKE, FAKE + 64, FAKE, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
+    assert f(FAKE, FAKE + 64, FAKE, 1.0, 5, 5, ctypes.byref(w), 1, 64, 1, None, FAKE, ws, None) == INVALID
     assert lib.avits_block_workspace_bytes(1, 10, 1, 64, 256, 1) > 0
     assert lib.avits_block_workspace_bytes(3, 10, 1, 64, 256, 1) == 0
 
@@ -143,18 +165,18 @@ def test_block_qk_validation(lib):
     assert ws >= 10 * 128 * 2 and lib.avits_block_qk_workspace_bytes(10, 2, 64, 0) >= 10 * 128 * 4
     assert lib.avits_block_qk_workspace_bytes(10, 0, 64, 1) == 0
     q, k = FAKE + 4096, FAKE + 8192
-    assert f(FAKE, FAKE, 5, 5, None, 2, 64, 1, q, k, FAKE, ws, None) == INVALID                 # null weights
-    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, FAKE, ws, None) == INVALID      # missing weights
-    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 96, 1, q, k, FAKE, ws, None) == UNSUPPORTED
-    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 3, q, k, FAKE, ws, None) == UNSUPPORTED
-    assert f(FAKE, FAKE, 0, 0, ctypes.byref(w), 2, 64, 1, None, None, None, 0, None) == 0     # S == 0
+    assert f(FAKE, FAKE, 1.0, 5, 5, None, 2, 64, 1, q, k, FAKE, ws, None) == INVALID                 # null weights
+    assert f(FAKE, FAKE, 1.0, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, FAKE, ws, None) == INVALID      # missing weights
+    assert f(FAKE, FAKE, 1.0, 5, 5, ctypes.byref(w), 2, 96, 1, q, k, FAKE, ws, None) == UNSUPPORTED
+    assert f(FAKE, FAKE, 1.0, 5, 5, ctypes.byref(w), 2, 64, 3, q, k, FAKE, ws, None) == UNSUPPORTED
+    assert f(FAKE, FAKE, 1.0, 0, 0, ctypes.byref(w), 2, 64, 1, None, None, None, 0, None) == 0     # S == 0
     for part in ("txt", "img"):
         for name, _ in _binding._DoubleStream._fields_:
             setattr(getattr(w, part), name, FAKE)
-    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, q, FAKE, ws, None) == INVALID      # q aliases k
-    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, None, k, FAKE, ws, None) == INVALID
-    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, FAKE, ws - 1, None) == WORKSPACE
-    assert f(FAKE, FAKE, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, None, ws, None) == WORKSPACE
+    assert f(FAKE, FAKE, 1.0, 5, 5, ctypes.byref(w), 2, 64, 1, q, q, FAKE, ws, None) == INVALID      # q aliases k
+    assert f(FAKE, FAKE, 1.0, 5, 5, ctypes.byref(w), 2, 64, 1, None, k, FAKE, ws, None) == INVALID
+    assert f(FAKE, FAKE, 1.0, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, FAKE, ws - 1, None) == WORKSPACE
+    assert f(FAKE, FAKE, 1.0, 5, 5, ctypes.byref(w), 2, 64, 1, q, k, None, ws, None) == WORKSPACE
     assert b"block_qk" in lib.avits_last_error()
 
 
