@@ -2,8 +2,9 @@
 // Section 3.3.1, Eqs. joint_qk and dit_attn), and its LSE-only form.
 //
 // bf16: one 256-thread workgroup per (128 query rows, head), 32 rows per
-// wave, two workgroups per CU.  Key tiles of 64 rows and the matching V^T
-// tile are prefetched into registers one tile ahead and staged in padded LDS.
+// wave, two workgroups per CU, the row blocks of one head on one XCD.  Key
+// tiles of 64 rows and the matching V^T tile are prefetched into registers
+// one tile ahead and staged in padded LDS.
 // Both products run on v_mfma_f32_32x32x16_bf16 in transposed form:
 //   S^T = K Q^T   -> each lane holds 16 keys x 1 query row (row = lane % 32),
 //   O^T = V^T P^T -> each lane holds 16 head-dim values of the same row,
@@ -13,7 +14,7 @@
 // permutation on both operands).  Softmax runs in the log2 domain with fp32
 // statistics.
 // fp32: one thread per query row on the VALU (exactness path).
-#include <stdlib.h>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -28,30 +29,54 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Work unit -> (head, row block) with the units of one XCD contiguous and
+// head-major, so the row blocks of a head share one L2 (workgroup b runs on
+// XCD b mod 8).
+__device__ __forceinline__ void attn_unit(int64_t n_rb, int H, int64_t& head, int64_t& rb) {
+  const int64_t U = n_rb * H;
+  const int64_t b = blockIdx.x, x = b % 8;
+  int64_t start = 0;
+  for (int64_t y = 0; y < x; ++y) start += (U - y + 7) / 8;
+  const int64_t u = start + b / 8;
+  head = u / n_rb;
+  rb = u % n_rb;
+}
+
 // Lane l of a 32x32 MFMA output tile holds row 8*(r/4) + 4*(l/32) + r%4 of
 // column l%32 in register r.  With S^T = K Q^T the column is the query row
-// and the row is the key, so key(r, h) = 8*(r/4) + 4*h + r%4 (h = l/32).
-template <int DH, bool WITH_V, int KT>
+// and the row is the LDS key row.  Key rows are stored in LDS with bits 2 and
+// 3 of their index within the tile swapped, so register r of lane half h
+// holds key 16*(r/8) + 8h + 4*((r/4)%2) + r%4 of its 32-key sub-tile: for
+// the 16-key chunk c of the P^T operand, lane half h then holds the
+// contiguous keys 16c + 8h .. +7, and each V^T operand is a single 16-byte
+// LDS read (V^T rows padded to a 16-byte multiple).  The last, partial key
+// tile runs through its own instance of the tile body (key masking, V^T
+// zeroing), so full tiles carry no tail arithmetic; the text-mass sum is
+// compiled in only when MASS is set.
+template <int DH, bool WITH_V, bool MASS>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
-  constexpr int kKT = KT;           // keys per tile (32 or 64)
-  constexpr int kC = DH / 16;       // 16-wide head-dim chunks (MFMA k)
-  constexpr int kKL = DH + 8;       // padded K row (elements)
-  constexpr int kVL = kKT + 4;      // padded V^T row: 2 mod 4 words keeps 32 rows of 8-byte reads conflict-free
-  constexpr int kKP = kKT * DH / 8 / 256;  // 16-byte K pieces per thread per tile
-  constexpr int kVP = DH * kKT / 8 / 256;  // 16-byte V^T pieces per thread per tile
-  // Two LDS buffers: tile t + 1 is stored while tile t is consumed.
+  constexpr int NW = kRows / 32;             // waves
+  constexpr int kKT = 64;                    // keys per tile
+  constexpr int kT = 64 * NW;                // threads
+  constexpr int kC = DH / 16;
+  constexpr int kKL = DH + 8;                // padded K row (elements), 16-byte multiple
+  constexpr int kVL = kKT + 8;               // padded V^T row (elements), 16-byte multiple
+  constexpr int kKP = kKT * DH / 8 / kT;     // 16-byte K pieces per thread per tile
+  constexpr int kVP = DH * kKT / 8 / kT;     // 16-byte V^T pieces per thread per tile
+  static_assert(kKP >= 1 && kVP >= 1, "tile too small for the workgroup");
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][kKT * kKL];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][WITH_V ? DH * kVL : 8];
 
-  const int h = blockIdx.y;
+  int64_t hh, rb;
+  attn_unit((a.Sq + 32 * NW - 1) / (32 * NW), a.H, hh, rb);
+  const int h = int(hh);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int l32 = lane % 32, hi = lane / 32;
-  const int64_t row = int64_t(blockIdx.x) * kRows + wave * 32 + l32;
+  const int64_t row = rb * (32 * NW) + wave * 32 + l32;
   const bf16_t* Q = static_cast<const bf16_t*>(a.q);
-  const bf16_t* K = static_cast<const bf16_t*>(a.k);
-  const bf16_t* VT = static_cast<const bf16_t*>(a.vt);
+  const bf16_t* K = static_cast<const bf16_t*>(a.k) + int64_t(h) * a.k_head;
+  const bf16_t* VT = static_cast<const bf16_t*>(a.vt) + int64_t(h) * DH * a.ldvt;
 
-  // Q^T fragments (B operand): lane holds head-dim 16c + 8hi .. +7 of its row.
   bf16x8 qf[kC];
   {
     const bf16_t* src = Q + std::min<int64_t>(row, a.Sq - 1) * a.q_tok + h * a.q_head + 8 * hi;
@@ -59,37 +84,61 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
     for (int c = 0; c < kC; ++c) qf[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + 16 * c));
   }
   const float scale2 = kLog2e * rsqrtf(float(DH));
-  float mrow = -INFINITY, lrow = 0.f;
-  float trow = 0.f;  // the part of lrow from keys < a.mass_keys (when a.mass is set)
+  float mrow = -INFINITY, lrow = 0.f, trow = 0.f;
   f32x16 oacc[WITH_V ? DH / 32 : 1];
 #pragma unroll
   for (int dt = 0; dt < (WITH_V ? DH / 32 : 1); ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
 
-  // Register prefetch of the next K / V^T tile.
+  // Per-thread piece coordinates (fixed over the tiles).
+  int k_key[kKP], k_dst[kKP], v_dv[kVP], v_kc[kVP];
+  const bf16_t* k_src[kKP];
+  const bf16_t* v_src[kVP];
+#pragma unroll
+  for (int j = 0; j < kKP; ++j) {
+    const int p = tid + kT * j;
+    const int kk = p / (DH / 8), col = (p % (DH / 8)) * 8;
+    k_key[j] = kk;
+    const int rowp = (kk & ~12) | ((kk & 4) << 1) | ((kk & 8) >> 1);
+    k_dst[j] = rowp * kKL + col;
+    k_src[j] = K + int64_t(kk) * a.k_tok + col;
+  }
+#pragma unroll
+  for (int j = 0; j < kVP; ++j) {
+    const int p = tid + kT * j;
+    v_dv[j] = p / (kKT / 8);
+    v_kc[j] = (p % (kKT / 8)) * 8;
+    v_src[j] = VT + int64_t(v_dv[j]) * a.ldvt + v_kc[j];
+  }
+  // Register prefetch of the next tile.
   u32x4 kreg[kKP], vreg[WITH_V ? kVP : 1];
-  auto load_tile = [&](int64_t k0) {
+  // Tile at key k0; `last` when it is the partial tile at the end.
+  auto load_tile = [&](int64_t k0, bool last) {
+    if (!last) {
 #pragma unroll
-    for (int j = 0; j < kKP; ++j) {
-      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
-      const int64_t kr = std::min<int64_t>(k0 + key, a.Sk - 1);
-      kreg[j] = *reinterpret_cast<const u32x4*>(K + kr * a.k_tok + h * a.k_head + col);
-    }
-    if constexpr (WITH_V) {
-      const bf16_t* vsrc = VT + int64_t(h) * DH * a.ldvt + k0;
+      for (int j = 0; j < kKP; ++j) kreg[j] = *reinterpret_cast<const u32x4*>(k_src[j] + k0 * a.k_tok);
+      if constexpr (WITH_V) {
 #pragma unroll
-      for (int j = 0; j < kVP; ++j) {
-        const int p = tid + 256 * j, dv = p / (kKT / 8), kc = (p % (kKT / 8)) * 8;
-        vreg[j] = *reinterpret_cast<const u32x4*>(vsrc + int64_t(dv) * a.ldvt + kc);
-        // Keys past the end (the row padding up to ldvt) may hold anything:
-        // zero them so that 0-probability keys contribute exactly 0.
-        const int64_t key0 = k0 + kc;
-        if (key0 + 8 > a.Sk) {
+        for (int j = 0; j < kVP; ++j) vreg[j] = *reinterpret_cast<const u32x4*>(v_src[j] + k0);
+      }
+    } else {
+      // Clamp key rows; zero V^T beyond the end so that 0-probability keys
+      // contribute exactly 0.
+      const int rem = int(a.Sk - k0);
+#pragma unroll
+      for (int j = 0; j < kKP; ++j) {
+        const int kk = std::min(k_key[j], rem - 1);
+        kreg[j] = *reinterpret_cast<const u32x4*>(k_src[j] + (k0 + kk - k_key[j]) * a.k_tok);
+      }
+      if constexpr (WITH_V) {
+#pragma unroll
+        for (int j = 0; j < kVP; ++j) {
+          vreg[j] = *reinterpret_cast<const u32x4*>(v_src[j] + k0);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int64_t kk = key0 + 2 * e;
-            vreg[j][e] = (kk < a.Sk ? vreg[j][e] & 0xffffu : 0u) | (kk + 1 < a.Sk ? vreg[j][e] & 0xffff0000u : 0u);
+            const int kk = v_kc[j] + 2 * e;
+            vreg[j][e] = (kk < rem ? vreg[j][e] & 0xffffu : 0u) | (kk + 1 < rem ? vreg[j][e] & 0xffff0000u : 0u);
           }
         }
       }
@@ -97,29 +146,27 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   };
   auto store_tile = [&](int buf) {
 #pragma unroll
-    for (int j = 0; j < kKP; ++j) {
-      const int p = tid + 256 * j, key = p / (DH / 8), col = (p % (DH / 8)) * 8;
-      *reinterpret_cast<u32x4*>(&Ks[buf][key * kKL + col]) = kreg[j];
-    }
+    for (int j = 0; j < kKP; ++j) *reinterpret_cast<u32x4*>(&Ks[buf][k_dst[j]]) = kreg[j];
     if constexpr (WITH_V) {
 #pragma unroll
-      for (int j = 0; j < kVP; ++j) {
-        const int p = tid + 256 * j, dv = p / (kKT / 8), kc = (p % (kKT / 8)) * 8;
-        *reinterpret_cast<u32x4*>(&Vs[buf][dv * kVL + kc]) = vreg[j];
-      }
+      for (int j = 0; j < kVP; ++j) *reinterpret_cast<u32x4*>(&Vs[buf][v_dv[j] * kVL + v_kc[j]]) = vreg[j];
     }
   };
+  // Key (within the tile) of accumulator register r of sub-tile t, less 8 h.
+  auto key_of = [](int t, int r) { return 32 * t + 16 * (r / 8) + 4 * ((r / 4) & 1) + (r % 4); };
 
-  load_tile(0);
-  store_tile(0);
-  lds_barrier();
+  const int64_t n_full = a.Sk / kKT;
+  const bool has_tail = a.Sk % kKT != 0;
+  const int64_t n_tiles = n_full + (has_tail ? 1 : 0);
   int buf = 0;
-  for (int64_t k0 = 0; k0 < a.Sk; k0 += kKT, buf ^= 1) {
-    const bool more = k0 + kKT < a.Sk;
-    if (more) load_tile(k0 + kKT);
+  // Key tile `it`: prefetch tile it + 1 into registers, consume tile it from
+  // LDS, then stage tile it + 1 in the other LDS buffer.
+  auto tile = [&](int64_t it, auto tail_tag) {
+    constexpr bool kTail = decltype(tail_tag)::value;
+    const int64_t k0 = it * kKT;
+    const bool more = it + 1 < n_tiles;
+    if (more) load_tile(k0 + kKT, it + 1 == n_full);
 
-    // Raw logits of the tile: KT/32 sub-tiles of 32 keys.  Keys past the end
-    // (last tile only) are set to -inf.
     f32x16 s[kKT / 32];
 #pragma unroll
     for (int t = 0; t < kKT / 32; ++t) {
@@ -133,23 +180,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
       }
       s[t] = acc;
     }
-    if (k0 + kKT > a.Sk) {
+    if constexpr (kTail) {
+      const int lim = int(a.Sk - k0) - 8 * hi;
 #pragma unroll
       for (int t = 0; t < kKT / 32; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int64_t key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
-          if (key >= a.Sk) s[t][r] = -INFINITY;
-        }
+        for (int r = 0; r < 16; ++r)
+          if (key_of(t, r) >= lim) s[t][r] = -INFINITY;
     }
-    // Online softmax in the log2 domain; a row lives in lanes l32 and l32 + 32.
-    // exp2 is the hardware instruction (about 1 ulp; results below 2^-126
-    // flush to zero, far below what a sum of at least one term of size 1 can
-    // register).
-    // The running max is raised only when the tile max exceeds it by more
-    // than 8 (a factor 256), so most tiles skip the rescale of the output
-    // accumulators; exponents stay <= 2^8, exact in the fp32 sums and
-    // representable in bf16.
     float mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < kKT / 32; ++t)
@@ -172,28 +210,30 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
         ls += e;
       }
     lrow = lrow * corr + ls;
-    if (a.mass && k0 < a.mass_keys) {
-      float ts = ls;  // whole tile below mass_keys, else only its leading keys
-      if (k0 + kKT > a.mass_keys) {
-        ts = 0.f;
+    if constexpr (MASS) {
+      if (k0 < a.mass_keys) {
+        float ts = ls;
+        if (k0 + kKT > a.mass_keys) {
+          ts = 0.f;
+          const int lim = int(a.mass_keys - k0) - 8 * hi;
 #pragma unroll
-        for (int t = 0; t < kKT / 32; ++t)
+          for (int t = 0; t < kKT / 32; ++t)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int64_t key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
-            ts += key < a.mass_keys ? s[t][r] : 0.f;
-          }
+            for (int r = 0; r < 16; ++r) ts += key_of(t, r) < lim ? s[t][r] : 0.f;
+        }
+        trow = trow * corr + ts;
+      } else {
+        trow *= corr;
       }
-      trow = trow * corr + ts;
     }
     if constexpr (WITH_V) {
       if (__any(raise)) {
+        // Rare (the max rises by more than 8): keep it a branch, not a
+        // multiply by 1 on every tile.
+        asm volatile("" ::: "memory");
 #pragma unroll
         for (int dt = 0; dt < DH / 32; ++dt) oacc[dt] *= corr;
       }
-      // P^T operand for 16-key chunk c (keys 16c .. 16c + 15 of the tile):
-      // registers 8(c%2) .. 8(c%2) + 7 of sub-tile c/2 hold keys
-      // 16c + 4hi + {0..3} and 16c + 8 + 4hi + {0..3}.
 #pragma unroll
       for (int c = 0; c < kKT / 16; ++c) {
         const f32x16& st = s[c / 2];
@@ -203,28 +243,31 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
         const bf16x8 pf = as_bf16x8(pv);
 #pragma unroll
         for (int dt = 0; dt < DH / 32; ++dt) {
-          const bf16_t* vr = &Vs[buf][(32 * dt + l32) * kVL + 16 * c + 4 * hi];
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
-          const u32x2 up = *reinterpret_cast<const u32x2*>(vr + 8);
-          const u32x4 vv = {lo[0], lo[1], up[0], up[1]};
+          const u32x4 vv = *reinterpret_cast<const u32x4*>(&Vs[buf][(32 * dt + l32) * kVL + 16 * c + 8 * hi]);
           oacc[dt] = mfma32(as_bf16x8(vv), pf, oacc[dt]);
         }
       }
     }
     if (more) store_tile(buf ^ 1);
     lds_barrier();
-  }
+    buf ^= 1;
+  };
+
+  load_tile(0, n_full == 0);
+  store_tile(0);
+  lds_barrier();
+  for (int64_t it = 0; it < n_full; ++it) tile(it, std::integral_constant<bool, false>());
+  if (has_tail) tile(n_full, std::integral_constant<bool, true>());
 
   float l = lrow + __shfl_xor(lrow, 32, kWave);
   const float tm = trow + __shfl_xor(trow, 32, kWave);
   if (row >= a.Sq) return;
   if (a.lse && hi == 0) a.lse[int64_t(h) * a.Sq + row] = (mrow + log2f(l)) * kLn2;
-  if (a.mass && hi == 0) {
+  if (MASS && hi == 0) {
     float* dst = a.mass + int64_t(h) * a.Sq + row;
     *dst = (a.mass_accumulate ? *dst : 0.f) + tm / l;
   }
   if constexpr (WITH_V) {
-    // oacc[dt][r] = O[row][32 dt + 8(r/4) + 4hi + r%4].
     const float inv = 1.f / l;
     bf16_t* dst = static_cast<bf16_t*>(a.o) + row * a.ldo + int64_t(h) * DH + 4 * hi;
 #pragma unroll
@@ -307,22 +350,14 @@ __global__ __launch_bounds__(kFRows) void attn_f32_kernel(const AttnArgs a) {
   }
 }
 
-// Key tile: 64 keys when V is used, 32 keys otherwise; AVITS_ATTN_KT
-// (32 or 64) overrides it for tuning.
 template <int DH>
 void launch_dh(const AttnArgs& a, int dtype, hipStream_t s) {
   const bool with_v = a.vt != nullptr;
   if (dtype == AVITS_BF16) {
-    int kt = 64;
-    if (const char* env = getenv("AVITS_ATTN_KT")) kt = atoi(env) == 32 ? 32 : 64;
-    const dim3 grid(unsigned(ceil_div64(a.Sq, kRows)), unsigned(a.H));
-    if (with_v) {
-      if (kt == 32) hipLaunchKernelGGL((attn_bf16_kernel<DH, true, 32>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((attn_bf16_kernel<DH, true, 64>), grid, dim3(256), 0, s, a);
-    } else {
-      if (kt == 32) hipLaunchKernelGGL((attn_bf16_kernel<DH, false, 32>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((attn_bf16_kernel<DH, false, 64>), grid, dim3(256), 0, s, a);
-    }
+    const dim3 grid(static_cast<unsigned>(ceil_div64(a.Sq, kRows) * a.H));
+    if (with_v) hipLaunchKernelGGL((attn_bf16_kernel<DH, true, false>), grid, dim3(256), 0, s, a);
+    else if (a.mass) hipLaunchKernelGGL((attn_bf16_kernel<DH, false, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<DH, false, false>), grid, dim3(256), 0, s, a);
   } else {
     const dim3 grid(unsigned(ceil_div64(a.Sq, kFRows)), unsigned(a.H));
     if (with_v) hipLaunchKernelGGL((attn_f32_kernel<DH, true>), grid, dim3(kFRows), 0, s, a);
