@@ -6,6 +6,7 @@ from __future__ import annotations
 
 import concurrent.futures as cf
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -43,6 +44,27 @@ def _run(cmd):
     return r.stdout
 
 
+# Kernels whose loads are asynchronous inline assembly (the destination is
+# written after the instruction issues): a spilled destination would be saved
+# before the data lands, so these must compile without scratch.
+NO_SCRATCH = {"gemm.hip": "gemm_bf16_kernel"}
+_USAGE = ["-Rpass-analysis=kernel-resource-usage"]
+
+
+def _check_no_scratch(src: str, out: str) -> None:
+    want = NO_SCRATCH[src]
+    name = None
+    for line in out.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and name and want in name and int(m.group(1)) != 0:
+            raise RuntimeError(f"{src}: {name} uses {m.group(1)} bytes of scratch per lane; its asynchronous "
+                               "loads require a spill-free build")
+
+
 def build(verbose: bool = False, jobs: int | None = None) -> str:
     """Compile every HIP source for gfx950 and link libavits.so; returns its path."""
     os.makedirs(BUILD, exist_ok=True)
@@ -52,11 +74,14 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     for src in SOURCES:
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
         objs.append(obj)
-        cmds.append([cc, *CXXFLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src), "-o", obj])
+        extra = _USAGE if src in NO_SCRATCH else []
+        cmds.append([cc, *CXXFLAGS, *extra, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src), "-o", obj])
     jobs = jobs or min(len(cmds), os.cpu_count() or 4, 8)
     with cf.ThreadPoolExecutor(jobs) as ex:
-        for out in ex.map(_run, cmds):
-            if verbose and out.strip():
+        for src, out in zip(SOURCES, ex.map(_run, cmds)):
+            if src in NO_SCRATCH:
+                _check_no_scratch(src, out)
+            elif verbose and out.strip():
                 print(out)
     tmp = LIB + ".tmp"
     _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])

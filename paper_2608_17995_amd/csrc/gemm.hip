@@ -414,7 +414,11 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
     }
   }
   pl.waves = 8;
-  pl.stages = pl.bn == 256 ? 1 : 2;  // two stages do not fit the 256-wide tile's registers
+  // Two register stages do not fit the 256-wide tile's registers.  The staged
+  // loads are asynchronous inline assembly, so an instance that spilled a
+  // destination register would read it before the load lands: every
+  // instance must build without scratch (the build checks it).
+  pl.stages = pl.bn == 256 ? 1 : 2;
   // Tuning override "BN,SPLITS[,8[,STAGES]]" (e.g. AVITS_GEMM_TILE=256,3,8,1),
   // for one launch family with AVITS_GEMM_TILE_<family> (e.g. _gemm_o).
   const char* env = nullptr;
@@ -432,7 +436,7 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
       pl.bn = bn;
       pl.splits = sp;
       pl.waves = wv;
-      pl.stages = stg;
+      pl.stages = bn == 256 ? 1 : stg;  // the 256-wide tile has one register stage only
       pl.tiles = tiles_of(a, kBM, bn);
     }
   }
@@ -456,7 +460,6 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
     TimedLaunch timed(family, s);  // the GEMM kernel alone; the reduce is its own family
     switch (pl.bn * 100 + pl.waves * 10 + pl.stages) {
       case 25681: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
-      case 25682: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 19281: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 19282: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 12881: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
