@@ -8,11 +8,13 @@
 //    waves per SIMD hide each other's LDS and barrier waits.
 //  - The MFMA computes C^T = W A^T, so each lane owns groups of four
 //    consecutive output columns of one row (8-byte stores in the epilogue).
-//  - k-tiles are staged global -> registers -> LDS with two register stages
-//    and two LDS buffers, one barrier per k-tile: while tile t is
-//    multiplied, tile t+1 waits in registers and tile t+2 is in flight.  LDS rows are 128 bytes (64 bf16) with the 16-byte chunk index
+//  - k-tiles are staged global -> registers -> LDS through two LDS buffers,
+//    one barrier per k-tile: while tile t is multiplied, tile t+1 is in
+//    flight (and, for the 128-wide tile, tile t+2 too).  LDS rows are 128 bytes (64 bf16) with the 16-byte chunk index
 //    XOR-swizzled by (row / 2) mod 8, which makes both the staging writes and
 //    the 16-byte fragment reads of 16 consecutive rows bank-conflict free.
+//  - The epilogue goes through LDS wave by wave so that every store covers
+//    whole row segments (or, for the transposed store, column runs).
 //  - Small-N GEMMs (the N = D projections) are split along K when the tile
 //    grid would leave most of the 256 CUs idle: each split writes fp32
 //    partials and a reduce kernel sums them in split order (deterministic)
@@ -29,9 +31,14 @@ namespace {
 constexpr int kBM = 256, kBK = 64;
 constexpr int kCUs = 256;
 
-__device__ __forceinline__ float gelu_tanh(float x) {
+// GELU with the tanh approximation written through the logistic function:
+// 0.5 (1 + tanh(u)) = 1 / (1 + exp(-2u)), on the hardware exp2 and
+// reciprocal (about 1 ulp each; the result is rounded to bf16).  Large |x|
+// saturate to x and -0.
+__device__ __forceinline__ float gelu_fast(float x) {
   const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
-  return 0.5f * x * (1.f + tanhf(u));
+  const float e = __builtin_amdgcn_exp2f(-2.f * 1.4426950408889634f * u);
+  return x * __builtin_amdgcn_rcpf(1.f + e);
 }
 
 __device__ __forceinline__ f32x16 mfma32x32x16(const bf16x8& a, const bf16x8& b, const f32x16& c) {
@@ -62,7 +69,7 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, const GemmProblem& 
   }
   if (mode == EPI_GELU) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) v[r] = gelu_tanh(v[r]);
+    for (int r = 0; r < 4; ++r) v[r] = gelu_fast(v[r]);
   } else if (mode == EPI_RESID_GATE) {
     const T* res = static_cast<const T*>(p.resid);
     const T* gt = static_cast<const T*>(p.gate);
@@ -118,6 +125,148 @@ __device__ __forceinline__ bool map_tile(const GemmArgs& a, int bm, int bn, int 
   return m0 < a.p[prob].M && n0 < a.N;
 }
 
+// Epilogue through LDS, wave by wave.  The MFMA layout gives each lane four
+// consecutive columns of one row, so storing straight from the accumulators
+// would send every store instruction to 32 different rows.  Instead each wave
+// turns its block around in its own LDS region, 32 rows at a time (no
+// workgroup barrier: a wave's LDS operations complete in order): it writes
+// the 32 x WN fp32 accumulators, reads them back row-major (WN / 4 lanes per
+// row, four columns each) and stores whole row segments; the columns of a
+// transposed region are read down the rows instead (four lanes per column,
+// eight rows each), so each column's 32 rows go out as one 64-byte run.  A
+// lane keeps the same columns for all rows, so its bias, gate, output region
+// and mode are loaded once.  The LDS column of a value is XOR-swizzled by 8
+// times its 8-row group (WN is a multiple of 32), so the down-the-rows reads
+// of a half-wave hit 32 distinct banks and 4-column groups stay aligned.  Split-K
+// partials take the row-major path without the epilogue.  The caller passes
+// the main loop's LDS once every wave is done with it.
+template <int WM, int WN, int TM, int TN>
+__device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const GemmProblem& p, int prob, int64_t m0,
+                                                int64_t n0, int ks, int splits, float* __restrict__ partial,
+                                                const f32x16 (&acc)[TM][TN], float* sm, int wave, int wm, int wn,
+                                                int lane) {
+  constexpr int P = WN + 4;                  // LDS row pitch (floats)
+  constexpr int kLPR = WN / 4;               // lanes per row
+  constexpr int kRPI = kWave / kLPR;         // rows per row-major sweep
+  constexpr int kIt = 32 / kRPI;             // row-major sweeps per 32-row block
+  constexpr int kTIt = WN * 4 / kWave;       // down-the-rows sweeps per 32-row block
+  static_assert(32 % kRPI == 0 && (WN * 4) % kWave == 0, "epilogue lane layout");
+  float* reg = sm + wave * 32 * P;
+  const int l32 = lane % 32, hi = lane / 32;
+  auto swz_col = [](int row, int col) { return col ^ (((row >> 3) & 3) << 3); };
+  auto mode_of = [&](int64_t n) { return n < a.n_split ? a.mode0 : n < a.n_split2 ? a.mode1 : a.mode2; };
+
+  // Row-major role of this lane: columns n .. n + 3, rows r0 + kRPI * it.
+  const int c4 = lane % kLPR, r0 = lane / kLPR;
+  const int64_t nb = n0 + wn * WN, n = nb + 4 * c4;
+  const bool lane_ok = r0 < kRPI && n < a.N;
+  const int mode = lane_ok ? mode_of(n) : EPI_STORE;
+  bf16_t* out = nullptr;
+  int64_t col = 0, ldo = 0;
+  if (n < a.n_split) { out = static_cast<bf16_t*>(p.out0); col = n; ldo = p.ld0; }
+  else if (n < a.n_split2) { out = static_cast<bf16_t*>(p.out1); col = n - a.n_split; ldo = p.ld1; }
+  else { out = static_cast<bf16_t*>(p.out2); col = n - a.n_split2; ldo = p.ld2; }
+  float bias[4] = {0.f, 0.f, 0.f, 0.f}, gate[4] = {0.f, 0.f, 0.f, 0.f};
+  if (lane_ok && splits == 1) {
+    if (p.bias) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) bias[r] = ld(static_cast<const bf16_t*>(p.bias), n + r);
+    }
+    if (mode == EPI_RESID_GATE) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) gate[r] = ld(static_cast<const bf16_t*>(p.gate), n + r);
+    }
+  }
+  const bool row_major = lane_ok && (splits > 1 || mode != EPI_STORE_T);
+  const bool has_t = splits == 1 && (a.mode0 == EPI_STORE_T || a.mode1 == EPI_STORE_T || a.mode2 == EPI_STORE_T);
+  const int64_t rows_all = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+  const int64_t grow0 = prob == 0 ? 0 : a.p[0].M;
+
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    // acc[i][j][4q + r] = C[row 32 i + l32][col 32 j + 8 q + 4 hi + r] of this wave's block.
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x16& c = acc[i][j];
+        *reinterpret_cast<float4*>(reg + l32 * P + swz_col(l32, 32 * j + 8 * q + 4 * hi)) =
+            make_float4(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
+      }
+    const int64_t mb = m0 + wm * WM + 32 * i;  // first output row of the block
+    if (row_major) {
+      float4 u[kIt];
+#pragma unroll
+      for (int it = 0; it < kIt; ++it) {
+        const int rr = r0 + kRPI * it;
+        u[it] = *reinterpret_cast<const float4*>(reg + rr * P + swz_col(rr, 4 * c4));
+      }
+      if (splits > 1) {
+#pragma unroll
+        for (int it = 0; it < kIt; ++it) {
+          const int64_t m = mb + r0 + kRPI * it;
+          if (m < p.M) *reinterpret_cast<float4*>(partial + (int64_t(ks) * rows_all + grow0 + m) * a.N + n) = u[it];
+        }
+      } else {
+        float res[kIt][4];
+        if (mode == EPI_RESID_GATE) {
+          const bf16_t* rp = static_cast<const bf16_t*>(p.resid);
+#pragma unroll
+          for (int it = 0; it < kIt; ++it) {
+            const int64_t m = std::min<int64_t>(mb + r0 + kRPI * it, p.M - 1);
+            const u32x2 w = *reinterpret_cast<const u32x2*>(rp + m * p.ldr + col);
+            res[it][0] = __uint_as_float(w[0] << 16);
+            res[it][1] = __uint_as_float(w[0] & 0xffff0000u);
+            res[it][2] = __uint_as_float(w[1] << 16);
+            res[it][3] = __uint_as_float(w[1] & 0xffff0000u);
+          }
+        }
+#pragma unroll
+        for (int it = 0; it < kIt; ++it) {
+          const int64_t m = mb + r0 + kRPI * it;
+          if (m >= p.M) continue;
+          float v[4] = {u[it].x + bias[0], u[it].y + bias[1], u[it].z + bias[2], u[it].w + bias[3]};
+          if (mode == EPI_GELU) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = gelu_fast(v[r]);
+          } else if (mode == EPI_RESID_GATE) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = res[it][r] + gate[r] * v[r];
+          }
+          const u32x2 w = {pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
+          *reinterpret_cast<u32x2*>(out + m * ldo + col) = w;
+        }
+      }
+    }
+    if (has_t) {
+#pragma unroll
+      for (int it = 0; it < kTIt; ++it) {
+        const int item = it * kWave + lane;
+        const int tc = item / 4, mc = item % 4;   // column of the block, 8-row group
+        const int64_t nt = nb + tc, m = mb + 8 * mc;
+        if (nt >= a.N || m >= p.M || mode_of(nt) != EPI_STORE_T) continue;
+        const bf16_t* bp = static_cast<const bf16_t*>(p.bias);
+        const float b = bp ? ld(bp, nt) : 0.f;
+        bf16_t* o;
+        int64_t c0, lo;
+        if (nt < a.n_split) { o = static_cast<bf16_t*>(p.out0); c0 = nt; lo = p.ld0; }
+        else if (nt < a.n_split2) { o = static_cast<bf16_t*>(p.out1); c0 = nt - a.n_split; lo = p.ld1; }
+        else { o = static_cast<bf16_t*>(p.out2); c0 = nt - a.n_split2; lo = p.ld2; }
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = reg[(8 * mc + e) * P + swz_col(8 * mc + e, tc)] + b;
+        bf16_t* dst = o + c0 * lo + m;
+        if (m + 8 <= p.M) {
+          const u32x4 w = {pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])};
+          *reinterpret_cast<u32x4*>(dst) = w;
+        } else {
+          for (int e = 0; m + e < p.M; ++e) st(dst, e, v[e]);
+        }
+      }
+    }
+  }
+}
+
 // Swizzled 16-byte chunk slot of (row, chunk) in a 128-byte LDS row.
 __device__ __forceinline__ int swz(int row, int chunk) { return row * 8 + (chunk ^ ((row >> 1) & 7)); }
 
@@ -136,7 +285,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(const
   int prob, ks;
   int64_t m0, n0;
   if (!map_tile(a, kBM, BN, splits, prob, m0, n0, ks)) return;
-  const GemmProblem& p = a.p[prob];
+  const GemmProblem p = prob ? a.p[1] : a.p[0];  // by value: a select, no indexed copy of the arguments
   const bf16_t* A = static_cast<const bf16_t*>(p.A);
   const bf16_t* W = static_cast<const bf16_t*>(p.W);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
@@ -287,6 +436,154 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(const
     }
   }
 
+  // The last barrier of the main loop has passed: LDS is free.
+  staged_epilogue<WM, WN, TM, TN>(a, p, prob, m0, n0, ks, splits, partial, acc,
+                                  reinterpret_cast<float*>(&lds[0][0]), wave, wm, wn, lane);
+}
+
+// Ping-pong form of the 256 x 256 x 64 kernel.  The 8 waves form two groups
+// of four (one wave of each group per SIMD); group g owns output rows
+// [128 g, 128 g + 128) and each of its waves a 128 x 64 block.  The groups
+// alternate between a compute phase (the 32 MFMAs of one k-tile, fragments
+// read from LDS) and a memory phase (stage half of a later k-tile into LDS
+// and issue the global loads of the half after it), one workgroup barrier
+// per phase, offset by one phase: while one group's waves issue MFMAs the
+// other group's waves on the same SIMDs do the memory work, so the matrix
+// pipe of each SIMD is fed from one wave or the other in every phase.
+//   phase 2t:     group 0 computes k-tile t;  group 1 stages its half of
+//                 tile t + 1 and loads its half of tile t + 2;
+//   phase 2t + 1: group 1 computes k-tile t;  group 0 stages / loads the same.
+// Tile t lives in LDS buffer t mod 2: it is read in phases 2t and 2t + 1 and
+// written in phases 2t - 2 and 2t - 1, after tile t - 2 left that buffer.
+__global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(const GemmArgs a, float* __restrict__ partial,
+                                                          int splits) {
+  constexpr int BN = 256, WM = 128, WN = 64;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int HALF = 4;                    // 16-byte chunks per thread per half-tile operand
+  __shared__ u32x4 lds[2][(kBM + BN) * 8];
+
+  int prob, ks;
+  int64_t m0, n0;
+  if (!map_tile(a, kBM, BN, splits, prob, m0, n0, ks)) return;
+  const GemmProblem p = prob ? a.p[1] : a.p[0];  // by value: a select, no indexed copy of the arguments
+  const bf16_t* A = static_cast<const bf16_t*>(p.A);
+  const bf16_t* W = static_cast<const bf16_t*>(p.W);
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int l32 = lane % 32, hi = lane / 32;
+  const int grp = __builtin_amdgcn_readfirstlane(wave / 4);
+  const int wm = grp, wn = wave % 4;
+
+  const int64_t nk = a.K / kBK;
+  const int64_t kt0 = nk * ks / splits, kt1 = nk * (ks + 1) / splits;
+  const int64_t n_t = kt1 - kt0;
+
+  // Staging of this group's half: A rows and W rows [128 grp, 128 grp + 128),
+  // thread tg moves chunk tg % 8 of rows tg / 8 + 32 j (one swizzle for all j).
+  const int tg = tid % 256;
+  const int row_t = tg / 8, kc_t = tg % 8;
+  const int slot_t = (128 * grp + row_t) * 8 + (kc_t ^ ((row_t >> 1) & 7));
+  uint32_t a_off[HALF], w_off[HALF];
+#pragma unroll
+  for (int j = 0; j < HALF; ++j) {
+    a_off[j] = uint32_t(((128 * grp + row_t + 32 * j) * p.lda + kc_t * 8) * 2);
+    w_off[j] = uint32_t(((128 * grp + row_t + 32 * j) * a.K + kc_t * 8) * 2);
+  }
+  const char* a_base = reinterpret_cast<const char*>(A + m0 * p.lda);
+  const char* w_base = reinterpret_cast<const char*>(W + n0 * a.K);
+  const int64_t a_bytes = (p.M - m0) * p.lda * 2, w_bytes = (a.N - n0) * a.K * 2;
+  // The staged loads stay in flight across the group's next compute phase
+  // (a loop-carried value), so they are compiler-visible buffer loads: the
+  // compiler places the vmcnt wait before the LDS store that consumes them.
+  u32x4 sa[HALF], sw[HALF];
+  auto load_half = [&](int64_t kt) {
+    const int64_t koff = kt * kBK * 2;
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(a_base + koff), 0, int(a_bytes - koff), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(w_base + koff), 0, int(w_bytes - koff), 0x00020000);
+#pragma unroll
+    for (int j = 0; j < HALF; ++j) sa[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, int(a_off[j]), 0, 0);
+#pragma unroll
+    for (int j = 0; j < HALF; ++j) sw[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, int(w_off[j]), 0, 0);
+  };
+  auto store_half = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < HALF; ++j) lds[buf][slot_t + 256 * j] = sa[j];
+#pragma unroll
+    for (int j = 0; j < HALF; ++j) lds[buf][kBM * 8 + slot_t + 256 * j] = sw[j];
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  auto compute = [&](int buf) {
+    const u32x4* L = lds[buf];
+    bf16x8 af[2][TM], wf[2][TN];
+    auto read = [&](int kk, int slot) {
+      const int chunk = 2 * kk + hi;
+#pragma unroll
+      for (int i = 0; i < TM; ++i) af[slot][i] = as_bf16x8(L[swz(wm * WM + 32 * i + l32, chunk)]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) wf[slot][j] = as_bf16x8(L[kBM * 8 + swz(wn * WN + 32 * j + l32, chunk)]);
+    };
+    read(0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      if (kk + 1 < kBK / 16) read(kk + 1, (kk + 1) & 1);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32x32x16(wf[kk & 1][j], af[kk & 1][i], acc[i][j]);
+      if (kk + 1 < kBK / 16) {
+#pragma unroll
+        for (int r = 0; r < TM + TN; ++r) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - (TM + TN), 0);
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x008, TM * TN, 0);
+      }
+    }
+  };
+
+  if (n_t > 0) {
+    load_half(kt0);
+    store_half(0);
+    if (n_t > 1) load_half(kt0 + 1);
+  }
+  lds_barrier();
+  // Memory phase of k-tile t: stage this group's half of tile t + 1, then
+  // issue its loads of tile t + 2.
+  auto memory = [&](int64_t t) {
+    if (t + 1 < n_t) {
+      store_half(int((t + 1) & 1));
+      if (t + 2 < n_t) load_half(kt0 + t + 2);
+    }
+  };
+  // Each group runs its own straight loop; both pass the same barriers.
+  if (grp == 0) {
+    for (int64_t t = 0; t < n_t; ++t) {
+      compute(int(t & 1));
+      lds_barrier();
+      memory(t);
+      lds_barrier();
+    }
+  } else {
+    for (int64_t t = 0; t < n_t; ++t) {
+      memory(t);
+      lds_barrier();
+      compute(int(t & 1));
+      lds_barrier();
+    }
+  }
+
   // acc[i][j][4q + r] = C[m0 + wm*WM + 32i + l32][n0 + wn*WN + 32j + 8q + 4hi + r].
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
@@ -338,7 +635,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmArgs a) {
   int prob, ks;
   int64_t m0, n0;
   if (!map_tile(a, kFB, kFB, 1, prob, m0, n0, ks)) return;
-  const GemmProblem& p = a.p[prob];
+  const GemmProblem p = prob ? a.p[1] : a.p[0];  // by value: a select, no indexed copy of the arguments
   const float* A = static_cast<const float*>(p.A);
   const float* W = static_cast<const float*>(p.W);
   const int tid = threadIdx.x, tx = tid % 16, ty = tid / 16;
@@ -414,11 +711,11 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
     }
   }
   pl.waves = 8;
-  // Two register stages do not fit the 256-wide tile's registers.  The staged
+  // Two register stages fit the registers of the 128-wide tile only.  The staged
   // loads are asynchronous inline assembly, so an instance that spilled a
   // destination register would read it before the load lands: every
   // instance must build without scratch (the build checks it).
-  pl.stages = pl.bn == 256 ? 1 : 2;
+  pl.stages = pl.bn == 128 ? 2 : 1;
   // Tuning override "BN,SPLITS[,8[,STAGES]]" (e.g. AVITS_GEMM_TILE=256,3,8,1),
   // for one launch family with AVITS_GEMM_TILE_<family> (e.g. _gemm_o).
   const char* env = nullptr;
@@ -436,7 +733,7 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
       pl.bn = bn;
       pl.splits = sp;
       pl.waves = wv;
-      pl.stages = bn == 256 ? 1 : stg;  // the 256-wide tile has one register stage only
+      pl.stages = bn == 128 ? stg : 1;  // the wider tiles have one register stage only
       pl.tiles = tiles_of(a, kBM, bn);
     }
   }
@@ -458,10 +755,13 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
     const dim3 grid(unsigned(pl.tiles * pl.splits));
     {
     TimedLaunch timed(family, s);  // the GEMM kernel alone; the reduce is its own family
+    const char* ppe = getenv("AVITS_GEMM_PP");
+    if (pl.bn == 256 && ppe && atoi(ppe) == 1) {
+      hipLaunchKernelGGL(gemm_bf16_pp_kernel, grid, dim3(512), 0, s, a, partial, pl.splits);
+    } else
     switch (pl.bn * 100 + pl.waves * 10 + pl.stages) {
       case 25681: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 19281: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
-      case 19282: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 12881: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
     }
