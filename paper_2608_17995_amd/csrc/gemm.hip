@@ -5,7 +5,9 @@
 //  - Macro tile 256 x BN (BN in {256, 192, 128}) x 64, one 512-thread
 //    workgroup of 8 waves (2 x 4, or 4 x 2 for BN = 192), each wave a
 //    128 x 64 (64 x 96) block of v_mfma_f32_32x32x16_bf16 tiles; two
-//    waves per SIMD hide each other's LDS and barrier waits.
+//    waves per SIMD hide each other's LDS and barrier waits.  The 256-wide
+//    tile runs the ping-pong form (gemm_bf16_pp_kernel): the two halves of
+//    the workgroup alternate compute and memory phases.
 //  - The MFMA computes C^T = W A^T, so each lane owns groups of four
 //    consecutive output columns of one row (8-byte stores in the epilogue).
 //  - k-tiles are staged global -> registers -> LDS through two LDS buffers,
@@ -584,29 +586,8 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(const GemmArgs a, flo
     }
   }
 
-  // acc[i][j][4q + r] = C[m0 + wm*WM + 32i + l32][n0 + wn*WN + 32j + 8q + 4hi + r].
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int64_t m = m0 + wm * WM + 32 * i + l32;
-    if (m >= p.M) continue;
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t n = n0 + wn * WN + 32 * j + 8 * q + 4 * hi;
-        if (n >= a.N) continue;
-        const f32x16& c = acc[i][j];
-        if (splits == 1) {
-          epilogue4<bf16_t>(a, p, m, n, c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
-        } else {
-          const int64_t grow = (prob == 0 ? 0 : a.p[0].M) + m;
-          const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
-          float* dst = partial + (int64_t(ks) * rows + grow) * a.N + n;
-          *reinterpret_cast<float4*>(dst) = make_float4(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
-        }
-      }
-    }
-  }
+  staged_epilogue<WM, WN, TM, TN>(a, p, prob, m0, n0, ks, splits, partial, acc,
+                                  reinterpret_cast<float*>(&lds[0][0]), wave, wm, wn, lane);
 }
 
 // Sum the split-K partials in split order and apply the epilogue.
@@ -686,11 +667,12 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
     return pl;
   }
   // Score every (column tile, K split) pair: busy fraction of the last wave
-  // of work units on the 256 CUs, times a per-tile factor (larger tiles move
-  // less L2 data per FLOP; measured on MI355X at the FLUX block shapes), times
-  // a factor for the extra fp32 partial traffic of a split.
+  // of work units on the 256 CUs, times a per-tile factor (the 256-wide tile
+  // runs the ping-pong kernel and moves less L2 data per FLOP; the factors
+  // are measured on MI355X at the FLUX block shapes), times a factor for the
+  // extra fp32 partial traffic of a split.
   const int cands[3] = {256, 192, 128};
-  const double eff[3] = {1.0, 0.97, 0.85};
+  const double eff[3] = {1.0, 0.74, 0.65};
   const int64_t nk = a.K / kBK;
   const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
   double best = -1.0;
@@ -755,12 +737,8 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
     const dim3 grid(unsigned(pl.tiles * pl.splits));
     {
     TimedLaunch timed(family, s);  // the GEMM kernel alone; the reduce is its own family
-    const char* ppe = getenv("AVITS_GEMM_PP");
-    if (pl.bn == 256 && ppe && atoi(ppe) == 1) {
-      hipLaunchKernelGGL(gemm_bf16_pp_kernel, grid, dim3(512), 0, s, a, partial, pl.splits);
-    } else
     switch (pl.bn * 100 + pl.waves * 10 + pl.stages) {
-      case 25681: hipLaunchKernelGGL((gemm_bf16_kernel<256, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
+      case 25681: hipLaunchKernelGGL(gemm_bf16_pp_kernel, grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 19281: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 12881: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
