@@ -12,7 +12,8 @@
 // Up to N = 16384 one 1024-thread workgroup does the whole selection: at the
 // sizes of a resolution transition (N = 4096 .. 16384 scores, 16-64 KiB) the
 // cost is latency, not bandwidth, and the keys stay in registers between
-// passes.  Larger N runs the same passes grid-wide (below).
+// passes (each thread holds consecutive elements, so the emission is one
+// workgroup scan).  Larger N runs the same passes grid-wide (below).
 #include "common.h"
 
 namespace avits {
@@ -59,16 +60,6 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
 // kRegKeys keys per thread stay in registers: N <= 16384.
 constexpr int kRegKeys = 16;
 
-// Calls f(i, key) for every element i = tid + kThreads * j < N.
-template <typename F>
-__device__ __forceinline__ void for_each_key(const uint32_t (&keys)[kRegKeys], int N, F&& f) {
-#pragma unroll
-  for (int j = 0; j < kRegKeys; ++j) {
-    const int i = threadIdx.x + kThreads * j;
-    if (i < N) f(i, keys[j]);
-  }
-}
-
 __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __restrict__ scores, int N, int k,
                                                                 int32_t* __restrict__ idx) {
   __shared__ uint32_t hist[kWaves][256];   // per-wave histograms: atomics contend only inside a wave
@@ -77,11 +68,14 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
   __shared__ uint32_t s_digit, s_above;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
 
+  // Thread t holds the q consecutive elements t q .. t q + q - 1, so the
+  // final emission needs a single workgroup scan.
+  const int q = (N + kThreads - 1) / kThreads;
   uint32_t keys[kRegKeys];
 #pragma unroll
   for (int j = 0; j < kRegKeys; ++j) {
-    const int i = tid + kThreads * j;
-    keys[j] = i < N ? order_key(scores[i]) : 0u;
+    const int i = tid * q + j;
+    keys[j] = j < q && i < N ? order_key(scores[i]) : 0u;
   }
 
   uint32_t prefix = 0u, mask = 0u;
@@ -89,9 +83,28 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int b = tid; b < kWaves * 256; b += kThreads) (&hist[0][0])[b] = 0u;
     __syncthreads();
-    for_each_key(keys, N, [&](int, uint32_t key) {
-      if ((key & mask) == prefix) atomicAdd(&hist[wave][(key >> shift) & 255u], 1u);
-    });
+    // Scores of one exponent share their top digits, so a wave first adds
+    // its most frequent-looking digit(s) with one ballot-counted atomic
+    // (two rounds in the first pass, one later), then the rest one by one.
+    const int rounds = shift == 24 ? 2 : 1;
+#pragma unroll
+    for (int j = 0; j < kRegKeys; ++j) {
+      if (j >= q) break;  // uniform
+      const int i = tid * q + j;
+      const uint32_t key = keys[j];
+      bool pending = i < N && (key & mask) == prefix;
+      const uint32_t digit = (key >> shift) & 255u;
+      for (int it = 0; it < rounds; ++it) {
+        const uint64_t act = __ballot(pending);
+        if (act == 0) break;
+        const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
+        const uint32_t d0 = __shfl(digit, leader, kWave);
+        const uint64_t same = __ballot(pending && digit == d0);
+        if (lane == leader) atomicAdd(&hist[wave][d0], uint32_t(__popcll(same)));
+        pending = pending && digit != d0;
+      }
+      if (pending) atomicAdd(&hist[wave][digit], 1u);
+    }
     __syncthreads();
     // Waves 0..3 own digits 64w .. 64w + 63: the count per digit and its
     // suffix sum inside the wave (shuffle scan from the high lanes down).
@@ -129,32 +142,38 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
     remaining -= s_above;
     __syncthreads();
   }
-  // T = prefix; `remaining` elements equal to T are still needed.  Emit in
-  // index order, one 1024-element chunk per block-wide scan.
+  // T = prefix; `remaining` elements equal to T are still needed.  One
+  // workgroup scan of the per-thread counts of keys > T and == T gives each
+  // thread its output offset; the threads' element ranges are consecutive,
+  // so the output is in index order and the first `need` keys equal to T
+  // (lowest indices) are the ones taken.
   const uint32_t T = prefix, need = remaining;
-  uint32_t eq_before = 0u, out_before = 0u;
-  const int nchunks = (N + kThreads - 1) / kThreads;
-  auto emit_chunk = [&](int i, uint32_t key) {
-    uint32_t gt = 0u, eq = 0u;
-    if (i < N) {
-      gt = key > T;
-      eq = key == T;
-    }
-    uint32_t tot;
-    // Pack both counts: low 16 bits equal-to-T, high 16 bits greater-than-T.
-    const uint32_t ex = block_exclusive_scan(eq | (gt << 16), wsum, &tot);
-    const uint32_t eq_ex = ex & 0xffffu, gt_ex = ex >> 16;
-    const uint32_t eq_tot = tot & 0xffffu, gt_tot = tot >> 16;
-    const uint32_t eq_quota = need > eq_before ? need - eq_before : 0u;  // eq still to take
-    const bool sel = gt || (eq && eq_ex < eq_quota);
-    const uint32_t at = out_before + gt_ex + min(eq_ex, eq_quota);
-    if (sel && at < uint32_t(k)) idx[at] = i;
-    out_before += gt_tot + min(eq_tot, eq_quota);
-    eq_before += eq_tot;
-  };
+  uint32_t gt_c = 0u, eq_c = 0u;
 #pragma unroll
-  for (int j = 0; j < kRegKeys; ++j)
-    if (j < nchunks) emit_chunk(tid + kThreads * j, keys[j]);
+  for (int j = 0; j < kRegKeys; ++j) {
+    if (j < q && tid * q + j < N) {
+      gt_c += keys[j] > T;
+      eq_c += keys[j] == T;
+    }
+  }
+  uint32_t tot;
+  // Packed counts: low 16 bits equal-to-T, high 16 bits greater-than-T (N <= 16384).
+  const uint32_t ex = block_exclusive_scan(eq_c | (gt_c << 16), wsum, &tot);
+  uint32_t eq_seen = ex & 0xffffu;
+  uint32_t at = (ex >> 16) + min(eq_seen, need);
+#pragma unroll
+  for (int j = 0; j < kRegKeys; ++j) {
+    const int i = tid * q + j;
+    if (j < q && i < N) {
+      const uint32_t key = keys[j];
+      if (key > T) {
+        idx[at++] = i;
+      } else if (key == T) {
+        if (eq_seen < need) idx[at++] = i;
+        ++eq_seen;
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
