@@ -434,7 +434,7 @@ def main(argv=None):
                    "lowres_grid": [w.H_lr, w.W_lr], "highres_grid": [w.H_hr, w.W_hr], "keep_ratio": w.rho,
                    "k": w.k, "seq_len": S, "alpha": w.alpha, "upsample": "nearest"},
         "roofline": {
-            "kernel": "gemm_bf16_kernel",
+            "kernel": "gemm_bf16_pp_kernel",
             "bound": "mfma",
             "achieved": round(gemm_tflops, 1),
             "peak": PEAK_BF16_TFLOPS,
