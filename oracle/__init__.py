@@ -17,7 +17,7 @@ from .importance import (  # noqa: F401
     spatial_importance, spatial_importance_bruteforce, joint_lse, step_variance,
     minmax_normalise, joint_score, score, text_attention_mass, score_from_mass,
 )
-from .selection import select_topk  # noqa: F401
+from .selection import select_topk, select_topk_perturbed, select_topk_batched  # noqa: F401
 from .relayout import (  # noqa: F401
     upsample_nearest, upsample_bilinear, gather_upsample, scatter, selected_positions,
     mixed_layout, gather_mixed, scatter_mixed,

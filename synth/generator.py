@@ -210,6 +210,12 @@ def random_lowres_selection(w: Workload, k: int, tid_offset: int = 0) -> np.ndar
     return np.sort(g.permutation(w.N_lr)[:k]).astype(np.int32)
 
 
+def tiebreak_noise(seed: int, n: int, std: float = 1e-6) -> np.ndarray:
+    """Seeded Gaussian perturbation for the selection's tie-break, fp32."""
+    g = rng(seed, _TID["scores_dup"] + 1)
+    return (g.standard_normal(size=n) * std).astype(np.float32)
+
+
 def quantised_scores(seed: int, n: int, levels: int) -> np.ndarray:
     """fp32 scores with heavy duplicates: ``levels`` distinct values in [0, 1)."""
     g = rng(seed, _TID["scores_dup"])
