@@ -101,6 +101,30 @@ int avits_select(const float* scores, int64_t N, int64_t k, int32_t* idx,
                  void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_select_perturbed — Eq. topk with the paper's tie-break by a small
+ * perturbation applied before the selection (Section 3.3): the keys are the
+ * fp32 sums scores[i] + delta[i] (one rounding), then as avits_select
+ * (ties of the sums still go to the lowest index).  delta [N] fp32 is the
+ * caller's seeded perturbation (e.g. 1e-6 times standard normal draws).
+ * Other arguments, workspace and errors as avits_select.
+ * ---------------------------------------------------------------------- */
+int avits_select_perturbed(const float* scores, const float* delta, int64_t N, int64_t k,
+                           int32_t* idx, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_select_batched — B independent selections in one launch (images of
+ * a batch with their own token counts and budgets).  Element b selects the
+ * top k[b] of scores[offsets[b] .. offsets[b + 1]) (perturbed by delta over
+ * the same range when delta is not NULL) and writes its indices, local to
+ * the element and ascending, to idx[sum_{c<b} k[c] ..].  offsets [B + 1] and
+ * k [B] are host arrays (int64); scores, delta, idx device arrays.
+ * Requires 1 <= B <= 64, offsets[0] == 0, 1 <= N_b <= 16384 and
+ * 0 <= k[b] <= N_b.  No workspace.
+ * ---------------------------------------------------------------------- */
+int avits_select_batched(const float* scores, const float* delta, int32_t B, const int64_t* offsets,
+                         const int64_t* k, int32_t* idx, void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_gather_upsample — Stage-2 re-layout (Section 3.2).
  *
  * With N = 4*H_lr*W_lr high-res tokens in raster order on a (2H_lr)x(2W_lr)

@@ -43,6 +43,10 @@ _SIGS = {
                                    _size, _c_void_p]),
     "avits_select_workspace_bytes": (_size, [_i64]),
     "avits_select": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _size, _c_void_p]),
+    "avits_select_perturbed": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _c_void_p, _c_void_p, _size,
+                                              _c_void_p]),
+    "avits_select_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _i32, _c_void_p, _c_void_p, _c_void_p,
+                                            _c_void_p]),
     "avits_gather_upsample": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _i64, _i32, _i32, _i64,
                                              _i64, ctypes.c_int, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p,
                                              _c_void_p]),
@@ -172,6 +176,26 @@ def avits_select(scores, k, idx, workspace=None, stream=None):
     ws, wsp, wsb = _workspace(workspace, avits_select_workspace_bytes(N), scores.device)
     _check(load().avits_select(_dev(scores, "scores", torch.float32), N, k, _dev(idx, "idx", torch.int32),
                                wsp, wsb, _stream(stream)))
+    return idx
+
+
+def avits_select_perturbed(scores, delta, k, idx, workspace=None, stream=None):
+    import torch
+    N = scores.shape[0]
+    ws, wsp, wsb = _workspace(workspace, avits_select_workspace_bytes(N), scores.device)
+    _check(load().avits_select_perturbed(_dev(scores, "scores", torch.float32), _dev(delta, "delta", torch.float32),
+                                         N, k, _dev(idx, "idx", torch.int32), wsp, wsb, _stream(stream)))
+    return idx
+
+
+def avits_select_batched(scores, offsets, k, idx, delta=None, stream=None):
+    """offsets, k: host sequences of ints (B + 1 and B); idx holds sum(k) entries."""
+    import torch
+    B = len(k)
+    off = (ctypes.c_int64 * (B + 1))(*[int(o) for o in offsets])
+    kk = (ctypes.c_int64 * B)(*[int(x) for x in k])
+    _check(load().avits_select_batched(_dev(scores, "scores", torch.float32), _dev(delta, "delta", torch.float32),
+                                       B, off, kk, _dev(idx, "idx", torch.int32), _stream(stream)))
     return idx
 
 

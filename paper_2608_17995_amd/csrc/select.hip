@@ -29,6 +29,13 @@ __device__ __forceinline__ uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Key of element i: of scores[i], or of the fp32 sum scores[i] + delta[i]
+// when a perturbation is given (the seeded tie-break of Eq. topk).
+__device__ __forceinline__ uint32_t key_at(const float* __restrict__ scores, const float* __restrict__ delta,
+                                           int64_t i) {
+  return order_key(delta ? scores[i] + delta[i] : scores[i]);
+}
+
 __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
 #pragma unroll
   for (int o = 1; o < kWave; o <<= 1) v += __shfl_xor(v, o, kWave);
@@ -60,8 +67,8 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
 // kRegKeys keys per thread stay in registers: N <= 16384.
 constexpr int kRegKeys = 16;
 
-__global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __restrict__ scores, int N, int k,
-                                                                int32_t* __restrict__ idx) {
+__device__ __forceinline__ void select_block(const float* __restrict__ scores, const float* __restrict__ delta,
+                                             int N, int k, int32_t* __restrict__ idx) {
   __shared__ uint32_t hist[kWaves][256];   // per-wave histograms: atomics contend only inside a wave
   __shared__ uint32_t tot_s[256], suf_s[256];
   __shared__ uint32_t wsum[kWaves];
@@ -75,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
 #pragma unroll
   for (int j = 0; j < kRegKeys; ++j) {
     const int i = tid * q + j;
-    keys[j] = j < q && i < N ? order_key(scores[i]) : 0u;
+    keys[j] = j < q && i < N ? key_at(scores, delta, i) : 0u;
   }
 
   uint32_t prefix = 0u, mask = 0u;
@@ -176,6 +183,32 @@ __global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __r
   }
 }
 
+__global__ __launch_bounds__(kThreads) void radix_select_kernel(const float* __restrict__ scores,
+                                                                const float* __restrict__ delta, int N, int k,
+                                                                int32_t* __restrict__ idx) {
+  select_block(scores, delta, N, k, idx);
+}
+
+// B independent selections, one workgroup each: element b selects the top
+// k[b] of scores[off[b] .. off[b + 1]) and writes local indices at
+// idx + out[b].
+constexpr int kMaxBatch = 64;
+struct SelBatch {
+  int64_t off[kMaxBatch + 1];
+  int64_t out[kMaxBatch];
+  int32_t k[kMaxBatch];
+};
+
+__global__ __launch_bounds__(kThreads) void radix_select_batched_kernel(const float* __restrict__ scores,
+                                                                        const float* __restrict__ delta,
+                                                                        const SelBatch bt, int32_t* __restrict__ idx) {
+  const int b = blockIdx.x;
+  const int64_t o = bt.off[b];
+  const int N = int(bt.off[b + 1] - o), k = bt.k[b];
+  if (k == 0) return;
+  select_block(scores + o, delta ? delta + o : nullptr, N, k, idx + bt.out[b]);
+}
+
 // ---------------------------------------------------------------------------
 // Grid-wide radix select for N above what one workgroup holds in registers:
 // the same four digit passes and index-order emission, spread over the GPU.
@@ -209,24 +242,30 @@ __global__ __launch_bounds__(kGT) void select_init_kernel(SelState* __restrict__
 }
 
 // Keys of elements i0 .. i0 + 3; live[e] is false past the end of the scores.
-__device__ __forceinline__ void load_keys4(const float* __restrict__ scores, int64_t N, int64_t i0, uint32_t (&key)[4],
-                                           bool (&live)[4]) {
-  if (i0 + 3 < N && (reinterpret_cast<uintptr_t>(scores + i0) & 15) == 0) {
-    const float4 v = *reinterpret_cast<const float4*>(scores + i0);
+__device__ __forceinline__ void load_keys4(const float* __restrict__ scores, const float* __restrict__ delta,
+                                           int64_t N, int64_t i0, uint32_t (&key)[4], bool (&live)[4]) {
+  if (i0 + 3 < N && (reinterpret_cast<uintptr_t>(scores + i0) & 15) == 0 &&
+      (!delta || (reinterpret_cast<uintptr_t>(delta + i0) & 15) == 0)) {
+    float4 v = *reinterpret_cast<const float4*>(scores + i0);
+    if (delta) {
+      const float4 d = *reinterpret_cast<const float4*>(delta + i0);
+      v.x += d.x; v.y += d.y; v.z += d.z; v.w += d.w;
+    }
     key[0] = order_key(v.x); key[1] = order_key(v.y); key[2] = order_key(v.z); key[3] = order_key(v.w);
     live[0] = live[1] = live[2] = live[3] = true;
   } else {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       live[e] = i0 + e < N;
-      key[e] = live[e] ? order_key(scores[i0 + e]) : 0u;
+      key[e] = live[e] ? key_at(scores, delta, i0 + e) : 0u;
     }
   }
 }
 
 constexpr int kSubHist = 4;  // LDS histogram copies per wave (lane % 4): spreads atomics on one bin
 
-__global__ __launch_bounds__(kGT) void select_hist_kernel(const float* __restrict__ scores, int64_t N, int pass,
+__global__ __launch_bounds__(kGT) void select_hist_kernel(const float* __restrict__ scores,
+    const float* __restrict__ delta, int64_t N, int pass,
                                                           SelState* __restrict__ st) {
   __shared__ uint32_t hs[kGWaves * kSubHist][256];
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
@@ -260,7 +299,7 @@ __global__ __launch_bounds__(kGT) void select_hist_kernel(const float* __restric
   for (int64_t g = int64_t(blockIdx.x) * kGT + tid; g - tid < groups; g += int64_t(gridDim.x) * kGT) {
     uint32_t key[4];
     bool live[4];
-    load_keys4(scores, N, 4 * g, key, live);  // past the end: live = false
+    load_keys4(scores, delta, N, 4 * g, key, live);  // past the end: live = false
 #pragma unroll
     for (int e = 0; e < 4; ++e) count(key[e], live[e]);
   }
@@ -298,13 +337,13 @@ __global__ __launch_bounds__(256) void select_scan_kernel(int pass, SelState* __
 }
 
 // Sixteen consecutive elements of thread t of chunk `chunk`: t * 16 ..
-__device__ __forceinline__ void chunk_keys(const float* __restrict__ scores, int64_t N, int64_t i0, uint32_t (&key)[16],
-                                           bool (&live)[16]) {
+__device__ __forceinline__ void chunk_keys(const float* __restrict__ scores, const float* __restrict__ delta,
+                                           int64_t N, int64_t i0, uint32_t (&key)[16], bool (&live)[16]) {
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     uint32_t k4[4];
     bool l4[4];
-    load_keys4(scores, N, i0 + 4 * q, k4, l4);
+    load_keys4(scores, delta, N, i0 + 4 * q, k4, l4);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       key[4 * q + e] = k4[e];
@@ -335,7 +374,8 @@ __device__ __forceinline__ uint32_t grid_block_scan(uint32_t v, uint32_t* wsum, 
   return before + incl - v;
 }
 
-__global__ __launch_bounds__(kGT) void select_count_kernel(const float* __restrict__ scores, int64_t N,
+__global__ __launch_bounds__(kGT) void select_count_kernel(const float* __restrict__ scores,
+    const float* __restrict__ delta, int64_t N,
                                                            const SelState* __restrict__ st,
                                                            uint32_t* __restrict__ cnt) {
   __shared__ uint32_t wsum[kGWaves];
@@ -343,7 +383,7 @@ __global__ __launch_bounds__(kGT) void select_count_kernel(const float* __restri
   const int64_t i0 = int64_t(blockIdx.x) * kChunk + 16 * threadIdx.x;
   uint32_t key[16];
   bool live[16];
-  chunk_keys(scores, N, i0, key, live);
+  chunk_keys(scores, delta, N, i0, key, live);
   uint32_t packed = 0u;  // keys > T in the high 16 bits, keys == T in the low
 #pragma unroll
   for (int e = 0; e < 16; ++e) packed += live[e] ? ((key[e] > T) << 16) | uint32_t(key[e] == T) : 0u;
@@ -403,7 +443,8 @@ __global__ __launch_bounds__(kThreads) void select_offsets_kernel(const uint32_t
 // 16-byte load).  Counts per wave first (keys stay in registers), a 4-entry
 // scan in LDS, then each round ranks its lanes with a wave scan, so
 // neighbouring lanes store neighbouring output positions.
-__global__ __launch_bounds__(kGT) void select_emit_kernel(const float* __restrict__ scores, int64_t N,
+__global__ __launch_bounds__(kGT) void select_emit_kernel(const float* __restrict__ scores,
+    const float* __restrict__ delta, int64_t N,
                                                           const SelState* __restrict__ st,
                                                           const uint32_t* __restrict__ off, int64_t k,
                                                           int32_t* __restrict__ idx) {
@@ -417,7 +458,7 @@ __global__ __launch_bounds__(kGT) void select_emit_kernel(const float* __restric
   uint32_t packed = 0u;  // keys > T in the high 16 bits, keys == T in the low
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
-    load_keys4(scores, N, w0 + 4 * (r * kWave + lane), key[r], live[r]);
+    load_keys4(scores, delta, N, w0 + 4 * (r * kWave + lane), key[r], live[r]);
 #pragma unroll
     for (int e = 0; e < 4; ++e) packed += live[r][e] ? ((key[r][e] > T) << 16) | uint32_t(key[r][e] == T) : 0u;
   }
@@ -486,8 +527,8 @@ extern "C" size_t avits_select_workspace_bytes(int64_t N) {
   return select_ws_layout(nullptr, N).bytes;
 }
 
-extern "C" int avits_select(const float* scores, int64_t N, int64_t k, int32_t* idx, void* workspace,
-                            size_t workspace_bytes, void* stream) {
+static int select_impl(const float* scores, const float* delta, int64_t N, int64_t k, int32_t* idx, void* workspace,
+                       size_t workspace_bytes, void* stream) {
   AVITS_REQUIRE(N >= 1 && N <= INT32_MAX, "select: N=%lld outside [1, 2^31)", (long long)N);
   AVITS_REQUIRE(k >= 0 && k <= N, "select: k=%lld outside [0, N=%lld]", (long long)k, (long long)N);
   if (k == 0) return AVITS_OK;
@@ -495,7 +536,7 @@ extern "C" int avits_select(const float* scores, int64_t N, int64_t k, int32_t* 
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (N <= kOneBlockMax) {
     TimedLaunch timed("select", s);
-    hipLaunchKernelGGL(radix_select_kernel, dim3(1), dim3(kThreads), 0, s, scores, int(N), int(k), idx);
+    hipLaunchKernelGGL(radix_select_kernel, dim3(1), dim3(kThreads), 0, s, scores, delta, int(N), int(k), idx);
     return launch_status("select");
   }
   const SelWs need = select_ws_layout(nullptr, N);
@@ -508,11 +549,49 @@ extern "C" int avits_select(const float* scores, int64_t N, int64_t k, int32_t* 
   TimedLaunch timed("select", s);
   hipLaunchKernelGGL(select_init_kernel, dim3(1), dim3(kGT), 0, s, ws.st, uint32_t(k));
   for (int pass = 0; pass < 4; ++pass) {
-    hipLaunchKernelGGL(select_hist_kernel, dim3(hblocks), dim3(kGT), 0, s, scores, N, pass, ws.st);
+    hipLaunchKernelGGL(select_hist_kernel, dim3(hblocks), dim3(kGT), 0, s, scores, delta, N, pass, ws.st);
     hipLaunchKernelGGL(select_scan_kernel, dim3(1), dim3(256), 0, s, pass, ws.st);
   }
-  hipLaunchKernelGGL(select_count_kernel, dim3(nchunks), dim3(kGT), 0, s, scores, N, ws.st, ws.cnt);
+  hipLaunchKernelGGL(select_count_kernel, dim3(nchunks), dim3(kGT), 0, s, scores, delta, N, ws.st, ws.cnt);
   hipLaunchKernelGGL(select_offsets_kernel, dim3(1), dim3(kThreads), 0, s, ws.cnt, nchunks, ws.st, ws.off);
-  hipLaunchKernelGGL(select_emit_kernel, dim3(nchunks), dim3(kGT), 0, s, scores, N, ws.st, ws.off, k, idx);
+  hipLaunchKernelGGL(select_emit_kernel, dim3(nchunks), dim3(kGT), 0, s, scores, delta, N, ws.st, ws.off, k, idx);
   return launch_status("select");
+}
+
+extern "C" int avits_select(const float* scores, int64_t N, int64_t k, int32_t* idx, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  return select_impl(scores, nullptr, N, k, idx, workspace, workspace_bytes, stream);
+}
+
+extern "C" int avits_select_perturbed(const float* scores, const float* delta, int64_t N, int64_t k, int32_t* idx,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
+  AVITS_REQUIRE(k == 0 || delta, "select_perturbed: null delta");
+  return select_impl(scores, delta, N, k, idx, workspace, workspace_bytes, stream);
+}
+
+extern "C" int avits_select_batched(const float* scores, const float* delta, int32_t B, const int64_t* offsets,
+                                    const int64_t* k, int32_t* idx, void* stream) {
+  AVITS_REQUIRE(B >= 1 && B <= kMaxBatch, "select_batched: B=%d outside [1, %d]", B, kMaxBatch);
+  AVITS_REQUIRE(offsets && k, "select_batched: null offsets/k");
+  SelBatch bt{};
+  int64_t out = 0;
+  AVITS_REQUIRE(offsets[0] == 0, "select_batched: offsets[0]=%lld must be 0", (long long)offsets[0]);
+  for (int b = 0; b < B; ++b) {
+    const int64_t n = offsets[b + 1] - offsets[b];
+    AVITS_REQUIRE(n >= 1 && n <= kOneBlockMax, "select_batched: element %d has N=%lld outside [1, %d]", b,
+                  (long long)n, kOneBlockMax);
+    AVITS_REQUIRE(k[b] >= 0 && k[b] <= n, "select_batched: element %d has k=%lld outside [0, N=%lld]", b,
+                  (long long)k[b], (long long)n);
+    bt.off[b] = offsets[b];
+    bt.k[b] = int32_t(k[b]);
+    bt.out[b] = out;
+    out += k[b];
+  }
+  bt.off[B] = offsets[B];
+  if (out == 0) return AVITS_OK;
+  AVITS_REQUIRE(scores && idx, "select_batched: null scores/idx");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  TimedLaunch timed("select", s);
+  hipLaunchKernelGGL(radix_select_batched_kernel, dim3(unsigned(B)), dim3(kThreads), 0, s, scores, delta, bt, idx);
+  return launch_status("select_batched");
 }

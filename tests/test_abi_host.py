@@ -69,6 +69,29 @@ def _score(lib, **kw):
                            a["alpha"], a["eps"], a["dtype"], a["S"], None, None, a["ws"], a["wsb"], None)
 
 
+def test_select_perturbed_and_batched_validation(lib):
+    import ctypes
+    f = lib.avits_select_perturbed
+    assert f(FAKE, None, 10, 3, FAKE, None, 0, None) == INVALID          # delta required
+    assert f(FAKE, FAKE, 10, 11, FAKE, None, 0, None) == INVALID         # k > N
+    assert f(FAKE, FAKE, 20000, 5, FAKE, None, 0, None) == WORKSPACE     # grid path needs workspace
+    assert f(None, None, 10, 0, None, None, 0, None) == 0                # k == 0: no-op
+    b = lib.avits_select_batched
+    I64 = ctypes.c_int64
+
+    def arr(*v):
+        return (I64 * len(v))(*v)
+
+    assert b(FAKE, None, 0, arr(0), arr(), FAKE, None) == INVALID                    # B < 1
+    assert b(FAKE, None, 65, arr(*range(66)), arr(*([1] * 65)), FAKE, None) == INVALID  # B > 64
+    assert b(FAKE, None, 2, arr(1, 5, 9), arr(1, 1), FAKE, None) == INVALID           # offsets[0] != 0
+    assert b(FAKE, None, 2, arr(0, 5, 5), arr(1, 0), FAKE, None) == INVALID           # empty element
+    assert b(FAKE, None, 2, arr(0, 5, 9), arr(6, 1), FAKE, None) == INVALID           # k > N_b
+    assert b(FAKE, None, 1, arr(0, 16385), arr(1), FAKE, None) == INVALID             # N_b > 16384
+    assert b(None, None, 2, arr(0, 5, 9), arr(0, 0), None, None) == 0                 # nothing to select
+    assert b(None, None, 2, arr(0, 5, 9), arr(1, 0), None, None) == INVALID           # null scores/idx
+
+
 def test_score_validation(lib):
     assert _score(lib, N=0) == INVALID
     assert _score(lib, L=0) == INVALID

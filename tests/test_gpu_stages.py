@@ -160,6 +160,42 @@ def test_select_grid_workspace(gpu):
     assert e.value.code == -3
 
 
+# The paper's tie-break perturbation (Section 3.3): keys are the fp32 sums
+# scores + delta; both paths (one workgroup, grid-wide).
+@pytest.mark.parametrize("n,k,levels", [(4096, 1229, 8), (777, 300, 2), (16384, 4915, 3), (70_000, 21_000, 4),
+                                        (1 << 20, 314573, 8)])
+def test_select_perturbed(gpu, n, k, levels):
+    s = G.quantised_scores(n, n, levels)
+    d = G.tiebreak_noise(n, n)
+    idx = torch.full((k,), -7, dtype=torch.int32, device="cuda")
+    gpu.avits_select_perturbed(dev(s), dev(d), k, idx)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(idx), oracle.select_topk_perturbed(s, d, k))
+
+
+@pytest.mark.parametrize("perturbed", [False, True], ids=["plain", "perturbed"])
+def test_select_batched(gpu, perturbed):
+    sizes = [4096, 1, 1000, 16384, 64, 4096, 257]
+    ks = [1229, 1, 0, 4915, 64, 0, 100]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    s = G.quantised_scores(11, int(off[-1]), 6)
+    d = G.tiebreak_noise(11, int(off[-1])) if perturbed else None
+    idx = torch.full((sum(ks) + 4,), -7, dtype=torch.int32, device="cuda")
+    gpu.avits_select_batched(dev(s), off.tolist(), ks, idx, delta=dev(d) if perturbed else None)
+    torch.cuda.synchronize()
+    raw = host(idx)
+    np.testing.assert_array_equal(raw[:sum(ks)], oracle.select_topk_batched(s, off, ks, delta=d))
+    assert np.all(raw[sum(ks):] == -7)
+    # Element by element, the batched result equals the single selection.
+    o = 0
+    for b in range(len(sizes)):
+        if ks[b]:
+            one, _ = _select(gpu, s[off[b]:off[b + 1]] if d is None else
+                             (s[off[b]:off[b + 1]] + d[off[b]:off[b + 1]]).astype(np.float32), ks[b])
+            np.testing.assert_array_equal(raw[o:o + ks[b]], one)
+        o += ks[b]
+
+
 def _gather(gpu, w, k, mode, alias, seed=0):
     lay = G.layout_inputs(w)
     idx = G.random_selection(w, k, seed)
