@@ -24,5 +24,5 @@ from .relayout import (  # noqa: F401
 )
 from .block import (  # noqa: F401
     layer_norm, rms_norm, rope_angles, apply_rope, attention, gelu_tanh,
-    double_block, single_block, block_qk,
+    double_block, single_block, block_qk, block_batched,
 )

@@ -219,3 +219,30 @@ def single_block(x, pos, w: dict, H: int, rows=None):
     cat = np.concatenate([o.reshape(-1, D), mlp], axis=1)
     y = cat @ _f64(w["w_out"]).T + _f64(w["b_out"])
     return x[rows] + mod[2] * y, lse
+
+
+def block_batched(x, pos, txt_off, img_off, H: int, w_txt: dict | None = None, w_img: dict | None = None,
+                  single: dict | None = None):
+    """B images through one block, rows packed by stream: the text rows of all
+    images first (image b's at txt_off[b]:txt_off[b+1]), then their image rows
+    (image b's at T + img_off[b]:img_off[b+1], T = txt_off[-1]).  Each image
+    is its own joint sequence [text_b; image_b] (Section 3.3.1 per image):
+    its rows attend only to its own rows.  Returns (out [S, D], lse [H, S])
+    in the packed row order."""
+    x = _f64(x)
+    pos = np.asarray(pos)
+    S, D = x.shape
+    T = int(txt_off[-1])
+    out = np.empty_like(x)
+    lse = np.empty((H, S))
+    for b in range(len(txt_off) - 1):
+        rows = np.concatenate([np.arange(txt_off[b], txt_off[b + 1]),
+                               T + np.arange(img_off[b], img_off[b + 1])]).astype(np.int64)
+        n_txt = int(txt_off[b + 1] - txt_off[b])
+        if single is not None:
+            o, l_ = single_block(x[rows], pos[rows], single, H)
+        else:
+            o, l_ = double_block(x[rows], pos[rows], n_txt, w_txt, w_img, H)
+        out[rows] = o
+        lse[:, rows] = l_
+    return out, lse

@@ -331,3 +331,80 @@ def test_block_qk_softmax_normaliser_is_the_blocks():
     q0, _ = oracle.block_qk(x, np.zeros_like(pos), 4, wt, wi, 2)
     g = np.stack([np.asarray(wt["g_q"], float)] * 4 + [np.asarray(wi["g_q"], float)] * 5)[:, None, :]
     np.testing.assert_allclose(np.sqrt(((q0 / g) ** 2).mean(-1)), np.ones((9, 2)), atol=1e-6)
+
+
+# ---------------------------------------------------------------------------
+# Several images through one block, rows packed by stream.
+
+def _brute_double_packed(x, pos, is_txt, seg, wt, wi, H):
+    """Scalar double block on the packed rows: stream weights by is_txt[i],
+    attention of row i restricted to the rows j with seg[j] == seg[i]."""
+    S, D = len(x), len(x[0])
+    d = D // H
+    Q, K, V = [], [], []
+    for i in range(S):
+        w = wt if is_txt[i] else wi
+        mod = w["mod"]
+        h = [a * (1 + s) + t for a, s, t in zip(_vec_ln(x[i]), mod[1], mod[0])]
+        qkv = _matvec(w["w_qkv"], w["b_qkv"], h)
+        Q.append([_rope_head(_rms(hq, w["g_q"]), pos[i], d) for hq in _heads(qkv[:D], H, d)])
+        K.append([_rope_head(_rms(hk, w["g_k"]), pos[i], d) for hk in _heads(qkv[D:2 * D], H, d)])
+        V.append(_heads(qkv[2 * D:], H, d))
+    O, LSE = [None] * S, [[0.0] * S for _ in range(H)]
+    for i in range(S):
+        js = [j for j in range(S) if seg[j] == seg[i]]
+        o, l_ = _attend([Q[i]], [K[j] for j in js], [V[j] for j in js], H, d)
+        O[i] = o[0]
+        for h in range(H):
+            LSE[h][i] = l_[h][0]
+    out = []
+    for i in range(S):
+        w = wt if is_txt[i] else wi
+        mod = w["mod"]
+        att = _matvec(w["w_o"], w["b_o"], O[i])
+        y = [a + g * b for a, g, b in zip(x[i], mod[2], att)]
+        h2 = [a * (1 + s) + t for a, s, t in zip(_vec_ln(y), mod[4], mod[3])]
+        m = [_gelu(a) for a in _matvec(w["w_mlp1"], w["b_mlp1"], h2)]
+        mlp = _matvec(w["w_mlp2"], w["b_mlp2"], m)
+        out.append([a + g * b for a, g, b in zip(y, mod[5], mlp)])
+    return np.array(out), np.array(LSE)
+
+
+def test_block_batched_matches_masked_bruteforce():
+    # Three images: (text, image) rows (2, 2), (0, 1), (1, 2); text rows first.
+    txt_off, img_off = [0, 2, 2, 3], [0, 2, 3, 5]
+    S = txt_off[-1] + img_off[-1]
+    x = generator.block_input(_TINY, S, 3)
+    pos = np.array([[0, 0, 0], [0, 0, 0], [0, 0, 0], [0, 1, 2], [0, 3, 3], [0, 2, 2], [1, 1, 0], [0, 0, 1]],
+                   dtype=np.int32)
+    is_txt = [True] * 3 + [False] * 5
+    seg = [0, 0, 2] + [0, 0, 1, 2, 2]
+    wt = generator.double_stream_weights(_TINY, 0, 0)
+    wi = generator.double_stream_weights(_TINY, 0, 1)
+    out, lse = oracle.block_batched(x, pos, txt_off, img_off, 2, wt, wi)
+    ref, ref_lse = _brute_double_packed(x.astype(float).tolist(), pos.tolist(), is_txt, seg, _lists(wt), _lists(wi), 2)
+    np.testing.assert_allclose(out, ref, atol=1e-11)
+    np.testing.assert_allclose(lse, ref_lse, atol=1e-11)
+    # One image reduces to the plain block; images do not see each other.
+    o1, l1 = oracle.block_batched(x[[0, 1, 3, 4]], pos[[0, 1, 3, 4]], [0, 2], [0, 2], 2, wt, wi)
+    p1, pl1 = oracle.double_block(x[[0, 1, 3, 4]], pos[[0, 1, 3, 4]], 2, wt, wi, 2)
+    np.testing.assert_array_equal(o1, p1)
+    np.testing.assert_array_equal(l1, pl1)
+    x2 = x.copy()
+    x2[[2, 6, 7]] += 1.0   # image 2's rows
+    out2, _ = oracle.block_batched(x2, pos, txt_off, img_off, 2, wt, wi)
+    np.testing.assert_array_equal(out2[[0, 1, 3, 4, 5]], out[[0, 1, 3, 4, 5]])
+
+
+def test_block_batched_single_kind():
+    txt_off, img_off = [0, 1, 3], [0, 2, 3]
+    S = 6
+    x = generator.block_input(_TINY, S, 4)
+    pos, _ = _tiny_inputs(S)[1], None
+    w = generator.single_block_weights(_TINY, 0)
+    out, lse = oracle.block_batched(x, pos, txt_off, img_off, 2, single=w)
+    # Image 1 = text row 1..2 and image row 5; image 0 = text row 0 and image rows 3, 4.
+    for rows in ([0, 3, 4], [1, 2, 5]):
+        ref, ref_lse = _brute_single(x[rows].astype(float).tolist(), pos[rows].tolist(), _lists(w), 2)
+        np.testing.assert_allclose(out[rows], ref, atol=1e-11)
+        np.testing.assert_allclose(lse[:, rows], ref_lse, atol=1e-11)
