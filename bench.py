@@ -271,6 +271,44 @@ def _mixed_stage2(avits, torch, w, text, bw, reps: int = 10) -> dict:
     }
 
 
+def _batched_block(avits, torch, w, bw, x, reps: int = 10) -> dict:
+    """Two images of the workload (a CFG pair: same weights, own text and own
+    selection) through one double block in one pass, rows packed by stream
+    and attention block-diagonal, against two single-image passes."""
+    L, I = w.L, w.R + w.k
+    S = 2 * (L + I)
+    xb = torch.cat([x[:L], x[:L], x[L:], x[L:]]).contiguous()
+    pos = torch.zeros(S, 3, dtype=torch.int32, device="cuda")
+    pos1 = torch.zeros(L + I, 3, dtype=torch.int32, device="cuda")
+    out = torch.empty_like(xb)
+    out1 = torch.empty_like(x)
+    ws = torch.empty(avits.avits_block_workspace_bytes(avits.BLOCK_DOUBLE, S, w.H, w.d, w.mlp_ratio * w.D,
+                                                       avits.BF16), dtype=torch.uint8, device="cuda")
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record()
+        for _ in range(reps):
+            fn()
+        e[1].record()
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / reps
+
+    t_b = timed(lambda: avits.avits_block_forward_batched(xb, out, pos, [0, L, 2 * L], [0, I, 2 * I], bw, w.H,
+                                                          workspace=ws))
+
+    def two():
+        for _ in range(2):
+            avits.avits_block_forward(x, out1, pos1, L, I, bw, w.H, workspace=ws)
+
+    t_2 = timed(two)
+    return {"images": 2, "rows": S, "batched_ms": round(t_b, 4), "two_single_ms": round(t_2, 4),
+            "speedup": round(t_2 / t_b, 3)}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -466,6 +504,7 @@ def main(argv=None):
     result["fused_scoring"] = _fused_scoring(avits, torch, w, q, k_all, kt, high, fp, lse)
     result["select_sweep"] = _select_sweep(avits, torch)
     result["mixed_stage2"] = _mixed_stage2(avits, torch, w, text, bw)
+    result["batched_block"] = _batched_block(avits, torch, w, bw, step.compact)
     if not args.no_cpu_baseline:
         host = dict(si)
         host.update(lay)

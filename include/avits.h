@@ -214,6 +214,25 @@ int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, float
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_block_forward_batched — B images through one block in one pass: the
+ * rows of all images are packed by stream, the text rows of images 0..B-1
+ * first (image b's at [txt_off[b], txt_off[b+1])), then their image rows
+ * (image b's at txt_off[B] + [img_off[b], img_off[b+1])).  Every row-wise
+ * stage runs over all rows at once; the joint attention is block diagonal:
+ * image b's rows attend to image b's rows only (Eq. joint_qk per image), so
+ * each image's output equals avits_block_forward on that image alone.
+ * txt_off, img_off [B + 1] host int64 arrays starting at 0; each image has
+ * at least one row; 1 <= B <= 16.  bf16 only (AVITS_ERR_UNSUPPORTED
+ * otherwise).  Workspace: avits_block_workspace_bytes(kind, S, H, d, F,
+ * dtype) with S = txt_off[B] + img_off[B].  lse_out [H, S] is per packed row.
+ * Other arguments and errors as avits_block_forward.
+ * ---------------------------------------------------------------------- */
+int avits_block_forward_batched(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,
+                                int32_t B, const int64_t* txt_off, const int64_t* img_off,
+                                const avits_block_weights* w, int32_t H, int32_t d, int dtype,
+                                float* lse_out, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_block_qk — the first stage of a block alone (the attention probe of
  * Section 3.3.1: the queries and keys whose joint softmax defines the
  * image-to-text attention mass of Eq. spatial): for each row,

@@ -29,17 +29,62 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// One workgroup's work: a head, its query rows [q_lo, q_hi) and up to two key
+// ranges [ks[r], ks[r] + kn[r]).
+struct AttnUnit {
+  int h;
+  int64_t q_lo, q_hi;
+  int64_t ks[2], kn[2];
+};
+
+// Number of row blocks of `rows` query rows per head.
+__host__ __device__ inline int64_t attn_row_blocks(const AttnArgs& a, int rows) {
+  if (a.segs.n == 0) return (a.Sq + rows - 1) / rows;
+  int64_t v = 0;
+  for (int b = 0; b < a.segs.n; ++b)
+    for (int r = 0; r < 2; ++r) v += (a.segs.len[b][r] + rows - 1) / rows;
+  return v;
+}
+
 // Work unit -> (head, row block) with the units of one XCD contiguous and
 // head-major, so the row blocks of a head share one L2 (workgroup b runs on
-// XCD b mod 8).
-__device__ __forceinline__ void attn_unit(int64_t n_rb, int H, int64_t& head, int64_t& rb) {
-  const int64_t U = n_rb * H;
-  const int64_t b = blockIdx.x, x = b % 8;
+// XCD b mod 8).  With sequences, the row blocks of a head enumerate each
+// sequence's two row ranges in turn, and the keys are that sequence's rows.
+__device__ __forceinline__ AttnUnit attn_unit(const AttnArgs& a, int rows) {
+  const int64_t n_rb = attn_row_blocks(a, rows);
+  const int64_t U = n_rb * a.H;
+  const int64_t bid = blockIdx.x, x = bid % 8;
   int64_t start = 0;
   for (int64_t y = 0; y < x; ++y) start += (U - y + 7) / 8;
-  const int64_t u = start + b / 8;
-  head = u / n_rb;
-  rb = u % n_rb;
+  const int64_t u = start + bid / 8;
+  AttnUnit w;
+  w.h = int(u / n_rb);
+  int64_t rb = u % n_rb;
+  if (a.segs.n == 0) {
+    w.q_lo = rb * rows;
+    w.q_hi = std::min<int64_t>(a.Sq, w.q_lo + rows);
+    w.ks[0] = 0; w.kn[0] = a.Sk;
+    w.ks[1] = 0; w.kn[1] = 0;
+    return w;
+  }
+  for (int b = 0; b < a.segs.n; ++b) {
+    for (int r = 0; r < 2; ++r) {
+      const int64_t nb = (a.segs.len[b][r] + rows - 1) / rows;
+      if (rb < nb) {
+        w.q_lo = a.segs.start[b][r] + rb * rows;
+        w.q_hi = std::min<int64_t>(a.segs.start[b][r] + a.segs.len[b][r], w.q_lo + rows);
+        for (int k = 0; k < 2; ++k) {
+          w.ks[k] = a.segs.start[b][k];
+          w.kn[k] = a.segs.len[b][k];
+        }
+        return w;
+      }
+      rb -= nb;
+    }
+  }
+  w.q_lo = w.q_hi = 0;  // not reached: the grid has exactly n_rb * H units
+  w.ks[0] = w.ks[1] = 0; w.kn[0] = w.kn[1] = 0;
+  return w;
 }
 
 // Lane l of a 32x32 MFMA output tile holds row 8*(r/4) + 4*(l/32) + r%4 of
@@ -67,19 +112,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][kKT * kKL];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][WITH_V ? DH * kVL : 8];
 
-  int64_t hh, rb;
-  attn_unit((a.Sq + 32 * NW - 1) / (32 * NW), a.H, hh, rb);
-  const int h = int(hh);
+  const AttnUnit un = attn_unit(a, 32 * NW);
+  const int h = un.h;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int l32 = lane % 32, hi = lane / 32;
-  const int64_t row = rb * (32 * NW) + wave * 32 + l32;
+  const int64_t row = un.q_lo + wave * 32 + l32;
   const bf16_t* Q = static_cast<const bf16_t*>(a.q);
   const bf16_t* K = static_cast<const bf16_t*>(a.k) + int64_t(h) * a.k_head;
   const bf16_t* VT = static_cast<const bf16_t*>(a.vt) + int64_t(h) * DH * a.ldvt;
 
   bf16x8 qf[kC];
   {
-    const bf16_t* src = Q + std::min<int64_t>(row, a.Sq - 1) * a.q_tok + h * a.q_head + 8 * hi;
+    const bf16_t* src = Q + std::min<int64_t>(row, un.q_hi - 1) * a.q_tok + h * a.q_head + 8 * hi;
 #pragma unroll
     for (int c = 0; c < kC; ++c) qf[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + 16 * c));
   }
@@ -113,9 +157,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   }
   // Register prefetch of the next tile.
   u32x4 kreg[kKP], vreg[WITH_V ? kVP : 1];
-  // Tile at key k0; `last` when it is the partial tile at the end.
-  auto load_tile = [&](int64_t k0, bool last) {
-    if (!last) {
+  // Tile of key rows k0 .. k0 + rem - 1 (rem < kKT: the partial tile at the
+  // end of a key range).
+  auto load_tile = [&](int64_t k0, int rem) {
+    if (rem == kKT) {
 #pragma unroll
       for (int j = 0; j < kKP; ++j) kreg[j] = *reinterpret_cast<const u32x4*>(k_src[j] + k0 * a.k_tok);
       if constexpr (WITH_V) {
@@ -125,7 +170,6 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
     } else {
       // Clamp key rows; zero V^T beyond the end so that 0-probability keys
       // contribute exactly 0.
-      const int rem = int(a.Sk - k0);
 #pragma unroll
       for (int j = 0; j < kKP; ++j) {
         const int kk = std::min(k_key[j], rem - 1);
@@ -155,17 +199,29 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   // Key (within the tile) of accumulator register r of sub-tile t, less 8 h.
   auto key_of = [](int t, int r) { return 32 * t + 16 * (r / 8) + 4 * ((r / 4) & 1) + (r % 4); };
 
-  const int64_t n_full = a.Sk / kKT;
-  const bool has_tail = a.Sk % kKT != 0;
-  const int64_t n_tiles = n_full + (has_tail ? 1 : 0);
+  // Key tiles: ceil(kn[0] / kKT) over the first range, then the second's.
+  const int64_t t0 = (un.kn[0] + kKT - 1) / kKT;
+  const int64_t n_tiles = t0 + (un.kn[1] + kKT - 1) / kKT;
+  auto tile_at = [&](int64_t it, int64_t& base, int& rem) {
+    const int r = it < t0 ? 0 : 1;
+    const int64_t local = (r == 0 ? it : it - t0) * kKT;
+    base = un.ks[r] + local;
+    rem = int(std::min<int64_t>(kKT, un.kn[r] - local));
+  };
   int buf = 0;
-  // Key tile `it`: prefetch tile it + 1 into registers, consume tile it from
-  // LDS, then stage tile it + 1 in the other LDS buffer.
-  auto tile = [&](int64_t it, auto tail_tag) {
+  // Key tile `it` (rows k0 .. k0 + rem - 1; its key index within a range
+  // starting at 0 is k0 - ks[0] for the text-mass test): prefetch tile it + 1
+  // into registers, consume tile it from LDS, stage tile it + 1 in the other
+  // LDS buffer.
+  auto tile = [&](int64_t it, int64_t k0, int rem, auto tail_tag) {
     constexpr bool kTail = decltype(tail_tag)::value;
-    const int64_t k0 = it * kKT;
     const bool more = it + 1 < n_tiles;
-    if (more) load_tile(k0 + kKT, it + 1 == n_full);
+    if (more) {
+      int64_t nb;
+      int nr;
+      tile_at(it + 1, nb, nr);
+      load_tile(nb, nr);
+    }
 
     f32x16 s[kKT / 32];
 #pragma unroll
@@ -181,7 +237,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
       s[t] = acc;
     }
     if constexpr (kTail) {
-      const int lim = int(a.Sk - k0) - 8 * hi;
+      const int lim = rem - 8 * hi;
 #pragma unroll
       for (int t = 0; t < kKT / 32; ++t)
 #pragma unroll
@@ -253,15 +309,25 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
     buf ^= 1;
   };
 
-  load_tile(0, n_full == 0);
+  {
+    int64_t b0;
+    int r0;
+    tile_at(0, b0, r0);
+    load_tile(b0, r0);
+  }
   store_tile(0);
   lds_barrier();
-  for (int64_t it = 0; it < n_full; ++it) tile(it, std::integral_constant<bool, false>());
-  if (has_tail) tile(n_full, std::integral_constant<bool, true>());
+  for (int64_t it = 0; it < n_tiles; ++it) {
+    int64_t k0;
+    int rem;
+    tile_at(it, k0, rem);
+    if (rem == kKT) tile(it, k0, rem, std::integral_constant<bool, false>());
+    else tile(it, k0, rem, std::integral_constant<bool, true>());
+  }
 
   float l = lrow + __shfl_xor(lrow, 32, kWave);
   const float tm = trow + __shfl_xor(trow, 32, kWave);
-  if (row >= a.Sq) return;
+  if (row >= un.q_hi) return;
   if (a.lse && hi == 0) a.lse[int64_t(h) * a.Sq + row] = (mrow + log2f(l)) * kLn2;
   if (MASS && hi == 0) {
     float* dst = a.mass + int64_t(h) * a.Sq + row;
@@ -354,7 +420,7 @@ template <int DH>
 void launch_dh(const AttnArgs& a, int dtype, hipStream_t s) {
   const bool with_v = a.vt != nullptr;
   if (dtype == AVITS_BF16) {
-    const dim3 grid(static_cast<unsigned>(ceil_div64(a.Sq, kRows) * a.H));
+    const dim3 grid(static_cast<unsigned>(attn_row_blocks(a, kRows) * a.H));
     if (with_v) hipLaunchKernelGGL((attn_bf16_kernel<DH, true, false>), grid, dim3(256), 0, s, a);
     else if (a.mass) hipLaunchKernelGGL((attn_bf16_kernel<DH, false, true>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((attn_bf16_kernel<DH, false, false>), grid, dim3(256), 0, s, a);
@@ -369,6 +435,8 @@ void launch_dh(const AttnArgs& a, int dtype, hipStream_t s) {
 
 int launch_attention(const AttnArgs& a, int dtype, hipStream_t s) {
   if (a.Sq == 0) return AVITS_OK;
+  if (a.segs.n > 0 && (dtype != AVITS_BF16 || a.mass))
+    return set_error(AVITS_ERR_UNSUPPORTED, "attention: packed sequences need bf16 and no text mass");
   TimedLaunch timed(a.vt ? "attention" : "joint_lse", s);
   if (a.d == 128) launch_dh<128>(a, dtype, s);
   else launch_dh<64>(a, dtype, s);

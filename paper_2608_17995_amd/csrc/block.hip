@@ -333,7 +333,7 @@ int run_block_qk(const void* x_in, const int32_t* pos, float pos_scale, int64_t 
 template <typename T>
 int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale, int64_t n_txt, int64_t n_img,
               const avits_block_weights* w, int H, int d, int dtype, float* lse_out, const BlockWs& ws,
-              hipStream_t s) {
+              hipStream_t s, const AttnSegs* segs = nullptr) {
   const int64_t S = n_txt + n_img, D = int64_t(H) * d, F = w->mlp_hidden;
   const bool dbl = w->kind == AVITS_BLOCK_DOUBLE;
   const T* x = static_cast<const T*>(x_in);
@@ -392,9 +392,10 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
   // 3. q/k RMSNorm + RoPE in place.
   if ((rc = launch_qk_norm_rope<T>(qk, qk + D, 2 * D, pos, pos_scale, S, n_txt, H, d, w, s)) != AVITS_OK) return rc;
 
-  // 4. joint attention over all S rows.
+  // 4. joint attention over all S rows (or within each packed sequence).
   {
     AttnArgs a{};
+    if (segs) a.segs = *segs;
     a.q = qk; a.q_tok = 2 * D; a.q_head = d;
     a.k = qk + D; a.k_tok = 2 * D; a.k_head = d;
     a.vt = vt; a.ldvt = ws.ldvt;
@@ -554,4 +555,41 @@ extern "C" int avits_block_forward(const void* x_in, void* x_out, const int32_t*
   if (dtype == AVITS_BF16)
     return run_block<bf16_t>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, lse_out, ws, s);
   return run_block<float>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, lse_out, ws, s);
+}
+
+extern "C" int avits_block_forward_batched(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,
+                                           int32_t B, const int64_t* txt_off, const int64_t* img_off,
+                                           const avits_block_weights* w, int32_t H, int32_t d, int dtype,
+                                           float* lse_out, void* workspace, size_t workspace_bytes,
+                                           void* stream) {
+  AVITS_REQUIRE(B >= 1 && B <= kMaxSeqs, "block_forward_batched: B=%d outside [1, %d]", B, kMaxSeqs);
+  AVITS_REQUIRE(txt_off && img_off, "block_forward_batched: null txt_off/img_off");
+  AVITS_REQUIRE(txt_off[0] == 0 && img_off[0] == 0, "block_forward_batched: offsets must start at 0");
+  AttnSegs segs{};
+  segs.n = B;
+  const int64_t n_txt = txt_off[B], n_img = img_off[B];
+  for (int b = 0; b < B; ++b) {
+    const int64_t lt = txt_off[b + 1] - txt_off[b], li = img_off[b + 1] - img_off[b];
+    AVITS_REQUIRE(lt >= 0 && li >= 0 && lt + li >= 1,
+                  "block_forward_batched: sequence %d has %lld text and %lld image rows", b, (long long)lt,
+                  (long long)li);
+    segs.start[b][0] = txt_off[b];
+    segs.len[b][0] = lt;
+    segs.start[b][1] = n_txt + img_off[b];
+    segs.len[b][1] = li;
+  }
+  int rc = check_block_args("block_forward_batched", x_in, pos, pos_scale, n_txt, n_img, w, H, d, dtype);
+  if (rc != AVITS_OK) return rc;
+  if (dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "block_forward_batched: packed sequences need bf16 (dtype %d)", dtype);
+  const int64_t S = n_txt + n_img;
+  AVITS_REQUIRE(x_out, "block_forward_batched: null x_out");
+  AVITS_REQUIRE(x_in != x_out, "block_forward_batched: x_out must not alias x_in");
+  const BlockWs need = block_ws_layout(nullptr, w->kind, S, H, d, w->mlp_hidden, 2);
+  if (!workspace || workspace_bytes < need.bytes)
+    return set_error(AVITS_ERR_WORKSPACE, "block_forward_batched: workspace of %zu bytes, need %zu",
+                     workspace_bytes, need.bytes);
+  const BlockWs ws = block_ws_layout(static_cast<char*>(workspace), w->kind, S, H, d, w->mlp_hidden, 2);
+  return run_block<bf16_t>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, lse_out, ws,
+                           static_cast<hipStream_t>(stream), &segs);
 }

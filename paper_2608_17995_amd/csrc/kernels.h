@@ -71,6 +71,16 @@ inline size_t gemm_partial_reserve(int64_t S, int64_t D) { return size_t(4) * si
 // the key tile (the padding keys are read but masked, whatever they hold);
 // o is [Sq, H*d] with row stride ldo.  Without v (vt == null) only the
 // log-sum-exp is produced.
+// Block-diagonal attention over packed sequences: sequence b is the union
+// of two row ranges (its text rows and its image rows when the rows are
+// packed by stream); its rows attend to its own rows only.
+constexpr int kMaxSeqs = 16;
+struct AttnSegs {
+  int n;                        // 0: one sequence, all rows (no segments)
+  int64_t start[kMaxSeqs][2];
+  int64_t len[kMaxSeqs][2];
+};
+
 struct AttnArgs {
   const void* q;
   int64_t q_tok, q_head;
@@ -86,6 +96,7 @@ struct AttnArgs {
   int mass_accumulate; // add to `mass` instead of overwriting it
   int64_t Sq, Sk;
   int H, d;
+  AttnSegs segs;       // n > 0: queries and keys per sequence (Sq == Sk == packed rows)
 };
 
 constexpr int kAttnKeyTile = 64;  // key padding unit expected for vt

@@ -179,6 +179,27 @@ def test_block_validation(lib):
     assert lib.avits_block_workspace_bytes(3, 10, 1, 64, 256, 1) == 0
 
 
+def test_block_batched_validation(lib):
+    import ctypes
+    f = lib.avits_block_forward_batched
+    w = _binding._BlockWeights()
+    w.kind = 0
+    w.mlp_hidden = 256
+    ws = 1 << 30
+    I64 = ctypes.c_int64
+
+    def arr(*v):
+        return (I64 * len(v))(*v)
+
+    args = lambda B, to, io, dt=1: f(FAKE, FAKE + 64, FAKE, 1.0, B, to, io, ctypes.byref(w), 1, 64, dt, None, FAKE, ws, None)
+    assert args(0, arr(0), arr(0)) == INVALID                      # B < 1
+    assert args(17, arr(*range(18)), arr(*range(18))) == INVALID   # B > 16
+    assert args(2, arr(1, 2, 3), arr(0, 1, 2)) == INVALID          # txt_off[0] != 0
+    assert args(2, arr(0, 1, 1), arr(0, 1, 1)) == INVALID          # empty image
+    assert args(2, arr(0, 2, 1), arr(0, 0, 3)) == INVALID          # decreasing offsets
+    assert args(1, arr(0, 2), arr(0, 3)) == INVALID                # missing weights
+
+
 def test_block_qk_validation(lib):
     import ctypes
     w = _binding._BlockWeights()

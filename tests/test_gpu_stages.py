@@ -330,6 +330,47 @@ def test_block_relayout_equivariance(gpu):
     assert rel_l2(out2 - x[perm], out[perm] - x[perm]) < 1e-2
 
 
+@pytest.mark.parametrize("kind", ["double", "single"])
+def test_block_batched(gpu, kind):
+    # Several images through one block: rows packed by stream (text rows of
+    # all images, then their image rows); attention within each image only.
+    w = C.TINY_BF16
+    txt = [32, 0, 7, 129]
+    img = [200, 77, 1, 64]
+    txt_off = np.concatenate([[0], np.cumsum(txt)]).astype(int).tolist()
+    img_off = np.concatenate([[0], np.cumsum(img)]).astype(int).tolist()
+    S = txt_off[-1] + img_off[-1]
+    x, pos = _block_inputs(w, txt_off[-1], img_off[-1], seed=21)
+    if kind == "double":
+        wt, wi = G.double_stream_weights(w, 0, 0), G.double_stream_weights(w, 0, 1)
+        bw = gpu.BlockWeights(gpu.BLOCK_DOUBLE, txt=double_weights_dev(wt, w.dtype), img=double_weights_dev(wi, w.dtype))
+        ref, ref_lse = oracle.block_batched(x, pos, txt_off, img_off, w.H, wt, wi)
+    else:
+        ws_ = G.single_block_weights(w, 0)
+        bw = gpu.BlockWeights(gpu.BLOCK_SINGLE, single=double_weights_dev(ws_, w.dtype))
+        ref, ref_lse = oracle.block_batched(x, pos, txt_off, img_off, w.H, single=ws_)
+    t_x = dev(x, w.dtype)
+    out = torch.empty_like(t_x)
+    lse = torch.empty(w.H, S, device="cuda")
+    gpu.avits_block_forward_batched(t_x, out, dev(pos), txt_off, img_off, bw, w.H, lse_out=lse)
+    torch.cuda.synchronize()
+    got = host(out)
+    T = txt_off[-1]
+    for b in range(len(txt)):
+        rows = np.concatenate([np.arange(txt_off[b], txt_off[b + 1]), T + np.arange(img_off[b], img_off[b + 1])])
+        assert_close(got[rows] - x[rows], ref[rows] - x[rows], w.dtype, f"image {b} block update")
+        assert_close(host(lse)[:, rows], ref_lse[:, rows], w.dtype, f"image {b} lse")
+    # Changing one image's rows leaves the others' outputs bit for bit.
+    x2 = x.copy()
+    r3 = np.concatenate([np.arange(txt_off[3], txt_off[4]), T + np.arange(img_off[3], img_off[4])])
+    x2[r3] = G.round_to(x2[r3] + 0.5, w.dtype)
+    out2 = torch.empty_like(t_x)
+    gpu.avits_block_forward_batched(dev(x2, w.dtype), out2, dev(pos), txt_off, img_off, bw, w.H)
+    torch.cuda.synchronize()
+    keep = np.setdiff1d(np.arange(S), r3)
+    np.testing.assert_array_equal(host(out2)[keep], got[keep])
+
+
 def _run_block_qk(gpu, w, x, pos, n_txt, bw):
     t_x = dev(x, w.dtype)
     q = torch.empty_like(t_x)
