@@ -41,8 +41,10 @@ struct AttnUnit {
 __host__ __device__ inline int64_t attn_row_blocks(const AttnArgs& a, int rows) {
   if (a.segs.n == 0) return (a.Sq + rows - 1) / rows;
   int64_t v = 0;
-  for (int b = 0; b < a.segs.n; ++b)
-    for (int r = 0; r < 2; ++r) v += (a.segs.len[b][r] + rows - 1) / rows;
+#pragma unroll
+  for (int b = 0; b < kMaxSeqs; ++b)  // static indices: no private copy of the arguments
+#pragma unroll
+    for (int r = 0; r < 2; ++r) v += b < a.segs.n ? (a.segs.len[b][r] + rows - 1) / rows : 0;
   return v;
 }
 
@@ -67,24 +69,30 @@ __device__ __forceinline__ AttnUnit attn_unit(const AttnArgs& a, int rows) {
     w.ks[1] = 0; w.kn[1] = 0;
     return w;
   }
-  for (int b = 0; b < a.segs.n; ++b) {
+  // Static indices throughout (a dynamically indexed argument array would be
+  // copied to private memory).
+  w.q_lo = w.q_hi = 0;
+  w.ks[0] = w.ks[1] = 0;
+  w.kn[0] = w.kn[1] = 0;
+  bool found = false;
+#pragma unroll
+  for (int b = 0; b < kMaxSeqs; ++b) {
+#pragma unroll
     for (int r = 0; r < 2; ++r) {
-      const int64_t nb = (a.segs.len[b][r] + rows - 1) / rows;
-      if (rb < nb) {
+      const int64_t nb = b < a.segs.n ? (a.segs.len[b][r] + rows - 1) / rows : 0;
+      if (!found && rb < nb) {
+        found = true;
         w.q_lo = a.segs.start[b][r] + rb * rows;
         w.q_hi = std::min<int64_t>(a.segs.start[b][r] + a.segs.len[b][r], w.q_lo + rows);
-        for (int k = 0; k < 2; ++k) {
-          w.ks[k] = a.segs.start[b][k];
-          w.kn[k] = a.segs.len[b][k];
-        }
-        return w;
+        w.ks[0] = a.segs.start[b][0];
+        w.kn[0] = a.segs.len[b][0];
+        w.ks[1] = a.segs.start[b][1];
+        w.kn[1] = a.segs.len[b][1];
       }
-      rb -= nb;
+      if (!found) rb -= nb;
     }
   }
-  w.q_lo = w.q_hi = 0;  // not reached: the grid has exactly n_rb * H units
-  w.ks[0] = w.ks[1] = 0; w.kn[0] = w.kn[1] = 0;
-  return w;
+  return w;  // every unit of the grid (n_rb * H of them) finds its range
 }
 
 // Lane l of a 32x32 MFMA output tile holds row 8*(r/4) + 4*(l/32) + r%4 of
@@ -203,10 +211,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   const int64_t t0 = (un.kn[0] + kKT - 1) / kKT;
   const int64_t n_tiles = t0 + (un.kn[1] + kKT - 1) / kKT;
   auto tile_at = [&](int64_t it, int64_t& base, int& rem) {
-    const int r = it < t0 ? 0 : 1;
-    const int64_t local = (r == 0 ? it : it - t0) * kKT;
-    base = un.ks[r] + local;
-    rem = int(std::min<int64_t>(kKT, un.kn[r] - local));
+    const bool first = it < t0;  // selects, not a dynamic index into un.ks / un.kn
+    const int64_t local = (first ? it : it - t0) * kKT;
+    base = (first ? un.ks[0] : un.ks[1]) + local;
+    rem = int(std::min<int64_t>(kKT, (first ? un.kn[0] : un.kn[1]) - local));
   };
   int buf = 0;
   // Key tile `it` (rows k0 .. k0 + rem - 1; its key index within a range
@@ -317,12 +325,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   }
   store_tile(0);
   lds_barrier();
-  for (int64_t it = 0; it < n_tiles; ++it) {
-    int64_t k0;
-    int rem;
-    tile_at(it, k0, rem);
-    if (rem == kKT) tile(it, k0, rem, std::integral_constant<bool, false>());
-    else tile(it, k0, rem, std::integral_constant<bool, true>());
+  // Per key range: its full tiles, then its partial tile through the tail
+  // instance of the body (so the hot loop holds the full-tile body only).
+  int64_t it = 0;
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    const int64_t n_full = un.kn[r] / kKT;
+    const int rem_last = int(un.kn[r] % kKT);
+    for (int64_t f = 0; f < n_full; ++f, ++it) tile(it, un.ks[r] + f * kKT, kKT, std::integral_constant<bool, false>());
+    if (rem_last) {
+      tile(it, un.ks[r] + n_full * kKT, rem_last, std::integral_constant<bool, true>());
+      ++it;
+    }
   }
 
   float l = lrow + __shfl_xor(lrow, 32, kWave);
