@@ -428,10 +428,21 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
       p.out0 = xmid + r0 * D; p.ld0 = D; p.resid = x + r0 * D; p.ldr = D;
       p.gate = mod_row(streams[i].dw->mod, 2);
     }
-    if ((rc = launch_gemm(g, dtype, s, "gemm_o", ws.partial, ws.partial_bytes)) != AVITS_OK) return rc;
+    // 6. the second modulated layer norm rides on the split-K reduce when
+    //    the projection is split (bf16), else runs on its own.
+    GemmPostLN ln{};
+    ln.out = h;
+    ln.ld = D;
+    for (int i = 0; i < nst; ++i) {
+      ln.shift[i] = mod_row(streams[i].dw->mod, 3);
+      ln.scale[i] = mod_row(streams[i].dw->mod, 4);
+    }
+    if ((rc = launch_gemm(g, dtype, s, "gemm_o", ws.partial, ws.partial_bytes,
+                          sizeof(T) == 2 ? &ln : nullptr)) != AVITS_OK)
+      return rc;
+    if (!(sizeof(T) == 2 && ln.done) && (rc = launch_ln_mod<T>(xmid, h, S, D, n_txt, w, 3, s)) != AVITS_OK)
+      return rc;
   }
-  // 6. second modulated layer norm.
-  if ((rc = launch_ln_mod<T>(xmid, h, S, D, n_txt, w, 3, s)) != AVITS_OK) return rc;
   // 7. MLP in + GELU.
   T* mlp = reinterpret_cast<T*>(ws.mlp);
   {

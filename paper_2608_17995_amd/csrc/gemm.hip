@@ -91,6 +91,99 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, const GemmProblem& 
   }
 }
 
+// Split-K reduce fused with the modulated layer norm that follows the
+// output projection: one wave per output row (N = D columns, 8 per chunk,
+// chunk c of lane l at columns 8 (l + 64 c)).  The row's partials are summed
+// in split order, the bias and gated residual applied as epilogue4 does, the
+// result rounded to bf16 and stored; the layer norm then reads those bf16
+// values with the chunk layout and summation order of ln_mod_kernel, so both
+// routes give the same bits.
+constexpr int kRlnChunks = 8;  // rows up to 64 * 8 * 8 = 4096 columns
+template <int SPLITS>
+__global__ __launch_bounds__(256) void splitk_reduce_ln_kernel(const GemmArgs a, const float* __restrict__ partial,
+                                                               const GemmPostLN post) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+  const int64_t grow = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave;
+  if (grow >= rows) return;
+  const bool second = grow >= a.p[0].M;
+  const int64_t m = second ? grow - a.p[0].M : grow;
+  const GemmProblem& p = second ? a.p[1] : a.p[0];
+  const int64_t nchunk = a.N / 8;
+  const bf16_t* bias = static_cast<const bf16_t*>(p.bias);
+  const bf16_t* gate = static_cast<const bf16_t*>(p.gate);
+  const bf16_t* res = static_cast<const bf16_t*>(p.resid) + m * p.ldr;
+  bf16_t* y = static_cast<bf16_t*>(p.out0) + m * p.ld0;
+  u32x4 yv[kRlnChunks];
+#pragma unroll
+  for (int c = 0; c < kRlnChunks; ++c) {
+    const int64_t idx = lane + kWave * c;
+    if (idx >= nchunk) continue;
+    const int64_t n = 8 * idx;
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < SPLITS; ++k) {
+      const float* src = partial + (int64_t(k) * rows + grow) * a.N + n;
+      const float4 x0 = *reinterpret_cast<const float4*>(src), x1 = *reinterpret_cast<const float4*>(src + 4);
+      const float t[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = k == 0 ? t[e] : v[e] + t[e];
+    }
+    const u32x4 rw = *reinterpret_cast<const u32x4*>(res + n);
+    const u32x4 gw = *reinterpret_cast<const u32x4*>(gate + n);
+    const u32x4 bw = bias ? *reinterpret_cast<const u32x4*>(bias + n) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = __uint_as_float(rw[e] << 16) +
+                       __uint_as_float(gw[e] << 16) * (v[2 * e] + __uint_as_float(bw[e] << 16));
+      const float hi = __uint_as_float(rw[e] & 0xffff0000u) +
+                       __uint_as_float(gw[e] & 0xffff0000u) * (v[2 * e + 1] + __uint_as_float(bw[e] & 0xffff0000u));
+      yv[c][e] = pack_bf2(lo, hi);
+    }
+    *reinterpret_cast<u32x4*>(y + n) = yv[c];
+  }
+  // Modulated layer norm of the bf16 row.
+  const bf16_t* sc = static_cast<const bf16_t*>(post.scale[second ? 1 : 0]);
+  const bf16_t* sh = static_cast<const bf16_t*>(post.shift[second ? 1 : 0]);
+  bf16_t* hr = static_cast<bf16_t*>(post.out) + grow * post.ld;
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < kRlnChunks; ++c) {
+    if (lane + kWave * c >= nchunk) continue;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s += __uint_as_float(yv[c][e] << 16) + __uint_as_float(yv[c][e] & 0xffff0000u);
+  }
+  const float mean = wave_sum(s) / float(a.N);
+  float q = 0.f;
+#pragma unroll
+  for (int c = 0; c < kRlnChunks; ++c) {
+    if (lane + kWave * c >= nchunk) continue;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x0 = __uint_as_float(yv[c][e] << 16) - mean, x1 = __uint_as_float(yv[c][e] & 0xffff0000u) - mean;
+      q = fmaf(x0, x0, fmaf(x1, x1, q));
+    }
+  }
+  const float rstd = rsqrtf(wave_sum(q) / float(a.N) + 1e-6f);
+#pragma unroll
+  for (int c = 0; c < kRlnChunks; ++c) {
+    const int64_t idx = lane + kWave * c;
+    if (idx >= nchunk) continue;
+    const u32x4 g = reinterpret_cast<const u32x4*>(sc)[idx], t = reinterpret_cast<const u32x4*>(sh)[idx];
+    u32x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = (__uint_as_float(yv[c][e] << 16) - mean) * rstd * (1.f + __uint_as_float(g[e] << 16)) +
+                       __uint_as_float(t[e] << 16);
+      const float hi = (__uint_as_float(yv[c][e] & 0xffff0000u) - mean) * rstd *
+                           (1.f + __uint_as_float(g[e] & 0xffff0000u)) +
+                       __uint_as_float(t[e] & 0xffff0000u);
+      o[e] = pack_bf2(lo, hi);
+    }
+    reinterpret_cast<u32x4*>(hr)[idx] = o;
+  }
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs (each with its own
 // L2).  Renumber them so that XCD x runs a contiguous range of logical ids:
 // neighbouring logical tiles share weight / activation tiles in one L2.
@@ -729,7 +822,7 @@ size_t gemm_partial_bytes(const GemmArgs& a, const GemmPlan& pl) {
 }
 
 int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family, float* partial,
-                size_t partial_bytes) {
+                size_t partial_bytes, GemmPostLN* post_ln) {
   GemmPlan pl = plan_gemm(a, dtype, partial ? partial_bytes : 0, family);
   if (pl.tiles == 0) return AVITS_OK;
   if (pl.splits > 1 && (!partial || partial_bytes < gemm_partial_bytes(a, pl))) pl.splits = 1;
@@ -744,9 +837,19 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
       default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
     }
     }
-    if (pl.splits > 1) {
+    if (post_ln) post_ln->done = false;
+    const int64_t rows_all = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+    if (pl.splits > 1 && post_ln && a.mode0 == EPI_RESID_GATE && a.n_split >= a.N && a.N % 8 == 0 &&
+        a.N <= int64_t(kWave) * 8 * kRlnChunks) {
       TimedLaunch timed_reduce("splitk_reduce", s);
-      const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+      const dim3 rgrid(unsigned(ceil_div64(rows_all, 4)));
+      if (pl.splits == 2) hipLaunchKernelGGL(splitk_reduce_ln_kernel<2>, rgrid, dim3(256), 0, s, a, partial, *post_ln);
+      else if (pl.splits == 3) hipLaunchKernelGGL(splitk_reduce_ln_kernel<3>, rgrid, dim3(256), 0, s, a, partial, *post_ln);
+      else hipLaunchKernelGGL(splitk_reduce_ln_kernel<4>, rgrid, dim3(256), 0, s, a, partial, *post_ln);
+      post_ln->done = true;
+    } else if (pl.splits > 1) {
+      TimedLaunch timed_reduce("splitk_reduce", s);
+      const int64_t rows = rows_all;
       const int64_t work = rows * (a.N / 4);
       hipLaunchKernelGGL(splitk_reduce_kernel, dim3(unsigned(ceil_div64(work, 256))), dim3(256), 0, s, a,
                          (const float*)partial, pl.splits);

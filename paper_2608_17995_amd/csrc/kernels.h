@@ -58,8 +58,21 @@ size_t gemm_partial_bytes(const GemmArgs& a, const GemmPlan& pl);
 // `partial` is scratch for split-K partial sums; when it is null or smaller
 // than the plan needs, the GEMM runs unsplit.
 // `family` names the timing family of the launch (see avits_timing_read).
+// Optional modulated layer norm of the GEMM's output rows, fused into the
+// split-K reduce when the GEMM is split: out = LN(y) * (1 + scale[p]) +
+// shift[p] for the rows of problem p, y the bf16 result rows (layer norm
+// without affine, eps 1e-6, biased variance, as the block's other LN).
+// `done` reports whether it ran; when not, the caller normalises itself.
+struct GemmPostLN {
+  void* out;
+  int64_t ld;
+  const void* shift[2];
+  const void* scale[2];
+  bool done;
+};
+
 int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family, float* partial = nullptr,
-                size_t partial_bytes = 0);
+                size_t partial_bytes = 0, GemmPostLN* post_ln = nullptr);
 
 // Bytes of split-K scratch the block reserves: up to 4 splits of an [S, D] fp32 output.
 inline size_t gemm_partial_reserve(int64_t S, int64_t D) { return size_t(4) * size_t(S) * size_t(D) * sizeof(float); }
