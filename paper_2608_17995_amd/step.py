@@ -313,3 +313,87 @@ class MixedStage2:
         B.avits_scatter_mixed(self.x, self.idx if self.K else None, self.H_lr, self.W_lr, self.LR,
                               canvas_hr if self.K else None, state_lr if self.K < self.Mp else None, stream)
         return canvas_hr, state_lr
+
+
+class BatchedStep:
+    """One selective-upsampling step for B images at once (a CFG pair, or
+    several prompts): each image has its own scores, budget k_b, text rows
+    and canvas; one selection launch covers all images, and one block pass
+    runs every image's compacted sequence, rows packed by stream (the text
+    rows of all images, then their [reference; selected] rows) with
+    block-diagonal attention.
+
+      score    per image: S_b from its own q, text keys, LSE and features
+      select   avits_select_batched over the B score vectors (k_b each)
+      gather   per image: its text rows into the text area (avits_scatter of
+               the rows), [ref_b; X_prev,b[idx_b]] into its image area
+               (avits_gather_upsample), its canvas filled by upsampling
+      block    avits_block_forward_batched over the packed rows
+      scatter  per image: canvas_b[idx_b] = its selected output rows
+
+    Buffers are allocated once; run() enqueues library calls only.
+    """
+
+    def __init__(self, shape: StepShape, ks: list, weights: B.BlockWeights, prefix_pos, dtype, device="cuda",
+                 alpha=0.5, eps=1e-8, mode=B.UP_NEAREST):
+        import torch
+        s = shape
+        self.shape, self.ks, self.weights, self.alpha, self.eps, self.mode = s, list(ks), weights, alpha, eps, mode
+        Bn = len(self.ks)
+        if not 1 <= Bn <= 16 or any(not 0 <= k <= s.N for k in self.ks):
+            raise ValueError("1 <= B <= 16 images with 0 <= k_b <= N")
+        i32, f32 = torch.int32, torch.float32
+        self.txt_off = [s.L * b for b in range(Bn + 1)]
+        self.img_off = [0]
+        for k in self.ks:
+            self.img_off.append(self.img_off[-1] + s.R + k)
+        T = self.txt_off[-1]
+        self.S_tot = T + self.img_off[-1]
+        self.scores = torch.empty(Bn * s.N, dtype=f32, device=device)
+        self.idx = torch.empty(max(sum(self.ks), 1), dtype=i32, device=device)
+        self.out_off = [sum(self.ks[:b]) for b in range(Bn + 1)]
+        self.x = torch.empty(self.S_tot, s.D, dtype=dtype, device=device)
+        self.x_out = torch.empty(self.S_tot, s.D, dtype=dtype, device=device)
+        self.pos = torch.zeros(self.S_tot, 3, dtype=i32, device=device)
+        prefix_pos = torch.as_tensor(prefix_pos, dtype=i32).to(device)
+        for b in range(Bn):
+            self.pos[self.txt_off[b]:self.txt_off[b + 1]].copy_(prefix_pos[:s.L])
+            a0 = T + self.img_off[b]
+            self.pos[a0:a0 + s.R].copy_(prefix_pos[s.L:s.L + s.R])
+        # Row indices of each image's text area in the packed rows (for the text-row copy).
+        self.txt_rows = [torch.arange(self.txt_off[b], self.txt_off[b + 1], dtype=i32, device=device)
+                         for b in range(Bn)]
+        d = s.D // s.H
+        code = B.BF16 if dtype == torch.bfloat16 else B.F32
+        self.ws_score = torch.empty(max(B.avits_score_workspace_bytes(s.N, s.H), 1), dtype=torch.uint8, device=device)
+        self.ws_block = torch.empty(
+            max(B.avits_block_workspace_bytes(weights.kind, self.S_tot, s.H, d, s.mlp_hidden, code), 1),
+            dtype=torch.uint8, device=device)
+
+    def run(self, latent_q, text_k, row_lse, feat_t, feat_prev, lowres, highres_prev, text, ref, stream=None):
+        """Lists over the images: latent_q[b], text_k[b], row_lse[b], feat_t[b],
+        feat_prev[b], lowres[b], highres_prev[b] (its canvas, updated in place),
+        text[b] [L, D], ref[b] [R, D] or None."""
+        s = self.shape
+        T = self.txt_off[-1]
+        Bn = len(self.ks)
+        for b in range(Bn):
+            B.avits_score(latent_q[b], text_k[b], row_lse[b], feat_t[b], feat_prev[b], self.alpha, self.eps,
+                          self.scores[b * s.N:(b + 1) * s.N], workspace=self.ws_score, stream=stream)
+        if sum(self.ks):
+            B.avits_select_batched(self.scores, [b * s.N for b in range(Bn + 1)], self.ks, self.idx, stream=stream)
+        for b in range(Bn):
+            if s.L:
+                B.avits_scatter(text[b], self.txt_rows[b], 0, self.x, stream)
+            a0 = T + self.img_off[b]
+            idx_b = self.idx[self.out_off[b]:self.out_off[b + 1]]
+            B.avits_gather_upsample(lowres[b], highres_prev[b], ref[b] if s.R else None, idx_b, s.H_lr, s.W_lr,
+                                    self.x[a0:a0 + s.R + self.ks[b]], self.pos[a0 + s.R:a0 + s.R + self.ks[b]],
+                                    highres_prev[b], self.mode, stream)
+        B.avits_block_forward_batched(self.x, self.x_out, self.pos, self.txt_off, self.img_off, self.weights, s.H,
+                                      workspace=self.ws_block, stream=stream)
+        for b in range(Bn):
+            if self.ks[b]:
+                idx_b = self.idx[self.out_off[b]:self.out_off[b + 1]]
+                B.avits_scatter(self.x_out, idx_b, T + self.img_off[b] + s.R, highres_prev[b], stream)
+        return highres_prev
