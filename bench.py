@@ -447,6 +447,8 @@ def main(argv=None):
     gemm_per_launch_flops = fl["gemm"] * args.steps / gemm_n
     gemm_avg_s = gemm_tot_ms / gemm_n / 1e3
     gemm_tflops = gemm_per_launch_flops / gemm_avg_s / 1e12
+    red_ms, _ = avits.avits_timing_read("splitk_reduce")
+    gemm_red_tflops = fl["gemm"] * args.steps / ((gemm_tot_ms + red_ms) / 1e3) / 1e12
     traffic = measured_traffic()
     attn_ms, attn_n = avits.avits_timing_read("attention")
     attn_tflops = fl["attention"] / (attn_ms / attn_n / 1e3) / 1e12   # one launch per step
@@ -483,6 +485,9 @@ def main(argv=None):
             "algorithmic_bytes_per_launch": int(gemm_bytes * args.steps / gemm_n),
             "flops_per_launch": int(gemm_per_launch_flops),
             "avg_launch_us": round(gemm_avg_s * 1e6, 2),
+            # The projections with their split-K / split-tail reduce kernels
+            # (one of which also does the second modulated layer norm).
+            "achieved_with_reduces": round(gemm_red_tflops, 1),
         },
         "stages_ms": {s: round(v, 4) for s, v in stage_ms.items()},
         "launch_families": fam,

@@ -20,7 +20,12 @@
 //  - Small-N GEMMs (the N = D projections) are split along K when the tile
 //    grid would leave most of the 256 CUs idle: each split writes fp32
 //    partials and a reduce kernel sums them in split order (deterministic)
-//    and applies the epilogue.
+//    and applies the epilogue.  When the 256-wide tiles overrun the last
+//    full wave of workgroups by a few (the MLP-in projection of the FLUX
+//    block: 336 tiles on 256 CUs), only those last tiles are split (the
+//    split tail): they run after the whole tiles, in 2-4 k splits, and a
+//    small reduce sums their partials, so the partial wave takes a fraction
+//    of a tile's time instead of a whole one.
 // fp32 path: 64x64 tiles on the VALU (the exactness path).
 #include <stdio.h>
 #include <stdlib.h>
@@ -194,30 +199,62 @@ __device__ __forceinline__ int64_t xcd_logical_id(int64_t bid, int64_t grid) {
   return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
 }
 
-// Logical id -> (problem, tile origin, k split).  Tiles of one problem come
-// first; within a problem, consecutive ids walk down the rows of one column
-// block so neighbouring workgroups share the weight tile; the k splits of a
-// tile are adjacent.
-__device__ __forceinline__ bool map_tile(const GemmArgs& a, int bm, int bn, int splits, int& prob, int64_t& m0,
-                                         int64_t& n0, int& ks) {
+// Logical tile -> (problem, tile origin).  Tiles of one problem come first;
+// within a problem, consecutive tiles walk down the rows of one column block
+// so neighbouring workgroups share the weight tile.
+__device__ __forceinline__ bool decode_tile(const GemmArgs& a, int bm, int bn, int64_t tile, int& prob, int64_t& m0,
+                                            int64_t& n0) {
   const int64_t tn = (a.N + bn - 1) / bn;
-  int64_t bid = xcd_logical_id(blockIdx.x, gridDim.x);
-  ks = int(bid % splits);
-  bid /= splits;
   const int64_t tm0 = (a.p[0].M + bm - 1) / bm;
   const int64_t t0 = tm0 * tn;
   prob = 0;
   int64_t tm = tm0;
-  if (bid >= t0) {
-    bid -= t0;
+  if (tile >= t0) {
+    tile -= t0;
     prob = 1;
     if (a.nprob < 2) return false;
     tm = (a.p[1].M + bm - 1) / bm;
   }
   if (tm == 0) return false;
-  m0 = (bid % tm) * bm;
-  n0 = (bid / tm) * bn;
+  m0 = (tile % tm) * bm;
+  n0 = (tile / tm) * bn;
   return m0 < a.p[prob].M && n0 < a.N;
+}
+
+__device__ __forceinline__ int64_t tiles_total(const GemmArgs& a, int bm, int bn) {
+  const int64_t tn = (a.N + bn - 1) / bn;
+  return ((a.p[0].M + bm - 1) / bm + (a.nprob > 1 ? (a.p[1].M + bm - 1) / bm : 0)) * tn;
+}
+
+// Workgroup -> (problem, tile origin, k split): the k splits of a tile are
+// adjacent logical ids.
+__device__ __forceinline__ bool map_tile(const GemmArgs& a, int bm, int bn, int splits, int& prob, int64_t& m0,
+                                         int64_t& n0, int& ks) {
+  const int64_t bid = xcd_logical_id(blockIdx.x, gridDim.x);
+  ks = int(bid % splits);
+  return decode_tile(a, bm, bn, bid / splits, prob, m0, n0);
+}
+
+// Split tail.  When the tiles overrun the last full wave of workgroups on the
+// chip by a few, the first F = tiles - tail tiles run whole (workgroups
+// 0 .. F - 1) and the last `tail` tiles run in `tsp` k splits each
+// (workgroups F onwards, dispatched after the whole tiles): the partial wave
+// takes 1 / tsp of a tile's time instead of a whole one.  The two classes are
+// renumbered for the XCDs separately.  tidx is the tile's index in the tail
+// (-1 for a whole tile).
+__device__ __forceinline__ bool map_tile_tail(const GemmArgs& a, int bm, int bn, int64_t tail, int tsp, int& prob,
+                                              int64_t& m0, int64_t& n0, int& ks, int64_t& tidx) {
+  const int64_t F = tiles_total(a, bm, bn) - tail;
+  const int64_t bid = blockIdx.x;
+  if (bid < F) {
+    ks = 0;
+    tidx = -1;
+    return decode_tile(a, bm, bn, xcd_logical_id(bid, F), prob, m0, n0);
+  }
+  const int64_t u = xcd_logical_id(bid - F, int64_t(gridDim.x) - F);
+  tidx = u / tsp;
+  ks = int(u % tsp);
+  return decode_tile(a, bm, bn, F + tidx, prob, m0, n0);
 }
 
 // Epilogue through LDS, wave by wave.  The MFMA layout gives each lane four
@@ -236,8 +273,8 @@ __device__ __forceinline__ bool map_tile(const GemmArgs& a, int bm, int bn, int 
 // partials take the row-major path without the epilogue.  The caller passes
 // the main loop's LDS once every wave is done with it.
 template <int WM, int WN, int TM, int TN>
-__device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const GemmProblem& p, int prob, int64_t m0,
-                                                int64_t n0, int ks, int splits, float* __restrict__ partial,
+__device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const GemmProblem& p, int64_t m0, int64_t n0,
+                                                bool part, float* __restrict__ pbase, int64_t pld,
                                                 const f32x16 (&acc)[TM][TN], float* sm, int wave, int wm, int wn,
                                                 int lane) {
   constexpr int P = WN + 4;                  // LDS row pitch (floats)
@@ -262,7 +299,7 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const GemmPro
   else if (n < a.n_split2) { out = static_cast<bf16_t*>(p.out1); col = n - a.n_split; ldo = p.ld1; }
   else { out = static_cast<bf16_t*>(p.out2); col = n - a.n_split2; ldo = p.ld2; }
   float bias[4] = {0.f, 0.f, 0.f, 0.f}, gate[4] = {0.f, 0.f, 0.f, 0.f};
-  if (lane_ok && splits == 1) {
+  if (lane_ok && !part) {
     if (p.bias) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) bias[r] = ld(static_cast<const bf16_t*>(p.bias), n + r);
@@ -272,10 +309,8 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const GemmPro
       for (int r = 0; r < 4; ++r) gate[r] = ld(static_cast<const bf16_t*>(p.gate), n + r);
     }
   }
-  const bool row_major = lane_ok && (splits > 1 || mode != EPI_STORE_T);
-  const bool has_t = splits == 1 && (a.mode0 == EPI_STORE_T || a.mode1 == EPI_STORE_T || a.mode2 == EPI_STORE_T);
-  const int64_t rows_all = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
-  const int64_t grow0 = prob == 0 ? 0 : a.p[0].M;
+  const bool row_major = lane_ok && (part || mode != EPI_STORE_T);
+  const bool has_t = !part && (a.mode0 == EPI_STORE_T || a.mode1 == EPI_STORE_T || a.mode2 == EPI_STORE_T);
 
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
@@ -296,11 +331,11 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const GemmPro
         const int rr = r0 + kRPI * it;
         u[it] = *reinterpret_cast<const float4*>(reg + rr * P + swz_col(rr, 4 * c4));
       }
-      if (splits > 1) {
+      if (part) {
 #pragma unroll
         for (int it = 0; it < kIt; ++it) {
           const int64_t m = mb + r0 + kRPI * it;
-          if (m < p.M) *reinterpret_cast<float4*>(partial + (int64_t(ks) * rows_all + grow0 + m) * a.N + n) = u[it];
+          if (m < p.M) *reinterpret_cast<float4*>(pbase + (m - m0) * pld + (n - n0)) = u[it];
         }
       } else {
         float res[kIt][4];
@@ -532,7 +567,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(const
   }
 
   // The last barrier of the main loop has passed: LDS is free.
-  staged_epilogue<WM, WN, TM, TN>(a, p, prob, m0, n0, ks, splits, partial, acc,
+  const int64_t rows_all = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+  float* pbase = splits > 1 ? partial + (int64_t(ks) * rows_all + (prob ? a.p[0].M : 0) + m0) * a.N + n0 : nullptr;
+  staged_epilogue<WM, WN, TM, TN>(a, p, m0, n0, splits > 1, pbase, a.N, acc,
                                   reinterpret_cast<float*>(&lds[0][0]), wave, wm, wn, lane);
 }
 
@@ -551,15 +588,17 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(const
 // Tile t lives in LDS buffer t mod 2: it is read in phases 2t and 2t + 1 and
 // written in phases 2t - 2 and 2t - 1, after tile t - 2 left that buffer.
 __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(const GemmArgs a, float* __restrict__ partial,
-                                                          int splits) {
+                                                          int splits, int64_t tail, int tsp) {
   constexpr int BN = 256, WM = 128, WN = 64;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int HALF = 4;                    // 16-byte chunks per thread per half-tile operand
   __shared__ u32x4 lds[2][(kBM + BN) * 8];
 
   int prob, ks;
-  int64_t m0, n0;
-  if (!map_tile(a, kBM, BN, splits, prob, m0, n0, ks)) return;
+  int64_t m0, n0, tidx = -1;
+  if (tail > 0 ? !map_tile_tail(a, kBM, BN, tail, tsp, prob, m0, n0, ks, tidx)
+               : !map_tile(a, kBM, BN, splits, prob, m0, n0, ks))
+    return;
   const GemmProblem p = prob ? a.p[1] : a.p[0];  // by value: a select, no indexed copy of the arguments
   const bf16_t* A = static_cast<const bf16_t*>(p.A);
   const bf16_t* W = static_cast<const bf16_t*>(p.W);
@@ -568,8 +607,9 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(const GemmArgs a, flo
   const int grp = __builtin_amdgcn_readfirstlane(wave / 4);
   const int wm = grp, wn = wave % 4;
 
+  const int nsp = tidx >= 0 ? tsp : splits;
   const int64_t nk = a.K / kBK;
-  const int64_t kt0 = nk * ks / splits, kt1 = nk * (ks + 1) / splits;
+  const int64_t kt0 = nk * ks / nsp, kt1 = nk * (ks + 1) / nsp;
   const int64_t n_t = kt1 - kt0;
 
   // Staging of this group's half: A rows and W rows [128 grp, 128 grp + 128),
@@ -679,8 +719,43 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(const GemmArgs a, flo
     }
   }
 
-  staged_epilogue<WM, WN, TM, TN>(a, p, prob, m0, n0, ks, splits, partial, acc,
+  // Split partials: a tail tile's go to its own 256 x 256 block (split-major),
+  // a fully split launch's to rows of the [split][row][N] array.
+  float* pbase = nullptr;
+  int64_t pld = a.N;
+  if (tidx >= 0) {
+    pbase = partial + (tidx * tsp + ks) * int64_t(kBM * BN);
+    pld = BN;
+  } else if (splits > 1) {
+    const int64_t rows_all = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
+    pbase = partial + (int64_t(ks) * rows_all + (prob ? a.p[0].M : 0) + m0) * a.N + n0;
+  }
+  staged_epilogue<WM, WN, TM, TN>(a, p, m0, n0, pbase != nullptr, pbase, pld, acc,
                                   reinterpret_cast<float*>(&lds[0][0]), wave, wm, wn, lane);
+}
+
+// Sum the k splits of each tail tile in split order and apply the epilogue.
+// Block b covers rows 4 (b mod 64) .. + 3 of tail tile b / 64, one thread per
+// four columns.
+__global__ __launch_bounds__(256) void tail_reduce_kernel(const GemmArgs a, const float* __restrict__ partial,
+                                                          int64_t tail, int tsp) {
+  constexpr int BN = 256;
+  const int64_t t = blockIdx.x / (kBM / 4);
+  const int r = int(blockIdx.x % (kBM / 4)) * 4 + int(threadIdx.x) / 64;
+  const int c = (int(threadIdx.x) % 64) * 4;
+  int prob;
+  int64_t m0, n0;
+  if (!decode_tile(a, kBM, BN, tiles_total(a, kBM, BN) - tail + t, prob, m0, n0)) return;
+  const GemmProblem p = prob ? a.p[1] : a.p[0];
+  const int64_t m = m0 + r, n = n0 + c;
+  if (m >= p.M || n >= a.N) return;
+  const float* src = partial + t * tsp * int64_t(kBM * BN) + r * BN + c;
+  float4 s = *reinterpret_cast<const float4*>(src);
+  for (int k = 1; k < tsp; ++k) {
+    const float4 u = *reinterpret_cast<const float4*>(src + int64_t(k) * kBM * BN);
+    s.x += u.x; s.y += u.y; s.z += u.z; s.w += u.w;
+  }
+  epilogue4<bf16_t>(a, p, m, n, s.x, s.y, s.z, s.w);
 }
 
 // Sum the split-K partials in split order and apply the epilogue.
@@ -782,6 +857,26 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
         pl.bn = cands[c];
         pl.tiles = t;
         pl.splits = sp;
+        pl.tail = 0;
+        pl.tail_splits = 1;
+      }
+    }
+    // The 256-wide tile may instead split only the tiles that overrun the
+    // last full wave (the tail): the partial wave then takes 1 / tsp of a
+    // tile's time.
+    const int64_t full = t / kCUs, rem = t % kCUs;
+    if (cands[c] != 256 || full == 0 || rem == 0) continue;
+    for (int tsp = 2; tsp <= 4; ++tsp) {
+      if (rem * tsp > kCUs || nk / tsp < 4 || size_t(rem * tsp) * kBM * 256 * sizeof(float) > partial_bytes) break;
+      const double fill = double(t) / double(kCUs) / (double(full) + 1.0 / tsp);
+      const double score = fill * eff[c] * 0.95;
+      if (score > best + 1e-9) {
+        best = score;
+        pl.bn = 256;
+        pl.tiles = t;
+        pl.splits = 1;
+        pl.tail = rem;
+        pl.tail_splits = tsp;
       }
     }
   }
@@ -810,12 +905,15 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
       pl.waves = wv;
       pl.stages = bn == 128 ? stg : 1;  // the wider tiles have one register stage only
       pl.tiles = tiles_of(a, kBM, bn);
+      pl.tail = 0;
+      pl.tail_splits = 1;
     }
   }
   return pl;
 }
 
 size_t gemm_partial_bytes(const GemmArgs& a, const GemmPlan& pl) {
+  if (pl.tail > 0) return size_t(pl.tail) * size_t(pl.tail_splits) * kBM * size_t(pl.bn) * sizeof(float);
   if (pl.splits <= 1) return 0;
   const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
   return size_t(pl.splits) * size_t(rows) * size_t(a.N) * sizeof(float);
@@ -825,19 +923,30 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
                 size_t partial_bytes, GemmPostLN* post_ln) {
   GemmPlan pl = plan_gemm(a, dtype, partial ? partial_bytes : 0, family);
   if (pl.tiles == 0) return AVITS_OK;
-  if (pl.splits > 1 && (!partial || partial_bytes < gemm_partial_bytes(a, pl))) pl.splits = 1;
+  if ((pl.splits > 1 || pl.tail > 0) && (!partial || partial_bytes < gemm_partial_bytes(a, pl))) {
+    pl.splits = 1;
+    pl.tail = 0;
+  }
   if (dtype == AVITS_BF16) {
-    const dim3 grid(unsigned(pl.tiles * pl.splits));
+    const dim3 grid(unsigned(pl.tiles * pl.splits + pl.tail * (pl.tail_splits - 1)));
     {
     TimedLaunch timed(family, s);  // the GEMM kernel alone; the reduce is its own family
     switch (pl.bn * 100 + pl.waves * 10 + pl.stages) {
-      case 25681: hipLaunchKernelGGL(gemm_bf16_pp_kernel, grid, dim3(512), 0, s, a, partial, pl.splits); break;
+      case 25681:
+        hipLaunchKernelGGL(gemm_bf16_pp_kernel, grid, dim3(512), 0, s, a, partial, pl.splits, pl.tail,
+                           pl.tail_splits);
+        break;
       case 19281: hipLaunchKernelGGL((gemm_bf16_kernel<192, 4, 2, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       case 12881: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 1>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
       default: hipLaunchKernelGGL((gemm_bf16_kernel<128, 2, 4, 2>), grid, dim3(512), 0, s, a, partial, pl.splits); break;
     }
     }
     if (post_ln) post_ln->done = false;
+    if (pl.tail > 0) {
+      TimedLaunch timed_reduce("splitk_reduce", s);
+      hipLaunchKernelGGL(tail_reduce_kernel, dim3(unsigned(pl.tail * (kBM / 4))), dim3(256), 0, s, a,
+                         (const float*)partial, pl.tail, pl.tail_splits);
+    }
     const int64_t rows_all = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
     if (pl.splits > 1 && post_ln && a.mode0 == EPI_RESID_GATE && a.n_split >= a.N && a.N % 8 == 0 &&
         a.N <= int64_t(kWave) * 8 * kRlnChunks) {

@@ -52,6 +52,8 @@ struct GemmPlan {
   int waves = 8;       // waves per workgroup
   int stages = 2;      // register staging depth of the k-tile pipeline (1 or 2)
   int64_t tiles = 0;   // output tiles
+  int64_t tail = 0;    // last tiles run in tail_splits k splits (256-wide tile, splits == 1)
+  int tail_splits = 1;
 };
 GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const char* family = nullptr);
 size_t gemm_partial_bytes(const GemmArgs& a, const GemmPlan& pl);
