@@ -96,6 +96,54 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, const GemmProblem& 
   }
 }
 
+// Eight consecutive columns of one row (bf16 output): 16-byte loads of the
+// bias, gate and residual and one 16-byte store when the eight columns share
+// one output region with a row-major mode and aligned strides; otherwise two
+// epilogue4 calls.  Same arithmetic, in the same order, as epilogue4.
+__device__ __forceinline__ void epilogue8(const GemmArgs& a, const GemmProblem& p, int64_t m, int64_t n,
+                                          const float (&v)[8]) {
+  const bool r0 = n < a.n_split, r1 = n < a.n_split2;
+  int mode;
+  bf16_t* out;
+  int64_t col, ldo;
+  if (r0) { mode = a.mode0; out = static_cast<bf16_t*>(p.out0); col = n; ldo = p.ld0; }
+  else if (r1) { mode = a.mode1; out = static_cast<bf16_t*>(p.out1); col = n - a.n_split; ldo = p.ld1; }
+  else { mode = a.mode2; out = static_cast<bf16_t*>(p.out2); col = n - a.n_split2; ldo = p.ld2; }
+  const bool same = r0 == (n + 7 < a.n_split) && r1 == (n + 7 < a.n_split2);
+  const bool aligned = ((col | ldo) & 7) == 0 && (mode != EPI_RESID_GATE || (p.ldr & 7) == 0);
+  if (!same || !aligned || mode == EPI_STORE_T) {
+    epilogue4<bf16_t>(a, p, m, n, v[0], v[1], v[2], v[3]);
+    epilogue4<bf16_t>(a, p, m, n + 4, v[4], v[5], v[6], v[7]);
+    return;
+  }
+  float x[8];
+  if (p.bias) {
+    const u32x4 b = *reinterpret_cast<const u32x4*>(static_cast<const bf16_t*>(p.bias) + n);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = v[2 * e] + __uint_as_float(b[e] << 16);
+      x[2 * e + 1] = v[2 * e + 1] + __uint_as_float(b[e] & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = v[e];
+  }
+  if (mode == EPI_GELU) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = gelu_fast(x[e]);
+  } else if (mode == EPI_RESID_GATE) {
+    const u32x4 r = *reinterpret_cast<const u32x4*>(static_cast<const bf16_t*>(p.resid) + m * p.ldr + col);
+    const u32x4 g = *reinterpret_cast<const u32x4*>(static_cast<const bf16_t*>(p.gate) + n);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(r[e] << 16) + __uint_as_float(g[e] << 16) * x[2 * e];
+      x[2 * e + 1] = __uint_as_float(r[e] & 0xffff0000u) + __uint_as_float(g[e] & 0xffff0000u) * x[2 * e + 1];
+    }
+  }
+  const u32x4 w = {pack_bf2(x[0], x[1]), pack_bf2(x[2], x[3]), pack_bf2(x[4], x[5]), pack_bf2(x[6], x[7])};
+  *reinterpret_cast<u32x4*>(out + m * ldo + col) = w;
+}
+
 // Split-K reduce fused with the modulated layer norm that follows the
 // output projection: one wave per output row (N = D columns, 8 per chunk,
 // chunk c of lane l at columns 8 (l + 64 c)).  The row's partials are summed
@@ -659,12 +707,16 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(const GemmArgs a, flo
   auto compute = [&](int buf) {
     const u32x4* L = lds[buf];
     bf16x8 af[2][TM], wf[2][TN];
+    // Fragments are read in the order the next k step's MFMAs (i-major)
+    // consume them, so the first MFMAs wait on the oldest reads.
     auto read = [&](int kk, int slot) {
       const int chunk = 2 * kk + hi;
+      wf[slot][0] = as_bf16x8(L[kBM * 8 + swz(wn * WN + l32, chunk)]);
+      af[slot][0] = as_bf16x8(L[swz(wm * WM + l32, chunk)]);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) af[slot][i] = as_bf16x8(L[swz(wm * WM + 32 * i + l32, chunk)]);
+      for (int j = 1; j < TN; ++j) wf[slot][j] = as_bf16x8(L[kBM * 8 + swz(wn * WN + 32 * j + l32, chunk)]);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) wf[slot][j] = as_bf16x8(L[kBM * 8 + swz(wn * WN + 32 * j + l32, chunk)]);
+      for (int i = 1; i < TM; ++i) af[slot][i] = as_bf16x8(L[swz(wm * WM + 32 * i + l32, chunk)]);
     };
     read(0, 0);
     __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);
@@ -735,14 +787,14 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(const GemmArgs a, flo
 }
 
 // Sum the k splits of each tail tile in split order and apply the epilogue.
-// Block b covers rows 4 (b mod 64) .. + 3 of tail tile b / 64, one thread per
-// four columns.
+// Block b covers rows 8 (b mod 32) .. + 7 of tail tile b / 32, one thread per
+// eight columns.
 __global__ __launch_bounds__(256) void tail_reduce_kernel(const GemmArgs a, const float* __restrict__ partial,
                                                           int64_t tail, int tsp) {
   constexpr int BN = 256;
-  const int64_t t = blockIdx.x / (kBM / 4);
-  const int r = int(blockIdx.x % (kBM / 4)) * 4 + int(threadIdx.x) / 64;
-  const int c = (int(threadIdx.x) % 64) * 4;
+  const int64_t t = blockIdx.x / (kBM / 8);
+  const int r = int(blockIdx.x % (kBM / 8)) * 8 + int(threadIdx.x) / 32;
+  const int c = (int(threadIdx.x) % 32) * 8;
   int prob;
   int64_t m0, n0;
   if (!decode_tile(a, kBM, BN, tiles_total(a, kBM, BN) - tail + t, prob, m0, n0)) return;
@@ -750,30 +802,42 @@ __global__ __launch_bounds__(256) void tail_reduce_kernel(const GemmArgs a, cons
   const int64_t m = m0 + r, n = n0 + c;
   if (m >= p.M || n >= a.N) return;
   const float* src = partial + t * tsp * int64_t(kBM * BN) + r * BN + c;
-  float4 s = *reinterpret_cast<const float4*>(src);
-  for (int k = 1; k < tsp; ++k) {
-    const float4 u = *reinterpret_cast<const float4*>(src + int64_t(k) * kBM * BN);
-    s.x += u.x; s.y += u.y; s.z += u.z; s.w += u.w;
+  float v[8];
+  {
+    const float4 x0 = *reinterpret_cast<const float4*>(src), x1 = *reinterpret_cast<const float4*>(src + 4);
+    v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w; v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
   }
-  epilogue4<bf16_t>(a, p, m, n, s.x, s.y, s.z, s.w);
+  for (int k = 1; k < tsp; ++k) {
+    const float* q = src + int64_t(k) * kBM * BN;
+    const float4 x0 = *reinterpret_cast<const float4*>(q), x1 = *reinterpret_cast<const float4*>(q + 4);
+    v[0] += x0.x; v[1] += x0.y; v[2] += x0.z; v[3] += x0.w; v[4] += x1.x; v[5] += x1.y; v[6] += x1.z; v[7] += x1.w;
+  }
+  epilogue8(a, p, m, n, v);
 }
 
-// Sum the split-K partials in split order and apply the epilogue.
+// Sum the split-K partials in split order and apply the epilogue: one thread
+// per eight columns of a row.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmArgs a, const float* __restrict__ partial,
                                                             int splits) {
   const int64_t rows = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
-  const int64_t groups = a.N / 4;
+  const int64_t groups = a.N / 8;
   const int64_t g = int64_t(blockIdx.x) * 256 + threadIdx.x;
   if (g >= rows * groups) return;
-  const int64_t grow = g / groups, n = (g % groups) * 4;
-  float4 s = *reinterpret_cast<const float4*>(partial + grow * a.N + n);
-  for (int k = 1; k < splits; ++k) {
-    const float4 t = *reinterpret_cast<const float4*>(partial + (int64_t(k) * rows + grow) * a.N + n);
-    s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
+  const int64_t grow = g / groups, n = (g % groups) * 8;
+  const float* src = partial + grow * a.N + n;
+  float v[8];
+  {
+    const float4 x0 = *reinterpret_cast<const float4*>(src), x1 = *reinterpret_cast<const float4*>(src + 4);
+    v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w; v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
   }
-  const int prob = grow < a.p[0].M ? 0 : 1;
-  const int64_t m = prob == 0 ? grow : grow - a.p[0].M;
-  epilogue4<bf16_t>(a, a.p[prob], m, n, s.x, s.y, s.z, s.w);
+  for (int k = 1; k < splits; ++k) {
+    const float* q = src + int64_t(k) * rows * a.N;
+    const float4 x0 = *reinterpret_cast<const float4*>(q), x1 = *reinterpret_cast<const float4*>(q + 4);
+    v[0] += x0.x; v[1] += x0.y; v[2] += x0.z; v[3] += x0.w; v[4] += x1.x; v[5] += x1.y; v[6] += x1.z; v[7] += x1.w;
+  }
+  const bool second = grow >= a.p[0].M;
+  const GemmProblem p = second ? a.p[1] : a.p[0];
+  epilogue8(a, p, second ? grow - a.p[0].M : grow, n, v);
 }
 
 // fp32 VALU GEMM: 64x64 tile, 16x16 threads, 4x4 outputs per thread.
@@ -923,7 +987,8 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
                 size_t partial_bytes, GemmPostLN* post_ln) {
   GemmPlan pl = plan_gemm(a, dtype, partial ? partial_bytes : 0, family);
   if (pl.tiles == 0) return AVITS_OK;
-  if ((pl.splits > 1 || pl.tail > 0) && (!partial || partial_bytes < gemm_partial_bytes(a, pl))) {
+  // The reduce kernels take eight columns per thread.
+  if ((pl.splits > 1 || pl.tail > 0) && (!partial || partial_bytes < gemm_partial_bytes(a, pl) || a.N % 8 != 0)) {
     pl.splits = 1;
     pl.tail = 0;
   }
@@ -944,7 +1009,7 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
     if (post_ln) post_ln->done = false;
     if (pl.tail > 0) {
       TimedLaunch timed_reduce("splitk_reduce", s);
-      hipLaunchKernelGGL(tail_reduce_kernel, dim3(unsigned(pl.tail * (kBM / 4))), dim3(256), 0, s, a,
+      hipLaunchKernelGGL(tail_reduce_kernel, dim3(unsigned(pl.tail * (kBM / 8))), dim3(256), 0, s, a,
                          (const float*)partial, pl.tail, pl.tail_splits);
     }
     const int64_t rows_all = a.p[0].M + (a.nprob > 1 ? a.p[1].M : 0);
@@ -959,7 +1024,7 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
     } else if (pl.splits > 1) {
       TimedLaunch timed_reduce("splitk_reduce", s);
       const int64_t rows = rows_all;
-      const int64_t work = rows * (a.N / 4);
+      const int64_t work = rows * (a.N / 8);
       hipLaunchKernelGGL(splitk_reduce_kernel, dim3(unsigned(ceil_div64(work, 256))), dim3(256), 0, s, a,
                          (const float*)partial, pl.splits);
     }
