@@ -13,7 +13,16 @@
 // the B operand of the second (the contraction over keys uses the same key
 // permutation on both operands).  Softmax runs in the log2 domain with fp32
 // statistics.
+// Load balance: 128-row units of one head each take one of the two workgroup
+// slots of a CU, so a grid that overruns the first slot of every CU by a few
+// units leaves most CUs with one unit and some with two.  The launcher then
+// splits the overrun units (or, for small grids, every unit) along the keys:
+// each piece writes its unnormalised output and (max, sum) per row, and a
+// combine kernel merges the pieces in key order.
 // fp32: one thread per query row on the VALU (exactness path).
+#include <stdio.h>
+#include <stdlib.h>
+
 #include <type_traits>
 
 #include "kernels.h"
@@ -48,17 +57,39 @@ __host__ __device__ inline int64_t attn_row_blocks(const AttnArgs& a, int rows) 
   return v;
 }
 
+// Workgroup b of a class of n runs on XCD b mod 8: renumber so that each
+// XCD takes a contiguous range of the class's logical ids.
+__device__ __forceinline__ int64_t attn_xcd_id(int64_t b, int64_t n) {
+  const int64_t x = b % 8;
+  int64_t start = 0;
+  for (int64_t y = 0; y < x; ++y) start += (n - y + 7) / 8;
+  return start + b / 8;
+}
+
 // Work unit -> (head, row block) with the units of one XCD contiguous and
-// head-major, so the row blocks of a head share one L2 (workgroup b runs on
-// XCD b mod 8).  With sequences, the row blocks of a head enumerate each
-// sequence's two row ranges in turn, and the keys are that sequence's rows.
-__device__ __forceinline__ AttnUnit attn_unit(const AttnArgs& a, int rows) {
+// head-major, so the row blocks of a head share one L2.  With sequences, the
+// row blocks of a head enumerate each sequence's two row ranges in turn, and
+// the keys are that sequence's rows.  Split tail (one sequence only): units
+// below split_from take workgroups 0 .. split_from - 1; each later unit runs
+// in ksp pieces (workgroups split_from onwards, dispatched after the whole
+// units), piece p over key tiles [T p / ksp, T (p + 1) / ksp) of the unit's
+// T key tiles; `piece` is the piece's slot in the partial buffer (-1 for a
+// whole unit).
+__device__ __forceinline__ AttnUnit attn_unit(const AttnArgs& a, int rows, int64_t& piece) {
   const int64_t n_rb = attn_row_blocks(a, rows);
   const int64_t U = n_rb * a.H;
-  const int64_t bid = blockIdx.x, x = bid % 8;
-  int64_t start = 0;
-  for (int64_t y = 0; y < x; ++y) start += (U - y + 7) / 8;
-  const int64_t u = start + bid / 8;
+  const int64_t bid = blockIdx.x;
+  int64_t u;
+  int p = 0;
+  piece = -1;
+  if (bid < a.split_from) {
+    u = attn_xcd_id(bid, std::min<int64_t>(a.split_from, U));
+  } else {
+    const int64_t v = attn_xcd_id(bid - a.split_from, int64_t(gridDim.x) - a.split_from);
+    u = a.split_from + v / a.ksp;
+    p = int(v % a.ksp);
+    piece = v;
+  }
   AttnUnit w;
   w.h = int(u / n_rb);
   int64_t rb = u % n_rb;
@@ -67,6 +98,12 @@ __device__ __forceinline__ AttnUnit attn_unit(const AttnArgs& a, int rows) {
     w.q_hi = std::min<int64_t>(a.Sq, w.q_lo + rows);
     w.ks[0] = 0; w.kn[0] = a.Sk;
     w.ks[1] = 0; w.kn[1] = 0;
+    if (piece >= 0) {
+      const int64_t T = (a.Sk + 63) / 64;
+      const int64_t t_lo = T * p / a.ksp, t_hi = T * (p + 1) / a.ksp;
+      w.ks[0] = 64 * t_lo;
+      w.kn[0] = std::min<int64_t>(a.Sk, 64 * t_hi) - 64 * t_lo;
+    }
     return w;
   }
   // Static indices throughout (a dynamically indexed argument array would be
@@ -120,7 +157,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][kKT * kKL];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][WITH_V ? DH * kVL : 8];
 
-  const AttnUnit un = attn_unit(a, 32 * NW);
+  int64_t piece;
+  const AttnUnit un = attn_unit(a, 32 * NW, piece);
   const int h = un.h;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int l32 = lane % 32, hi = lane / 32;
@@ -342,6 +380,26 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   float l = lrow + __shfl_xor(lrow, 32, kWave);
   const float tm = trow + __shfl_xor(trow, 32, kWave);
   if (row >= un.q_hi) return;
+  if constexpr (WITH_V && !MASS) {
+    if (piece >= 0) {
+      // A key piece: its unnormalised output and (max, sum) per row, in the
+      // output's column order, for the combine kernel.
+      const int64_t lr = row - un.q_lo;
+      float* po = a.part + (piece * kRows + lr) * DH + 4 * hi;
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x16& o = oacc[dt];
+          *reinterpret_cast<float4*>(po + 32 * dt + 8 * q) = make_float4(o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]);
+        }
+      if (hi == 0) {
+        float* pm = a.part_ml + (piece * kRows + lr) * 2;
+        *reinterpret_cast<float2*>(pm) = make_float2(mrow, l);
+      }
+      return;
+    }
+  }
   if (a.lse && hi == 0) a.lse[int64_t(h) * a.Sq + row] = (mrow + log2f(l)) * kLn2;
   if (MASS && hi == 0) {
     float* dst = a.mass + int64_t(h) * a.Sq + row;
@@ -430,14 +488,136 @@ __global__ __launch_bounds__(kFRows) void attn_f32_kernel(const AttnArgs a) {
   }
 }
 
+// Combine the key pieces of each split unit: 16 lanes per query row, eight
+// output columns per lane (DH = 128; four for DH = 64), every piece's loads
+// issued together.  With m_p, l_p the piece's running max (log2 domain) and
+// sum, and O_p its unnormalised output, the row's output is
+// sum_p 2^(m_p - m) O_p / sum_p 2^(m_p - m) l_p with m = max_p m_p, and its
+// log-sum-exp (m + log2 of the denominator) ln 2: the single-pass result up
+// to rounding.  Pieces are summed in key order.
+constexpr int kMaxPieces = 4;
 template <int DH>
-void launch_dh(const AttnArgs& a, int dtype, hipStream_t s) {
+__global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a) {
+  constexpr int kLPR = 16, kCols = DH / kLPR;  // lanes per row, columns per lane
+  const int sub = threadIdx.x % kLPR;
+  const int64_t n_rb = attn_row_blocks(a, kRows);
+  const int64_t n_split = n_rb * a.H - a.split_from;
+  const int64_t g = int64_t(blockIdx.x) * (256 / kLPR) + threadIdx.x / kLPR;  // split unit * kRows + row
+  if (g >= n_split * kRows) return;
+  const int64_t su = g / kRows, lr = g % kRows;
+  const int64_t u = a.split_from + su;
+  const int h = int(u / n_rb);
+  const int64_t row = (u % n_rb) * kRows + lr;
+  if (row >= a.Sq) return;
+  float2 ml[kMaxPieces];
+  float o[kMaxPieces][kCols];
+#pragma unroll
+  for (int p = 0; p < kMaxPieces; ++p) {
+    if (p < a.ksp) {
+      const int64_t pc = (su * a.ksp + p) * kRows + lr;
+      ml[p] = *reinterpret_cast<const float2*>(a.part_ml + pc * 2);
+      const float* po = a.part + pc * DH + sub * kCols;
+#pragma unroll
+      for (int e = 0; e < kCols; e += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(po + e);
+        o[p][e] = v.x; o[p][e + 1] = v.y; o[p][e + 2] = v.z; o[p][e + 3] = v.w;
+      }
+    }
+  }
+  float m = -INFINITY;
+#pragma unroll
+  for (int p = 0; p < kMaxPieces; ++p)
+    if (p < a.ksp) m = fmaxf(m, ml[p].x);
+  float den = 0.f, acc[kCols];
+#pragma unroll
+  for (int e = 0; e < kCols; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int p = 0; p < kMaxPieces; ++p) {
+    if (p < a.ksp) {
+      const float wgt = __builtin_amdgcn_exp2f(ml[p].x - m);
+      den = fmaf(wgt, ml[p].y, den);
+#pragma unroll
+      for (int e = 0; e < kCols; ++e) acc[e] = fmaf(wgt, o[p][e], acc[e]);
+    }
+  }
+  const float inv = 1.f / den;
+  bf16_t* dst = static_cast<bf16_t*>(a.o) + row * a.ldo + int64_t(h) * DH + sub * kCols;
+  if constexpr (kCols == 8) {
+    *reinterpret_cast<u32x4*>(dst) = u32x4{pack_bf2(acc[0] * inv, acc[1] * inv), pack_bf2(acc[2] * inv, acc[3] * inv),
+                                           pack_bf2(acc[4] * inv, acc[5] * inv), pack_bf2(acc[6] * inv, acc[7] * inv)};
+  } else {
+    *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf2(acc[0] * inv, acc[1] * inv), pack_bf2(acc[2] * inv, acc[3] * inv)};
+  }
+  if (a.lse && sub == 0) a.lse[int64_t(h) * a.Sq + row] = (m + log2f(den)) * kLn2;
+}
+
+// Split-tail plan for the bf16 kernel with V over one sequence: whole units
+// fill the first workgroup slot of every CU, and the units beyond it run in
+// key pieces (or, with fewer units than CUs, every unit is split so that
+// the CUs are busy).  Returns ksp (1: no split) and sets split_from and the
+// partial pointers.
+constexpr int kAttnCUs = 256;
+int plan_attn_split(AttnArgs& a, int DH) {
+  a.split_from = INT64_MAX;
+  a.ksp = 1;
+  a.part_ml = nullptr;
+  if (!a.part || !a.vt || a.mass || a.segs.n > 0) return 1;
+  const int64_t U = attn_row_blocks(a, kRows) * a.H;
+  const int64_t T = (a.Sk + 63) / 64;
+  int64_t from, ksp;
+  // Measured on MI355X at S = 1741 (28 key tiles): with at most 128 units,
+  // pieces one per CU are fastest; up to 256 units, two per CU; beyond, the
+  // overflow units in two pieces each (the partial wave then costs half a
+  // unit; finer pieces lose more to the combine than they gain).
+  if (2 * U <= kAttnCUs) {
+    from = 0;
+    ksp = std::min<int64_t>(kMaxPieces, kAttnCUs / U);
+  } else if (U <= kAttnCUs) {
+    from = 0;
+    ksp = std::min<int64_t>(kMaxPieces, 2 * kAttnCUs / U);
+  } else if (U < 2 * kAttnCUs) {
+    from = kAttnCUs;
+    ksp = 2;
+  } else {
+    return 1;
+  }
+  // Tuning override "FROM,KSP" (e.g. AVITS_ATTN_SPLIT=256,3; KSP 1 disables).
+  if (const char* env = getenv("AVITS_ATTN_SPLIT")) {
+    long long f = 0, k = 0;
+    if (sscanf(env, "%lld,%lld", &f, &k) == 2 && f >= 0 && f <= U && k >= 1 && k <= kMaxPieces) {
+      from = f;
+      ksp = k;
+    }
+  }
+  ksp = std::min<int64_t>(ksp, T);  // at least one key tile per piece
+  auto need = [&](int64_t k) { return size_t((U - from) * k) * kRows * (DH + 2) * sizeof(float); };
+  while (ksp >= 2 && need(ksp) > a.part_bytes) --ksp;
+  if (ksp < 2) return 1;
+  const int64_t pieces = (U - from) * ksp;
+  a.split_from = from;
+  a.ksp = int(ksp);
+  a.part_ml = a.part + pieces * kRows * DH;
+  return int(ksp);
+}
+
+template <int DH>
+void launch_dh(AttnArgs a, int dtype, hipStream_t s) {
   const bool with_v = a.vt != nullptr;
   if (dtype == AVITS_BF16) {
-    const dim3 grid(static_cast<unsigned>(attn_row_blocks(a, kRows) * a.H));
-    if (with_v) hipLaunchKernelGGL((attn_bf16_kernel<DH, true, false>), grid, dim3(256), 0, s, a);
-    else if (a.mass) hipLaunchKernelGGL((attn_bf16_kernel<DH, false, true>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<DH, false, false>), grid, dim3(256), 0, s, a);
+    const int64_t U = attn_row_blocks(a, kRows) * a.H;
+    const int ksp = plan_attn_split(a, DH);
+    const dim3 grid(static_cast<unsigned>(ksp > 1 ? a.split_from + (U - a.split_from) * ksp : U));
+    if (with_v) {
+      hipLaunchKernelGGL((attn_bf16_kernel<DH, true, false>), grid, dim3(256), 0, s, a);
+      if (ksp > 1) {
+        const int64_t rows = (U - a.split_from) * kRows;
+        hipLaunchKernelGGL((attn_combine_kernel<DH>), dim3(unsigned(ceil_div64(rows, 16))), dim3(256), 0, s, a);
+      }
+    } else if (a.mass) {
+      hipLaunchKernelGGL((attn_bf16_kernel<DH, false, true>), grid, dim3(256), 0, s, a);
+    } else {
+      hipLaunchKernelGGL((attn_bf16_kernel<DH, false, false>), grid, dim3(256), 0, s, a);
+    }
   } else {
     const dim3 grid(unsigned(ceil_div64(a.Sq, kFRows)), unsigned(a.H));
     if (with_v) hipLaunchKernelGGL((attn_f32_kernel<DH, true>), grid, dim3(kFRows), 0, s, a);

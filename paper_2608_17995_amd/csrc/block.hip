@@ -402,6 +402,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
     a.o = ws.o; a.ldo = dbl ? D : D + F;
     a.lse = lse_out;
     a.Sq = S; a.Sk = S; a.H = H; a.d = d;
+    a.part = ws.partial; a.part_bytes = ws.partial_bytes;  // no GEMM partials are live here
     if ((rc = launch_attention(a, dtype, s)) != AVITS_OK) return rc;
   }
 

@@ -112,6 +112,14 @@ struct AttnArgs {
   int64_t Sq, Sk;
   int H, d;
   AttnSegs segs;       // n > 0: queries and keys per sequence (Sq == Sk == packed rows)
+  // Scratch for the split tail (bf16 with V, one sequence): the last units of
+  // the grid may run in key pieces whose unnormalised partial outputs are
+  // combined by a second kernel.  Null: never split.
+  float* part;
+  size_t part_bytes;
+  float* part_ml;      // set by the launcher: the (max, sum) partials, after the outputs
+  int64_t split_from;  // set by the launcher: units >= split_from run in ksp pieces
+  int ksp;
 };
 
 constexpr int kAttnKeyTile = 64;  // key padding unit expected for vt
