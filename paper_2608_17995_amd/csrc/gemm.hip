@@ -950,8 +950,9 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
   // destination register would read it before the load lands: every
   // instance must build without scratch (the build checks it).
   pl.stages = pl.bn == 128 ? 2 : 1;
-  // Tuning override "BN,SPLITS[,8[,STAGES]]" (e.g. AVITS_GEMM_TILE=256,3,8,1),
-  // for one launch family with AVITS_GEMM_TILE_<family> (e.g. _gemm_o).
+  // Tuning override "BN,SPLITS[,8[,STAGES[,TAIL,TSP]]]" (e.g. AVITS_GEMM_TILE=256,3,8,1),
+  // for one launch family with AVITS_GEMM_TILE_<family> (e.g. _gemm_o).  TAIL > 0
+  // (256-wide tile, SPLITS 1) runs the last min(TAIL, tiles) tiles in TSP k splits.
   const char* env = nullptr;
   if (family) {
     char name[64];
@@ -960,8 +961,8 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
   }
   if (!env) env = getenv("AVITS_GEMM_TILE");
   if (env) {
-    int bn = 0, sp = 0, wv = 8, stg = 2;
-    const int got = sscanf(env, "%d,%d,%d,%d", &bn, &sp, &wv, &stg);
+    int bn = 0, sp = 0, wv = 8, stg = 2, tail = 0, tsp = 1;
+    const int got = sscanf(env, "%d,%d,%d,%d,%d,%d", &bn, &sp, &wv, &stg, &tail, &tsp);
     if (got >= 2 && (bn == 256 || bn == 192 || bn == 128) && sp >= 1 && sp <= 4 && wv == 8 &&
         (stg == 1 || stg == 2)) {
       pl.bn = bn;
@@ -971,6 +972,10 @@ GemmPlan plan_gemm(const GemmArgs& a, int dtype, size_t partial_bytes, const cha
       pl.tiles = tiles_of(a, kBM, bn);
       pl.tail = 0;
       pl.tail_splits = 1;
+      if (got == 6 && bn == 256 && sp == 1 && tail > 0 && tsp >= 2 && tsp <= 4 && nk / tsp >= 1) {
+        pl.tail = std::min<int64_t>(tail, pl.tiles);
+        pl.tail_splits = tsp;
+      }
     }
   }
   return pl;

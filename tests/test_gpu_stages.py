@@ -318,6 +318,50 @@ def test_single_block(gpu, w):
     assert_close(host(lse), ref_lse, w.dtype, "lse")
 
 
+# ---------------------------------------------------------------------------
+# Load-balance forms, forced at small shapes through the tuning overrides:
+# the attention's key pieces merged by the combine kernel, and the GEMM's
+# split tail (the last tiles in k splits, reduced by a second kernel).  Each
+# form must still give the oracle's block.
+
+def _balanced_block(gpu, kind, seed):
+    w = C.TINY_BF16
+    n_txt, n_img = 40, 555  # 5 row blocks x 2 heads = 10 attention units, 10 key tiles
+    x, pos = _block_inputs(w, n_txt, n_img, seed=seed)
+    S = n_txt + n_img
+    if kind == "double":
+        wt, wi = G.double_stream_weights(w, 0, 0), G.double_stream_weights(w, 0, 1)
+        bw = gpu.BlockWeights(gpu.BLOCK_DOUBLE, txt=double_weights_dev(wt, w.dtype), img=double_weights_dev(wi, w.dtype))
+        ref, ref_lse = oracle.double_block(x, pos, n_txt, wt, wi, w.H)
+    else:
+        ws_ = G.single_block_weights(w, 0)
+        bw = gpu.BlockWeights(gpu.BLOCK_SINGLE, single=double_weights_dev(ws_, w.dtype))
+        ref, ref_lse = oracle.single_block(x, pos, ws_, w.H)
+    t_x = dev(x, w.dtype)
+    out = torch.empty_like(t_x)
+    lse = torch.empty(w.H, S, device="cuda")
+    gpu.avits_block_forward(t_x, out, dev(pos), n_txt, n_img, bw, w.H, lse_out=lse)
+    torch.cuda.synchronize()
+    assert_close(host(out) - x, ref - x, w.dtype, f"{kind} block update")
+    assert_close(host(lse), ref_lse, w.dtype, f"{kind} lse")
+    return host(out)
+
+
+@pytest.mark.parametrize("cfg", ["0,1", "0,2", "0,3", "0,4", "3,2", "5,4", "9,3"])
+@pytest.mark.parametrize("kind", ["double", "single"])
+def test_attention_key_pieces(gpu, monkeypatch, kind, cfg):
+    monkeypatch.setenv("AVITS_ATTN_SPLIT", cfg)
+    _balanced_block(gpu, kind, seed=31)
+
+
+@pytest.mark.parametrize("tail,tsp", [(1, 2), (3, 3), (7, 4), (100, 2)])
+@pytest.mark.parametrize("kind", ["double", "single"])
+def test_gemm_split_tail(gpu, monkeypatch, kind, tail, tsp):
+    monkeypatch.setenv("AVITS_GEMM_TILE", f"256,1,8,1,{tail},{tsp}")
+    _balanced_block(gpu, kind, seed=37)
+
+
+
 def test_block_relayout_equivariance(gpu):
     # RoPE reads positions, not sequence slots: shuffling image rows with their
     # positions shuffles the outputs (bit-exact is not expected: summation order).
