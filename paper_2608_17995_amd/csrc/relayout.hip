@@ -31,13 +31,24 @@ __device__ __forceinline__ void wave_copy_row(const char* __restrict__ src, char
 }
 
 // First position in the ascending idx[0..k) not below p.
-__device__ __forceinline__ int64_t lower_bound(const int32_t* idx, int64_t k, int64_t p) {
-  int64_t lo = 0, hi = k;
-  while (lo < hi) {
-    int64_t mid = (lo + hi) >> 1;
-    if (idx[mid] < p) lo = mid + 1; else hi = mid;
+// Number of entries of the ascending idx[0, k) below p, by the whole wave
+// (p uniform): each round samples 64 evenly spaced entries of the remaining
+// range [lo, hi] in one load and keeps the stretch between the last sample
+// below p and the first at or above it, so k <= 4096 takes two dependent
+// loads instead of a binary search's twelve.
+__device__ __forceinline__ int64_t wave_lower_bound(const int32_t* idx, int64_t k, int64_t p, int lane) {
+  int64_t lo = 0, hi = k;  // the answer lies in [lo, hi]
+  while (hi - lo > kWave) {
+    const int64_t step = (hi - lo + kWave - 1) / kWave;
+    const int64_t at = lo + int64_t(lane) * step;
+    const int c = __popcll(__ballot(at < hi && idx[at] < p));  // samples below p
+    if (c == 0) return lo;
+    const int64_t nhi = std::min<int64_t>(hi, lo + int64_t(c) * step);
+    lo += int64_t(c - 1) * step + 1;
+    hi = nhi;
   }
-  return lo;
+  const int64_t at = lo + lane;
+  return lo + __popcll(__ballot(at < hi && idx[at] < p));
 }
 
 template <typename T>
@@ -99,7 +110,7 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
   }
   const int64_t p = j - k;
   if (p >= N) return;
-  const int64_t at = lower_bound(idx, k, p);
+  const int64_t at = wave_lower_bound(idx, k, p, lane);
   if (at < k && idx[at] == p) return;  // selected: handled by its own job
   if (mode == AVITS_UP_NEAREST) {
     const int64_t src_row = int64_t((p / W_hr) >> 1) * W_lr + ((p % W_hr) >> 1);
@@ -167,7 +178,7 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_mixed_kernel(
   const int64_t p = job - n_prefix;
   if (p >= Mp) return;
   const int r = int(p / W_lr), c = int(p % W_lr);
-  const int64_t at = lower_bound(idx, k, p);
+  const int64_t at = wave_lower_bound(idx, k, p, lane);
   T* body = compact + n_prefix * D;
   if (at < k && idx[at] == p) {
     const int W_hr = 2 * W_lr;
@@ -181,6 +192,9 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_mixed_kernel(
       for (int ch = 0; ch < 4; ++ch)
         bilinear_row(lowres, dst[ch], int64_t(2 * r + (ch >> 1)) * W_hr + 2 * c + (ch & 1), H_lr, W_lr, D, lane);
     }
+    // Selected parents of low-res rows before r, and before r + 1.
+    const int64_t row0 = children ? wave_lower_bound(idx, k, int64_t(r) * W_lr, lane) : 0;
+    const int64_t row1 = children ? wave_lower_bound(idx, k, int64_t(r + 1) * W_lr, lane) : 0;
     if (lane < 4) {
       const int dr = lane >> 1, dc = lane & 1;
       int32_t* ps = pos + 3 * (4 * at + lane);
@@ -191,8 +205,6 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_mixed_kernel(
         // Rank of child (2r+dr, 2c+dc) among all children in high-res raster
         // order: the children of earlier low-res rows, then row 2r+dr's
         // share of this row's selected parents, then the parents to the left.
-        const int64_t row0 = lower_bound(idx, k, int64_t(r) * W_lr);
-        const int64_t row1 = lower_bound(idx, k, int64_t(r + 1) * W_lr);
         const int64_t rank = 4 * row0 + dr * 2 * (row1 - row0) + 2 * (at - row0) + dc;
         if (rank >= 0 && rank < 4 * k) children[rank] = int32_t(int64_t(2 * r + dr) * W_hr + 2 * c + dc);
       }
@@ -220,7 +232,7 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void scatter_mixed_kernel(
   const int64_t Mp = int64_t(H_lr) * W_lr;
   if (p >= Mp) return;
   const int64_t row_bytes = D * int64_t(sizeof(T));
-  const int64_t at = lower_bound(idx, k, p);
+  const int64_t at = wave_lower_bound(idx, k, p, lane);
   const T* body = out + row_offset * D;
   if (at < k && idx[at] == p) {
     const int r = int(p / W_lr), c = int(p % W_lr), W_hr = 2 * W_lr;
