@@ -66,30 +66,11 @@ __device__ __forceinline__ int64_t attn_xcd_id(int64_t b, int64_t n) {
   return start + b / 8;
 }
 
-// Work unit -> (head, row block) with the units of one XCD contiguous and
-// head-major, so the row blocks of a head share one L2.  With sequences, the
-// row blocks of a head enumerate each sequence's two row ranges in turn, and
-// the keys are that sequence's rows.  Split tail (one sequence only): units
-// below split_from take workgroups 0 .. split_from - 1; each later unit runs
-// in ksp pieces (workgroups split_from onwards, dispatched after the whole
-// units), piece p over key tiles [T p / ksp, T (p + 1) / ksp) of the unit's
-// T key tiles; `piece` is the piece's slot in the partial buffer (-1 for a
-// whole unit).
-__device__ __forceinline__ AttnUnit attn_unit(const AttnArgs& a, int rows, int64_t& piece) {
+// Unit u -> its head, query rows [q_lo, q_hi) and key ranges.  With
+// sequences, the row blocks of a head enumerate each sequence's two row
+// ranges in turn, and the keys are that sequence's rows.
+__device__ __forceinline__ AttnUnit attn_decode(const AttnArgs& a, int rows, int64_t u) {
   const int64_t n_rb = attn_row_blocks(a, rows);
-  const int64_t U = n_rb * a.H;
-  const int64_t bid = blockIdx.x;
-  int64_t u;
-  int p = 0;
-  piece = -1;
-  if (bid < a.split_from) {
-    u = attn_xcd_id(bid, std::min<int64_t>(a.split_from, U));
-  } else {
-    const int64_t v = attn_xcd_id(bid - a.split_from, int64_t(gridDim.x) - a.split_from);
-    u = a.split_from + v / a.ksp;
-    p = int(v % a.ksp);
-    piece = v;
-  }
   AttnUnit w;
   w.h = int(u / n_rb);
   int64_t rb = u % n_rb;
@@ -98,12 +79,6 @@ __device__ __forceinline__ AttnUnit attn_unit(const AttnArgs& a, int rows, int64
     w.q_hi = std::min<int64_t>(a.Sq, w.q_lo + rows);
     w.ks[0] = 0; w.kn[0] = a.Sk;
     w.ks[1] = 0; w.kn[1] = 0;
-    if (piece >= 0) {
-      const int64_t T = (a.Sk + 63) / 64;
-      const int64_t t_lo = T * p / a.ksp, t_hi = T * (p + 1) / a.ksp;
-      w.ks[0] = 64 * t_lo;
-      w.kn[0] = std::min<int64_t>(a.Sk, 64 * t_hi) - 64 * t_lo;
-    }
     return w;
   }
   // Static indices throughout (a dynamically indexed argument array would be
@@ -130,6 +105,44 @@ __device__ __forceinline__ AttnUnit attn_unit(const AttnArgs& a, int rows, int64
     }
   }
   return w;  // every unit of the grid (n_rb * H of them) finds its range
+}
+
+// Workgroup -> unit, with the units of one XCD contiguous and head-major, so
+// the row blocks of a head share one L2.  Split tail: units below split_from
+// take workgroups 0 .. split_from - 1; each later unit runs in ksp pieces
+// (workgroups split_from onwards, dispatched after the whole units), piece p
+// over key tiles [T p / ksp, T (p + 1) / ksp) of the unit's T key tiles (the
+// tiles of its first key range, then of its second); `piece` is the piece's
+// slot in the partial buffer (-1 for a whole unit).
+__device__ __forceinline__ AttnUnit attn_unit(const AttnArgs& a, int rows, int64_t& piece) {
+  const int64_t U = attn_row_blocks(a, rows) * a.H;
+  const int64_t bid = blockIdx.x;
+  int64_t u;
+  int p = 0;
+  piece = -1;
+  if (bid < a.split_from) {
+    u = attn_xcd_id(bid, std::min<int64_t>(a.split_from, U));
+  } else {
+    const int64_t v = attn_xcd_id(bid - a.split_from, int64_t(gridDim.x) - a.split_from);
+    u = a.split_from + v / a.ksp;
+    p = int(v % a.ksp);
+    piece = v;
+  }
+  AttnUnit w = attn_decode(a, rows, u);
+  if (piece >= 0) {
+    const int64_t t0 = (w.kn[0] + 63) / 64, T = t0 + (w.kn[1] + 63) / 64;
+    const int64_t t_lo = T * p / a.ksp, t_hi = T * (p + 1) / a.ksp;
+    // The piece's share of each range (either may be empty).
+    const int64_t a0 = std::min(t_lo, t0), b0 = std::min(t_hi, t0);
+    const int64_t a1 = std::max(t_lo, t0) - t0, b1 = std::max(t_hi, t0) - t0;
+    const int64_t n0 = std::max<int64_t>(0, std::min<int64_t>(w.kn[0], 64 * b0) - 64 * a0);
+    const int64_t n1 = std::max<int64_t>(0, std::min<int64_t>(w.kn[1], 64 * b1) - 64 * a1);
+    w.ks[0] += 64 * a0;
+    w.kn[0] = n0;
+    w.ks[1] += 64 * a1;
+    w.kn[1] = n1;
+  }
+  return w;
 }
 
 // Lane l of a 32x32 MFMA output tile holds row 8*(r/4) + 4*(l/32) + r%4 of
@@ -505,10 +518,10 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a) {
   const int64_t g = int64_t(blockIdx.x) * (256 / kLPR) + threadIdx.x / kLPR;  // split unit * kRows + row
   if (g >= n_split * kRows) return;
   const int64_t su = g / kRows, lr = g % kRows;
-  const int64_t u = a.split_from + su;
-  const int h = int(u / n_rb);
-  const int64_t row = (u % n_rb) * kRows + lr;
-  if (row >= a.Sq) return;
+  const AttnUnit un = attn_decode(a, kRows, a.split_from + su);
+  const int h = un.h;
+  const int64_t row = un.q_lo + lr;
+  if (row >= un.q_hi) return;
   float2 ml[kMaxPieces];
   float o[kMaxPieces][kCols];
 #pragma unroll
@@ -551,7 +564,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a) {
   if (a.lse && sub == 0) a.lse[int64_t(h) * a.Sq + row] = (m + log2f(den)) * kLn2;
 }
 
-// Split-tail plan for the bf16 kernel with V over one sequence: whole units
+// Split-tail plan for the bf16 kernel with V (one sequence or packed ones): whole units
 // fill the first workgroup slot of every CU, and the units beyond it run in
 // key pieces (or, with fewer units than CUs, every unit is split so that
 // the CUs are busy).  Returns ksp (1: no split) and sets split_from and the
@@ -561,25 +574,34 @@ int plan_attn_split(AttnArgs& a, int DH) {
   a.split_from = INT64_MAX;
   a.ksp = 1;
   a.part_ml = nullptr;
-  if (!a.part || !a.vt || a.mass || a.segs.n > 0) return 1;
+  if (!a.part || !a.vt || a.mass) return 1;
   const int64_t U = attn_row_blocks(a, kRows) * a.H;
-  const int64_t T = (a.Sk + 63) / 64;
+  // Fewest key tiles of any unit (every piece must get at least one).
+  int64_t T = (a.Sk + 63) / 64;
+  if (a.segs.n > 0) {
+    T = INT64_MAX;
+    for (int b = 0; b < a.segs.n; ++b)
+      T = std::min<int64_t>(T, (a.segs.len[b][0] + 63) / 64 + (a.segs.len[b][1] + 63) / 64);
+  }
   int64_t from, ksp;
   // Measured on MI355X at S = 1741 (28 key tiles): with at most 128 units,
-  // pieces one per CU are fastest; up to 256 units, two per CU; beyond, the
-  // overflow units in two pieces each (the partial wave then costs half a
-  // unit; finer pieces lose more to the combine than they gain).
+  // pieces one per CU are fastest; up to 256 units, two per CU; for 336
+  // units, 256 whole and the rest in two pieces each (finer pieces lose more
+  // to the combine than they gain).
   if (2 * U <= kAttnCUs) {
     from = 0;
     ksp = std::min<int64_t>(kMaxPieces, kAttnCUs / U);
   } else if (U <= kAttnCUs) {
     from = 0;
     ksp = std::min<int64_t>(kMaxPieces, 2 * kAttnCUs / U);
-  } else if (U < 2 * kAttnCUs) {
-    from = kAttnCUs;
-    ksp = 2;
   } else {
-    return 1;
+    // Both slots of every CU make a round of 2 * 256 units.  A last round of
+    // at most 256 units runs in two pieces each; a fuller one keeps one whole
+    // unit per CU and splits the rest.
+    const int64_t rem = U % (2 * kAttnCUs), base = U - rem;
+    if (rem == 0) return 1;
+    from = rem <= kAttnCUs ? base : base + kAttnCUs;
+    ksp = 2;
   }
   // Tuning override "FROM,KSP" (e.g. AVITS_ATTN_SPLIT=256,3; KSP 1 disables).
   if (const char* env = getenv("AVITS_ATTN_SPLIT")) {
@@ -589,6 +611,7 @@ int plan_attn_split(AttnArgs& a, int DH) {
       ksp = k;
     }
   }
+  if (from >= U) return 1;
   ksp = std::min<int64_t>(ksp, T);  // at least one key tile per piece
   auto need = [&](int64_t k) { return size_t((U - from) * k) * kRows * (DH + 2) * sizeof(float); };
   while (ksp >= 2 && need(ksp) > a.part_bytes) --ksp;
