@@ -596,10 +596,11 @@ int plan_attn_split(AttnArgs& a, int DH) {
     ksp = std::min<int64_t>(kMaxPieces, 2 * kAttnCUs / U);
   } else {
     // Both slots of every CU make a round of 2 * 256 units.  A last round of
-    // at most 256 units runs in two pieces each; a fuller one keeps one whole
-    // unit per CU and splits the rest.
+    // at most 256 units runs in two pieces each; one of up to 384 keeps one
+    // whole unit per CU and splits the rest; a fuller one is balanced enough
+    // already (984 units at S = 5171: 403 us unsplit, 415 split).
     const int64_t rem = U % (2 * kAttnCUs), base = U - rem;
-    if (rem == 0) return 1;
+    if (rem == 0 || rem > kAttnCUs + kAttnCUs / 2) return 1;
     from = rem <= kAttnCUs ? base : base + kAttnCUs;
     ksp = 2;
   }
