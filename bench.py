@@ -314,6 +314,44 @@ def _batched_block(avits, torch, w, bw, x, reps: int = 10) -> dict:
             "speedup": round(t_2 / t_b, 3)}
 
 
+def _batched_step(avits, torch, w, bw, shape, prefix_pos, q, kt, lse, feat, fp, low, text, ref, single_step,
+                  reps: int = 10) -> dict:
+    """A CFG pair through the whole step at once (BatchedStep: per-image score,
+    one batched selection, per-image gather into the packed rows, one batched
+    block, per-image scatter) against two single-image steps."""
+    from paper_2608_17995_amd.step import BatchedStep
+    bstep = BatchedStep(shape, [w.k, w.k], bw, prefix_pos, torch.bfloat16, alpha=w.alpha)
+    canv = [feat.clone(), feat.clone()]
+    refs = [ref, ref] if w.R else [None, None]
+
+    def batched():
+        bstep.run([q, q], [kt, kt], [lse, lse], canv, [fp, fp], [low, low], canv, [text, text], refs)
+
+    canvas1 = feat.clone()
+
+    def two():
+        for _ in range(2):
+            single_step.run(q, kt, lse, canvas1, fp, low, canvas1, torch.cat([text, ref]) if w.R else text)
+
+    def timed(fn):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record()
+        for _ in range(reps):
+            fn()
+        e[1].record()
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / reps
+
+    t_b, t_2 = float("inf"), float("inf")
+    for _ in range(3):
+        t_2 = min(t_2, timed(two))
+        t_b = min(t_b, timed(batched))
+    return {"images": 2, "batched_ms": round(t_b, 4), "two_single_ms": round(t_2, 4), "speedup": round(t_2 / t_b, 3)}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -515,6 +553,8 @@ def main(argv=None):
     result["select_sweep"] = _select_sweep(avits, torch)
     result["mixed_stage2"] = _mixed_stage2(avits, torch, w, text, bw)
     result["batched_block"] = _batched_block(avits, torch, w, bw, step.compact)
+    result["batched_step"] = _batched_step(avits, torch, w, bw, shape, torch.from_numpy(G.prefix_positions(w)).cuda(),
+                                           q, kt, lse, high, fp, low, cuda(lay["text"]), cuda(lay["ref"]), step)
     if not args.no_cpu_baseline:
         host = dict(si)
         host.update(lay)
