@@ -316,16 +316,21 @@ def _batched_block(avits, torch, w, bw, x, reps: int = 10) -> dict:
 
 def _batched_step(avits, torch, w, bw, shape, prefix_pos, q, kt, lse, feat, fp, low, text, ref, single_step,
                   reps: int = 10) -> dict:
-    """A CFG pair through the whole step at once (BatchedStep: per-image score,
-    one batched selection, per-image gather into the packed rows, one batched
-    block, per-image scatter) against two single-image steps."""
+    """A CFG pair through the whole step at once (BatchedStep: one scoring
+    launch over the stacked pair, one batched selection, per-image gather into
+    the packed rows, one batched block, per-image scatter) against two
+    single-image steps.  The stacked score inputs are resident before timing."""
     from paper_2608_17995_amd.step import BatchedStep
     bstep = BatchedStep(shape, [w.k, w.k], bw, prefix_pos, torch.bfloat16, alpha=w.alpha)
     canv = [feat.clone(), feat.clone()]
     refs = [ref, ref] if w.R else [None, None]
+    q2, kt2, lse2, fp2 = (torch.stack([t, t]) for t in (q, kt, lse, fp))
+    feat2 = torch.stack([feat, feat])
 
     def batched():
-        bstep.run([q, q], [kt, kt], [lse, lse], canv, [fp, fp], [low, low], canv, [text, text], refs)
+        # feat_t of the pair: the canvases' contents before this step (equal
+        # for both images of the pair here).
+        bstep.run(q2, kt2, lse2, feat2, fp2, [low, low], canv, [text, text], refs)
 
     canvas1 = feat.clone()
 

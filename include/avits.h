@@ -88,6 +88,28 @@ int avits_score(const void* latent_q, const void* text_k, const float* row_lse,
                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_score_batched — avits_score over B equally shaped images in one
+ * pass (Section 3.3, applied per image: a CFG pair, or several prompts at
+ * one resolution).  Image b's min-max normalisation (Eq. joint) uses its own
+ * A and V only, so its scores equal avits_score on image b alone.
+ *
+ * Inputs are stacked image-major, each image laid out as in avits_score:
+ * latent_q [B, N, H, d], text_k [B, L, H, d] (every image has L text keys),
+ * row_lse [B, H, N], feat_t and feat_prev [B, N, D_f]; outputs scores, and
+ * a_raw / v_raw when not NULL, [B, N] fp32.  All device pointers, owned by
+ * the caller.  workspace >= avits_score_batched_workspace_bytes(B, N, H)
+ * (which returns 0 for arguments outside the limits).  Requires
+ * 1 <= B <= 4096 and the limits of avits_score; errors as avits_score.
+ * ---------------------------------------------------------------------- */
+size_t avits_score_batched_workspace_bytes(int64_t B, int64_t N, int32_t H);
+int avits_score_batched(const void* latent_q, const void* text_k, const float* row_lse,
+                        const void* feat_t, const void* feat_prev,
+                        int64_t B, int64_t N, int64_t L, int32_t H, int32_t d, int64_t D_f,
+                        float alpha, float eps, int dtype,
+                        float* scores, float* a_raw, float* v_raw,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_select — top-K selection (Eq. topk).
  *
  * Writes the indices of the k largest scores to idx[0..k) in strictly

@@ -41,6 +41,10 @@ _SIGS = {
     "avits_score": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i32, _i32,
                                    _i64, _f32, _f32, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                    _size, _c_void_p]),
+    "avits_score_batched_workspace_bytes": (_size, [_i64, _i64, _i32]),
+    "avits_score_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i64,
+                                           _i32, _i32, _i64, _f32, _f32, ctypes.c_int, _c_void_p, _c_void_p,
+                                           _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_select_workspace_bytes": (_size, [_i64]),
     "avits_select": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_select_perturbed": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _c_void_p, _c_void_p, _size,
@@ -164,6 +168,33 @@ def avits_score(latent_q, text_k, row_lse, feat_t, feat_prev, alpha, eps, scores
     _check(load().avits_score(
         _dev(latent_q, "latent_q"), _dev(text_k, "text_k", dt), _dev(row_lse, "row_lse", torch.float32),
         _dev(feat_t, "feat_t", dt), _dev(feat_prev, "feat_prev", dt), N, L, H, d, D_f, alpha, eps,
+        _dtype_code(latent_q), _dev(scores, "scores", torch.float32), _dev(a_raw, "a_raw", torch.float32),
+        _dev(v_raw, "v_raw", torch.float32), wsp, wsb, _stream(stream)))
+    return scores
+
+
+def avits_score_batched_workspace_bytes(B: int, N: int, H: int) -> int:
+    return load().avits_score_batched_workspace_bytes(B, N, H)
+
+
+def avits_score_batched(latent_q, text_k, row_lse, feat_t, feat_prev, alpha, eps, scores,
+                        a_raw=None, v_raw=None, workspace=None, stream=None):
+    """Stacked images: latent_q [B, N, H, d], text_k [B, L, H, d], row_lse
+    [B, H, N], feat_t / feat_prev [B, N, D_f]; scores (and a_raw, v_raw)
+    [B, N]."""
+    import torch
+    Bn, N, H, d = latent_q.shape
+    L = text_k.shape[1]
+    D_f = feat_t.shape[2]
+    dt = latent_q.dtype
+    if (tuple(text_k.shape) != (Bn, L, H, d) or tuple(row_lse.shape) != (Bn, H, N)
+            or tuple(feat_t.shape) != (Bn, N, D_f) or tuple(feat_prev.shape) != (Bn, N, D_f)
+            or tuple(scores.shape) != (Bn, N) or any(t is not None and t.numel() != Bn * N for t in (a_raw, v_raw))):
+        raise ValueError("avits_score_batched: inputs must be stacked over the same B images of one shape")
+    ws, wsp, wsb = _workspace(workspace, avits_score_batched_workspace_bytes(Bn, N, H), latent_q.device)
+    _check(load().avits_score_batched(
+        _dev(latent_q, "latent_q"), _dev(text_k, "text_k", dt), _dev(row_lse, "row_lse", torch.float32),
+        _dev(feat_t, "feat_t", dt), _dev(feat_prev, "feat_prev", dt), Bn, N, L, H, d, D_f, alpha, eps,
         _dtype_code(latent_q), _dev(scores, "scores", torch.float32), _dev(a_raw, "a_raw", torch.float32),
         _dev(v_raw, "v_raw", torch.float32), wsp, wsb, _stream(stream)))
     return scores

@@ -21,6 +21,7 @@ namespace {
 constexpr int kSpRows = 128;     // image rows per spatial workgroup (4 waves x 32)
 constexpr int kSpKeys = 64;      // text keys per LDS tile
 constexpr int kTmpBlocks = 512;  // max workgroups of the temporal pass
+constexpr int kMaxScoreImages = 4096;  // images of one batched launch (grid y / z)
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
@@ -53,6 +54,16 @@ __global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
   const int wrow0 = blockIdx.x * kSpRows + wave * 32;  // this wave's 32 rows
   const int row = wrow0 + l32;
   const int64_t qstride = int64_t(H) * DH;
+  {  // image blockIdx.z of a stack of equally shaped images
+    const int64_t img = blockIdx.z;
+    q += img * N * qstride;
+    ktxt += img * L * qstride;
+    lse += img * H * N;
+    ft += img * N * Df;
+    fp += img * N * Df;
+    part_a += img * H * N;
+    part_v += img * H * N;
+  }
 
   // ---- temporal slice: lane pairs j = 0 .. npairs - 1 cover row
   // wrow0 + j rpi + lane / nch, chunk lane % nch (rpi = 64 / nch rows per
@@ -214,6 +225,14 @@ __global__ __launch_bounds__(64) void combine_kernel(const float* __restrict__ p
                                                      float* __restrict__ a_out, float* __restrict__ v_out,
                                                      float4* __restrict__ mm) {
   const int64_t i = int64_t(blockIdx.x) * kWave + threadIdx.x;
+  {  // image blockIdx.y: its partials, outputs and min/max slots
+    const int64_t img = blockIdx.y;
+    part_a += img * H * N;
+    part_v += img * H * N;
+    a_out += img * N;
+    v_out += img * N;
+    mm += img * gridDim.x;
+  }
   float amin = INFINITY, amax = -INFINITY, vmin = INFINITY, vmax = -INFINITY;
   if (i < N) {
     float sa = 0.f, sv = 0.f;
@@ -255,6 +274,13 @@ __global__ __launch_bounds__(128) void spatial_f32_kernel(const float* __restric
   __shared__ float ks[kSpKeys * DH];
   const int h = blockIdx.y;
   const int row = blockIdx.x * 128 + threadIdx.x;
+  {  // image blockIdx.z
+    const int64_t img = blockIdx.z;
+    q += img * N * H * DH;
+    ktxt += img * L * H * DH;
+    lse += img * H * N;
+    part += img * H * N;
+  }
   const bool ok = row < N;
   float qr[DH];
 #pragma unroll
@@ -290,6 +316,15 @@ __global__ __launch_bounds__(256) void temporal_kernel(const T* __restrict__ ft,
   __shared__ float4 red[4];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int64_t wstep = int64_t(gridDim.x) * 4;
+  {  // image blockIdx.y
+    const int64_t img = blockIdx.y;
+    ft += img * N * Df;
+    fp += img * N * Df;
+    part += img * H * N;
+    a_out += img * N;
+    v_out += img * N;
+    mm += img * gridDim.x;
+  }
   float amin = INFINITY, amax = -INFINITY, vmin = INFINITY, vmax = -INFINITY;
   constexpr int kVec = 16 / sizeof(T);
   const bool vec = (Df % kVec) == 0;
@@ -446,6 +481,13 @@ __global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__
                                                        const float4* __restrict__ mm, int n_mm, int64_t N,
                                                        float alpha, float eps, float* __restrict__ scores) {
   __shared__ float4 red[256];
+  {  // image blockIdx.y: its raw terms, min/max partials and scores
+    const int64_t img = blockIdx.y;
+    a += img * N;
+    v += img * N;
+    mm += img * n_mm;
+    scores += img * N;
+  }
   float4 r = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
   for (int i = threadIdx.x; i < n_mm; i += 256) {
     const float4 m = mm[i];
@@ -481,17 +523,89 @@ struct ScoreWs {
   size_t bytes;
 };
 
-ScoreWs score_ws_layout(char* base, int64_t N, int32_t H) {
+// B images' buffers, image-major: part / part_v [B][H][N], a / v [B][N],
+// mm [B][max(kTmpBlocks, ceil(N / 64))].
+ScoreWs score_ws_layout(char* base, int64_t N, int32_t H, int64_t B = 1) {
   ScoreWs w;
   size_t off = 0;
-  w.part = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * size_t(N) * H);
-  w.part_v = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * size_t(N) * H);
-  w.a = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * size_t(N));
-  w.v = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * size_t(N));
+  const size_t nb = size_t(N) * size_t(B);
+  w.part = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * nb * H);
+  w.part_v = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * nb * H);
+  w.a = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * nb);
+  w.v = reinterpret_cast<float*>(base + off); off += align256(sizeof(float) * nb);
   w.mm = reinterpret_cast<float4*>(base + off);
-  off += align256(sizeof(float4) * size_t(std::max<int64_t>(kTmpBlocks, (N + kWave - 1) / kWave)));
+  off += align256(sizeof(float4) * size_t(B) * size_t(std::max<int64_t>(kTmpBlocks, (N + kWave - 1) / kWave)));
   w.bytes = off;
   return w;
+}
+
+// B >= 1 equally shaped images, stacked image-major; each is scored with
+// its own min/max.  Every kernel takes the image from its last grid index.
+int score_launch(const char* who, const void* latent_q, const void* text_k, const float* row_lse,
+                 const void* feat_t, const void* feat_prev, int64_t B, int64_t N, int64_t L, int32_t H, int32_t d,
+                 int64_t D_f, float alpha, float eps, int dtype, float* scores, float* a_raw, float* v_raw,
+                 void* workspace, size_t workspace_bytes, void* stream) {
+  AVITS_REQUIRE(B >= 1 && B <= kMaxScoreImages, "%s: B=%lld images outside [1, %d]", who, (long long)B,
+                kMaxScoreImages);
+  AVITS_REQUIRE(N >= 1 && N <= INT32_MAX, "%s: N=%lld outside [1, 2^31)", who, (long long)N);
+  AVITS_REQUIRE(L >= 1 && L <= INT32_MAX, "%s: L=%lld outside [1, 2^31)", who, (long long)L);
+  AVITS_REQUIRE(H >= 1 && D_f >= 1, "%s: H=%d and D_f=%lld must be >= 1", who, H, (long long)D_f);
+  AVITS_REQUIRE(alpha >= 0.f && alpha <= 1.f, "%s: alpha=%g outside [0, 1]", who, alpha);
+  AVITS_REQUIRE(eps >= 0.f, "%s: eps=%g < 0", who, eps);
+  if (d != 64 && d != 128) return set_error(AVITS_ERR_UNSUPPORTED, "%s: head dim %d (need 64 or 128)", who, d);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "%s: dtype %d unsupported", who, dtype);
+  AVITS_REQUIRE(latent_q && text_k && row_lse && feat_t && feat_prev && scores, "%s: null input/output pointer",
+                who);
+  const ScoreWs need = score_ws_layout(nullptr, N, H, B);
+  if (!workspace || workspace_bytes < need.bytes)
+    return set_error(AVITS_ERR_WORKSPACE, "%s: workspace of %zu bytes, need %zu", who, workspace_bytes, need.bytes);
+  ScoreWs ws = score_ws_layout(static_cast<char*>(workspace), N, H, B);
+  float* a_dst = a_raw ? a_raw : ws.a;
+  float* v_dst = v_raw ? v_raw : ws.v;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  const int n = int(N), l = int(L);
+  const unsigned nimg = unsigned(B);
+  int nmm;
+  if (dtype == AVITS_BF16) {
+    {
+      TimedLaunch timed("score_spatial", s);
+      const dim3 grid(unsigned((N + kSpRows - 1) / kSpRows), unsigned(H), nimg);
+      if (d == 128)
+        hipLaunchKernelGGL(spatial_temporal_bf16_kernel<128>, grid, dim3(256), 0, s, (const bf16_t*)latent_q,
+                           (const bf16_t*)text_k, row_lse, (const bf16_t*)feat_t, (const bf16_t*)feat_prev, n, l, H,
+                           D_f, ws.part, ws.part_v);
+      else
+        hipLaunchKernelGGL(spatial_temporal_bf16_kernel<64>, grid, dim3(256), 0, s, (const bf16_t*)latent_q,
+                           (const bf16_t*)text_k, row_lse, (const bf16_t*)feat_t, (const bf16_t*)feat_prev, n, l, H,
+                           D_f, ws.part, ws.part_v);
+    }
+    nmm = int((N + kWave - 1) / kWave);
+    TimedLaunch timed("score_combine", s);
+    hipLaunchKernelGGL(combine_kernel, dim3(nmm, nimg), dim3(kWave), 0, s, ws.part, ws.part_v, N, H, D_f, a_dst,
+                       v_dst, ws.mm);
+  } else {
+    {
+      TimedLaunch timed("score_spatial", s);
+      const dim3 grid(unsigned((N + 127) / 128), unsigned(H), nimg);
+      if (d == 128)
+        hipLaunchKernelGGL(spatial_f32_kernel<128>, grid, dim3(128), 0, s, (const float*)latent_q,
+                           (const float*)text_k, row_lse, n, l, H, ws.part);
+      else
+        hipLaunchKernelGGL(spatial_f32_kernel<64>, grid, dim3(128), 0, s, (const float*)latent_q,
+                           (const float*)text_k, row_lse, n, l, H, ws.part);
+    }
+    nmm = int(std::min<int64_t>(kTmpBlocks, (N + 3) / 4));
+    TimedLaunch timed("score_combine", s);
+    hipLaunchKernelGGL(temporal_kernel<float>, dim3(nmm, nimg), dim3(256), 0, s, (const float*)feat_t,
+                       (const float*)feat_prev, ws.part, N, H, D_f, a_dst, v_dst, ws.mm);
+  }
+  const int fblocks = int(std::min<int64_t>(256, (N + 255) / 256));
+  TimedLaunch timed("score_finalize", s);
+  hipLaunchKernelGGL(finalize_kernel, dim3(fblocks, nimg), dim3(256), 0, s, a_dst, v_dst, ws.mm, nmm, N, alpha,
+                     eps, scores);
+  return launch_status(who);
 }
 
 }  // namespace
@@ -504,67 +618,26 @@ extern "C" size_t avits_score_workspace_bytes(int64_t N, int32_t H) {
   return score_ws_layout(nullptr, N, H).bytes;
 }
 
+extern "C" size_t avits_score_batched_workspace_bytes(int64_t B, int64_t N, int32_t H) {
+  if (B < 1 || B > kMaxScoreImages || N < 1 || H < 1) return 0;
+  return score_ws_layout(nullptr, N, H, B).bytes;
+}
+
 extern "C" int avits_score(const void* latent_q, const void* text_k, const float* row_lse, const void* feat_t,
                            const void* feat_prev, int64_t N, int64_t L, int32_t H, int32_t d, int64_t D_f,
                            float alpha, float eps, int dtype, float* scores, float* a_raw, float* v_raw,
                            void* workspace, size_t workspace_bytes, void* stream) {
-  AVITS_REQUIRE(N >= 1 && N <= INT32_MAX, "score: N=%lld outside [1, 2^31)", (long long)N);
-  AVITS_REQUIRE(L >= 1 && L <= INT32_MAX, "score: L=%lld outside [1, 2^31)", (long long)L);
-  AVITS_REQUIRE(H >= 1 && D_f >= 1, "score: H=%d and D_f=%lld must be >= 1", H, (long long)D_f);
-  AVITS_REQUIRE(alpha >= 0.f && alpha <= 1.f, "score: alpha=%g outside [0, 1]", alpha);
-  AVITS_REQUIRE(eps >= 0.f, "score: eps=%g < 0", eps);
-  if (d != 64 && d != 128) return set_error(AVITS_ERR_UNSUPPORTED, "score: head dim %d (need 64 or 128)", d);
-  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
-    return set_error(AVITS_ERR_UNSUPPORTED, "score: dtype %d unsupported", dtype);
-  AVITS_REQUIRE(latent_q && text_k && row_lse && feat_t && feat_prev && scores, "score: null input/output pointer");
-  const ScoreWs need = score_ws_layout(nullptr, N, H);
-  if (!workspace || workspace_bytes < need.bytes)
-    return set_error(AVITS_ERR_WORKSPACE, "score: workspace of %zu bytes, need %zu", workspace_bytes, need.bytes);
-  ScoreWs ws = score_ws_layout(static_cast<char*>(workspace), N, H);
-  float* a_dst = a_raw ? a_raw : ws.a;
-  float* v_dst = v_raw ? v_raw : ws.v;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  return score_launch("score", latent_q, text_k, row_lse, feat_t, feat_prev, 1, N, L, H, d, D_f, alpha, eps, dtype,
+                      scores, a_raw, v_raw, workspace, workspace_bytes, stream);
+}
 
-  const int n = int(N), l = int(L);
-  int nmm;
-  if (dtype == AVITS_BF16) {
-    {
-      TimedLaunch timed("score_spatial", s);
-      const dim3 grid(unsigned((N + kSpRows - 1) / kSpRows), unsigned(H));
-      if (d == 128)
-        hipLaunchKernelGGL(spatial_temporal_bf16_kernel<128>, grid, dim3(256), 0, s, (const bf16_t*)latent_q,
-                           (const bf16_t*)text_k, row_lse, (const bf16_t*)feat_t, (const bf16_t*)feat_prev, n, l, H,
-                           D_f, ws.part, ws.part_v);
-      else
-        hipLaunchKernelGGL(spatial_temporal_bf16_kernel<64>, grid, dim3(256), 0, s, (const bf16_t*)latent_q,
-                           (const bf16_t*)text_k, row_lse, (const bf16_t*)feat_t, (const bf16_t*)feat_prev, n, l, H,
-                           D_f, ws.part, ws.part_v);
-    }
-    nmm = int((N + kWave - 1) / kWave);
-    TimedLaunch timed("score_combine", s);
-    hipLaunchKernelGGL(combine_kernel, dim3(nmm), dim3(kWave), 0, s, ws.part, ws.part_v, N, H, D_f, a_dst, v_dst,
-                       ws.mm);
-  } else {
-    {
-      TimedLaunch timed("score_spatial", s);
-      const dim3 grid(unsigned((N + 127) / 128), unsigned(H));
-      if (d == 128)
-        hipLaunchKernelGGL(spatial_f32_kernel<128>, grid, dim3(128), 0, s, (const float*)latent_q,
-                           (const float*)text_k, row_lse, n, l, H, ws.part);
-      else
-        hipLaunchKernelGGL(spatial_f32_kernel<64>, grid, dim3(128), 0, s, (const float*)latent_q,
-                           (const float*)text_k, row_lse, n, l, H, ws.part);
-    }
-    nmm = int(std::min<int64_t>(kTmpBlocks, (N + 3) / 4));
-    TimedLaunch timed("score_combine", s);
-    hipLaunchKernelGGL(temporal_kernel<float>, dim3(nmm), dim3(256), 0, s, (const float*)feat_t,
-                       (const float*)feat_prev, ws.part, N, H, D_f, a_dst, v_dst, ws.mm);
-  }
-  const int fblocks = int(std::min<int64_t>(256, (N + 255) / 256));
-  TimedLaunch timed("score_finalize", s);
-  hipLaunchKernelGGL(finalize_kernel, dim3(fblocks), dim3(256), 0, s, a_dst, v_dst, ws.mm, nmm, N, alpha, eps,
-                     scores);
-  return launch_status("score");
+extern "C" int avits_score_batched(const void* latent_q, const void* text_k, const float* row_lse,
+                                   const void* feat_t, const void* feat_prev, int64_t B, int64_t N, int64_t L,
+                                   int32_t H, int32_t d, int64_t D_f, float alpha, float eps, int dtype,
+                                   float* scores, float* a_raw, float* v_raw, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+  return score_launch("score_batched", latent_q, text_k, row_lse, feat_t, feat_prev, B, N, L, H, d, D_f, alpha, eps,
+                      dtype, scores, a_raw, v_raw, workspace, workspace_bytes, stream);
 }
 
 extern "C" int avits_score_from_mass(const float* mass, int32_t H, int32_t count, const void* const* snapshots,

@@ -323,7 +323,8 @@ class BatchedStep:
     rows of all images, then their [reference; selected] rows) with
     block-diagonal attention.
 
-      score    per image: S_b from its own q, text keys, LSE and features
+      score    S_b from image b's own q, text keys, LSE and features; one
+               avits_score_batched launch when the inputs come stacked
       select   avits_select_batched over the B score vectors (k_b each)
       gather   per image: its text rows into the text area (avits_scatter of
                the rows), [ref_b; X_prev,b[idx_b]] into its image area
@@ -365,21 +366,30 @@ class BatchedStep:
                          for b in range(Bn)]
         d = s.D // s.H
         code = B.BF16 if dtype == torch.bfloat16 else B.F32
-        self.ws_score = torch.empty(max(B.avits_score_workspace_bytes(s.N, s.H), 1), dtype=torch.uint8, device=device)
+        self.ws_score = torch.empty(max(B.avits_score_batched_workspace_bytes(Bn, s.N, s.H), 1), dtype=torch.uint8,
+                                    device=device)
         self.ws_block = torch.empty(
             max(B.avits_block_workspace_bytes(weights.kind, self.S_tot, s.H, d, s.mlp_hidden, code), 1),
             dtype=torch.uint8, device=device)
 
     def run(self, latent_q, text_k, row_lse, feat_t, feat_prev, lowres, highres_prev, text, ref, stream=None):
-        """Lists over the images: latent_q[b], text_k[b], row_lse[b], feat_t[b],
-        feat_prev[b], lowres[b], highres_prev[b] (its canvas, updated in place),
-        text[b] [L, D], ref[b] [R, D] or None."""
+        """Lists over the images: lowres[b], highres_prev[b] (its canvas,
+        updated in place), text[b] [L, D], ref[b] [R, D] or None.  The score
+        inputs are either lists too (latent_q[b], text_k[b], row_lse[b],
+        feat_t[b], feat_prev[b]; one scoring launch per image) or tensors
+        stacked over the images ([B, N, H, d], [B, L, H, d], [B, H, N],
+        [B, N, D_f] twice; one launch for all)."""
+        import torch
         s = self.shape
         T = self.txt_off[-1]
         Bn = len(self.ks)
-        for b in range(Bn):
-            B.avits_score(latent_q[b], text_k[b], row_lse[b], feat_t[b], feat_prev[b], self.alpha, self.eps,
-                          self.scores[b * s.N:(b + 1) * s.N], workspace=self.ws_score, stream=stream)
+        if torch.is_tensor(latent_q):
+            B.avits_score_batched(latent_q, text_k, row_lse, feat_t, feat_prev, self.alpha, self.eps,
+                                  self.scores.view(Bn, s.N), workspace=self.ws_score, stream=stream)
+        else:
+            for b in range(Bn):
+                B.avits_score(latent_q[b], text_k[b], row_lse[b], feat_t[b], feat_prev[b], self.alpha, self.eps,
+                              self.scores[b * s.N:(b + 1) * s.N], workspace=self.ws_score, stream=stream)
         if sum(self.ks):
             B.avits_select_batched(self.scores, [b * s.N for b in range(Bn + 1)], self.ks, self.idx, stream=stream)
         for b in range(Bn):

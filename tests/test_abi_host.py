@@ -107,6 +107,29 @@ def test_score_validation(lib):
     assert _score(lib, wsb=need - 1) == WORKSPACE
 
 
+def test_score_batched_validation(lib):
+    def call(**kw):
+        a = dict(q=FAKE, B=2, N=16, L=4, H=2, d=64, Df=8, alpha=0.5, dtype=1, ws=FAKE, wsb=1 << 30)
+        a.update(kw)
+        return lib.avits_score_batched(a["q"], FAKE, FAKE, FAKE, FAKE, a["B"], a["N"], a["L"], a["H"], a["d"],
+                                       a["Df"], a["alpha"], 1e-8, a["dtype"], FAKE, None, None, a["ws"], a["wsb"],
+                                       None)
+
+    assert call(B=0) == INVALID
+    assert call(B=4097) == INVALID
+    assert call(N=0) == INVALID
+    assert call(alpha=2.0) == INVALID
+    assert call(d=32) == UNSUPPORTED
+    assert call(q=None) == INVALID
+    assert lib.avits_score_batched_workspace_bytes(0, 16, 2) == 0
+    one = lib.avits_score_workspace_bytes(16, 2)
+    assert lib.avits_score_batched_workspace_bytes(1, 16, 2) == one
+    need = lib.avits_score_batched_workspace_bytes(3, 16, 2)
+    assert need >= 3 * 16 * 2 * 4 * 2 and need > one      # per-image partials of A and V
+    assert call(B=3, wsb=need - 1) == WORKSPACE
+    assert call(B=3, ws=None) == WORKSPACE
+
+
 def test_gather_and_scatter_validation(lib):
     g = lib.avits_gather_upsample
     # k > N (N = 4*2*2 = 16)

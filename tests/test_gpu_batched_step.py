@@ -1,5 +1,6 @@
 """A selective step over several images at once (a CFG pair and a third
-prompt with nothing selected): each image scored on its own, one selection
+prompt with nothing selected): each image scored on its own (one launch per
+image, or one launch over the stacked images), one selection
 launch over all of them, one block pass over the rows packed by stream, and
 each image's canvas updated from its own rows.  Every stage is checked
 against the oracle on the GPU's inputs of that stage: indices, gathered rows,
@@ -20,8 +21,9 @@ from _gpu import assert_close, dev, double_weights_dev, host
 pytestmark = pytest.mark.gpu
 
 
+@pytest.mark.parametrize("stacked", [False, True], ids=["score_per_image", "score_stacked"])
 @pytest.mark.parametrize("base", [C.TINY_BF16, C.TINY_BF16_REF], ids=lambda w: w.name)
-def test_batched_step(gpu, base):
+def test_batched_step(gpu, base, stacked):
     ws = [base, base.replace(seed=base.seed + 1, rho=0.45), base.replace(seed=base.seed + 2)]
     ks = [ws[0].k, ws[1].k, 0]
     Bn = len(ws)
@@ -35,10 +37,12 @@ def test_batched_step(gpu, base):
     lay = [G.layout_inputs(w, s["feat_t"]) for w, s in zip(ws, si)]
     lse = [oracle.joint_lse(s["latent_q"], np.concatenate([s["text_k"], s["ref_k"], s["latent_k"]])) for s in si]
     canvases = [dev(l["highres_prev"], base.dtype) for l in lay]
-    step.run([dev(s["latent_q"], base.dtype) for s in si], [dev(s["text_k"], base.dtype) for s in si],
-             [dev(x) for x in lse], canvases, [dev(s["feat_prev"], base.dtype) for s in si],
-             [dev(l["lowres"], base.dtype) for l in lay], canvases, [dev(l["text"], base.dtype) for l in lay],
-             [dev(l["ref"], base.dtype) for l in lay])
+    score_in = [[dev(s["latent_q"], base.dtype) for s in si], [dev(s["text_k"], base.dtype) for s in si],
+                [dev(x) for x in lse], canvases, [dev(s["feat_prev"], base.dtype) for s in si]]
+    if stacked:  # one scoring launch over the stacked images (feat_t: a copy of the canvases)
+        score_in = [torch.stack(t) for t in score_in]
+    step.run(*score_in, [dev(l["lowres"], base.dtype) for l in lay], canvases,
+             [dev(l["text"], base.dtype) for l in lay], [dev(l["ref"], base.dtype) for l in lay])
     torch.cuda.synchronize()
     scores, idx_all = step.scores.cpu().numpy(), step.idx.cpu().numpy()
     x, pos, x_out = host(step.x), step.pos.cpu().numpy(), host(step.x_out)

@@ -76,6 +76,60 @@ def test_score_without_optional_outputs_and_small_feature_width(gpu, w):
     assert np.abs(host(S) - s_ref).max() < 1e-4
 
 
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+def test_score_batched(gpu, w):
+    """Three images of one shape in one launch: each matches the oracle, and
+    is bit-identical to avits_score on that image alone (own min-max)."""
+    ws = [w, w.replace(seed=w.seed + 1), w.replace(seed=w.seed + 2)]
+    si = [G.score_inputs(x) for x in ws]
+    lse = [_lse_gpu(gpu, x, s) for x, s in zip(ws, si)]
+    stack = lambda key: torch.stack([dev(s[key], w.dtype) for s in si])  # noqa: E731
+    S = torch.empty(len(ws), w.N, device="cuda")
+    A = torch.empty_like(S)
+    V = torch.empty_like(S)
+    gpu.avits_score_batched(stack("latent_q"), stack("text_k"), torch.stack(lse), stack("feat_t"),
+                            stack("feat_prev"), w.alpha, w.eps_minmax, S, A, V)
+    torch.cuda.synchronize()
+    for b, (x, s) in enumerate(zip(ws, si)):
+        s_ref, a_ref, v_ref = oracle.score(s["latent_q"], s["text_k"], host(lse[b]), s["feat_t"], s["feat_prev"],
+                                           w.alpha, w.eps_minmax)
+        assert_close(host(A[b]), a_ref, w.dtype, f"image {b} A")
+        assert_close(host(V[b]), v_ref, w.dtype, f"image {b} V")
+        assert np.abs(host(S[b]) - s_ref).max() < 1e-4
+        one = torch.empty(w.N, device="cuda")
+        gpu.avits_score(dev(s["latent_q"], w.dtype), dev(s["text_k"], w.dtype), lse[b], dev(s["feat_t"], w.dtype),
+                        dev(s["feat_prev"], w.dtype), w.alpha, w.eps_minmax, one)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host(S[b]), host(one), err_msg=f"image {b} vs its own launch")
+
+
+def test_score_batched_flux_pair(gpu):
+    """The CFG pair at the FLUX 1024^2 shape (N = 4096, L = 512, 24 heads):
+    each image's scores are bit-identical to its own single-image launch,
+    and a sample of rows matches the oracle."""
+    w = C.FLUX_1024
+    ws = [w, w.replace(seed=w.seed + 1)]
+    si = [G.score_inputs(x) for x in ws]
+    lse = [_lse_gpu(gpu, x, s) for x, s in zip(ws, si)]
+    stack = lambda key: torch.stack([dev(s[key], w.dtype) for s in si])  # noqa: E731
+    S = torch.empty(2, w.N, device="cuda")
+    A = torch.empty_like(S)
+    V = torch.empty_like(S)
+    gpu.avits_score_batched(stack("latent_q"), stack("text_k"), torch.stack(lse), stack("feat_t"),
+                            stack("feat_prev"), w.alpha, w.eps_minmax, S, A, V)
+    rows = np.random.default_rng(5).choice(w.N, 64, replace=False)
+    for b, s in enumerate(si):
+        one = torch.empty(w.N, device="cuda")
+        gpu.avits_score(dev(s["latent_q"], w.dtype), dev(s["text_k"], w.dtype), lse[b], dev(s["feat_t"], w.dtype),
+                        dev(s["feat_prev"], w.dtype), w.alpha, w.eps_minmax, one)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host(S[b]), host(one), err_msg=f"image {b}")
+        _, a_ref, v_ref = oracle.score(s["latent_q"][rows], s["text_k"], host(lse[b])[:, rows], s["feat_t"][rows],
+                                       s["feat_prev"][rows], w.alpha, w.eps_minmax)
+        np.testing.assert_allclose(host(A[b])[rows], a_ref, rtol=1e-4, atol=1e-7)
+        np.testing.assert_allclose(host(V[b])[rows], v_ref, rtol=1e-4)
+
+
 def _select(gpu, scores_np, k):
     s = torch.from_numpy(np.ascontiguousarray(scores_np, dtype=np.float32)).cuda()
     idx = torch.full((max(k, 1),), -7, dtype=torch.int32, device="cuda")
