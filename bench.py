@@ -316,21 +316,20 @@ def _batched_block(avits, torch, w, bw, x, reps: int = 10) -> dict:
 
 def _batched_step(avits, torch, w, bw, shape, prefix_pos, q, kt, lse, feat, fp, low, text, ref, single_step,
                   reps: int = 10) -> dict:
-    """A CFG pair through the whole step at once (BatchedStep: one scoring
-    launch over the stacked pair, one batched selection, per-image gather into
-    the packed rows, one batched block, per-image scatter) against two
-    single-image steps.  The stacked score inputs are resident before timing."""
+    """A CFG pair through the whole step at once (BatchedStep on inputs stacked
+    over the pair: one scoring launch, one selection, one gather, one block,
+    one scatter) against two single-image steps.  The stacked inputs are
+    resident before timing."""
     from paper_2608_17995_amd.step import BatchedStep
     bstep = BatchedStep(shape, [w.k, w.k], bw, prefix_pos, torch.bfloat16, alpha=w.alpha)
-    canv = [feat.clone(), feat.clone()]
-    refs = [ref, ref] if w.R else [None, None]
-    q2, kt2, lse2, fp2 = (torch.stack([t, t]) for t in (q, kt, lse, fp))
-    feat2 = torch.stack([feat, feat])
+    q2, kt2, lse2, fp2, low2, text2 = (torch.stack([t, t]) for t in (q, kt, lse, fp, low, text))
+    feat2, canv2 = torch.stack([feat, feat]), torch.stack([feat, feat])
+    ref2 = torch.stack([ref, ref]) if w.R else None
 
     def batched():
         # feat_t of the pair: the canvases' contents before this step (equal
         # for both images of the pair here).
-        bstep.run(q2, kt2, lse2, feat2, fp2, [low, low], canv, [text, text], refs)
+        bstep.run(q2, kt2, lse2, feat2, fp2, low2, canv2, text2, ref2)
 
     canvas1 = feat.clone()
 

@@ -170,6 +170,30 @@ int avits_gather_upsample(const void* lowres, const void* highres_prev, const vo
                           void* compact, int32_t* pos_sel, void* canvas, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_gather_upsample_batched — the Stage-2 re-layout of Section 3.2 for
+ * B equally shaped images in one launch, each with its own selection, its
+ * rows placed anywhere in one packed compact buffer (e.g. the image rows of
+ * avits_block_forward_batched).  For image b, with idx_b = idx[idx_off[b] ..
+ * idx_off[b + 1]) (ascending, unique, < N) and k_b its length, it does what
+ * avits_gather_upsample does with
+ *   lowres + b*(N/4)*D, highres_prev + b*N*D, prefix + b*n_prefix*D,
+ *   compact rows from row_off[b], canvas + b*N*D,
+ * and writes pos[row_off[b] + n_prefix + j] = (0, idx_b[j] / W_hr,
+ * idx_b[j] % W_hr): pos is indexed like compact's rows (the prefix rows'
+ * positions are the caller's).  lowres [B, H_lr*W_lr, D], highres_prev and
+ * canvas [B, N, D] (canvas may alias highres_prev, as one stack), prefix
+ * [B, n_prefix, D] or NULL when n_prefix == 0; idx_off [B + 1] and row_off
+ * [B] are host int64 arrays (idx_off[0] == 0); device buffers are the
+ * caller's.  1 <= B <= 64; each k_b in [0, N]; rows of different images must
+ * not overlap in compact.  Errors as avits_gather_upsample.
+ * ---------------------------------------------------------------------- */
+int avits_gather_upsample_batched(const void* lowres, const void* highres_prev, const void* prefix,
+                                  const int32_t* idx, const int64_t* idx_off, int32_t B,
+                                  int32_t H_lr, int32_t W_lr, int64_t n_prefix, int64_t D, int mode,
+                                  int dtype, void* compact, const int64_t* row_off, int32_t* pos,
+                                  void* canvas, void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_block_forward — one MMDiT joint-attention block on the compacted
  * sequence (Section 3.3.1: joint self-attention over [C; Z], Eq. joint_qk,
  * with the model's QK-normalisation), FLUX-style:
@@ -283,6 +307,19 @@ int avits_block_qk(const void* x_in, const int32_t* pos, float pos_scale, int64_
  * ---------------------------------------------------------------------- */
 int avits_scatter(const void* out, const int32_t* idx, int64_t k, int64_t row_offset,
                   int64_t D, int dtype, void* canvas, void* stream);
+
+/* ------------------------------------------------------------------------
+ * avits_scatter_batched — the Stage-3 re-layout for B images in one launch:
+ * for image b and j < k_b = idx_off[b + 1] - idx_off[b],
+ *   canvas[b*N + idx[idx_off[b] + j]] = out[row_off[b] + j].
+ * out [*, D] (the packed block output), idx the concatenated selections
+ * (each unique, < N), canvas [B, N, D]; idx_off [B + 1] and row_off [B] are
+ * host int64 arrays (idx_off[0] == 0).  1 <= B <= 64, each k_b in [0, N];
+ * nothing is enqueued when every k_b is 0.  Errors as avits_scatter.
+ * ---------------------------------------------------------------------- */
+int avits_scatter_batched(const void* out, const int32_t* idx, const int64_t* idx_off, int32_t B,
+                          const int64_t* row_off, int64_t N, int64_t D, int dtype, void* canvas,
+                          void* stream);
 
 /* ------------------------------------------------------------------------
  * avits_gather_mixed — the mixed-resolution sequence of Stage 2 (Section

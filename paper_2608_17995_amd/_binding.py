@@ -65,6 +65,11 @@ _SIGS = {
     "avits_block_qk": (ctypes.c_int, [_c_void_p, _c_void_p, _f32, _i64, _i64, ctypes.POINTER(_BlockWeights), _i32, _i32,
                                       ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, ctypes.c_int, _c_void_p, _c_void_p]),
+    "avits_gather_upsample_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i32,
+                                                     _i32, _i32, _i64, _i64, ctypes.c_int, ctypes.c_int, _c_void_p,
+                                                     _c_void_p, _c_void_p, _c_void_p, _c_void_p]),
+    "avits_scatter_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i32, _c_void_p, _i64, _i64,
+                                             ctypes.c_int, _c_void_p, _c_void_p]),
     "avits_gather_mixed": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _i32, _i32, _i64, _i64,
                                           ctypes.c_int, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _c_void_p]),
     "avits_scatter_mixed": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i32, _i32, _i64, _i64, ctypes.c_int,
@@ -244,6 +249,47 @@ def avits_gather_upsample(lowres, highres_prev, prefix, idx, H_lr, W_lr, compact
         H_lr, W_lr, n_prefix, lowres.shape[1], mode, _dtype_code(lowres), _dev(compact, "compact", dt),
         _dev(pos_sel, "pos_sel", torch.int32), _dev(canvas, "canvas", dt), _stream(stream)))
     return compact, pos_sel, canvas
+
+
+def _host_i64(values, n, name):
+    values = [int(v) for v in values]
+    if len(values) != n:
+        raise ValueError(f"{name}: {len(values)} entries, expected {n}")
+    return (ctypes.c_int64 * n)(*values)
+
+
+def avits_gather_upsample_batched(lowres, highres_prev, prefix, idx, idx_off, H_lr, W_lr, compact, row_off, pos,
+                                  canvas, mode=UP_NEAREST, stream=None):
+    """Stacked images: lowres [B, H_lr*W_lr, D], highres_prev / canvas
+    [B, N, D], prefix [B, n_prefix, D] or None; idx the concatenated
+    selections, idx_off (B + 1) and row_off (B) host sequences; pos is
+    indexed like compact's rows."""
+    import torch
+    dt = lowres.dtype
+    Bn, _, D = lowres.shape
+    n_prefix = 0 if prefix is None else prefix.shape[1]
+    if prefix is not None and (prefix.shape[0] != Bn or prefix.shape[2] != D):
+        raise ValueError("avits_gather_upsample_batched: prefix must be [B, n_prefix, D]")
+    if highres_prev.shape[0] != Bn or canvas.shape[0] != Bn:
+        raise ValueError("avits_gather_upsample_batched: highres_prev and canvas must be stacked over B images")
+    _check(load().avits_gather_upsample_batched(
+        _dev(lowres, "lowres"), _dev(highres_prev, "highres_prev", dt),
+        _dev(prefix, "prefix", dt) if n_prefix else None, _dev(idx, "idx", torch.int32),
+        _host_i64(idx_off, Bn + 1, "idx_off"), Bn, H_lr, W_lr, n_prefix, D, mode, _dtype_code(lowres),
+        _dev(compact, "compact", dt), _host_i64(row_off, Bn, "row_off"), _dev(pos, "pos", torch.int32),
+        _dev(canvas, "canvas", dt), _stream(stream)))
+    return compact, pos, canvas
+
+
+def avits_scatter_batched(out, idx, idx_off, row_off, canvas, stream=None):
+    """canvas [B, N, D]; idx the concatenated selections; idx_off (B + 1),
+    row_off (B) host sequences."""
+    import torch
+    Bn, N, D = canvas.shape
+    _check(load().avits_scatter_batched(
+        _dev(out, "out", canvas.dtype), _dev(idx, "idx", torch.int32), _host_i64(idx_off, Bn + 1, "idx_off"), Bn,
+        _host_i64(row_off, Bn, "row_off"), N, D, _dtype_code(canvas), _dev(canvas, "canvas"), _stream(stream)))
+    return canvas
 
 
 def avits_scatter(out, idx, row_offset, canvas, stream=None):

@@ -80,16 +80,37 @@ __device__ __forceinline__ void bilinear_row(const T* __restrict__ low, T* __res
   }
 }
 
+// Where image b of a stack finds its selection and puts its rows: idx
+// entries [idx_off[b], idx_off[b + 1]), compact rows from row_off[b], pos
+// rows from pos_off[b].  A single image is the stack of one.
+constexpr int kMaxRelayoutImages = 64;
+struct ImageRows {
+  int64_t idx_off[kMaxRelayoutImages + 1];
+  int64_t row_off[kMaxRelayoutImages];
+  int64_t pos_off[kMaxRelayoutImages];
+};
+
+// Image blockIdx.y of a stack of equally shaped images (lowres [B, N/4, D],
+// highres / canvas [B, N, D], prefix [B, n_prefix, D]).
 template <typename T>
 __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
     const T* __restrict__ lowres, const T* highres, const T* __restrict__ prefix,
-    const int32_t* __restrict__ idx, int64_t k, int H_lr, int W_lr, int64_t n_prefix, int64_t D,
+    const int32_t* __restrict__ idx, const ImageRows im, int H_lr, int W_lr, int64_t n_prefix, int64_t D,
     int mode, T* __restrict__ compact, int32_t* __restrict__ pos_sel, T* canvas, int canvas_aliases) {
   const int lane = threadIdx.x % kWave;
   const int64_t job = int64_t(blockIdx.x) * kRowsPerBlock + threadIdx.x / kWave;
   const int W_hr = 2 * W_lr;
   const int64_t N = int64_t(4) * H_lr * W_lr;
   const int64_t row_bytes = D * int64_t(sizeof(T));
+  const int b = blockIdx.y;
+  const int64_t k = im.idx_off[b + 1] - im.idx_off[b];
+  lowres += int64_t(b) * (N / 4) * D;
+  highres += int64_t(b) * N * D;
+  canvas += int64_t(b) * N * D;
+  if (prefix) prefix += int64_t(b) * n_prefix * D;
+  idx += im.idx_off[b];
+  compact += im.row_off[b] * D;
+  pos_sel += im.pos_off[b] * 3;
   if (job < n_prefix) {
     wave_copy_row(reinterpret_cast<const char*>(prefix + job * D),
                   reinterpret_cast<char*>(compact + job * D), row_bytes, lane);
@@ -121,13 +142,20 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
   }
 }
 
+// Image blockIdx.y: its selection idx[idx_off[b] ..), its rows of `out`
+// from row_off[b], its canvas at b N D.
 template <typename T>
 __global__ __launch_bounds__(kWave * kRowsPerBlock) void scatter_kernel(
-    const T* __restrict__ out, const int32_t* __restrict__ idx, int64_t k, int64_t row_offset,
+    const T* __restrict__ out, const int32_t* __restrict__ idx, const ImageRows im, int64_t N,
     int64_t D, T* __restrict__ canvas) {
   const int lane = threadIdx.x % kWave;
   const int64_t j = int64_t(blockIdx.x) * kRowsPerBlock + threadIdx.x / kWave;
+  const int b = blockIdx.y;
+  const int64_t k = im.idx_off[b + 1] - im.idx_off[b];
   if (j >= k) return;
+  idx += im.idx_off[b];
+  const int64_t row_offset = im.row_off[b];
+  canvas += int64_t(b) * N * D;
   wave_copy_row(reinterpret_cast<const char*>(out + (row_offset + j) * D),
                 reinterpret_cast<char*>(canvas + int64_t(idx[j]) * D), D * int64_t(sizeof(T)), lane);
 }
@@ -256,6 +284,45 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 using namespace avits;
 
+namespace {
+
+// One launch over the B images of `im`; k_max is the largest selection.
+int launch_gather(const void* lowres, const void* highres_prev, const void* prefix, const int32_t* idx,
+                  const ImageRows& im, int B, int64_t k_max, int32_t H_lr, int32_t W_lr, int64_t n_prefix,
+                  int64_t D, int mode, int dtype, void* compact, int32_t* pos_sel, void* canvas, void* stream,
+                  const char* who) {
+  const int64_t N = int64_t(4) * H_lr * W_lr;
+  const int64_t jobs = n_prefix + k_max + N;
+  const dim3 grid(unsigned(ceil_div(jobs, kRowsPerBlock)), unsigned(B)), block(kWave * kRowsPerBlock);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int alias = canvas == highres_prev;
+  TimedLaunch timed("gather_upsample", s);
+  if (dtype == AVITS_F32)
+    hipLaunchKernelGGL(gather_upsample_kernel<float>, grid, block, 0, s, (const float*)lowres,
+                       (const float*)highres_prev, (const float*)prefix, idx, im, H_lr, W_lr, n_prefix, D,
+                       mode, (float*)compact, pos_sel, (float*)canvas, alias);
+  else
+    hipLaunchKernelGGL(gather_upsample_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)lowres,
+                       (const bf16_t*)highres_prev, (const bf16_t*)prefix, idx, im, H_lr, W_lr, n_prefix, D,
+                       mode, (bf16_t*)compact, pos_sel, (bf16_t*)canvas, alias);
+  return launch_status(who);
+}
+
+int launch_scatter(const void* out, const int32_t* idx, const ImageRows& im, int B, int64_t k_max, int64_t N,
+                   int64_t D, int dtype, void* canvas, void* stream, const char* who) {
+  const dim3 grid(unsigned(ceil_div(k_max, kRowsPerBlock)), unsigned(B)), block(kWave * kRowsPerBlock);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  TimedLaunch timed("scatter", s);
+  if (dtype == AVITS_F32)
+    hipLaunchKernelGGL(scatter_kernel<float>, grid, block, 0, s, (const float*)out, idx, im, N, D, (float*)canvas);
+  else
+    hipLaunchKernelGGL(scatter_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)out, idx, im, N, D,
+                       (bf16_t*)canvas);
+  return launch_status(who);
+}
+
+}  // namespace
+
 extern "C" int avits_gather_upsample(const void* lowres, const void* highres_prev, const void* prefix,
                                      const int32_t* idx, int64_t k, int32_t H_lr, int32_t W_lr,
                                      int64_t n_prefix, int64_t D, int mode, int dtype, void* compact,
@@ -274,20 +341,10 @@ extern "C" int avits_gather_upsample(const void* lowres, const void* highres_pre
   AVITS_REQUIRE(n_prefix == 0 || prefix, "gather_upsample: null prefix with n_prefix=%lld", (long long)n_prefix);
   AVITS_REQUIRE(n_prefix + k == 0 || compact, "gather_upsample: null compact");
   AVITS_REQUIRE(k == 0 || (idx && pos_sel), "gather_upsample: null idx/pos_sel with k=%lld", (long long)k);
-  const int64_t jobs = n_prefix + k + N;
-  const dim3 grid(unsigned(ceil_div(jobs, kRowsPerBlock))), block(kWave * kRowsPerBlock);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const int alias = canvas == highres_prev;
-  TimedLaunch timed("gather_upsample", s);
-  if (dtype == AVITS_F32)
-    hipLaunchKernelGGL(gather_upsample_kernel<float>, grid, block, 0, s, (const float*)lowres,
-                       (const float*)highres_prev, (const float*)prefix, idx, k, H_lr, W_lr, n_prefix, D,
-                       mode, (float*)compact, pos_sel, (float*)canvas, alias);
-  else
-    hipLaunchKernelGGL(gather_upsample_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)lowres,
-                       (const bf16_t*)highres_prev, (const bf16_t*)prefix, idx, k, H_lr, W_lr, n_prefix, D,
-                       mode, (bf16_t*)compact, pos_sel, (bf16_t*)canvas, alias);
-  return launch_status("gather_upsample");
+  ImageRows im{};
+  im.idx_off[1] = k;
+  return launch_gather(lowres, highres_prev, prefix, idx, im, 1, k, H_lr, W_lr, n_prefix, D, mode, dtype, compact,
+                       pos_sel, canvas, stream, "gather_upsample");
 }
 
 extern "C" int avits_scatter(const void* out, const int32_t* idx, int64_t k, int64_t row_offset, int64_t D,
@@ -300,16 +357,82 @@ extern "C" int avits_scatter(const void* out, const int32_t* idx, int64_t k, int
   AVITS_REQUIRE((D * esz) % 16 == 0, "scatter: a row of D=%lld elements must be a multiple of 16 bytes", (long long)D);
   if (k == 0) return AVITS_OK;
   AVITS_REQUIRE(out && idx && canvas, "scatter: null pointer");
-  const dim3 grid(unsigned(ceil_div(k, kRowsPerBlock))), block(kWave * kRowsPerBlock);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  TimedLaunch timed("scatter", s);
-  if (dtype == AVITS_F32)
-    hipLaunchKernelGGL(scatter_kernel<float>, grid, block, 0, s, (const float*)out, idx, k, row_offset, D,
-                       (float*)canvas);
-  else
-    hipLaunchKernelGGL(scatter_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)out, idx, k, row_offset, D,
-                       (bf16_t*)canvas);
-  return launch_status("scatter");
+  ImageRows im{};
+  im.idx_off[1] = k;
+  im.row_off[0] = row_offset;
+  return launch_scatter(out, idx, im, 1, k, 0, D, dtype, canvas, stream, "scatter");
+}
+
+extern "C" int avits_gather_upsample_batched(const void* lowres, const void* highres_prev, const void* prefix,
+                                             const int32_t* idx, const int64_t* idx_off, int32_t B,
+                                             int32_t H_lr, int32_t W_lr, int64_t n_prefix, int64_t D, int mode,
+                                             int dtype, void* compact, const int64_t* row_off, int32_t* pos,
+                                             void* canvas, void* stream) {
+  AVITS_REQUIRE(B >= 1 && B <= kMaxRelayoutImages, "gather_upsample_batched: B=%d outside [1, %d]", B,
+                kMaxRelayoutImages);
+  AVITS_REQUIRE(idx_off && row_off, "gather_upsample_batched: null idx_off/row_off");
+  AVITS_REQUIRE(H_lr >= 1 && W_lr >= 1, "gather_upsample_batched: H_lr=%d W_lr=%d must be >= 1", H_lr, W_lr);
+  const int64_t N = int64_t(4) * H_lr * W_lr;
+  AVITS_REQUIRE(n_prefix >= 0, "gather_upsample_batched: n_prefix=%lld < 0", (long long)n_prefix);
+  AVITS_REQUIRE(D >= 1, "gather_upsample_batched: D=%lld < 1", (long long)D);
+  AVITS_REQUIRE(mode == AVITS_UP_NEAREST || mode == AVITS_UP_BILINEAR, "gather_upsample_batched: bad mode %d",
+                mode);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "gather_upsample_batched: dtype %d unsupported", dtype);
+  const int64_t esz = dtype == AVITS_F32 ? 4 : 2;
+  AVITS_REQUIRE((D * esz) % 16 == 0,
+                "gather_upsample_batched: a row of D=%lld elements must be a multiple of 16 bytes", (long long)D);
+  AVITS_REQUIRE(idx_off[0] == 0, "gather_upsample_batched: idx_off[0]=%lld, must be 0", (long long)idx_off[0]);
+  ImageRows im{};
+  int64_t k_max = 0;
+  for (int b = 0; b < B; ++b) {
+    const int64_t k = idx_off[b + 1] - idx_off[b];
+    AVITS_REQUIRE(k >= 0 && k <= N, "gather_upsample_batched: image %d selects k=%lld outside [0, N=%lld]", b,
+                  (long long)k, (long long)N);
+    AVITS_REQUIRE(row_off[b] >= 0, "gather_upsample_batched: row_off[%d]=%lld < 0", b, (long long)row_off[b]);
+    im.idx_off[b] = idx_off[b];
+    im.row_off[b] = row_off[b];
+    im.pos_off[b] = row_off[b] + n_prefix;
+    k_max = std::max(k_max, k);
+  }
+  im.idx_off[B] = idx_off[B];
+  AVITS_REQUIRE(lowres && highres_prev && canvas, "gather_upsample_batched: null lowres/highres_prev/canvas");
+  AVITS_REQUIRE(n_prefix == 0 || prefix, "gather_upsample_batched: null prefix with n_prefix=%lld",
+                (long long)n_prefix);
+  AVITS_REQUIRE(n_prefix + k_max == 0 || compact, "gather_upsample_batched: null compact");
+  AVITS_REQUIRE(k_max == 0 || (idx && pos), "gather_upsample_batched: null idx/pos");
+  return launch_gather(lowres, highres_prev, prefix, idx, im, B, k_max, H_lr, W_lr, n_prefix, D, mode, dtype,
+                       compact, pos, canvas, stream, "gather_upsample_batched");
+}
+
+extern "C" int avits_scatter_batched(const void* out, const int32_t* idx, const int64_t* idx_off, int32_t B,
+                                     const int64_t* row_off, int64_t N, int64_t D, int dtype, void* canvas,
+                                     void* stream) {
+  AVITS_REQUIRE(B >= 1 && B <= kMaxRelayoutImages, "scatter_batched: B=%d outside [1, %d]", B,
+                kMaxRelayoutImages);
+  AVITS_REQUIRE(idx_off && row_off, "scatter_batched: null idx_off/row_off");
+  AVITS_REQUIRE(N >= 1 && D >= 1, "scatter_batched: N=%lld and D=%lld must be >= 1", (long long)N, (long long)D);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "scatter_batched: dtype %d unsupported", dtype);
+  const int64_t esz = dtype == AVITS_F32 ? 4 : 2;
+  AVITS_REQUIRE((D * esz) % 16 == 0, "scatter_batched: a row of D=%lld elements must be a multiple of 16 bytes",
+                (long long)D);
+  AVITS_REQUIRE(idx_off[0] == 0, "scatter_batched: idx_off[0]=%lld, must be 0", (long long)idx_off[0]);
+  ImageRows im{};
+  int64_t k_max = 0;
+  for (int b = 0; b < B; ++b) {
+    const int64_t k = idx_off[b + 1] - idx_off[b];
+    AVITS_REQUIRE(k >= 0 && k <= N, "scatter_batched: image %d selects k=%lld outside [0, N=%lld]", b,
+                  (long long)k, (long long)N);
+    AVITS_REQUIRE(row_off[b] >= 0, "scatter_batched: row_off[%d]=%lld < 0", b, (long long)row_off[b]);
+    im.idx_off[b] = idx_off[b];
+    im.row_off[b] = row_off[b];
+    k_max = std::max(k_max, k);
+  }
+  im.idx_off[B] = idx_off[B];
+  if (k_max == 0) return AVITS_OK;
+  AVITS_REQUIRE(out && idx && canvas, "scatter_batched: null pointer");
+  return launch_scatter(out, idx, im, B, k_max, N, D, dtype, canvas, stream, "scatter_batched");
 }
 
 extern "C" int avits_gather_mixed(const void* lowres, const void* prefix, const int32_t* idx, int64_t k,

@@ -326,11 +326,13 @@ class BatchedStep:
       score    S_b from image b's own q, text keys, LSE and features; one
                avits_score_batched launch when the inputs come stacked
       select   avits_select_batched over the B score vectors (k_b each)
-      gather   per image: its text rows into the text area (avits_scatter of
-               the rows), [ref_b; X_prev,b[idx_b]] into its image area
-               (avits_gather_upsample), its canvas filled by upsampling
+      gather   the text rows into the text area (avits_scatter of the
+               rows), [ref_b; X_prev,b[idx_b]] into image b's area and its
+               canvas filled by upsampling (avits_gather_upsample, or one
+               avits_gather_upsample_batched launch for stacked images)
       block    avits_block_forward_batched over the packed rows
-      scatter  per image: canvas_b[idx_b] = its selected output rows
+      scatter  canvas_b[idx_b] = image b's selected output rows (one
+               avits_scatter_batched launch for stacked canvases)
 
     Buffers are allocated once; run() enqueues library calls only.
     """
@@ -364,6 +366,7 @@ class BatchedStep:
         # Row indices of each image's text area in the packed rows (for the text-row copy).
         self.txt_rows = [torch.arange(self.txt_off[b], self.txt_off[b + 1], dtype=i32, device=device)
                          for b in range(Bn)]
+        self.txt_rows_all = torch.arange(T, dtype=i32, device=device)
         d = s.D // s.H
         code = B.BF16 if dtype == torch.bfloat16 else B.F32
         self.ws_score = torch.empty(max(B.avits_score_batched_workspace_bytes(Bn, s.N, s.H), 1), dtype=torch.uint8,
@@ -373,12 +376,17 @@ class BatchedStep:
             dtype=torch.uint8, device=device)
 
     def run(self, latent_q, text_k, row_lse, feat_t, feat_prev, lowres, highres_prev, text, ref, stream=None):
-        """Lists over the images: lowres[b], highres_prev[b] (its canvas,
-        updated in place), text[b] [L, D], ref[b] [R, D] or None.  The score
-        inputs are either lists too (latent_q[b], text_k[b], row_lse[b],
-        feat_t[b], feat_prev[b]; one scoring launch per image) or tensors
-        stacked over the images ([B, N, H, d], [B, L, H, d], [B, H, N],
-        [B, N, D_f] twice; one launch for all)."""
+        """Per-image inputs, given either as lists over the images (one launch
+        per image for that stage) or as tensors stacked over the images (one
+        launch for all):
+
+          score inputs   latent_q [B, N, H, d], text_k [B, L, H, d],
+                         row_lse [B, H, N], feat_t, feat_prev [B, N, D_f]
+          layout inputs  lowres [B, N/4, D], highres_prev [B, N, D] (the
+                         canvases, updated in place), text [B, L, D],
+                         ref [B, R, D] or None
+
+        Lists hold the per-image tensors of the same shapes without the B."""
         import torch
         s = self.shape
         T = self.txt_off[-1]
@@ -392,18 +400,30 @@ class BatchedStep:
                               self.scores[b * s.N:(b + 1) * s.N], workspace=self.ws_score, stream=stream)
         if sum(self.ks):
             B.avits_select_batched(self.scores, [b * s.N for b in range(Bn + 1)], self.ks, self.idx, stream=stream)
-        for b in range(Bn):
+        img_rows = [T + a for a in self.img_off[:-1]]
+        if torch.is_tensor(highres_prev):
             if s.L:
-                B.avits_scatter(text[b], self.txt_rows[b], 0, self.x, stream)
-            a0 = T + self.img_off[b]
-            idx_b = self.idx[self.out_off[b]:self.out_off[b + 1]]
-            B.avits_gather_upsample(lowres[b], highres_prev[b], ref[b] if s.R else None, idx_b, s.H_lr, s.W_lr,
-                                    self.x[a0:a0 + s.R + self.ks[b]], self.pos[a0 + s.R:a0 + s.R + self.ks[b]],
-                                    highres_prev[b], self.mode, stream)
+                B.avits_scatter(text.view(T, s.D), self.txt_rows_all, 0, self.x, stream)
+            B.avits_gather_upsample_batched(lowres, highres_prev, ref if s.R else None, self.idx, self.out_off,
+                                            s.H_lr, s.W_lr, self.x, img_rows, self.pos, highres_prev, self.mode,
+                                            stream)
+        else:
+            for b in range(Bn):
+                if s.L:
+                    B.avits_scatter(text[b], self.txt_rows[b], 0, self.x, stream)
+                a0 = img_rows[b]
+                idx_b = self.idx[self.out_off[b]:self.out_off[b + 1]]
+                B.avits_gather_upsample(lowres[b], highres_prev[b], ref[b] if s.R else None, idx_b, s.H_lr,
+                                        s.W_lr, self.x[a0:a0 + s.R + self.ks[b]],
+                                        self.pos[a0 + s.R:a0 + s.R + self.ks[b]], highres_prev[b], self.mode, stream)
         B.avits_block_forward_batched(self.x, self.x_out, self.pos, self.txt_off, self.img_off, self.weights, s.H,
                                       workspace=self.ws_block, stream=stream)
-        for b in range(Bn):
-            if self.ks[b]:
-                idx_b = self.idx[self.out_off[b]:self.out_off[b + 1]]
-                B.avits_scatter(self.x_out, idx_b, T + self.img_off[b] + s.R, highres_prev[b], stream)
+        if torch.is_tensor(highres_prev):
+            B.avits_scatter_batched(self.x_out, self.idx, self.out_off, [a + s.R for a in img_rows], highres_prev,
+                                    stream)
+        else:
+            for b in range(Bn):
+                if self.ks[b]:
+                    idx_b = self.idx[self.out_off[b]:self.out_off[b + 1]]
+                    B.avits_scatter(self.x_out, idx_b, img_rows[b] + s.R, highres_prev[b], stream)
         return highres_prev

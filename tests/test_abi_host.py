@@ -146,6 +146,43 @@ def test_gather_and_scatter_validation(lib):
     assert s(FAKE, FAKE, 3, 0, 64, 3, FAKE, None) == UNSUPPORTED
 
 
+def test_batched_gather_and_scatter_validation(lib):
+    import ctypes
+    I64 = ctypes.c_int64
+
+    def arr(*v):
+        return (I64 * len(v))(*v)
+
+    g = lib.avits_gather_upsample_batched
+    # (lowres, highres, prefix, idx, idx_off, B, H_lr, W_lr, n_prefix, D, mode, dtype, compact, row_off, pos,
+    #  canvas, stream); N = 16
+    ok = dict(idx_off=arr(0, 3, 5), B=2, row_off=arr(0, 3))
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return g(FAKE, FAKE, None, FAKE, a["idx_off"], a["B"], 2, 2, 0, 64, 0, 1, FAKE, a["row_off"], FAKE, FAKE,
+                 None)
+
+    assert call(B=0) == INVALID
+    assert call(B=65) == INVALID
+    assert call(idx_off=None) == INVALID
+    assert call(idx_off=arr(1, 3, 5)) == INVALID        # idx_off[0] != 0
+    assert call(idx_off=arr(0, 3, 2)) == INVALID        # negative k_b
+    assert call(idx_off=arr(0, 17, 18)) == INVALID      # k_b > N
+    assert call(row_off=arr(0, -1)) == INVALID
+    assert g(FAKE, FAKE, None, FAKE, arr(0, 1), 1, 2, 2, 0, 60, 0, 1, FAKE, arr(0), FAKE, FAKE, None) == INVALID
+    assert g(FAKE, FAKE, None, FAKE, arr(0, 1), 1, 2, 2, 0, 64, 0, 9, FAKE, arr(0), FAKE, FAKE, None) == UNSUPPORTED
+    s = lib.avits_scatter_batched
+    # (out, idx, idx_off, B, row_off, N, D, dtype, canvas, stream)
+    assert s(FAKE, FAKE, arr(0, 2), 0, arr(0), 16, 64, 1, FAKE, None) == INVALID      # B < 1
+    assert s(FAKE, FAKE, arr(0, 17), 1, arr(0), 16, 64, 1, FAKE, None) == INVALID     # k_b > N
+    assert s(FAKE, FAKE, arr(0, 2), 1, arr(-1), 16, 64, 1, FAKE, None) == INVALID     # row_off < 0
+    assert s(None, None, arr(0, 0, 0), 2, arr(0, 0), 16, 64, 1, None, None) == 0      # nothing selected
+    assert s(None, FAKE, arr(0, 2), 1, arr(0), 16, 64, 1, FAKE, None) == INVALID      # null out
+    assert s(FAKE, FAKE, arr(0, 2), 1, arr(0), 16, 64, 3, FAKE, None) == UNSUPPORTED
+
+
 def test_mixed_gather_and_scatter_validation(lib):
     g = lib.avits_gather_mixed
     # (lowres, prefix, idx, k, H_lr, W_lr, n_prefix, D, mode, dtype, compact, pos, children, stream)

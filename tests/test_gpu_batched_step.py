@@ -21,7 +21,7 @@ from _gpu import assert_close, dev, double_weights_dev, host
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("stacked", [False, True], ids=["score_per_image", "score_stacked"])
+@pytest.mark.parametrize("stacked", ["none", "score", "all"], ids=["per_image", "score_stacked", "all_stacked"])
 @pytest.mark.parametrize("base", [C.TINY_BF16, C.TINY_BF16_REF], ids=lambda w: w.name)
 def test_batched_step(gpu, base, stacked):
     ws = [base, base.replace(seed=base.seed + 1, rho=0.45), base.replace(seed=base.seed + 2)]
@@ -39,10 +39,14 @@ def test_batched_step(gpu, base, stacked):
     canvases = [dev(l["highres_prev"], base.dtype) for l in lay]
     score_in = [[dev(s["latent_q"], base.dtype) for s in si], [dev(s["text_k"], base.dtype) for s in si],
                 [dev(x) for x in lse], canvases, [dev(s["feat_prev"], base.dtype) for s in si]]
-    if stacked:  # one scoring launch over the stacked images (feat_t: a copy of the canvases)
+    lay_in = [[dev(l["lowres"], base.dtype) for l in lay], canvases, [dev(l["text"], base.dtype) for l in lay],
+              [dev(l["ref"], base.dtype) for l in lay]]
+    if stacked != "none":  # one scoring launch over the stacked images (feat_t: a copy of the canvases)
         score_in = [torch.stack(t) for t in score_in]
-    step.run(*score_in, [dev(l["lowres"], base.dtype) for l in lay], canvases,
-             [dev(l["text"], base.dtype) for l in lay], [dev(l["ref"], base.dtype) for l in lay])
+    if stacked == "all":   # one gather and one scatter launch for all images, canvases stacked
+        lay_in = [torch.stack(t) if t[0].numel() else None for t in lay_in]
+        canvases = lay_in[1]
+    step.run(*score_in, *lay_in)
     torch.cuda.synchronize()
     scores, idx_all = step.scores.cpu().numpy(), step.idx.cpu().numpy()
     x, pos, x_out = host(step.x), step.pos.cpu().numpy(), host(step.x_out)

@@ -312,6 +312,61 @@ def test_scatter_bitexact(gpu, w):
     np.testing.assert_array_equal(host(t_canvas), oracle.scatter(out, idx, w.LR, lay["highres_prev"]))
 
 
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+@pytest.mark.parametrize("mode,alias", [(0, False), (0, True), (1, False)], ids=["nearest", "nearest_in_place",
+                                                                                 "bilinear"])
+def test_gather_and_scatter_batched(gpu, w, mode, alias):
+    """Three images in one launch each way (k_b = the workload's k, none, all
+    N), their rows placed out of image order with gaps in one packed buffer:
+    every image's rows, positions and canvas equal the oracle's for that image
+    alone (bit-exact; bilinear bf16 within one ulp, as the single launch), and
+    rows between the images are left untouched."""
+    ws = [w.replace(seed=w.seed + i) for i in range(3)]
+    ks = [w.k, 0, w.N]
+    lays = [G.layout_inputs(x) for x in ws]
+    idxs = [G.random_selection(x, k, 7 + i) for i, (x, k) in enumerate(zip(ws, ks))]
+    R = w.R
+    row_off = [R + ks[1] + 5 + R + ks[2] + 3, R + ks[2] + 3, 0]       # image 2 first, then 1, then 0
+    rows = row_off[0] + R + ks[0] + 2
+    idx_off = [0, ks[0], ks[0] + ks[1], sum(ks)]
+    stack = lambda key: torch.stack([dev(l[key], w.dtype) for l in lays])  # noqa: E731
+    low, high = stack("lowres"), stack("highres_prev")
+    pre = stack("ref") if R else None
+    idx = dev(np.concatenate(idxs).astype(np.int32)) if sum(ks) else torch.zeros(1, dtype=torch.int32, device="cuda")
+    compact = torch.full((rows, w.D), 7.0, dtype=low.dtype, device="cuda")
+    pos = torch.full((rows, 3), -1, dtype=torch.int32, device="cuda")
+    canvas = high if alias else torch.full_like(high, 7.0)
+    gpu.avits_gather_upsample_batched(low, high, pre, idx, idx_off, w.H_lr, w.W_lr, compact, row_off, pos, canvas,
+                                      mode=mode)
+    torch.cuda.synchronize()
+    c, p, cv = host(compact), host(pos), host(canvas)
+    touched = np.zeros(rows, bool)
+    for b in range(3):
+        rc, rp, rcv = oracle.gather_upsample(lays[b]["lowres"], lays[b]["highres_prev"], lays[b]["ref"] if R else None,
+                                             idxs[b], w.H_lr, w.W_lr, "nearest" if mode == 0 else "bilinear")
+        a0 = row_off[b]
+        np.testing.assert_array_equal(c[a0:a0 + R + ks[b]], rc, err_msg=f"image {b} rows")
+        np.testing.assert_array_equal(p[a0 + R:a0 + R + ks[b]], rp, err_msg=f"image {b} positions")
+        if mode == 1 and w.dtype == "bf16":
+            assert np.all(np.abs(cv[b] - rcv) <= np.abs(rcv) * 2.0 ** -7 + 1e-30), f"image {b} canvas"
+        elif mode == 1:
+            assert np.abs(cv[b] - rcv).max() < 1e-5, f"image {b} canvas"
+        else:
+            np.testing.assert_array_equal(cv[b], rcv, err_msg=f"image {b} canvas")
+        touched[a0:a0 + R + ks[b]] = True
+    assert np.all(c[~touched] == 7.0) and np.all(p[~touched] == -1)
+    assert np.all(p[[row_off[b] + i for b in range(3) for i in range(R)]] == -1)  # prefix positions are the caller's
+
+    # Scatter the packed rows back: each image's canvas gets its own rows.
+    out = G.block_input(w, rows, 5)
+    canv = stack("highres_prev")
+    gpu.avits_scatter_batched(dev(out, w.dtype), idx, idx_off, [a + R for a in row_off], canv)
+    torch.cuda.synchronize()
+    for b in range(3):
+        np.testing.assert_array_equal(host(canv[b]), oracle.scatter(out, idxs[b], row_off[b] + R,
+                                                                    lays[b]["highres_prev"]), err_msg=f"image {b}")
+
+
 def _block_inputs(w, n_txt, n_img, seed=0):
     x = G.block_input(w, n_txt + n_img, seed)
     g = np.random.default_rng(1000 + seed)
