@@ -26,3 +26,4 @@ from .block import (  # noqa: F401
     layer_norm, rms_norm, rope_angles, apply_rope, attention, gelu_tanh,
     double_block, single_block, block_qk, block_batched,
 )
+from .sampler import linear, final_layer, euler_update, euler_integrate  # noqa: F401
