@@ -412,6 +412,48 @@ int avits_score_from_mass(const float* mass, int32_t H, int32_t count,
                           void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Around the path: the Stage-2 denoising steps of Section 3.2 advance only
+ * the selected tokens, with the Euler rule of Eq. euler applied to their
+ * latents.  Kept in compact form ([k, C], the selected rows in ascending
+ * token order), one Stage-2 step is
+ *     h = avits_linear(z_sel)                 latent -> hidden rows
+ *     blocks on [text; ref; h]                (avits_block_forward ...)
+ *     v = avits_final_layer(image rows)       hidden -> velocity [k, C]
+ *     avits_euler_update(z_sel, v, dt)        z_sel += dt * v
+ * and avits_scatter puts z_sel into the canvas when Stage 2 ends.  The
+ * embedder and the output layer are the model's (FLUX-style: a linear map;
+ * a modulated layer norm and a linear map), not the paper's.
+ *
+ * avits_linear: out[m, n] = sum_k x[m, k] w[n, k] + b[n] (b may be NULL).
+ * x [M, K], w [N, K], b [N], out [M, N], all of dtype, row-major, device
+ * pointers owned by the caller; fp32 accumulation, one rounding.  Requires
+ * 0 <= M < 2^31 (M == 0 enqueues nothing), K a positive multiple of 64, N a
+ * positive multiple of 8.
+ *
+ * avits_final_layer: out = avits_linear(LN(x) * (1 + scale) + shift, w, b)
+ * with LN the layer norm without affine parameters (eps 1e-6, biased
+ * variance, as in the block), mod [2, D] = (shift; scale).  x [M, D],
+ * w [C, D], b [C] or NULL, out [M, C]; D a positive multiple of 64, C of 8.
+ * The normalised rows are rounded to dtype in the workspace
+ * (>= avits_final_layer_workspace_bytes(M, D, dtype)) before the GEMM.
+ *
+ * avits_euler_update: z[i] = z[i] + dt * v[i] for i < n, in fp32, rounded
+ * once to dtype; z updated in place.  z and v 16-byte aligned device
+ * pointers, not overlapping; dt finite (negative when integrating from
+ * t = 1 towards t = 0); n == 0 enqueues nothing.
+ *
+ * Errors: AVITS_ERR_INVALID_ARG for shapes outside the limits or null
+ * pointers, AVITS_ERR_UNSUPPORTED for a dtype other than F32 / BF16,
+ * AVITS_ERR_WORKSPACE for a short workspace.
+ * ---------------------------------------------------------------------- */
+int avits_linear(const void* x, int64_t M, int64_t K, const void* w, const void* b, int64_t N, int dtype,
+                 void* out, void* stream);
+size_t avits_final_layer_workspace_bytes(int64_t M, int64_t D, int dtype);
+int avits_final_layer(const void* x, int64_t M, int64_t D, const void* mod, const void* w, const void* b,
+                      int64_t C, int dtype, void* out, void* workspace, size_t workspace_bytes, void* stream);
+int avits_euler_update(void* z, const void* v, int64_t n, float dt, int dtype, void* stream);
+
+/* ------------------------------------------------------------------------
  * Launch timing (instrumentation for benchmarks; not part of the method).
  * While enabled, every kernel the library enqueues is bracketed by a pair of
  * HIP events on the caller's stream.  avits_timing_read() waits for the
@@ -421,7 +463,8 @@ int avits_score_from_mass(const float* mass, int32_t H, int32_t count,
  * "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
  * "splitk_reduce", "qk_rope", "attention", "joint_lse" (also the
  * statistics pass of avits_joint_attention_stats), "gather_mixed",
- * "scatter_mixed"; "gemm" returns the
+ * "scatter_mixed", "linear", "final_linear" (the GEMM of avits_final_layer;
+ * its layer norm counts as "ln_mod"), "euler"; "gemm" returns the
  * sum of the six GEMM families (the GEMM kernels alone: the split-K
  * reduction that follows a split launch is "splitk_reduce").  Unknown
  * family -> AVITS_ERR_INVALID_ARG.

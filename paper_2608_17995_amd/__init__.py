@@ -17,5 +17,6 @@ from ._binding import (  # noqa: F401
     avits_block_qk_workspace_bytes, avits_block_qk,
     avits_joint_attention_stats, avits_score_from_mass,
     avits_gather_mixed, avits_scatter_mixed,
+    avits_linear, avits_final_layer_workspace_bytes, avits_final_layer, avits_euler_update,
     avits_timing_enable, avits_timing_reset, avits_timing_read,
 )

@@ -65,6 +65,12 @@ _SIGS = {
     "avits_block_qk": (ctypes.c_int, [_c_void_p, _c_void_p, _f32, _i64, _i64, ctypes.POINTER(_BlockWeights), _i32, _i32,
                                       ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, ctypes.c_int, _c_void_p, _c_void_p]),
+    "avits_linear": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _i64, ctypes.c_int, _c_void_p,
+                                    _c_void_p]),
+    "avits_final_layer_workspace_bytes": (_size, [_i64, _i64, ctypes.c_int]),
+    "avits_final_layer": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _c_void_p, _i64, ctypes.c_int,
+                                         _c_void_p, _c_void_p, _size, _c_void_p]),
+    "avits_euler_update": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _f32, ctypes.c_int, _c_void_p]),
     "avits_gather_upsample_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i32,
                                                      _i32, _i32, _i64, _i64, ctypes.c_int, ctypes.c_int, _c_void_p,
                                                      _c_void_p, _c_void_p, _c_void_p, _c_void_p]),
@@ -249,6 +255,44 @@ def avits_gather_upsample(lowres, highres_prev, prefix, idx, H_lr, W_lr, compact
         H_lr, W_lr, n_prefix, lowres.shape[1], mode, _dtype_code(lowres), _dev(compact, "compact", dt),
         _dev(pos_sel, "pos_sel", torch.int32), _dev(canvas, "canvas", dt), _stream(stream)))
     return compact, pos_sel, canvas
+
+
+def avits_linear(x, w, b, out, stream=None):
+    """out [M, N] = x [M, K] w[N, K]^T + b [N] (b may be None)."""
+    M, K = x.shape
+    N = w.shape[0]
+    dt = x.dtype
+    if tuple(w.shape) != (N, K) or tuple(out.shape) != (M, N) or (b is not None and b.numel() != N):
+        raise ValueError("avits_linear: x [M, K], w [N, K], b [N], out [M, N]")
+    _check(load().avits_linear(_dev(x, "x"), M, K, _dev(w, "w", dt), _dev(b, "b", dt), N, _dtype_code(x),
+                               _dev(out, "out", dt), _stream(stream)))
+    return out
+
+
+def avits_final_layer_workspace_bytes(M: int, D: int, dtype: int) -> int:
+    return load().avits_final_layer_workspace_bytes(M, D, dtype)
+
+
+def avits_final_layer(x, mod, w, b, out, workspace=None, stream=None):
+    """out [M, C] = (LN(x) (1 + mod[1]) + mod[0]) w^T + b; x [M, D], mod [2, D]."""
+    M, D = x.shape
+    C = w.shape[0]
+    dt = x.dtype
+    if tuple(mod.shape) != (2, D) or tuple(w.shape) != (C, D) or tuple(out.shape) != (M, C):
+        raise ValueError("avits_final_layer: x [M, D], mod [2, D], w [C, D], out [M, C]")
+    ws, wsp, wsb = _workspace(workspace, avits_final_layer_workspace_bytes(M, D, _dtype_code(x)), x.device)
+    _check(load().avits_final_layer(_dev(x, "x"), M, D, _dev(mod, "mod", dt), _dev(w, "w", dt), _dev(b, "b", dt), C,
+                                    _dtype_code(x), _dev(out, "out", dt), wsp, wsb, _stream(stream)))
+    return out
+
+
+def avits_euler_update(z, v, dt, stream=None):
+    """z += dt * v in place (fp32 arithmetic, one rounding)."""
+    if z.shape != v.shape:
+        raise ValueError("avits_euler_update: z and v must have one shape")
+    _check(load().avits_euler_update(_dev(z, "z"), _dev(v, "v", z.dtype), z.numel(), dt, _dtype_code(z),
+                                     _stream(stream)))
+    return z
 
 
 def _host_i64(values, n, name):

@@ -605,3 +605,120 @@ extern "C" int avits_block_forward_batched(const void* x_in, void* x_out, const 
   return run_block<bf16_t>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, lse_out, ws,
                            static_cast<hipStream_t>(stream), &segs);
 }
+
+// ---------------------------------------------------------------------------
+// Around the path, for the Stage-2 steps of Section 3.2 run on the selected
+// tokens alone: the model's latent embedder (a linear map into the hidden
+// width), its output layer (modulated layer norm, then a linear map back to
+// the latent channels), and the Euler update of Eq. euler on those tokens.
+namespace avits {
+namespace {
+
+// z = z + dt v, computed in fp32 and rounded once; 8 elements per thread.
+template <typename T>
+__global__ __launch_bounds__(256) void euler_kernel(T* __restrict__ z, const T* __restrict__ v, int64_t n,
+                                                    float dt) {
+  const int64_t i0 = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 8;
+  if (i0 >= n) return;
+  if (i0 + 8 <= n) {
+    float a[8], b[8];
+    load8(z, i0, a);
+    load8(v, i0, b);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) a[e] = fmaf(dt, b[e], a[e]);
+    store8(z + i0, a);
+  } else {
+    for (int64_t i = i0; i < n; ++i) st(z, i, fmaf(dt, ld(v, i), ld(z, i)));
+  }
+}
+
+int check_linear(const char* fn, int64_t M, int64_t K, int64_t N, int dtype) {
+  AVITS_REQUIRE(M >= 0 && M <= INT32_MAX, "%s: M=%lld outside [0, 2^31)", fn, (long long)M);
+  AVITS_REQUIRE(K >= 64 && K % 64 == 0, "%s: K=%lld must be a positive multiple of 64", fn, (long long)K);
+  AVITS_REQUIRE(N >= 8 && N % 8 == 0, "%s: N=%lld must be a positive multiple of 8", fn, (long long)N);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16) return set_error(AVITS_ERR_UNSUPPORTED, "%s: dtype %d", fn, dtype);
+  return AVITS_OK;
+}
+
+// out = x W^T + b (plain store epilogue, no split).
+int run_linear(const void* x, int64_t M, int64_t K, const void* w, const void* b, int64_t N, int dtype, void* out,
+               hipStream_t s, const char* family) {
+  GemmArgs g{};
+  g.nprob = 1;
+  g.N = N;
+  g.K = K;
+  g.n_split = g.n_split2 = N;
+  g.mode0 = g.mode1 = g.mode2 = EPI_STORE;
+  GemmProblem& p = g.p[0];
+  p.A = x; p.lda = K; p.W = w; p.bias = b; p.M = M;
+  p.out0 = out; p.ld0 = N;
+  return launch_gemm(g, dtype, s, family, nullptr, 0);
+}
+
+}  // namespace
+}  // namespace avits
+
+extern "C" int avits_linear(const void* x, int64_t M, int64_t K, const void* w, const void* b, int64_t N, int dtype,
+                            void* out, void* stream) {
+  int rc = check_linear("linear", M, K, N, dtype);
+  if (rc != AVITS_OK) return rc;
+  if (M == 0) return AVITS_OK;
+  AVITS_REQUIRE(x && w && out, "linear: null x/w/out");
+  rc = run_linear(x, M, K, w, b, N, dtype, out, static_cast<hipStream_t>(stream), "linear");
+  return rc != AVITS_OK ? rc : launch_status("linear");
+}
+
+extern "C" size_t avits_final_layer_workspace_bytes(int64_t M, int64_t D, int dtype) {
+  if (M < 0 || D < 1 || (dtype != AVITS_F32 && dtype != AVITS_BF16)) return 0;
+  return align_up(size_t(M) * size_t(D) * (dtype == AVITS_F32 ? 4 : 2), 256);
+}
+
+extern "C" int avits_final_layer(const void* x, int64_t M, int64_t D, const void* mod, const void* w, const void* b,
+                                 int64_t C, int dtype, void* out, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  int rc = check_linear("final_layer", M, D, C, dtype);
+  if (rc != AVITS_OK) return rc;
+  if (M == 0) return AVITS_OK;
+  AVITS_REQUIRE(x && mod && w && out, "final_layer: null x/mod/w/out");
+  const size_t need = avits_final_layer_workspace_bytes(M, D, dtype);
+  if (!workspace || workspace_bytes < need)
+    return set_error(AVITS_ERR_WORKSPACE, "final_layer: workspace of %zu bytes, need %zu", workspace_bytes, need);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const dim3 rows_grid(unsigned(ceil_div64(M, 4))), blk(256);
+  {
+    TimedLaunch timed("ln_mod", s);
+    if (dtype == AVITS_BF16) {
+      const bf16_t *sh = static_cast<const bf16_t*>(mod), *sc = sh + D;
+      hipLaunchKernelGGL(ln_mod_kernel<bf16_t>, rows_grid, blk, 0, s, static_cast<const bf16_t*>(x),
+                         static_cast<bf16_t*>(workspace), M, D, M, sh, sc, sh, sc);
+    } else {
+      const float *sh = static_cast<const float*>(mod), *sc = sh + D;
+      hipLaunchKernelGGL(ln_mod_kernel<float>, rows_grid, blk, 0, s, static_cast<const float*>(x),
+                         static_cast<float*>(workspace), M, D, M, sh, sc, sh, sc);
+    }
+  }
+  if ((rc = launch_status("final_layer ln_mod")) != AVITS_OK) return rc;
+  rc = run_linear(workspace, M, D, w, b, C, dtype, out, s, "final_linear");
+  return rc != AVITS_OK ? rc : launch_status("final_layer");
+}
+
+extern "C" int avits_euler_update(void* z, const void* v, int64_t n, float dt, int dtype, void* stream) {
+  AVITS_REQUIRE(n >= 0, "euler_update: n=%lld < 0", (long long)n);
+  AVITS_REQUIRE(std::isfinite(dt), "euler_update: dt=%g is not finite", dt);
+  if (dtype != AVITS_F32 && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "euler_update: dtype %d unsupported", dtype);
+  if (n == 0) return AVITS_OK;
+  AVITS_REQUIRE(z && v, "euler_update: null z/v");
+  AVITS_REQUIRE(reinterpret_cast<uintptr_t>(z) % 16 == 0 && reinterpret_cast<uintptr_t>(v) % 16 == 0,
+                "euler_update: z and v must be 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const dim3 grid(unsigned(ceil_div64(ceil_div64(n, 8), 256)));
+  TimedLaunch timed("euler", s);
+  if (dtype == AVITS_BF16)
+    hipLaunchKernelGGL(euler_kernel<bf16_t>, grid, dim3(256), 0, s, static_cast<bf16_t*>(z),
+                       static_cast<const bf16_t*>(v), n, dt);
+  else
+    hipLaunchKernelGGL(euler_kernel<float>, grid, dim3(256), 0, s, static_cast<float*>(z),
+                       static_cast<const float*>(v), n, dt);
+  return launch_status("euler_update");
+}

@@ -427,3 +427,71 @@ class BatchedStep:
                     idx_b = self.idx[self.out_off[b]:self.out_off[b + 1]]
                     B.avits_scatter(self.x_out, idx_b, img_rows[b] + s.R, highres_prev[b], stream)
         return highres_prev
+
+
+class SelectedEuler:
+    """Stage-2 denoising steps on the selected tokens alone (Section 3.2, with
+    the Euler rule of Eq. euler): their latents stay compact, z_sel [k, C] in
+    ascending token order, and each step runs
+
+      embed    avits_linear: z_sel -> hidden rows behind the prefix
+      blocks   the double blocks, then the single blocks, on [text; ref; rows]
+      output   avits_final_layer on the selected rows -> velocity v [k, C]
+      update   avits_euler_update: z_sel += dt v
+
+    ``finish`` scatters z_sel into the latent canvas (avits_scatter).  The
+    prefix rows (the text and reference hidden states) are rewritten at every
+    step, since the blocks overwrite their buffers.  Buffers are allocated
+    once; step() enqueues library calls only.
+    """
+
+    def __init__(self, k: int, L: int, R: int, C: int, D: int, H: int, mlp_hidden: int, doubles: list,
+                 singles: list, embed_w, embed_b, final_mod, final_w, final_b, pos, dtype, device="cuda"):
+        import torch
+        if k < 1 or not (doubles or singles):
+            raise ValueError("at least one selected token and one block")
+        self.k, self.L, self.R, self.C, self.D, self.H = k, L, R, C, D, H
+        self.doubles, self.singles = list(doubles), list(singles)
+        self.embed_w, self.embed_b = embed_w, embed_b
+        self.final_mod, self.final_w, self.final_b = final_mod, final_w, final_b
+        S = L + R + k
+        self.S = S
+        self.pos = torch.as_tensor(pos, dtype=torch.int32).to(device)
+        if tuple(self.pos.shape) != (S, 3):
+            raise ValueError("pos must hold the positions of [text; ref; selected] rows")
+        self.x = [torch.empty(S, D, dtype=dtype, device=device) for _ in range(2)]
+        self.v = torch.empty(k, C, dtype=dtype, device=device)
+        self.prefix_rows = torch.arange(L + R, dtype=torch.int32, device=device)
+        d = D // H
+        code = B.BF16 if dtype == torch.bfloat16 else B.F32
+        kinds = ([B.BLOCK_DOUBLE] if doubles else []) + ([B.BLOCK_SINGLE] if singles else [])
+        self.ws_block = torch.empty(max(max(B.avits_block_workspace_bytes(kd, S, H, d, mlp_hidden, code)
+                                            for kd in kinds), 1), dtype=torch.uint8, device=device)
+        self.ws_final = torch.empty(max(B.avits_final_layer_workspace_bytes(k, D, code), 1), dtype=torch.uint8,
+                                    device=device)
+        self.last = None  # the buffer holding the last block's output after step()
+
+    def step(self, z_sel, prefix, dt: float, stream=None, on_block=None):
+        """One Euler step of the selected latents z_sel [k, C] (in place);
+        prefix [L + R, D] holds the text and reference hidden rows."""
+        s0 = self.L + self.R
+        if s0:
+            B.avits_scatter(prefix, self.prefix_rows, 0, self.x[0], stream)
+        B.avits_linear(z_sel, self.embed_w, self.embed_b, self.x[0][s0:], stream)
+        cur = 0
+        for i, w in enumerate(self.doubles + self.singles):
+            B.avits_block_forward(self.x[cur], self.x[1 - cur], self.pos, self.L, self.R + self.k, w, self.H,
+                                  workspace=self.ws_block, stream=stream)
+            if on_block is not None:
+                on_block(i, self.x[cur], self.x[1 - cur])
+            cur = 1 - cur
+        self.last = self.x[cur]
+        B.avits_final_layer(self.last[s0:], self.final_mod, self.final_w, self.final_b, self.v,
+                            workspace=self.ws_final, stream=stream)
+        B.avits_euler_update(z_sel, self.v, dt, stream)
+        return z_sel
+
+    def finish(self, z_sel, idx, canvas, stream=None):
+        """canvas[idx[j]] = z_sel[j]: the selected latents back in place."""
+        B.avits_scatter(z_sel, idx, 0, canvas, stream)
+        return canvas

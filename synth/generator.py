@@ -192,6 +192,29 @@ def single_block_weights(w: Workload, block: int) -> dict:
     }
 
 
+LATENT_CHANNELS = 64  # FLUX's packed latent: 16 channels x a 2x2 patch
+
+
+def sampler_weights(w: Workload, C: int = LATENT_CHANNELS) -> dict:
+    """The model's latent embedder (C -> D) and output layer (D -> C) around
+    the blocks: embed_w [D, C], embed_b [D], final_mod [2, D] (shift; scale),
+    final_w [C, D], final_b [C]."""
+    D, dt, s = w.D, w.dtype, w.seed
+    base = 300000
+    return {
+        "embed_w": normal(s, base + 1, (D, C), dt, _wstd(w, C)),
+        "embed_b": normal(s, base + 2, (D,), dt, 0.02),
+        "final_mod": _mod(s, base + 3, 2, D, dt),
+        "final_w": normal(s, base + 4, (C, D), dt, _wstd(w, D)),
+        "final_b": normal(s, base + 5, (C,), dt, 0.02),
+    }
+
+
+def selected_latents(w: Workload, k: int, C: int = LATENT_CHANNELS, tid_offset: int = 0) -> np.ndarray:
+    """Latents of k selected tokens [k, C] ~ N(0, 1) (a noisy latent)."""
+    return normal(w.seed, 300100 + tid_offset, (k, C), w.dtype)
+
+
 def block_input(w: Workload, n_rows: int, tid_offset: int = 0) -> np.ndarray:
     """A stand-alone block input [n_rows, D] ~ N(0, 1)."""
     return normal(w.seed, _TID["x_block"] + tid_offset, (n_rows, w.D), w.dtype)

@@ -130,6 +130,32 @@ def test_score_batched_validation(lib):
     assert call(B=3, ws=None) == WORKSPACE
 
 
+def test_sampler_side_validation(lib):
+    f = lib.avits_linear
+    # (x, M, K, w, b, N, dtype, out, stream)
+    assert f(FAKE, -1, 64, FAKE, None, 8, 1, FAKE, None) == INVALID
+    assert f(FAKE, 4, 60, FAKE, None, 8, 1, FAKE, None) == INVALID        # K not a multiple of 64
+    assert f(FAKE, 4, 64, FAKE, None, 12, 1, FAKE, None) == INVALID       # N not a multiple of 8
+    assert f(FAKE, 4, 64, FAKE, None, 8, 5, FAKE, None) == UNSUPPORTED
+    assert f(None, 0, 64, None, None, 8, 1, None, None) == 0              # M == 0: no-op
+    assert f(None, 4, 64, FAKE, None, 8, 1, FAKE, None) == INVALID
+    g = lib.avits_final_layer
+    need = lib.avits_final_layer_workspace_bytes(16, 128, 1)
+    assert need >= 16 * 128 * 2
+    assert lib.avits_final_layer_workspace_bytes(16, 128, 7) == 0
+    # (x, M, D, mod, w, b, C, dtype, out, ws, wsb, stream)
+    assert g(FAKE, 16, 100, FAKE, FAKE, None, 64, 1, FAKE, FAKE, need, None) == INVALID
+    assert g(FAKE, 16, 128, None, FAKE, None, 64, 1, FAKE, FAKE, need, None) == INVALID
+    assert g(FAKE, 16, 128, FAKE, FAKE, None, 64, 1, FAKE, FAKE, need - 1, None) == WORKSPACE
+    assert g(FAKE, 16, 128, FAKE, FAKE, None, 64, 1, FAKE, None, need, None) == WORKSPACE
+    e = lib.avits_euler_update
+    assert e(FAKE, FAKE, -1, 0.1, 1, None) == INVALID
+    assert e(FAKE, FAKE, 8, float("nan"), 1, None) == INVALID
+    assert e(FAKE, FAKE, 8, 0.1, 3, None) == UNSUPPORTED
+    assert e(None, None, 0, 0.1, 1, None) == 0
+    assert e(FAKE + 2, FAKE, 8, 0.1, 1, None) == INVALID                  # misaligned
+
+
 def test_gather_and_scatter_validation(lib):
     g = lib.avits_gather_upsample
     # k > N (N = 4*2*2 = 16)
