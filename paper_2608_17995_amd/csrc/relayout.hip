@@ -12,22 +12,39 @@ namespace {
 
 constexpr int kRowsPerBlock = 4;  // one wavefront per row job
 
-// Copy `bytes` (multiple of 16) from src to dst with the 64 lanes of a wave,
-// four 16-byte chunks per lane in flight at a time.
+// Row copies by the 64 lanes of a wave: every lane loads up to kCopyBatch
+// 16-byte chunks (lane + 64 u) before storing any, so a row of up to 8 KB is
+// one round trip.  `n` counts 16-byte chunks; i0 is the batch's first chunk.
+constexpr int kCopyBatch = 8;
+__device__ __forceinline__ void load_chunks(const u32x4* __restrict__ s, int n, int i0, int lane,
+                                            u32x4 (&r)[kCopyBatch]) {
+  const u32x4* sl = s + (i0 + lane);  // one 64-bit base; chunk u at +1 KiB u
+  const int left = n - (i0 + lane);
+#pragma unroll
+  for (int u = 0; u < kCopyBatch; ++u)
+    if (u * kWave < left) r[u] = sl[u * kWave];
+}
+__device__ __forceinline__ void store_chunks(u32x4* __restrict__ d, int n, int i0, int lane,
+                                             const u32x4 (&r)[kCopyBatch]) {
+  u32x4* dl = d + (i0 + lane);
+  const int left = n - (i0 + lane);
+#pragma unroll
+  for (int u = 0; u < kCopyBatch; ++u)
+    if (u * kWave < left) dl[u * kWave] = r[u];
+}
+
+// Copy `bytes` (multiple of 16) from src to dst; chunks from `from` on.
 __device__ __forceinline__ void wave_copy_row(const char* __restrict__ src, char* __restrict__ dst,
-                                              int64_t bytes, int lane) {
+                                              int64_t bytes, int lane, int64_t from = 0) {
   const u32x4* s = reinterpret_cast<const u32x4*>(src);
   u32x4* d = reinterpret_cast<u32x4*>(dst);
-  const int64_t n = bytes / 16;
-  int64_t i = lane;
-  for (; i + 3 * kWave < n; i += 4 * kWave) {
-    const u32x4 a = s[i], b = s[i + kWave], c = s[i + 2 * kWave], e = s[i + 3 * kWave];
-    d[i] = a;
-    d[i + kWave] = b;
-    d[i + 2 * kWave] = c;
-    d[i + 3 * kWave] = e;
+  const int n = int(bytes / 16);
+#pragma unroll 1
+  for (int i0 = int(from); i0 < n; i0 += kCopyBatch * kWave) {
+    u32x4 r[kCopyBatch];
+    load_chunks(s, n, i0, lane, r);
+    store_chunks(d, n, i0, lane, r);
   }
-  for (; i < n; i += kWave) d[i] = s[i];
 }
 
 // First position in the ascending idx[0..k) not below p.
@@ -119,9 +136,19 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
   int64_t j = job - n_prefix;
   if (j < k) {
     const int64_t p = idx[j];
-    const char* src = reinterpret_cast<const char*>(highres + p * D);
-    wave_copy_row(src, reinterpret_cast<char*>(compact + (n_prefix + j) * D), row_bytes, lane);
-    if (!canvas_aliases) wave_copy_row(src, reinterpret_cast<char*>(canvas + p * D), row_bytes, lane);
+    // One read of the high-resolution row feeds the compact row and, when
+    // the canvas is a separate buffer, the canvas row.
+    const u32x4* src = reinterpret_cast<const u32x4*>(highres + p * D);
+    u32x4* to_compact = reinterpret_cast<u32x4*>(compact + (n_prefix + j) * D);
+    u32x4* to_canvas = reinterpret_cast<u32x4*>(canvas + p * D);
+    const int n = int(row_bytes / 16);
+#pragma unroll 1
+    for (int i0 = 0; i0 < n; i0 += kCopyBatch * kWave) {
+      u32x4 r[kCopyBatch];
+      load_chunks(src, n, i0, lane, r);
+      store_chunks(to_compact, n, i0, lane, r);
+      if (!canvas_aliases) store_chunks(to_canvas, n, i0, lane, r);
+    }
     if (lane == 0) {
       pos_sel[3 * j + 0] = 0;
       pos_sel[3 * j + 1] = int32_t(p / W_hr);

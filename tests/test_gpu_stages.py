@@ -4,6 +4,8 @@ Each stage's oracle runs on exactly the values the GPU stage consumed (the
 GPU's own upstream outputs copied to the host), so indices and layouts must
 match bit for bit and floats within the parity bar.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -303,6 +305,30 @@ def test_gather_bilinear(gpu, w):
 
 @pytest.mark.parametrize("w", TINY, ids=IDS)
 def test_scatter_bitexact(gpu, w):
+    lay = G.layout_inputs(w)
+    idx = G.random_selection(w, w.k, 3)
+    out = G.block_input(w, w.S, 5)
+    t_canvas = dev(lay["highres_prev"], w.dtype)
+    gpu.avits_scatter(dev(out, w.dtype), dev(idx), w.LR, t_canvas)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(t_canvas), oracle.scatter(out, idx, w.LR, lay["highres_prev"]))
+
+
+# Rows longer than one 8 KiB copy batch (64 lanes x 8 chunks of 16 bytes): a
+# second batch plus a partial tail, so every lane-chunk bound of the row copy
+# is taken.  fp32 D = 2304 is 9216 bytes per row (576 chunks: one full batch,
+# 64 chunks more); bf16 D = 4160 is 8320 bytes (520 chunks: 8 more).
+WIDE = [dataclasses.replace(C.TINY_F32_RAGGED, name="wide_f32_d2304", D=2304, H=3, d=768),
+        dataclasses.replace(C.TINY_F32_RAGGED, name="wide_bf16_d4160", dtype="bf16", D=4160, H=5, d=832)]
+
+
+@pytest.mark.parametrize("w", WIDE, ids=[w.name for w in WIDE])
+def test_gather_and_scatter_wide_rows(gpu, w):
+    for k, alias in ((w.k, False), (w.k, True), (0, False), (w.N, False)):
+        (compact, pos, canvas), (rc, rp, rcv), _ = _gather(gpu, w, k, 0, alias)
+        np.testing.assert_array_equal(compact, rc)
+        np.testing.assert_array_equal(pos, rp)
+        np.testing.assert_array_equal(canvas, rcv)
     lay = G.layout_inputs(w)
     idx = G.random_selection(w, w.k, 3)
     out = G.block_input(w, w.S, 5)
