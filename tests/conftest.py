@@ -33,3 +33,13 @@ def gpu():
     import paper_2608_17995_amd as avits
     avits.load()  # raises if libavits.so is missing
     return avits
+
+
+def pytest_sessionstart(session):
+    # A child run of the oracle pins with one planted mistake (see
+    # tests/oracle_mistakes.py); never set in an ordinary run.
+    name = os.environ.get("AVITS_PLANT_MISTAKE")
+    if name:
+        sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+        import oracle_mistakes
+        oracle_mistakes.plant(name)
