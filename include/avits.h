@@ -134,6 +134,27 @@ int avits_select_perturbed(const float* scores, const float* delta, int64_t N, i
                            int32_t* idx, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_select_noalloc — avits_select for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same selection, bit for bit, with
+ * no workspace argument.  The state of the grid path (N > 16384) lives in
+ * one fixed array of about 260 KiB in the library's device memory, one copy
+ * per GPU, held until the process ends; the call makes no hipMalloc,
+ * hipFree or other allocating call (the first call on a device looks the
+ * array's address up once).  Every call on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (other streams, other threads) race;
+ * calls on one stream are ordered and safe.  The array is re-initialised by
+ * every call, so nothing carries over between calls.
+ * scores [N] fp32, idx [k] int32: device pointers of the calling thread's
+ * current device, owned by the caller.  Requires 1 <= N <=
+ * avits_select_noalloc_max_n() (2^26) and 0 <= k <= N; otherwise
+ * AVITS_ERR_INVALID_ARG and nothing is enqueued.  Other errors as
+ * avits_select.
+ * ---------------------------------------------------------------------- */
+size_t avits_select_noalloc_max_n(void);
+int avits_select_noalloc(const float* scores, int64_t N, int64_t k, int32_t* idx, void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_select_batched — B independent selections in one launch (images of
  * a batch with their own token counts and budgets).  Element b selects the
  * top k[b] of scores[offsets[b] .. offsets[b + 1]) (perturbed by delta over

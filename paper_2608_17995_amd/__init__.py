@@ -12,6 +12,7 @@ from ._binding import (  # noqa: F401
     F32, BF16, UP_NEAREST, UP_BILINEAR, BLOCK_DOUBLE, BLOCK_SINGLE,
     avits_score_workspace_bytes, avits_score, avits_score_batched_workspace_bytes, avits_score_batched,
     avits_select_workspace_bytes, avits_select, avits_select_perturbed, avits_select_batched,
+    avits_select_noalloc, avits_select_noalloc_max_n,
     avits_gather_upsample, avits_scatter, avits_joint_lse, avits_gather_upsample_batched, avits_scatter_batched,
     avits_block_workspace_bytes, avits_block_forward, avits_block_forward_batched, BlockWeights,
     avits_block_qk_workspace_bytes, avits_block_qk,

@@ -47,6 +47,8 @@ _SIGS = {
                                            _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_select_workspace_bytes": (_size, [_i64]),
     "avits_select": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _size, _c_void_p]),
+    "avits_select_noalloc_max_n": (_size, []),
+    "avits_select_noalloc": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p]),
     "avits_select_perturbed": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _c_void_p, _c_void_p, _size,
                                               _c_void_p]),
     "avits_select_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _i32, _c_void_p, _c_void_p, _c_void_p,
@@ -221,6 +223,18 @@ def avits_select(scores, k, idx, workspace=None, stream=None):
     ws, wsp, wsb = _workspace(workspace, avits_select_workspace_bytes(N), scores.device)
     _check(load().avits_select(_dev(scores, "scores", torch.float32), N, k, _dev(idx, "idx", torch.int32),
                                wsp, wsb, _stream(stream)))
+    return idx
+
+
+def avits_select_noalloc_max_n() -> int:
+    return load().avits_select_noalloc_max_n()
+
+
+def avits_select_noalloc(scores, k, idx, stream=None):
+    """avits_select without a workspace (the library's fixed device array)."""
+    import torch
+    _check(load().avits_select_noalloc(_dev(scores, "scores", torch.float32), scores.shape[0], k,
+                                       _dev(idx, "idx", torch.int32), _stream(stream)))
     return idx
 
 

@@ -14,6 +14,8 @@
 // cost is latency, not bandwidth, and the keys stay in registers between
 // passes (each thread holds consecutive elements, so the emission is one
 // workgroup scan).  Larger N runs the same passes grid-wide (below).
+#include <mutex>
+
 #include "common.h"
 
 namespace avits {
@@ -515,6 +517,21 @@ SelWs select_ws_layout(char* base, int64_t N) {
   return w;
 }
 
+// Workspace bytes of the grid path for N scores (select_ws_layout's size,
+// usable in constant expressions).
+constexpr size_t select_ws_bytes(int64_t N) {
+  return (sizeof(SelState) + 255) / 256 * 256 + 2 * ((size_t((N + kChunk - 1) / kChunk) * 8 + 255) / 256 * 256);
+}
+
+// Allocation-free selection: the grid path's state lives in this file-scope
+// device array instead of a caller workspace.  Each GPU holds its own copy
+// until the process ends; its address on a device comes from
+// hipGetSymbolAddress (the array's name is not a device address in host
+// code).
+constexpr int64_t kNoAllocMaxN = int64_t(1) << 26;
+constexpr size_t kNoAllocBytes = select_ws_bytes(kNoAllocMaxN);
+__device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
 constexpr int64_t kOneBlockMax = int64_t(kThreads) * kRegKeys;  // 16384: one workgroup, keys in registers
 
 }  // namespace
@@ -567,6 +584,49 @@ extern "C" int avits_select_perturbed(const float* scores, const float* delta, i
                                       void* workspace, size_t workspace_bytes, void* stream) {
   AVITS_REQUIRE(k == 0 || delta, "select_perturbed: null delta");
   return select_impl(scores, delta, N, k, idx, workspace, workspace_bytes, stream);
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on the calling thread's current device,
+// looked up once per device.
+int scratch_on_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return set_error(AVITS_ERR_HIP, "select_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return set_error(AVITS_ERR_UNSUPPORTED, "select_noalloc: device %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_error(AVITS_ERR_HIP, "select_noalloc: hipGetSymbolAddress on device %d: %s", dev,
+                       hipGetErrorString(e));
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return AVITS_OK;
+}
+}  // namespace
+
+extern "C" size_t avits_select_noalloc_max_n(void) { return size_t(kNoAllocMaxN); }
+
+extern "C" int avits_select_noalloc(const float* scores, int64_t N, int64_t k, int32_t* idx, void* stream) {
+  AVITS_REQUIRE(N >= 1 && N <= kNoAllocMaxN, "select_noalloc: N=%lld outside [1, %lld]", (long long)N,
+                (long long)kNoAllocMaxN);
+  AVITS_REQUIRE(k >= 0 && k <= N, "select_noalloc: k=%lld outside [0, N=%lld]", (long long)k, (long long)N);
+  if (k == 0) return AVITS_OK;
+  AVITS_REQUIRE(scores && idx, "select_noalloc: null scores/idx");
+  if (N <= kOneBlockMax) return select_impl(scores, nullptr, N, k, idx, nullptr, 0, stream);
+  void* ws = nullptr;
+  const int rc = scratch_on_current_device(&ws);
+  if (rc != AVITS_OK) return rc;
+  static_assert(kNoAllocBytes >= select_ws_bytes(kNoAllocMaxN), "scratch holds the largest grid-path state");
+  return select_impl(scores, nullptr, N, k, idx, ws, kNoAllocBytes, stream);
 }
 
 extern "C" int avits_select_batched(const float* scores, const float* delta, int32_t B, const int64_t* offsets,
