@@ -6,8 +6,17 @@ double-stream MMDiT block on the compacted sequence -> scatter, at the
 FLUX-shaped 1024^2 workload (hidden 3072, 24x128 heads, 512 text tokens,
 64x64 high-res latent, keep ratio 0.3 -> k = 1229, S = 1741), bf16 storage
 with fp32 accumulation.  All inputs are resident in HBM before timing; the
-joint log-sum-exp the scorer consumes is produced once beforehand (it is the
-previous step's attention by-product) and timed separately.
+timed steps rotate over four copies of the step's inputs (at different
+addresses), so no step finds its inputs in the 256 MB last-level cache from
+the step before.  The joint log-sum-exp the scorer consumes is produced
+before timing (it is the previous step's attention by-product); a second
+figure times the step with it included.
+
+Further legs in the same run: the step at the Qwen-Image-Edit shape and at
+FLUX 2048^2 over keep ratios 0.1 / 0.3 / 0.5 / 1.0, the FLUX stack (19
+double + 38 single blocks, 4 denoising steps including the probe and the
+joint log-sum-exp), the select sweep, fused scoring, the mixed-resolution
+Stage 2 and the batched legs.
 
 Prints one JSON line.  Usage: python bench.py [--steps K] [--warmup W]
 """
@@ -54,6 +63,38 @@ def measured_traffic() -> dict | None:
                 if line.startswith("traffic_json: "):
                     rec = json.loads(line[len("traffic_json: "):])
                     return rec if rec.get("sources_sha256") == gemm_sources_sha256() else None
+    except OSError:
+        return None
+    return None
+
+
+# HBM traffic of the streaming stages (score, select, gather/upsample,
+# scatter), from the same two counter passes over the step's kernels; reported
+# only while the sources of those kernels hash to what they were then.
+STAGE_TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "stages_flux1024_hbm_traffic.md")
+STAGE_SOURCES = ("score.hip", "select.hip", "relayout.hip", "common.h")
+
+LEGS = ("fused_scoring", "select_sweep", "mixed_stage2", "batched", "workloads", "stack")
+
+
+def sources_sha256(files) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2608_17995_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_stage_traffic() -> dict | None:
+    """Per-stage counter-measured HBM bytes of the FLUX 1024^2 step, or None
+    when there is no summary or its kernels' sources changed since."""
+    try:
+        with open(STAGE_TRAFFIC_PROFILE) as fh:
+            for line in fh:
+                if line.startswith("traffic_json: "):
+                    rec = json.loads(line[len("traffic_json: "):])
+                    return rec if rec.get("sources_sha256") == sources_sha256(STAGE_SOURCES) else None
     except OSError:
         return None
     return None
@@ -128,7 +169,30 @@ def _cpu_baseline(w, host, row_lse, wt, wi):
         pass
     return {"value": round(dt * 1e3, 1), "unit": "ms", "cores": int(threads), "kind": "oracle",
             "sample": f"one full step (score, select, gather/upsample, double block, scatter) of {w.name} "
-                      f"in fp64 NumPy on the host; {os.cpu_count()} CPUs visible"}
+                      f"in fp64 NumPy on the host; {os.cpu_count()} CPUs visible",
+            "cpu_model": _cpu_model(), "cpus_visible": os.cpu_count(),
+            "cpus_usable": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None,
+            "blas": _blas_info()}
+
+
+def _cpu_model() -> str | None:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def _blas_info() -> list:
+    try:
+        from threadpoolctl import threadpool_info
+        return [{"api": i.get("internal_api"), "version": i.get("version"), "threads": i.get("num_threads"),
+                 "library": os.path.basename(i.get("filepath", ""))} for i in threadpool_info()]
+    except Exception:  # pragma: no cover
+        return []
 
 
 def _fused_scoring(avits, torch, w, q, k_all, kt, feat_t, feat_prev, lse, reps: int = 10) -> dict:
@@ -356,12 +420,210 @@ def _batched_step(avits, torch, w, bw, shape, prefix_pos, q, kt, lse, feat, fp, 
     return {"images": 2, "batched_ms": round(t_b, 4), "two_single_ms": round(t_2, 4), "speedup": round(t_2 / t_b, 3)}
 
 
+def _gpu_block_weights(avits, torch, w, gen, kind):
+    """Random-init bf16 weights of one block of the workload's architecture,
+    drawn on the GPU (timing legs only: N(0, 0.02) projections, modulation
+    shifts / scales N(0, 0.02), gates and RMSNorm gains 1 + N(0, 0.02))."""
+    D, F, d = w.D, w.mlp_ratio * w.D, w.d
+
+    def n(*shape, std=0.02, mean=0.0):
+        return (torch.randn(*shape, generator=gen, device="cuda") * std + mean).to(torch.bfloat16)
+
+    def mod(rows):
+        m = torch.randn(rows, D, generator=gen, device="cuda") * 0.02
+        m[2::3] += 1.0
+        return m.to(torch.bfloat16)
+
+    if kind == avits.BLOCK_SINGLE:
+        return avits.BlockWeights(avits.BLOCK_SINGLE, single={
+            "mod": mod(3), "w_in": n(3 * D + F, D), "b_in": n(3 * D + F), "g_q": n(d, mean=1.0),
+            "g_k": n(d, mean=1.0), "w_out": n(D, D + F), "b_out": n(D)})
+
+    def stream():
+        return {"mod": mod(6), "w_qkv": n(3 * D, D), "b_qkv": n(3 * D), "g_q": n(d, mean=1.0), "g_k": n(d, mean=1.0),
+                "w_o": n(D, D), "b_o": n(D), "w_mlp1": n(F, D), "b_mlp1": n(F), "w_mlp2": n(D, F), "b_mlp2": n(D)}
+    return avits.BlockWeights(avits.BLOCK_DOUBLE, txt=stream(), img=stream())
+
+
+def _timed_steps(torch, run, n_sets, steps, warmup, stages=None):
+    """ms per step of run(i) over `steps` steps (input set i % n_sets), after
+    `warmup` untimed steps; with `stages`, also ms per stage from events that
+    run(i, events) records between its stages."""
+    for i in range(warmup):
+        run(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        run(i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    if not stages:
+        return ms, None
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] for _ in range(steps)]
+    for i in range(steps):
+        run(i, evs[i])
+    torch.cuda.synchronize()
+    per = {st: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / steps for j, st in enumerate(stages)}
+    return ms, per
+
+
+STEP_STAGES = ("score", "select", "gather_upsample", "block", "scatter")
+
+
+def _input_sets(torch, base: dict, budget_bytes: float = 512e6, max_sets: int = 4) -> list:
+    """The step's inputs plus copies at other addresses, enough that the
+    inputs of one step are gone from the 256 MB last-level cache when that
+    set comes round again (at most max_sets sets)."""
+    import math
+    nbytes = sum(t.numel() * t.element_size() for t in base.values())
+    n = max(1, min(max_sets, math.ceil(budget_bytes / max(nbytes, 1))))
+    return [base] + [{k: v.clone() for k, v in base.items()} for _ in range(n - 1)]
+
+
+def _workload_legs(avits, torch, steps: int, warmup: int) -> list:
+    """The selective step at the Qwen-Image-Edit shape and at FLUX 2048^2 over
+    its keep ratios: the seeded scoring and layout inputs of the parity
+    tests, random-init weights drawn on the GPU, the joint log-sum-exp made in
+    set-up (and timed on its own).  One record per shape / keep ratio."""
+    import numpy as np
+    from paper_2608_17995_amd.step import SelectiveStep, StepShape
+    from synth import configs as C
+    from synth import generator as G
+
+    out = []
+    for base, rhos in ((C.QWEN_EDIT, (C.QWEN_EDIT.rho,)), (C.FLUX_2048, C.FLUX_2048_RHOS)):
+        w0 = base
+        si = G.score_inputs(w0)
+        lay = G.layout_inputs(w0, si["feat_t"])
+
+        def cuda(a):
+            return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16).cuda()
+
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(w0.seed)
+        bw = _gpu_block_weights(avits, torch, w0, gen, avits.BLOCK_DOUBLE)
+        first = {"q": cuda(si["latent_q"]), "kt": cuda(si["text_k"]), "fp": cuda(si["feat_prev"]),
+                 "high": cuda(lay["highres_prev"]), "low": cuda(lay["lowres"]),
+                 "prefix": cuda(np.concatenate([lay["text"], lay["ref"]])),
+                 "k_all": cuda(np.concatenate([si["text_k"], si["ref_k"], si["latent_k"]])),
+                 "lse": torch.empty(w0.H, w0.N, device="cuda")}
+        del si, lay
+        avits.avits_joint_lse(first["q"], first["k_all"], first["lse"])
+        sets = _input_sets(torch, first)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record()
+        for _ in range(3):
+            avits.avits_joint_lse(first["q"], first["k_all"], first["lse"])
+        e[1].record()
+        torch.cuda.synchronize()
+        lse_ms = e[0].elapsed_time(e[1]) / 3
+        prefix_pos = torch.from_numpy(G.prefix_positions(w0)).cuda()
+        for rho in rhos:
+            w = w0 if rho == w0.rho and base is C.QWEN_EDIT else w0.with_rho(rho)
+            shape = StepShape(N=w.N, H_lr=w.H_lr, W_lr=w.W_lr, L=w.L, R=w.R, k=w.k, D=w.D, H=w.H, D_f=w.Df,
+                              mlp_hidden=w.mlp_ratio * w.D)
+            step = SelectiveStep(shape, bw, prefix_pos, torch.bfloat16, alpha=w.alpha)
+
+            def run(i, ev=None, step=step):
+                st = sets[i % len(sets)]
+                if ev is not None:
+                    ev[0].record()
+                step.score(st["q"], st["kt"], st["lse"], st["high"], st["fp"])
+                if ev is not None:
+                    ev[1].record()
+                step.select()
+                if ev is not None:
+                    ev[2].record()
+                step.gather(st["low"], st["high"], st["prefix"])
+                if ev is not None:
+                    ev[3].record()
+                step.block()
+                if ev is not None:
+                    ev[4].record()
+                step.scatter(st["high"])
+                if ev is not None:
+                    ev[5].record()
+
+            ms, per = _timed_steps(torch, run, len(sets), steps, warmup, STEP_STAGES)
+            fl = block_flops(w.S, w.D, w.mlp_ratio * w.D)
+            by = stage_bytes(w)
+            out.append({
+                "workload": w.name, "N": w.N, "L": w.L, "R": w.R, "k": w.k, "seq_len": w.S,
+                "ms_per_step": round(ms, 4), "tokens_per_s": round(w.S / (ms / 1e3), 1),
+                "canvas_tokens_per_s": round(w.N / (ms / 1e3), 1),
+                "ms_per_step_with_joint_lse": round(ms + lse_ms, 4), "joint_lse_ms": round(lse_ms, 4),
+                "stages_ms": {k: round(v, 4) for k, v in per.items()},
+                "block_tflops": round(fl["total"] / (per["block"] / 1e3) / 1e12, 1),
+                "block_mfma_frac": round(fl["total"] / (per["block"] / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                "hbm_gbs": {k: round(by[k] / (per[k] / 1e3) / 1e9, 1)
+                            for k in ("score", "select", "gather_upsample", "scatter") if per[k] > 0},
+                "input_sets": len(sets)})
+            del step
+        del sets, first, bw
+        torch.cuda.empty_cache()
+    return out
+
+
+def _stack_leg(avits, torch) -> dict:
+    """The FLUX stack at the resolution transition (19 double + 38 single
+    blocks, 512 text tokens, 32x32 -> 64x64, k = 1229): 4 denoising steps,
+    each probe (double block 0's first stage on every image row) -> joint
+    log-sum-exp -> score -> select -> gather -> 57 blocks -> scatter.
+    Random-init weights drawn on the GPU; seeded features."""
+    import numpy as np
+    from paper_2608_17995_amd.step import StackStep, StepShape
+    from synth import configs as C
+    from synth import generator as G
+
+    w = C.FLUX_STACK
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(w.seed)
+    doubles = [_gpu_block_weights(avits, torch, w, gen, avits.BLOCK_DOUBLE) for _ in range(w.n_double)]
+    singles = [_gpu_block_weights(avits, torch, w, gen, avits.BLOCK_SINGLE) for _ in range(w.n_single)]
+
+    def cuda(a):
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16).cuda()
+
+    x0, x_m1, _ = G.feature_pair(w.seed, w.N, w.D, w.dtype)
+    lay = G.layout_inputs(w, x0)
+    low, text = cuda(lay["lowres"]), cuda(lay["text"])
+    shape = StepShape(N=w.N, H_lr=w.H_lr, W_lr=w.W_lr, L=w.L, R=w.R, k=w.k, D=w.D, H=w.H, D_f=w.Df,
+                      mlp_hidden=w.mlp_ratio * w.D)
+    st = StackStep(shape, doubles, singles, torch.from_numpy(G.prefix_positions(w)).cuda(), torch.bfloat16,
+                   alpha=w.alpha)
+    xs = [cuda(x_m1), cuda(x0)] + [torch.empty(w.N, w.D, dtype=torch.bfloat16, device="cuda")
+                                   for _ in range(w.steps)]
+    warm = torch.empty_like(xs[0])
+    st.run(xs[1], xs[0], low, text, warm)           # warm-up step (untimed)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(w.steps + 1)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    for s in range(w.steps):
+        st.run(xs[s + 1], xs[s], low, text, xs[s + 2])
+        ev[s + 1].record()
+    torch.cuda.synchronize()
+    total = (time.perf_counter() - t0) * 1e3
+    per = [ev[s].elapsed_time(ev[s + 1]) for s in range(w.steps)]
+    fl_blocks = (w.n_double + w.n_single) * block_flops(w.S, w.D, w.mlp_ratio * w.D)["total"]
+    fl_probe = 2 * (w.L + w.N) * w.D * 2 * w.D + 2 * w.N * (w.L + w.N) * w.D   # q/k projection + joint LSE
+    mean = sum(per) / len(per)
+    return {"workload": w.name, "blocks": w.n_double + w.n_single, "steps": w.steps, "k": w.k, "seq_len": w.S,
+            "ms_per_denoise_step": [round(x, 3) for x in per], "ms_per_denoise_step_mean": round(mean, 3),
+            "ms_total_4_steps": round(total, 3),
+            "tflops": round((fl_blocks + fl_probe) / (mean / 1e3) / 1e12, 1),
+            "includes": "probe (double block 0's q/k on all image rows), joint log-sum-exp, score, select, "
+                        "gather, 19 double + 38 single blocks, scatter"}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--legs", default="all",
+                    help="legs after the headline step: all, none, or a comma list of " + ", ".join(LEGS))
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 512 MiB device-to-device copy (a kernel of known traffic, the "
                          "reference for scaling FETCH_SIZE / WRITE_SIZE counters)")
@@ -429,36 +691,54 @@ def main(argv=None):
     torch.cuda.synchronize()
     joint_lse_ms = ev[0].elapsed_time(ev[1]) / 5
 
-    stages = ("score", "select", "gather_upsample", "block", "scatter")
+    stages = STEP_STAGES
+    # Four copies of the step's inputs at different addresses; step i reads
+    # set i % 4 (and updates that set's canvas in place).
+    sets = _input_sets(torch, {"q": q, "kt": kt, "fp": fp, "high": high, "low": low, "text": text,
+                               "k_all": k_all, "lse": lse}, max_sets=4)
+    if len(sets) < 4:
+        sets += [{k: v.clone() for k, v in sets[0].items()} for _ in range(4 - len(sets))]
 
-    def run_step(events=None):
-        def mark(i):
+    def run_step(i=0, events=None, with_lse=False):
+        st = sets[i % len(sets)]
+
+        def mark(j):
             if events is not None:
-                events[i].record()
+                events[j].record()
+        if with_lse:
+            avits.avits_joint_lse(st["q"], st["k_all"], st["lse"])
         mark(0)
-        step.score(q, kt, lse, high, fp)
+        step.score(st["q"], st["kt"], st["lse"], st["high"], st["fp"])
         mark(1)
         step.select()
         mark(2)
-        step.gather(low, high, text)
+        step.gather(st["low"], st["high"], st["text"])
         mark(3)
         step.block()
         mark(4)
-        step.scatter(high)
+        step.scatter(st["high"])
         mark(5)
 
-    for _ in range(args.warmup):
-        run_step()
+    for i in range(args.warmup):
+        run_step(i)
     torch.cuda.synchronize()
 
     # Timed region 1: K steps, nothing but the step's own launches -> value.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        run_step()
+    for i in range(args.steps):
+        run_step(i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
+
+    # Timed region 1b: the same steps with the joint log-sum-exp of each
+    # step's queries over its [text; image] keys made inside the step.
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        run_step(i, with_lse=True)
+    torch.cuda.synchronize()
+    ms_with_lse = (time.perf_counter() - t0) * 1e3 / args.steps
 
     # Timed region 2: the same K steps with stage events on the stream and the
     # library's own HIP events around every internal launch -> per-stage and
@@ -469,7 +749,7 @@ def main(argv=None):
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     for i in range(args.steps):
-        run_step(step_events[i])
+        run_step(i, step_events[i])
     torch.cuda.synchronize()
     t3 = time.perf_counter()
     avits.avits_timing_enable(False)
@@ -512,6 +792,8 @@ def main(argv=None):
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
         "ms_per_step_instrumented": round(ms_instrumented, 4),
+        "ms_per_step_with_joint_lse": round(ms_with_lse, 4),
+        "input_sets": len(sets),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -546,6 +828,7 @@ def main(argv=None):
         "hbm_gbs": {s: gbs(by[s], stage_ms[s]) for s in ("score", "select", "gather_upsample", "scatter")},
         "hbm_frac": {s: (round(gbs(by[s], stage_ms[s]) / PEAK_HBM_GBS, 4) if stage_ms[s] > 0 else None)
                      for s in ("score", "select", "gather_upsample", "scatter")},
+        "stage_traffic": measured_stage_traffic(),
         "algorithmic_bytes": by,
         "tokens_per_s": round(S / (ms_per_step / 1e3), 1),
         "canvas_tokens_per_s": round(w.N / (ms_per_step / 1e3), 1),
@@ -553,12 +836,23 @@ def main(argv=None):
         "input_generation_s": round(t_gen, 1),
         "copy_calibration_ms": None if copy_ms is None else round(copy_ms, 4),
     }
-    result["fused_scoring"] = _fused_scoring(avits, torch, w, q, k_all, kt, high, fp, lse)
-    result["select_sweep"] = _select_sweep(avits, torch)
-    result["mixed_stage2"] = _mixed_stage2(avits, torch, w, text, bw)
-    result["batched_block"] = _batched_block(avits, torch, w, bw, step.compact)
-    result["batched_step"] = _batched_step(avits, torch, w, bw, shape, torch.from_numpy(G.prefix_positions(w)).cuda(),
-                                           q, kt, lse, high, fp, low, cuda(lay["text"]), cuda(lay["ref"]), step)
+    legs = set(LEGS) if args.legs == "all" else set() if args.legs == "none" else set(args.legs.split(","))
+    if "fused_scoring" in legs:
+        result["fused_scoring"] = _fused_scoring(avits, torch, w, q, k_all, kt, high, fp, lse)
+    if "select_sweep" in legs:
+        result["select_sweep"] = _select_sweep(avits, torch)
+    if "mixed_stage2" in legs:
+        result["mixed_stage2"] = _mixed_stage2(avits, torch, w, text, bw)
+    if "batched" in legs:
+        result["batched_block"] = _batched_block(avits, torch, w, bw, step.compact)
+        result["batched_step"] = _batched_step(avits, torch, w, bw, shape,
+                                               torch.from_numpy(G.prefix_positions(w)).cuda(), q, kt, lse, high, fp,
+                                               low, cuda(lay["text"]), cuda(lay["ref"]), step)
+    del sets
+    if "workloads" in legs:
+        result["workloads"] = _workload_legs(avits, torch, max(5, args.steps // 2), 2)
+    if "stack" in legs:
+        result["stack"] = _stack_leg(avits, torch)
     if not args.no_cpu_baseline:
         host = dict(si)
         host.update(lay)
