@@ -27,3 +27,6 @@ from .block import (  # noqa: F401
     double_block, single_block, block_qk, block_batched,
 )
 from .sampler import linear, final_layer, euler_update, euler_integrate  # noqa: F401
+from .noise import (  # noqa: F401
+    philox4x32_10, box_muller, pixel_noise_bits, pixel_noise, block_noise, halfunit_noise, reinject,
+)

@@ -82,6 +82,20 @@ MISTAKES = {
     "positions_row_col_swapped": ("oracle.relayout", "selected_positions",
                                   [("pos[:, 1] = idx // W_hr\n    pos[:, 2] = idx % W_hr",
                                     "pos[:, 2] = idx // W_hr\n    pos[:, 1] = idx % W_hr")]),
+    # coordinate-bound noise
+    "philox_key_bumped_before_first_round": ("oracle.noise", "philox4x32_10", [("        if r:\n", "        if r >= 0:\n")]),
+    "philox_products_swapped": ("oracle.noise", "philox4x32_10",
+                                [("hi1 ^ x1 ^ k0, lo1, hi0 ^ x3 ^ k1, lo0", "hi0 ^ x1 ^ k0, lo0, hi1 ^ x3 ^ k1, lo1")]),
+    "uniform_without_half": ("oracle.noise", "uniform24", [("+ 0.5) * 2.0 ** -24", ") * 2.0 ** -24")]),
+    "box_muller_cos_sin_swapped": ("oracle.noise", "box_muller",
+                                   [("out[:, a] = r * np.cos(th)", "out[:, a] = r * np.sin(th)"),
+                                    ("out[:, a + 1] = r * np.sin(th)", "out[:, a + 1] = r * np.cos(th)")]),
+    "noise_channel_counter_word": ("oracle.noise", "pixel_noise_bits",
+                                   [("ctr[:, :, 1] = j[None, :]", "ctr[:, :, 2] = j[None, :]")]),
+    "block_noise_plain_mean": ("oracle.noise", "block_noise", [("return acc / 2.0", "return acc / 4.0")]),
+    "reinject_weights_swapped": ("oracle.noise", "reinject",
+                                 [("(1.0 - float(t)) * np.asarray(x, dtype=np.float64) + float(t) * np.asarray(eps",
+                                   "float(t) * np.asarray(x, dtype=np.float64) + (1.0 - float(t)) * np.asarray(eps")]),
     # sampler
     "final_layer_without_one": ("oracle.sampler", "final_layer", [("(1.0 + _f64(scale))", "_f64(scale)")]),
     "euler_sign": ("oracle.sampler", "euler_update", [("_f64(z) + float(dt)", "_f64(z) - float(dt)")]),
