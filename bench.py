@@ -74,7 +74,7 @@ def measured_traffic() -> dict | None:
 STAGE_TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "stages_flux1024_hbm_traffic.md")
 STAGE_SOURCES = ("score.hip", "select.hip", "relayout.hip", "common.h")
 
-LEGS = ("fused_scoring", "select_sweep", "mixed_stage2", "batched", "workloads", "stack")
+LEGS = ("fused_scoring", "block_mass", "select_sweep", "mixed_stage2", "batched", "workloads", "stack")
 
 
 def sources_sha256(files) -> str:
@@ -333,6 +333,43 @@ def _mixed_stage2(avits, torch, w, text, bw, reps: int = 10) -> dict:
         "scatter_mixed_gbs": round(scatter_bytes / (s_us / 1e6) / 1e9, 1) if s_us > 0 else None,
         "gather_mixed_bytes": gather_bytes, "scatter_mixed_bytes": scatter_bytes,
     }
+
+
+def _block_mass(avits, torch, w, bw, x, pos, reps: int = 10) -> dict:
+    """The block with the text attention mass taken inside its own joint
+    attention (avits_block_forward_ex, Section 3.3.1) against the plain
+    block, on the step's compacted rows: the cost of the spatial signal when
+    it comes from the backbone's attention pass itself."""
+    S = x.shape[0]
+    out = torch.empty_like(x)
+    mass = torch.zeros(w.H, S, device="cuda")
+    ws = torch.empty(avits.avits_block_workspace_bytes(avits.BLOCK_DOUBLE, S, w.H, w.d, w.mlp_ratio * w.D,
+                                                       avits.BF16), dtype=torch.uint8, device="cuda")
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record()
+        for _ in range(reps):
+            fn()
+        e[1].record()
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / reps
+
+    def plain():
+        avits.avits_block_forward(x, out, pos, w.L, S - w.L, bw, w.H, workspace=ws)
+
+    def with_mass():
+        avits.avits_block_forward_ex(x, out, pos, w.L, S - w.L, bw, w.H, mass_out=mass, mass_accumulate=True,
+                                     workspace=ws)
+
+    t_p, t_m = float("inf"), float("inf")
+    for _ in range(3):
+        t_p = min(t_p, timed(plain))
+        t_m = min(t_m, timed(with_mass))
+    return {"plain_ms": round(t_p, 4), "with_mass_ms": round(t_m, 4), "overhead": round(t_m / t_p - 1.0, 4)}
 
 
 def _batched_block(avits, torch, w, bw, x, reps: int = 10) -> dict:
@@ -839,6 +876,8 @@ def main(argv=None):
     legs = set(LEGS) if args.legs == "all" else set() if args.legs == "none" else set(args.legs.split(","))
     if "fused_scoring" in legs:
         result["fused_scoring"] = _fused_scoring(avits, torch, w, q, k_all, kt, high, fp, lse)
+    if "block_mass" in legs:
+        result["block_mass"] = _block_mass(avits, torch, w, bw, step.compact, step.pos)
     if "select_sweep" in legs:
         result["select_sweep"] = _select_sweep(avits, torch)
     if "mixed_stage2" in legs:

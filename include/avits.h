@@ -184,6 +184,8 @@ int avits_select_batched(const float* scores, const float* delta, int32_t B, con
  * lowres [H_lr*W_lr, D], highres_prev [N, D], prefix [n_prefix, D] (may be
  * NULL when n_prefix == 0), compact [n_prefix + k, D], pos_sel [k, 3] int32,
  * canvas [N, D].  The caller writes the prefix rows' positions itself.
+ * An idx entry outside [0, N) is skipped on the device (its compact row
+ * and position are left unwritten), so no access leaves the buffers.
  * ---------------------------------------------------------------------- */
 int avits_gather_upsample(const void* lowres, const void* highres_prev, const void* prefix,
                           const int32_t* idx, int64_t k, int32_t H_lr, int32_t W_lr,
@@ -281,6 +283,33 @@ int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, float
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_block_forward_ex — avits_block_forward with optional statistics of
+ * its joint attention, taken inside the same pass (Section 3.3.1: the
+ * attention maps of the backbone's own blocks are the spatial signal, Eq.
+ * spatial with the softmax of Eq. dit_attn):
+ *   lse[h, r]   = log sum_j exp(q_rh . k_jh / sqrt d)          (natural log)
+ *   mass[h, r] (+)= sum_{j < n_txt} softmax_j(q_rh . k_jh / sqrt d)
+ * over all S keys, j < n_txt being the text rows that lead the sequence.
+ * The text mass is tracked beside the softmax normaliser under the same
+ * running maximum, so it costs no second Q K^T pass.  With
+ * mass_accumulate != 0 it is added to what `mass` holds (the aggregation
+ * over blocks and collection steps of Section 3.3.1; avits_score_from_mass
+ * divides by their count).  outs may be NULL (= avits_block_forward without
+ * lse).  lse and mass [H, S] fp32 device buffers or NULL; other arguments
+ * and errors as avits_block_forward.
+ * ---------------------------------------------------------------------- */
+typedef struct avits_block_outputs {
+  float* lse;               /* [H, S] or NULL */
+  float* mass;              /* [H, S] or NULL */
+  int32_t mass_accumulate;  /* nonzero: mass += this block's mass */
+} avits_block_outputs;
+
+int avits_block_forward_ex(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,
+                           int64_t n_txt, int64_t n_img, const avits_block_weights* w,
+                           int32_t H, int32_t d, int dtype, const avits_block_outputs* outs,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_block_forward_batched — B images through one block in one pass: the
  * rows of all images are packed by stream, the text rows of images 0..B-1
  * first (image b's at [txt_off[b], txt_off[b+1])), then their image rows
@@ -322,12 +351,15 @@ int avits_block_qk(const void* x_in, const int32_t* pos, float pos_scale, int64_
                    void* stream);
 
 /* ------------------------------------------------------------------------
- * avits_scatter — Stage-3 re-layout: canvas[idx[j]] = out[row_offset + j]
- * for j < k.  out [row_offset + k, D], idx [k] int32 (unique, < rows of
- * canvas), canvas [*, D].  k == 0 enqueues nothing.
+ * avits_scatter — Stage-3 re-layout (Section 3.2): canvas[idx[j]] =
+ * out[row_offset + j] for j < k.  out [row_offset + k, D], idx [k] int32
+ * (unique, in [0, n_canvas)), canvas [n_canvas, D].  An index outside
+ * [0, n_canvas) is skipped on the device (its row is not written), so no
+ * access leaves the canvas.  k == 0 enqueues nothing.  Requires
+ * n_canvas >= 1.
  * ---------------------------------------------------------------------- */
 int avits_scatter(const void* out, const int32_t* idx, int64_t k, int64_t row_offset,
-                  int64_t D, int dtype, void* canvas, void* stream);
+                  int64_t D, int64_t n_canvas, int dtype, void* canvas, void* stream);
 
 /* ------------------------------------------------------------------------
  * avits_scatter_batched — the Stage-3 re-layout for B images in one launch:
@@ -475,6 +507,39 @@ int avits_final_layer(const void* x, int64_t M, int64_t D, const void* mod, cons
 int avits_euler_update(void* z, const void* v, int64_t n, float dt, int dtype, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_noise_reinject — coordinate-bound noise re-injection (Section 3.2:
+ * into the mixed-resolution sequence when Stage 2 starts, into the full
+ * grid when Stage 3 starts): for each of `rows` rows of x [rows, C],
+ *   x[r] <- (1 - t) x[r] + t eps(row r's coordinate)
+ * in fp32, rounded once to dtype (t == 1 writes eps without reading x).
+ * eps is one fixed standard-normal field over the H_hr x W_hr high-res grid:
+ * channel c of pixel p (raster index) is the Box-Muller normal of word c % 4
+ * of Philox-4x32-10 (Salmon et al., SC 2011) at counter (p, c / 4, 0, 0)
+ * and key (seed low 32 bits, seed high 32 bits), uniforms
+ * (w >> 8 + 1/2) 2^-24, words (0, 1) -> channels (4j, 4j + 1) as
+ * (r cos 2 pi u1, r sin 2 pi u1) with r = sqrt(-2 ln u0), words (2, 3) ->
+ * (4j + 2, 4j + 3).  A low-res token (a 2x2 block) takes the sum of its four
+ * children's noise halved.  A row's coordinate, by rows_kind:
+ *   0  raster rows of the high-res grid (row r = pixel r; rows <= H_hr W_hr)
+ *   1  positions in half units, pos [rows, 3] int32 (frame, Y, X), as
+ *      avits_gather_mixed writes them: even (Y, X) = pixel (Y/2, X/2), odd
+ *      (Y, X) = (4r+1, 4c+1) = low-res block (r, c)
+ *   2  raster rows of the low-res grid (row r = block r; rows <=
+ *      H_hr W_hr / 4): the downsampled noise, e.g. Stage 1's initial latent
+ * x device pointer [rows, C] (dtype), C a positive multiple of 4; pos device
+ * pointer (kind 1) or NULL.  Requires even H_hr, W_hr >= 2, 0 <= t <= 1.
+ * rows == 0 enqueues nothing.
+ *
+ * avits_noise_bits — the generator's raw stream for the parity checks:
+ * bits[i, c] = word c % 4 of Philox-4x32-10 at counter (first_pixel + i,
+ * c / 4, 0, 0), key as above; bits [n_pixels, C] uint32 device pointer.
+ * ---------------------------------------------------------------------- */
+int avits_noise_reinject(void* x, int64_t rows, int64_t C, const int32_t* pos, int32_t rows_kind,
+                         int32_t H_hr, int32_t W_hr, float t, uint64_t seed, int dtype, void* stream);
+int avits_noise_bits(int64_t first_pixel, int64_t n_pixels, int64_t C, uint64_t seed, uint32_t* bits,
+                     void* stream);
+
+/* ------------------------------------------------------------------------
  * Launch timing (instrumentation for benchmarks; not part of the method).
  * While enabled, every kernel the library enqueues is bracketed by a pair of
  * HIP events on the caller's stream.  avits_timing_read() waits for the
@@ -485,7 +550,7 @@ int avits_euler_update(void* z, const void* v, int64_t n, float dt, int dtype, v
  * "splitk_reduce", "qk_rope", "attention", "joint_lse" (also the
  * statistics pass of avits_joint_attention_stats), "gather_mixed",
  * "scatter_mixed", "linear", "final_linear" (the GEMM of avits_final_layer;
- * its layer norm counts as "ln_mod"), "euler"; "gemm" returns the
+ * its layer norm counts as "ln_mod"), "euler", "noise"; "gemm" returns the
  * sum of the six GEMM families (the GEMM kernels alone: the split-K
  * reduction that follows a split launch is "splitk_reduce").  Unknown
  * family -> AVITS_ERR_INVALID_ARG.

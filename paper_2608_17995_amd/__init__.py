@@ -14,10 +14,12 @@ from ._binding import (  # noqa: F401
     avits_select_workspace_bytes, avits_select, avits_select_perturbed, avits_select_batched,
     avits_select_noalloc, avits_select_noalloc_max_n,
     avits_gather_upsample, avits_scatter, avits_joint_lse, avits_gather_upsample_batched, avits_scatter_batched,
-    avits_block_workspace_bytes, avits_block_forward, avits_block_forward_batched, BlockWeights,
+    avits_block_workspace_bytes, avits_block_forward, avits_block_forward_ex, avits_block_forward_batched,
+    BlockWeights,
     avits_block_qk_workspace_bytes, avits_block_qk,
     avits_joint_attention_stats, avits_score_from_mass,
     avits_gather_mixed, avits_scatter_mixed,
     avits_linear, avits_final_layer_workspace_bytes, avits_final_layer, avits_euler_update,
+    avits_noise_reinject, avits_noise_bits, NOISE_RASTER, NOISE_HALF_UNITS, NOISE_LOWRES,
     avits_timing_enable, avits_timing_reset, avits_timing_read,
 )

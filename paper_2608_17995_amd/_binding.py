@@ -29,6 +29,10 @@ class _Single(ctypes.Structure):
     _fields_ = [(n, _c_void_p) for n in ("mod", "w_in", "b_in", "g_q", "g_k", "w_out", "b_out")]
 
 
+class _BlockOutputs(ctypes.Structure):
+    _fields_ = [("lse", ctypes.c_void_p), ("mass", ctypes.c_void_p), ("mass_accumulate", ctypes.c_int32)]
+
+
 class _BlockWeights(ctypes.Structure):
     _fields_ = [("kind", _i32), ("mlp_hidden", _i32), ("txt", _DoubleStream), ("img", _DoubleStream),
                 ("single", _Single)]
@@ -60,13 +64,20 @@ _SIGS = {
     "avits_block_forward": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _f32, _i64, _i64,
                                            ctypes.POINTER(_BlockWeights), _i32, _i32, ctypes.c_int, _c_void_p,
                                            _c_void_p, _size, _c_void_p]),
+    "avits_block_forward_ex": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _f32, _i64, _i64,
+                                              ctypes.POINTER(_BlockWeights), _i32, _i32, ctypes.c_int,
+                                              ctypes.POINTER(_BlockOutputs), _c_void_p, _size, _c_void_p]),
+    "avits_noise_reinject": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _i32, _f32,
+                                            ctypes.c_uint64, ctypes.c_int, _c_void_p]),
+    "avits_noise_bits": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_uint64, _c_void_p, _c_void_p]),
     "avits_block_forward_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _f32, _i32, _c_void_p, _c_void_p,
                                                    ctypes.POINTER(_BlockWeights), _i32, _i32, ctypes.c_int,
                                                    _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_block_qk_workspace_bytes": (_size, [_i64, _i32, _i32, ctypes.c_int]),
     "avits_block_qk": (ctypes.c_int, [_c_void_p, _c_void_p, _f32, _i64, _i64, ctypes.POINTER(_BlockWeights), _i32, _i32,
                                       ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _size, _c_void_p]),
-    "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, ctypes.c_int, _c_void_p, _c_void_p]),
+    "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, _i64, ctypes.c_int, _c_void_p,
+                                     _c_void_p]),
     "avits_linear": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _i64, ctypes.c_int, _c_void_p,
                                     _c_void_p]),
     "avits_final_layer_workspace_bytes": (_size, [_i64, _i64, ctypes.c_int]),
@@ -353,7 +364,8 @@ def avits_scatter_batched(out, idx, idx_off, row_off, canvas, stream=None):
 def avits_scatter(out, idx, row_offset, canvas, stream=None):
     import torch
     _check(load().avits_scatter(_dev(out, "out"), _dev(idx, "idx", torch.int32), idx.shape[0], row_offset,
-                                out.shape[1], _dtype_code(out), _dev(canvas, "canvas", out.dtype), _stream(stream)))
+                                out.shape[1], canvas.shape[0], _dtype_code(out), _dev(canvas, "canvas", out.dtype),
+                                _stream(stream)))
     return canvas
 
 
@@ -443,6 +455,50 @@ def avits_block_forward(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H
         _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), pos_scale, n_txt, n_img,
         ctypes.byref(weights.c), H, d, code, _dev(lse_out, "lse_out", torch.float32), wsp, wsb, _stream(stream)))
     return x_out
+
+
+def avits_block_forward_ex(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H, lse_out=None, mass_out=None,
+                           mass_accumulate=False, workspace=None, stream=None, pos_scale=1.0):
+    """avits_block_forward with the joint attention's statistics: lse_out and
+    mass_out [H, S] fp32 (the softmax mass of each row on the text keys
+    [0, n_txt), added to mass_out's contents when mass_accumulate)."""
+    import torch
+    S, D = x_in.shape
+    d = D // H
+    code = _dtype_code(x_in)
+    ws, wsp, wsb = _workspace(
+        workspace, avits_block_workspace_bytes(weights.kind, S, H, d, weights.c.mlp_hidden, code), x_in.device)
+    outs = _BlockOutputs(_dev(lse_out, "lse_out", torch.float32), _dev(mass_out, "mass_out", torch.float32),
+                         1 if mass_accumulate else 0)
+    _check(load().avits_block_forward_ex(
+        _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), pos_scale, n_txt, n_img,
+        ctypes.byref(weights.c), H, d, code, ctypes.byref(outs), wsp, wsb, _stream(stream)))
+    return x_out
+
+
+NOISE_RASTER, NOISE_HALF_UNITS, NOISE_LOWRES = 0, 1, 2
+
+
+def avits_noise_reinject(x, t, seed, H_hr, W_hr, pos=None, rows_kind=None, stream=None):
+    """x [rows, C] <- (1 - t) x + t eps at the rows' coordinates: raster
+    high-res rows (default), half-unit positions pos [rows, 3] (rows_kind
+    NOISE_HALF_UNITS, the default when pos is given) or raster low-res rows
+    (NOISE_LOWRES)."""
+    import torch
+    rows, C = x.shape
+    if rows_kind is None:
+        rows_kind = NOISE_RASTER if pos is None else NOISE_HALF_UNITS
+    _check(load().avits_noise_reinject(_dev(x, "x"), rows, C, _dev(pos, "pos", torch.int32), rows_kind, H_hr, W_hr,
+                                       float(t), int(seed), _dtype_code(x), _stream(stream)))
+    return x
+
+
+def avits_noise_bits(first_pixel, bits, seed, stream=None):
+    """bits [n_pixels, C] uint32 (a torch int32 tensor): the generator's words."""
+    import torch
+    n, C = bits.shape
+    _check(load().avits_noise_bits(first_pixel, n, C, int(seed), _dev(bits, "bits", torch.int32), _stream(stream)))
+    return bits
 
 
 def avits_block_qk_workspace_bytes(S: int, H: int, d: int, dtype: int) -> int:

@@ -19,7 +19,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libavits.so")
 ARCH = "gfx950"
 
-SOURCES = ("abi.hip", "score.hip", "select.hip", "relayout.hip", "gemm.hip", "attention.hip", "block.hip")
+SOURCES = ("abi.hip", "score.hip", "select.hip", "relayout.hip", "gemm.hip", "attention.hip", "block.hip",
+           "noise.hip")
 
 CXXFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

@@ -34,7 +34,7 @@ static const char* const kFamilies[] = {"score_spatial", "score_combine", "score
                                         "gather_upsample", "scatter", "ln_mod", "gemm_qkv", "gemm_o",
                                         "gemm_mlp_in", "gemm_mlp_out", "gemm_single_in", "gemm_single_out",
                                         "splitk_reduce", "qk_rope", "attention", "joint_lse",
-                                        "gather_mixed", "scatter_mixed", "linear", "final_linear", "euler"};
+                                        "gather_mixed", "scatter_mixed", "linear", "final_linear", "euler", "noise"};
 constexpr int kNumFamilies = sizeof(kFamilies) / sizeof(kFamilies[0]);
 
 struct Pending {

@@ -393,10 +393,10 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
   float l = lrow + __shfl_xor(lrow, 32, kWave);
   const float tm = trow + __shfl_xor(trow, 32, kWave);
   if (row >= un.q_hi) return;
-  if constexpr (WITH_V && !MASS) {
+  if constexpr (WITH_V) {
     if (piece >= 0) {
-      // A key piece: its unnormalised output and (max, sum) per row, in the
-      // output's column order, for the combine kernel.
+      // A key piece: its unnormalised output and (max, sum, text sum) per
+      // row, in the output's column order, for the combine kernel.
       const int64_t lr = row - un.q_lo;
       float* po = a.part + (piece * kRows + lr) * DH + 4 * hi;
 #pragma unroll
@@ -407,8 +407,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
           *reinterpret_cast<float4*>(po + 32 * dt + 8 * q) = make_float4(o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]);
         }
       if (hi == 0) {
-        float* pm = a.part_ml + (piece * kRows + lr) * 2;
-        *reinterpret_cast<float2*>(pm) = make_float2(mrow, l);
+        float* pm = a.part_ml + (piece * kRows + lr) * 4;
+        *reinterpret_cast<float4*>(pm) = make_float4(mrow, l, MASS ? tm : 0.f, 0.f);
       }
       return;
     }
@@ -507,7 +507,9 @@ __global__ __launch_bounds__(kFRows) void attn_f32_kernel(const AttnArgs a) {
 // sum, and O_p its unnormalised output, the row's output is
 // sum_p 2^(m_p - m) O_p / sum_p 2^(m_p - m) l_p with m = max_p m_p, and its
 // log-sum-exp (m + log2 of the denominator) ln 2: the single-pass result up
-// to rounding.  Pieces are summed in key order.
+// to rounding.  With a text mass, the pieces' text sums t_p merge the same
+// way: mass = sum_p 2^(m_p - m) t_p / sum_p 2^(m_p - m) l_p.  Pieces are
+// summed in key order.
 constexpr int kMaxPieces = 4;
 template <int DH>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a) {
@@ -522,13 +524,13 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a) {
   const int h = un.h;
   const int64_t row = un.q_lo + lr;
   if (row >= un.q_hi) return;
-  float2 ml[kMaxPieces];
+  float4 ml[kMaxPieces];
   float o[kMaxPieces][kCols];
 #pragma unroll
   for (int p = 0; p < kMaxPieces; ++p) {
     if (p < a.ksp) {
       const int64_t pc = (su * a.ksp + p) * kRows + lr;
-      ml[p] = *reinterpret_cast<const float2*>(a.part_ml + pc * 2);
+      ml[p] = *reinterpret_cast<const float4*>(a.part_ml + pc * 4);
       const float* po = a.part + pc * DH + sub * kCols;
 #pragma unroll
       for (int e = 0; e < kCols; e += 4) {
@@ -541,7 +543,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a) {
 #pragma unroll
   for (int p = 0; p < kMaxPieces; ++p)
     if (p < a.ksp) m = fmaxf(m, ml[p].x);
-  float den = 0.f, acc[kCols];
+  float den = 0.f, tden = 0.f, acc[kCols];
 #pragma unroll
   for (int e = 0; e < kCols; ++e) acc[e] = 0.f;
 #pragma unroll
@@ -549,6 +551,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a) {
     if (p < a.ksp) {
       const float wgt = __builtin_amdgcn_exp2f(ml[p].x - m);
       den = fmaf(wgt, ml[p].y, den);
+      tden = fmaf(wgt, ml[p].z, tden);
 #pragma unroll
       for (int e = 0; e < kCols; ++e) acc[e] = fmaf(wgt, o[p][e], acc[e]);
     }
@@ -562,6 +565,10 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const AttnArgs a) {
     *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf2(acc[0] * inv, acc[1] * inv), pack_bf2(acc[2] * inv, acc[3] * inv)};
   }
   if (a.lse && sub == 0) a.lse[int64_t(h) * a.Sq + row] = (m + log2f(den)) * kLn2;
+  if (a.mass && sub == 1) {
+    float* dst = a.mass + int64_t(h) * a.Sq + row;
+    *dst = (a.mass_accumulate ? *dst : 0.f) + tden * inv;
+  }
 }
 
 // Split-tail plan for the bf16 kernel with V (one sequence or packed ones): whole units
@@ -574,7 +581,7 @@ int plan_attn_split(AttnArgs& a, int DH) {
   a.split_from = INT64_MAX;
   a.ksp = 1;
   a.part_ml = nullptr;
-  if (!a.part || !a.vt || a.mass) return 1;
+  if (!a.part || !a.vt) return 1;
   const int64_t U = attn_row_blocks(a, kRows) * a.H;
   // Fewest key tiles of any unit (every piece must get at least one).
   int64_t T = (a.Sk + 63) / 64;
@@ -614,7 +621,7 @@ int plan_attn_split(AttnArgs& a, int DH) {
   }
   if (from >= U) return 1;
   ksp = std::min<int64_t>(ksp, T);  // at least one key tile per piece
-  auto need = [&](int64_t k) { return size_t((U - from) * k) * kRows * (DH + 2) * sizeof(float); };
+  auto need = [&](int64_t k) { return size_t((U - from) * k) * kRows * (DH + 4) * sizeof(float); };
   while (ksp >= 2 && need(ksp) > a.part_bytes) --ksp;
   if (ksp < 2) return 1;
   const int64_t pieces = (U - from) * ksp;
@@ -632,7 +639,8 @@ void launch_dh(AttnArgs a, int dtype, hipStream_t s) {
     const int ksp = plan_attn_split(a, DH);
     const dim3 grid(static_cast<unsigned>(ksp > 1 ? a.split_from + (U - a.split_from) * ksp : U));
     if (with_v) {
-      hipLaunchKernelGGL((attn_bf16_kernel<DH, true, false>), grid, dim3(256), 0, s, a);
+      if (a.mass) hipLaunchKernelGGL((attn_bf16_kernel<DH, true, true>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<DH, true, false>), grid, dim3(256), 0, s, a);
       if (ksp > 1) {
         const int64_t rows = (U - a.split_from) * kRows;
         hipLaunchKernelGGL((attn_combine_kernel<DH>), dim3(unsigned(ceil_div64(rows, 16))), dim3(256), 0, s, a);

@@ -333,7 +333,7 @@ int run_block_qk(const void* x_in, const int32_t* pos, float pos_scale, int64_t 
 template <typename T>
 int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale, int64_t n_txt, int64_t n_img,
               const avits_block_weights* w, int H, int d, int dtype, float* lse_out, const BlockWs& ws,
-              hipStream_t s, const AttnSegs* segs = nullptr) {
+              hipStream_t s, const AttnSegs* segs = nullptr, float* mass_out = nullptr, int mass_accumulate = 0) {
   const int64_t S = n_txt + n_img, D = int64_t(H) * d, F = w->mlp_hidden;
   const bool dbl = w->kind == AVITS_BLOCK_DOUBLE;
   const T* x = static_cast<const T*>(x_in);
@@ -401,6 +401,11 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
     a.vt = vt; a.ldvt = ws.ldvt;
     a.o = ws.o; a.ldo = dbl ? D : D + F;
     a.lse = lse_out;
+    // The text mass of Eq. spatial under the same running maximum: the
+    // softmax share of the keys [0, n_txt) (the text rows lead the sequence).
+    a.mass = mass_out;
+    a.mass_keys = n_txt;
+    a.mass_accumulate = mass_accumulate;
     a.Sq = S; a.Sk = S; a.H = H; a.d = d;
     a.part = ws.partial; a.part_bytes = ws.partial_bytes;  // no GEMM partials are live here
     if ((rc = launch_attention(a, dtype, s)) != AVITS_OK) return rc;
@@ -551,6 +556,18 @@ extern "C" int avits_block_forward(const void* x_in, void* x_out, const int32_t*
                                    int64_t n_txt, int64_t n_img, const avits_block_weights* w, int32_t H, int32_t d,
                                    int dtype, float* lse_out, void* workspace, size_t workspace_bytes,
                                    void* stream) {
+  avits_block_outputs o{};
+  o.lse = lse_out;
+  return avits_block_forward_ex(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, &o, workspace,
+                                workspace_bytes, stream);
+}
+
+extern "C" int avits_block_forward_ex(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,
+                                      int64_t n_txt, int64_t n_img, const avits_block_weights* w, int32_t H,
+                                      int32_t d, int dtype, const avits_block_outputs* outs, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  const avits_block_outputs none{};
+  if (!outs) outs = &none;
   int rc = check_block_args("block_forward", x_in, pos, pos_scale, n_txt, n_img, w, H, d, dtype);
   if (rc != AVITS_OK) return rc;
   const int64_t S = n_txt + n_img;
@@ -565,8 +582,10 @@ extern "C" int avits_block_forward(const void* x_in, void* x_out, const int32_t*
   const BlockWs ws = block_ws_layout(static_cast<char*>(workspace), w->kind, S, H, d, w->mlp_hidden, esz);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == AVITS_BF16)
-    return run_block<bf16_t>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, lse_out, ws, s);
-  return run_block<float>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, lse_out, ws, s);
+    return run_block<bf16_t>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, outs->lse, ws, s, nullptr,
+                             outs->mass, outs->mass_accumulate);
+  return run_block<float>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, outs->lse, ws, s, nullptr,
+                          outs->mass, outs->mass_accumulate);
 }
 
 extern "C" int avits_block_forward_batched(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,

@@ -95,6 +95,14 @@ __device__ __forceinline__ u32x4 buffer_rsrc(const void* base, uint32_t bytes) {
   return u32x4{uint32_t(b), uint32_t(b >> 32) & 0xffffu, bytes, 0x00020000u};
 }
 
+// The 32-bit range of a buffer resource over `bytes` bytes from its base.
+// Ranges of 4 GiB or more are capped at 2^32 - 1: every offset a kernel
+// issues against a resource is a tile's (far below 4 GiB), so only a range
+// that ends within reach of those offsets must be exact, and it then is.
+__device__ __forceinline__ uint32_t range32(int64_t bytes) {
+  return bytes >= int64_t(0xffffffffu) ? 0xffffffffu : uint32_t(bytes);
+}
+
 // 16-byte buffer load whose completion the caller waits for explicitly with
 // vm_wait<N>() followed by vm_ready() on the destination (the compiler does
 // not track the load, so it neither drains nor reorders around it).

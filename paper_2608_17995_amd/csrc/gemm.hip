@@ -494,8 +494,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_bf16_kernel(const
   };
   auto load_tile = [&](Stage& st, int64_t kt) {
     const int64_t koff = kt * kBK * 2;
-    const u32x4 ra = buffer_rsrc(a_base + koff, uint32_t(a_bytes - koff));
-    const u32x4 rw = buffer_rsrc(w_base + koff, uint32_t(w_bytes - koff));
+    const u32x4 ra = buffer_rsrc(a_base + koff, range32(a_bytes - koff));
+    const u32x4 rw = buffer_rsrc(w_base + koff, range32(w_bytes - koff));
 #pragma unroll
     for (int j = 0; j < CA; ++j) buffer_load16(st.a[j], ra, a_off[j]);
 #pragma unroll
@@ -681,9 +681,9 @@ __global__ __launch_bounds__(512) void gemm_bf16_pp_kernel(const GemmArgs a, flo
   auto load_half = [&](int64_t kt) {
     const int64_t koff = kt * kBK * 2;
     const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<char*>(a_base + koff), 0, int(a_bytes - koff), 0x00020000);
+        const_cast<char*>(a_base + koff), 0, int(range32(a_bytes - koff)), 0x00020000);
     const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<char*>(w_base + koff), 0, int(w_bytes - koff), 0x00020000);
+        const_cast<char*>(w_base + koff), 0, int(range32(w_bytes - koff)), 0x00020000);
 #pragma unroll
     for (int j = 0; j < HALF; ++j) sa[j] = __builtin_amdgcn_raw_buffer_load_b128(ra, int(a_off[j]), 0, 0);
 #pragma unroll

@@ -117,7 +117,7 @@ struct AttnArgs {
   // combined by a second kernel.  Null: never split.
   float* part;
   size_t part_bytes;
-  float* part_ml;      // set by the launcher: the (max, sum) partials, after the outputs
+  float* part_ml;      // set by the launcher: (max, sum, text sum, 0) per piece row, after the outputs
   int64_t split_from;  // set by the launcher: units >= split_from run in ksp pieces
   int ksp;
 };

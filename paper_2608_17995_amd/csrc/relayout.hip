@@ -136,6 +136,7 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
   int64_t j = job - n_prefix;
   if (j < k) {
     const int64_t p = idx[j];
+    if (p < 0 || p >= N) return;  // outside the grid: nothing is read or written for it
     // One read of the high-resolution row feeds the compact row and, when
     // the canvas is a separate buffer, the canvas row.
     const u32x4* src = reinterpret_cast<const u32x4*>(highres + p * D);
@@ -183,8 +184,10 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void scatter_kernel(
   idx += im.idx_off[b];
   const int64_t row_offset = im.row_off[b];
   canvas += int64_t(b) * N * D;
+  const int64_t p = idx[j];
+  if (p < 0 || p >= N) return;  // outside the canvas: skipped
   wave_copy_row(reinterpret_cast<const char*>(out + (row_offset + j) * D),
-                reinterpret_cast<char*>(canvas + int64_t(idx[j]) * D), D * int64_t(sizeof(T)), lane);
+                reinterpret_cast<char*>(canvas + p * D), D * int64_t(sizeof(T)), lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -375,9 +378,10 @@ extern "C" int avits_gather_upsample(const void* lowres, const void* highres_pre
 }
 
 extern "C" int avits_scatter(const void* out, const int32_t* idx, int64_t k, int64_t row_offset, int64_t D,
-                             int dtype, void* canvas, void* stream) {
+                             int64_t n_canvas, int dtype, void* canvas, void* stream) {
   AVITS_REQUIRE(k >= 0 && row_offset >= 0 && D >= 1, "scatter: bad k=%lld row_offset=%lld D=%lld",
                 (long long)k, (long long)row_offset, (long long)D);
+  AVITS_REQUIRE(n_canvas >= 1, "scatter: n_canvas=%lld must be >= 1", (long long)n_canvas);
   if (dtype != AVITS_F32 && dtype != AVITS_BF16)
     return set_error(AVITS_ERR_UNSUPPORTED, "scatter: dtype %d unsupported", dtype);
   const int64_t esz = dtype == AVITS_F32 ? 4 : 2;
@@ -387,7 +391,7 @@ extern "C" int avits_scatter(const void* out, const int32_t* idx, int64_t k, int
   ImageRows im{};
   im.idx_off[1] = k;
   im.row_off[0] = row_offset;
-  return launch_scatter(out, idx, im, 1, k, 0, D, dtype, canvas, stream, "scatter");
+  return launch_scatter(out, idx, im, 1, k, n_canvas, D, dtype, canvas, stream, "scatter");
 }
 
 extern "C" int avits_gather_upsample_batched(const void* lowres, const void* highres_prev, const void* prefix,

@@ -166,10 +166,11 @@ def test_gather_and_scatter_validation(lib):
     assert g(FAKE, FAKE, None, FAKE, 3, 2, 2, 4, 64, 0, 1, FAKE, FAKE, FAKE, None) == INVALID   # null prefix
     assert g(FAKE, FAKE, None, FAKE, 3, 2, 2, 0, 64, 0, 9, FAKE, FAKE, FAKE, None) == UNSUPPORTED
     s = lib.avits_scatter
-    assert s(FAKE, FAKE, -1, 0, 64, 1, FAKE, None) == INVALID
-    assert s(FAKE, FAKE, 0, 0, 64, 1, FAKE, None) == 0        # k == 0: no-op
-    assert s(None, FAKE, 3, 0, 64, 1, FAKE, None) == INVALID
-    assert s(FAKE, FAKE, 3, 0, 64, 3, FAKE, None) == UNSUPPORTED
+    assert s(FAKE, FAKE, -1, 0, 64, 16, 1, FAKE, None) == INVALID
+    assert s(FAKE, FAKE, 0, 0, 64, 16, 1, FAKE, None) == 0        # k == 0: no-op
+    assert s(None, FAKE, 3, 0, 64, 16, 1, FAKE, None) == INVALID
+    assert s(FAKE, FAKE, 3, 0, 64, 0, 1, FAKE, None) == INVALID     # n_canvas < 1
+    assert s(FAKE, FAKE, 3, 0, 64, 16, 3, FAKE, None) == UNSUPPORTED
 
 
 def test_batched_gather_and_scatter_validation(lib):
