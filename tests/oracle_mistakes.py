@@ -96,6 +96,16 @@ MISTAKES = {
     "reinject_weights_swapped": ("oracle.noise", "reinject",
                                  [("(1.0 - float(t)) * np.asarray(x, dtype=np.float64) + float(t) * np.asarray(eps",
                                    "float(t) * np.asarray(x, dtype=np.float64) + (1.0 - float(t)) * np.asarray(eps")]),
+    # three-stage sampler
+    "clean_estimate_sign_stage2": ("oracle.sampler", "transition12",
+                                   [("x0 = euler_update(z, v, -t_s)", "x0 = euler_update(z, v, t_s)")]),
+    "clean_estimate_sign_stage3": ("oracle.sampler", "transition23",
+                                   [("x0 = euler_update(z_mix, v, -t_s)", "x0 = euler_update(z_mix, v, t_s)")]),
+    "collection_starts_early": ("oracle.sampler", "stage1", [("collect = i >= n1", "collect = i >= n1 - 1")]),
+    "mass_of_text_rows": ("oracle.sampler", "stage1", [("mass += m[:, L:]", "mass += m[:, :Mp]")]),
+    "kept_rows_not_upsampled": ("oracle.sampler", "transition23",
+                                [("_, _, full = gather_upsample(state, canvas, None, children, H_lr, W_lr)",
+                                  "full = canvas")]),
     # sampler
     "final_layer_without_one": ("oracle.sampler", "final_layer", [("(1.0 + _f64(scale))", "_f64(scale)")]),
     "euler_sign": ("oracle.sampler", "euler_update", [("_f64(z) + float(dt)", "_f64(z) - float(dt)")]),
