@@ -74,7 +74,8 @@ def measured_traffic() -> dict | None:
 STAGE_TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "stages_flux1024_hbm_traffic.md")
 STAGE_SOURCES = ("score.hip", "select.hip", "relayout.hip", "common.h")
 
-LEGS = ("fused_scoring", "block_mass", "select_sweep", "mixed_stage2", "batched", "workloads", "stack")
+LEGS = ("fused_scoring", "block_mass", "select_sweep", "mixed_stage2", "batched", "workloads", "stack",
+        "three_stage")
 
 
 def sources_sha256(files) -> str:
@@ -653,6 +654,61 @@ def _stack_leg(avits, torch) -> dict:
                         "gather, 19 double + 38 single blocks, scatter"}
 
 
+def _three_stage_leg(avits, torch) -> dict:
+    """One image through the whole three-stage sampler of Section 3.2 at the
+    FLUX 1024^2 shape on the 57-block stack (random-init weights drawn on
+    the GPU, 64 latent channels, 512 text tokens): 18 Euler steps split
+    6 + 3 (Stage 1 at 32x32, the last 3 collecting snapshots and the text
+    mass of every double block) + 4 (Stage 2, K = floor(0.3 * 1024) = 307
+    tokens expanded: 2457 rows) + 5 (Stage 3 at 64x64: 4608 rows), with both
+    transitions (scores, selection, re-layout, coordinate-bound noise)."""
+    from paper_2608_17995_amd.step import ThreeStageSampler
+    from synth import configs as C
+    from synth import generator as G
+
+    w = C.FLUX_STACK
+    n1, nt, n2, n3, Cc = 6, 3, 4, 5, 64
+    K = C.mixed_keep_count(w.rho, w.N_lr)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(w.seed + 100)
+    doubles = [_gpu_block_weights(avits, torch, w, gen, avits.BLOCK_DOUBLE) for _ in range(w.n_double)]
+    singles = [_gpu_block_weights(avits, torch, w, gen, avits.BLOCK_SINGLE) for _ in range(w.n_single)]
+
+    def n(*shape, std=0.02, mean=0.0):
+        return (torch.randn(*shape, generator=gen, device="cuda") * std + mean).to(torch.bfloat16)
+
+    sw = {"embed_w": n(w.D, Cc), "embed_b": n(w.D), "final_mod": n(2, w.D), "final_w": n(Cc, w.D), "final_b": n(Cc)}
+    text = n(w.L, w.D, std=1.0)
+    samp = ThreeStageSampler(w.H_lr, w.W_lr, w.L, Cc, w.D, w.H, w.mlp_ratio * w.D, doubles, singles, sw,
+                             torch.from_numpy(G.prefix_positions(w)).cuda(), K, n1, nt, n2, n3, torch.bfloat16,
+                             seed=w.seed, alpha=w.alpha)
+    samp.run(text)                        # warm-up
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    t0 = time.perf_counter()
+    ev[0].record()
+    samp.stage1(text)
+    ev[1].record()
+    samp.transition12()
+    ev[2].record()
+    samp.stage2(text)
+    ev[3].record()
+    samp.transition23()
+    ev[4].record()
+    samp.stage3(text)
+    ev[5].record()
+    torch.cuda.synchronize()
+    total = (time.perf_counter() - t0) * 1e3
+    parts = [ev[i].elapsed_time(ev[i + 1]) for i in range(5)]
+    blocks = w.n_double + w.n_single
+    fl = sum(k * blocks * block_flops(S, w.D)["total"] for k, S in ((n1 + nt, samp.S1), (n2, samp.S2), (n3, samp.S3)))
+    return {"workload": w.name, "steps": [n1, nt, n2, n3], "K": K, "rows": [samp.S1, samp.S2, samp.S3],
+            "ms_total": round(total, 2), "ms": {"stage1": round(parts[0], 2), "transition12": round(parts[1], 3),
+                                                "stage2": round(parts[2], 2), "transition23": round(parts[3], 3),
+                                                "stage3": round(parts[4], 2)},
+            "tflops_blocks": round(fl / (total / 1e3) / 1e12, 1)}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -892,6 +948,8 @@ def main(argv=None):
         result["workloads"] = _workload_legs(avits, torch, max(5, args.steps // 2), 2)
     if "stack" in legs:
         result["stack"] = _stack_leg(avits, torch)
+    if "three_stage" in legs:
+        result["three_stage"] = _three_stage_leg(avits, torch)
     if not args.no_cpu_baseline:
         host = dict(si)
         host.update(lay)

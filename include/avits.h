@@ -375,6 +375,23 @@ int avits_scatter_batched(const void* out, const int32_t* idx, const int64_t* id
                           void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_grid_positions / avits_scale_positions — RoPE positions of grid
+ * tokens (Section 3.1: token i sits at spatial coordinate p_i = (r_i, c_i)):
+ *   avits_grid_positions:  pos[r] = (frame, (r / W) scale + offset,
+ *                                            (r % W) scale + offset)
+ *   for raster rows r < rows of a grid W wide (e.g. scale 1, offset 0: a
+ *   grid's own integer positions; scale 4, offset 1: low-res block centres
+ *   in half units of the 2x grid);
+ *   avits_scale_positions: dst[r] = src[r] * scale, all three coordinates
+ *   (e.g. scale 2: positions in half units).
+ * pos, src, dst [rows, 3] int32 device pointers (src and dst may be the
+ * same).  Requires W >= 1 and rows >= 0; rows == 0 enqueues nothing.
+ * ---------------------------------------------------------------------- */
+int avits_grid_positions(int32_t* pos, int64_t rows, int32_t W, int32_t frame, int32_t scale, int32_t offset,
+                         void* stream);
+int avits_scale_positions(const int32_t* src, int64_t rows, int32_t scale, int32_t* dst, void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_gather_mixed — the mixed-resolution sequence of Stage 2 (Section
  * 3.2): the tokens selected at low-res granularity are expanded to their four
  * high-res children by 2x upsampling; the other M' - K low-res tokens stay in
@@ -453,13 +470,15 @@ int avits_joint_attention_stats(const void* q, const void* k_all, int64_t N, int
  *   V_i = (1 / D_f) sum_c sum_k (z_k[i, c] - zbar[i, c])^2 / (N_T - 1)
  *   S_i = alpha (A_i - min A) / (max A - min A + eps)
  *       + (1 - alpha) (V_i - min V) / (max V - min V + eps)
- * mass [H, N] fp32 (the sum of `count` probes); snapshots: a host array of
+ * mass [H, N] fp32 with row stride mass_ld >= N (the sum of `count`
+ * probes; e.g. the image-row columns of a block's [H, S] mass, mass_ld = S
+ * and the pointer advanced by the text rows); snapshots: a host array of
  * n_t device pointers, snapshot k [N, D_f] (dtype), consecutive steps in
  * order; scores, a_raw, v_raw as avits_score.  workspace >=
  * avits_score_workspace_bytes(N, H).  Requires 2 <= n_t <= 16, count >= 1.  With one probe and n_t = 2 it computes what avits_score
  * computes, from the mass instead of the query/key recomputation.
  * ---------------------------------------------------------------------- */
-int avits_score_from_mass(const float* mass, int32_t H, int32_t count,
+int avits_score_from_mass(const float* mass, int64_t mass_ld, int32_t H, int32_t count,
                           const void* const* snapshots, int32_t n_t, int64_t N, int64_t D_f, float alpha, float eps,
                           int dtype, float* scores, float* a_raw, float* v_raw,
                           void* workspace, size_t workspace_bytes, void* stream);

@@ -21,5 +21,6 @@ from ._binding import (  # noqa: F401
     avits_gather_mixed, avits_scatter_mixed,
     avits_linear, avits_final_layer_workspace_bytes, avits_final_layer, avits_euler_update,
     avits_noise_reinject, avits_noise_bits, NOISE_RASTER, NOISE_HALF_UNITS, NOISE_LOWRES,
+    avits_grid_positions, avits_scale_positions,
     avits_timing_enable, avits_timing_reset, avits_timing_read,
 )

@@ -70,6 +70,8 @@ _SIGS = {
     "avits_noise_reinject": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _i32, _f32,
                                             ctypes.c_uint64, ctypes.c_int, _c_void_p]),
     "avits_noise_bits": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_uint64, _c_void_p, _c_void_p]),
+    "avits_grid_positions": (ctypes.c_int, [_c_void_p, _i64, _i32, _i32, _i32, _i32, _c_void_p]),
+    "avits_scale_positions": (ctypes.c_int, [_c_void_p, _i64, _i32, _c_void_p, _c_void_p]),
     "avits_block_forward_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _f32, _i32, _c_void_p, _c_void_p,
                                                    ctypes.POINTER(_BlockWeights), _i32, _i32, ctypes.c_int,
                                                    _c_void_p, _c_void_p, _size, _c_void_p]),
@@ -97,7 +99,7 @@ _SIGS = {
                                        _c_void_p]),
     "avits_joint_attention_stats": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, _i32, _i32, ctypes.c_int,
                                                    _c_void_p, _c_void_p, ctypes.c_int, _c_void_p]),
-    "avits_score_from_mass": (ctypes.c_int, [_c_void_p, _i32, _i32, ctypes.POINTER(_c_void_p), _i32, _i64, _i64,
+    "avits_score_from_mass": (ctypes.c_int, [_c_void_p, _i64, _i32, _i32, ctypes.POINTER(_c_void_p), _i32, _i64, _i64,
                                              _f32, _f32,
                                              ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _size,
                                              _c_void_p]),
@@ -476,6 +478,22 @@ def avits_block_forward_ex(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights
     return x_out
 
 
+def avits_grid_positions(pos, W, frame=0, scale=1, offset=0, stream=None):
+    """pos [rows, 3] int32 <- (frame, (r / W) scale + offset, (r % W) scale + offset)."""
+    import torch
+    _check(load().avits_grid_positions(_dev(pos, "pos", torch.int32), pos.shape[0], W, frame, scale, offset,
+                                       _stream(stream)))
+    return pos
+
+
+def avits_scale_positions(src, scale, dst, stream=None):
+    """dst [rows, 3] int32 <- src * scale."""
+    import torch
+    _check(load().avits_scale_positions(_dev(src, "src", torch.int32), src.shape[0], scale,
+                                        _dev(dst, "dst", torch.int32), _stream(stream)))
+    return dst
+
+
 NOISE_RASTER, NOISE_HALF_UNITS, NOISE_LOWRES = 0, 1, 2
 
 
@@ -549,9 +567,13 @@ def avits_joint_attention_stats(q, k_all, L, mass, lse=None, accumulate=False, s
 
 def avits_score_from_mass(mass, count, snapshots, alpha, eps, scores, a_raw=None, v_raw=None, workspace=None,
                           stream=None):
-    """mass [H, N] fp32 (sum of `count` probes); snapshots: N_T tensors [N, D_f], consecutive steps in order."""
+    """mass [H, N] fp32 (sum of `count` probes; rows may be strided, e.g.
+    the image columns mass_all[:, L:] of a block's [H, S] mass); snapshots:
+    N_T tensors [N, D_f], consecutive steps in order."""
     import torch
     H, N = mass.shape
+    if mass.dtype != torch.float32 or not mass.is_cuda or mass.stride(1) != 1 or mass.stride(0) < N:
+        raise AvitsError(-1, "mass must be a float32 GPU tensor [H, N] with unit column stride")
     snaps = list(snapshots)
     n_t = len(snaps)
     Df = snaps[0].shape[-1]
@@ -561,7 +583,7 @@ def avits_score_from_mass(mass, count, snapshots, alpha, eps, scores, a_raw=None
     ptrs = (_c_void_p * n_t)(*[_dev(z, "snapshot") for z in snaps])
     ws, wsp, wsb = _workspace(workspace, avits_score_workspace_bytes(N, H), mass.device)
     _check(load().avits_score_from_mass(
-        _dev(mass, "mass", torch.float32), H, count, ptrs, n_t, N, Df, alpha, eps, _dtype_code(snaps[0]),
+        mass.data_ptr(), mass.stride(0), H, count, ptrs, n_t, N, Df, alpha, eps, _dtype_code(snaps[0]),
         _dev(scores, "scores", torch.float32), _dev(a_raw, "a_raw", torch.float32), _dev(v_raw, "v_raw", torch.float32),
         wsp, wsb, _stream(stream)))
     return scores

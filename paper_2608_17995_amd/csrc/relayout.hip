@@ -351,7 +351,44 @@ int launch_scatter(const void* out, const int32_t* idx, const ImageRows& im, int
   return launch_status(who);
 }
 
+__global__ __launch_bounds__(256) void grid_positions_kernel(int32_t* __restrict__ pos, int64_t rows, int W,
+                                                             int frame, int scale, int offset) {
+  const int64_t r = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (r >= rows) return;
+  pos[3 * r + 0] = frame;
+  pos[3 * r + 1] = int32_t(r / W) * scale + offset;
+  pos[3 * r + 2] = int32_t(r % W) * scale + offset;
+}
+
+__global__ __launch_bounds__(256) void scale_positions_kernel(const int32_t* src, int64_t n, int scale,
+                                                              int32_t* dst) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i < n) dst[i] = src[i] * scale;
+}
+
 }  // namespace
+
+extern "C" int avits_grid_positions(int32_t* pos, int64_t rows, int32_t W, int32_t frame, int32_t scale,
+                                    int32_t offset, void* stream) {
+  AVITS_REQUIRE(rows >= 0 && W >= 1, "grid_positions: rows=%lld W=%d", (long long)rows, W);
+  AVITS_REQUIRE(rows <= INT32_MAX, "grid_positions: rows=%lld beyond 2^31", (long long)rows);
+  if (rows == 0) return AVITS_OK;
+  AVITS_REQUIRE(pos, "grid_positions: null pos");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(grid_positions_kernel, dim3(unsigned(ceil_div(rows, 256))), dim3(256), 0, s, pos, rows, W, frame,
+                     scale, offset);
+  return launch_status("grid_positions");
+}
+
+extern "C" int avits_scale_positions(const int32_t* src, int64_t rows, int32_t scale, int32_t* dst, void* stream) {
+  AVITS_REQUIRE(rows >= 0 && rows <= INT32_MAX / 3, "scale_positions: rows=%lld", (long long)rows);
+  if (rows == 0) return AVITS_OK;
+  AVITS_REQUIRE(src && dst, "scale_positions: null src/dst");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(scale_positions_kernel, dim3(unsigned(ceil_div(3 * rows, 256))), dim3(256), 0, s, src, 3 * rows,
+                     scale, dst);
+  return launch_status("scale_positions");
+}
 
 extern "C" int avits_gather_upsample(const void* lowres, const void* highres_prev, const void* prefix,
                                      const int32_t* idx, int64_t k, int32_t H_lr, int32_t W_lr,

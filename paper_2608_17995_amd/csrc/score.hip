@@ -398,7 +398,8 @@ struct Snapshots {
 };
 
 template <typename T>
-__global__ __launch_bounds__(256) void mass_temporal_kernel(const float* __restrict__ mass, int H, float inv,
+__global__ __launch_bounds__(256) void mass_temporal_kernel(const float* __restrict__ mass, int64_t mass_ld, int H,
+                                                            float inv,
                                                             const Snapshots zs, int n_t, int64_t N, int64_t Df,
                                                             float* __restrict__ a_out, float* __restrict__ v_out,
                                                             float4* __restrict__ mm) {
@@ -452,7 +453,7 @@ __global__ __launch_bounds__(256) void mass_temporal_kernel(const float* __restr
     }
     acc = wave_sum(acc);
     float ah = 0.f;
-    for (int h = lane; h < H; h += kWave) ah += mass[int64_t(h) * N + i];
+    for (int h = lane; h < H; h += kWave) ah += mass[int64_t(h) * mass_ld + i];
     ah = wave_sum(ah);
     const float A = ah * inv;
     const float V = acc / float(Df);
@@ -640,12 +641,14 @@ extern "C" int avits_score_batched(const void* latent_q, const void* text_k, con
                       dtype, scores, a_raw, v_raw, workspace, workspace_bytes, stream);
 }
 
-extern "C" int avits_score_from_mass(const float* mass, int32_t H, int32_t count, const void* const* snapshots,
+extern "C" int avits_score_from_mass(const float* mass, int64_t mass_ld, int32_t H, int32_t count,
+                                     const void* const* snapshots,
                                      int32_t n_t,
                                      int64_t N, int64_t D_f, float alpha, float eps, int dtype, float* scores,
                                      float* a_raw, float* v_raw, void* workspace, size_t workspace_bytes,
                                      void* stream) {
   AVITS_REQUIRE(N >= 1 && N <= INT32_MAX, "score_from_mass: N=%lld outside [1, 2^31)", (long long)N);
+  AVITS_REQUIRE(mass_ld >= N, "score_from_mass: mass_ld=%lld < N=%lld", (long long)mass_ld, (long long)N);
   AVITS_REQUIRE(H >= 1 && count >= 1 && D_f >= 1, "score_from_mass: H=%d count=%d D_f=%lld must be >= 1", H, count,
                 (long long)D_f);
   AVITS_REQUIRE(n_t >= 2 && n_t <= kMaxSnapshots, "score_from_mass: n_t=%d snapshots outside [2, %d]", n_t,
@@ -673,10 +676,10 @@ extern "C" int avits_score_from_mass(const float* mass, int32_t H, int32_t count
   {
     TimedLaunch timed("score_combine", s);
     if (dtype == AVITS_BF16)
-      hipLaunchKernelGGL(mass_temporal_kernel<bf16_t>, dim3(nmm), dim3(256), 0, s, mass, H, inv, zs, n_t, N, D_f,
+      hipLaunchKernelGGL(mass_temporal_kernel<bf16_t>, dim3(nmm), dim3(256), 0, s, mass, mass_ld, H, inv, zs, n_t, N, D_f,
                          a_dst, v_dst, ws.mm);
     else
-      hipLaunchKernelGGL(mass_temporal_kernel<float>, dim3(nmm), dim3(256), 0, s, mass, H, inv, zs, n_t, N, D_f,
+      hipLaunchKernelGGL(mass_temporal_kernel<float>, dim3(nmm), dim3(256), 0, s, mass, mass_ld, H, inv, zs, n_t, N, D_f,
                          a_dst, v_dst, ws.mm);
   }
   const int fblocks = int(std::min<int64_t>(256, (N + 255) / 256));

@@ -136,9 +136,8 @@ class StackStep:
         self.lse = torch.empty(s.H, s.N, dtype=f32, device=device)
         self.mass = torch.empty(s.H, s.N, dtype=f32, device=device)
         self.prefix_pos = torch.as_tensor(prefix_pos, dtype=i32).to(device)
-        r = torch.arange(s.N, dtype=i32, device=device)
-        W_hr = 2 * s.W_lr
-        self.img_pos = torch.stack([torch.zeros_like(r), r // W_hr, r % W_hr], dim=1).contiguous()
+        self.img_pos = torch.empty(s.N, 3, dtype=i32, device=device)
+        B.avits_grid_positions(self.img_pos, 2 * s.W_lr)      # (0, r, c) on the high-res grid
         self.scores = torch.empty(s.N, dtype=f32, device=device)
         self.a_raw = torch.empty(s.N, dtype=f32, device=device)
         self.v_raw = torch.empty(s.N, dtype=f32, device=device)
@@ -252,8 +251,8 @@ class MixedStage2:
         LR = self.LR
         prefix_pos = torch.as_tensor(prefix_pos, dtype=i32).to(device)
         self.prefix_pos = prefix_pos
-        r = torch.arange(Mp, dtype=i32, device=device)
-        self.lr_pos = torch.stack([torch.zeros_like(r), r // W_lr, r % W_lr], dim=1).contiguous()
+        self.lr_pos = torch.empty(Mp, 3, dtype=i32, device=device)
+        B.avits_grid_positions(self.lr_pos, W_lr)             # (0, r, c) on the low-res grid
         self.q_prefix = torch.empty(max(LR, 1), D, dtype=dtype, device=device)
         self.q_img = torch.empty(Mp, D, dtype=dtype, device=device)
         self.k_all = torch.empty(LR + Mp, D, dtype=dtype, device=device)
@@ -264,7 +263,8 @@ class MixedStage2:
         self.children = torch.empty(4 * K, dtype=i32, device=device)
         self.x = torch.empty(self.S, D, dtype=dtype, device=device)
         self.pos = torch.empty(self.S, 3, dtype=i32, device=device)
-        self.pos[:LR].copy_(2 * prefix_pos)     # half units
+        if LR:
+            B.avits_scale_positions(prefix_pos, 2, self.pos[:LR])   # half units
         self.buf = [torch.empty(self.S, D, dtype=dtype, device=device) for _ in range(2)]
         self.ws_score = torch.empty(max(B.avits_score_workspace_bytes(Mp, H), 1), dtype=torch.uint8, device=device)
         self.ws_select = torch.empty(max(B.avits_select_workspace_bytes(Mp), 1), dtype=torch.uint8, device=device)
@@ -495,3 +495,153 @@ class SelectedEuler:
         """canvas[idx[j]] = z_sel[j]: the selected latents back in place."""
         B.avits_scatter(z_sel, idx, 0, canvas, stream)
         return canvas
+
+
+class ThreeStageSampler:
+    """The three-stage dynamic-resolution sampler of Section 3.2 (Fig. 3a) on
+    one GPU, every step a library call:
+
+      stage 1      the low-res latent z1 [M', C] from the downsampled
+                   coordinate-bound noise, n1 + nt Euler steps (Eq. euler) of
+                   [text; embed(z1)] at the low-res grid positions; over the
+                   last nt steps the snapshots of z1 and the text mass of the
+                   image rows, taken inside every double block's own
+                   attention (avits_block_forward_ex, accumulated)
+      transition   scores from the mass and the snapshots (Eqs. spatial,
+                   step_var, joint) -> top K = floor(rho M') (Eq. topk) ->
+                   clean estimate z1 - t v -> the mixed sequence (selected
+                   tokens expanded 2x2, the rest kept) -> coordinate-bound
+                   noise re-injected at t
+      stage 2      n2 Euler steps of the mixed sequence (half-unit positions,
+                   pos_scale 0.5)
+      transition   clean estimate -> expanded rows to their pixels, kept rows
+                   upsampled around them -> noise re-injected at t; rows in
+                   raster order
+      stage 3      n3 Euler steps of the full grid
+
+    Each step embeds the latents (avits_linear), runs the double then the
+    single blocks on [text; rows], maps the image rows to the velocity
+    (avits_final_layer) and updates the latents (avits_euler_update).  The
+    time grid is uniform, t_i = 1 - i / (n1 + nt + n2 + n3).  Buffers are
+    allocated once; the stage methods enqueue library calls only.  After a
+    run, z1 / snaps / mass / scores / idx / z2 / z3 hold each stage's state.
+    """
+
+    def __init__(self, H_lr: int, W_lr: int, L: int, C: int, D: int, H: int, mlp_hidden: int, doubles: list,
+                 singles: list, sampler_w: dict, prefix_pos, K: int, n1: int, nt: int, n2: int, n3: int, dtype,
+                 seed: int, alpha=0.5, eps=1e-8, device="cuda"):
+        import torch
+        if not doubles:
+            raise ValueError("the text mass needs at least one double block")
+        Mp = H_lr * W_lr
+        if not 0 <= K <= Mp or nt < 2 or min(n1, n2, n3) < 0:
+            raise ValueError("0 <= K <= M', nt >= 2 snapshots, step counts >= 0")
+        self.H_lr, self.W_lr, self.L, self.C, self.D, self.H = H_lr, W_lr, L, C, D, H
+        self.Mp, self.N, self.K = Mp, 4 * Mp, K
+        self.doubles, self.singles, self.sw = list(doubles), list(singles), sampler_w
+        self.n1, self.nt, self.n2, self.n3 = n1, nt, n2, n3
+        self.seed, self.alpha, self.eps = seed, alpha, eps
+        n = n1 + nt + n2 + n3
+        self.t = [1.0 - i / n for i in range(n + 1)]
+        self.S1, self.S2, self.S3 = L + Mp, L + 4 * K + Mp - K, L + 4 * Mp
+        f32, i32 = torch.float32, torch.int32
+        mk = lambda *shape, dt=dtype: torch.empty(*shape, dtype=dt, device=device)  # noqa: E731
+        self.z1, self.v1 = mk(Mp, C), mk(Mp, C)
+        self.snaps = [mk(Mp, C) for _ in range(nt)]
+        self.mass = mk(H, self.S1, dt=f32)
+        self.scores = mk(Mp, dt=f32)
+        self.idx = mk(max(K, 1), dt=i32)
+        self.children = mk(max(4 * K, 1), dt=i32)
+        self.z2, self.v2 = mk(self.S2 - L, C), mk(self.S2 - L, C)
+        self.z3, self.v3 = mk(self.N, C), mk(self.N, C)
+        self.state = mk(Mp, C)
+        self.g_rows, self.g_pos = mk(max(4 * K, 1), C), mk(max(4 * K, 1), 3, dt=i32)
+        self.x = [mk(self.S3, D) for _ in range(2)]
+        prefix_pos = torch.as_tensor(prefix_pos, dtype=i32).to(device)
+        self.pos1, self.pos2, self.pos3 = mk(self.S1, 3, dt=i32), mk(self.S2, 3, dt=i32), mk(self.S3, 3, dt=i32)
+        if L:
+            self.pos1[:L].copy_(prefix_pos)
+            self.pos3[:L].copy_(prefix_pos)
+            B.avits_scale_positions(prefix_pos, 2, self.pos2[:L])       # half units
+        B.avits_grid_positions(self.pos1[L:], W_lr)                     # (0, r, c) low-res
+        B.avits_grid_positions(self.pos3[L:], 2 * W_lr)                 # (0, r, c) high-res
+        self.prefix_rows = torch.arange(max(L, 1), dtype=i32, device=device)
+        d = D // H
+        code = B.BF16 if dtype == torch.bfloat16 else B.F32
+        kinds = [B.BLOCK_DOUBLE] + ([B.BLOCK_SINGLE] if singles else [])
+        self.ws_block = mk(max(B.avits_block_workspace_bytes(kd, self.S3, H, d, mlp_hidden, code) for kd in kinds),
+                           dt=torch.uint8)
+        self.ws_final = mk(max(B.avits_final_layer_workspace_bytes(self.N, D, code), 1), dt=torch.uint8)
+        self.ws_score = mk(max(B.avits_score_workspace_bytes(Mp, H), 1), dt=torch.uint8)
+        self.ws_select = mk(max(B.avits_select_workspace_bytes(Mp), 1), dt=torch.uint8)
+
+    # One Euler step of latents z (rows behind the prefix) at positions pos.
+    def _step(self, z, v, pos, S, dt, prefix, pos_scale=1.0, collect=False, stream=None):
+        L = self.L
+        x0, x1 = self.x[0][:S], self.x[1][:S]
+        if L:
+            B.avits_scatter(prefix, self.prefix_rows[:L], 0, x0, stream)
+        B.avits_linear(z, self.sw["embed_w"], self.sw["embed_b"], x0[L:], stream)
+        cur, nxt = x0, x1
+        for i, w in enumerate(self.doubles + self.singles):
+            mass = self.mass if collect and i < len(self.doubles) else None
+            B.avits_block_forward_ex(cur, nxt, pos, L, S - L, w, self.H, mass_out=mass, mass_accumulate=True,
+                                     workspace=self.ws_block, stream=stream, pos_scale=pos_scale)
+            cur, nxt = nxt, cur
+        B.avits_final_layer(cur[L:], self.sw["final_mod"], self.sw["final_w"], self.sw["final_b"], v,
+                            workspace=self.ws_final, stream=stream)
+        B.avits_euler_update(z, v, dt, stream)
+
+    def stage1(self, prefix, stream=None):
+        B.avits_noise_reinject(self.z1, 1.0, self.seed, 2 * self.H_lr, 2 * self.W_lr, rows_kind=B.NOISE_LOWRES,
+                               stream=stream)
+        self.mass.zero_()
+        for i in range(self.n1 + self.nt):
+            self._step(self.z1, self.v1, self.pos1, self.S1, self.t[i + 1] - self.t[i], prefix,
+                       collect=i >= self.n1, stream=stream)
+            if i >= self.n1:
+                self.snaps[i - self.n1].copy_(self.z1)
+
+    def transition12(self, stream=None):
+        L, K = self.L, self.K
+        t_s = self.t[self.n1 + self.nt]
+        B.avits_score_from_mass(self.mass[:, L:], self.nt * len(self.doubles), self.snaps, self.alpha, self.eps,
+                                self.scores, workspace=self.ws_score, stream=stream)
+        if K:
+            B.avits_select(self.scores, K, self.idx[:K], self.ws_select, stream)
+        B.avits_euler_update(self.z1, self.v1, -t_s, stream)          # clean estimate z1 - t v
+        B.avits_gather_mixed(self.z1, None, self.idx[:K] if K else None, self.H_lr, self.W_lr, self.z2,
+                             self.pos2[L:], self.children[:4 * K] if K else None, stream=stream)
+        B.avits_noise_reinject(self.z2, t_s, self.seed, 2 * self.H_lr, 2 * self.W_lr, pos=self.pos2[L:],
+                               stream=stream)
+
+    def stage2(self, prefix, stream=None):
+        i0 = self.n1 + self.nt
+        for i in range(i0, i0 + self.n2):
+            self._step(self.z2, self.v2, self.pos2, self.S2, self.t[i + 1] - self.t[i], prefix, pos_scale=0.5,
+                       stream=stream)
+
+    def transition23(self, stream=None):
+        K, Mp = self.K, self.Mp
+        t_s = self.t[self.n1 + self.nt + self.n2]
+        B.avits_euler_update(self.z2, self.v2, -t_s, stream)          # clean estimate
+        B.avits_scatter_mixed(self.z2, self.idx[:K] if K else None, self.H_lr, self.W_lr, 0,
+                              self.z3 if K else None, self.state if K < Mp else None, stream)
+        # The kept tokens expanded by 2x nearest upsampling around the expanded rows.
+        B.avits_gather_upsample(self.state, self.z3, None, self.children[:4 * K], self.H_lr, self.W_lr,
+                                self.g_rows[:4 * K], self.g_pos[:4 * K], self.z3, B.UP_NEAREST, stream)
+        B.avits_noise_reinject(self.z3, t_s, self.seed, 2 * self.H_lr, 2 * self.W_lr, stream=stream)
+
+    def stage3(self, prefix, stream=None):
+        i0 = self.n1 + self.nt + self.n2
+        for i in range(i0, i0 + self.n3):
+            self._step(self.z3, self.v3, self.pos3, self.S3, self.t[i + 1] - self.t[i], prefix, stream=stream)
+
+    def run(self, prefix, stream=None):
+        """The whole sampler; returns z3 [N, C], the final latent in raster order."""
+        self.stage1(prefix, stream)
+        self.transition12(stream)
+        self.stage2(prefix, stream)
+        self.transition23(stream)
+        self.stage3(prefix, stream)
+        return self.z3

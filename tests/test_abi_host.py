@@ -322,12 +322,33 @@ def test_stats_and_mass_score_validation(lib):
     g = lib.avits_score_from_mass
     ws = lib.avits_score_workspace_bytes(16, 2)
     two = (ctypes.c_void_p * 2)(FAKE, FAKE)
-    assert g(FAKE, 2, 1, two, 1, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # n_t < 2
-    assert g(FAKE, 2, 1, two, 17, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # n_t > 16
-    assert g(FAKE, 2, 0, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # count < 1
-    assert g(FAKE, 2, 1, two, 2, 16, 8, 1.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # alpha
-    assert g(FAKE, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 9, FAKE, None, None, FAKE, ws, None) == UNSUPPORTED
-    assert g(FAKE, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws - 1, None) == WORKSPACE
-    assert g(None, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID
+    assert g(FAKE, 16, 2, 1, two, 1, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # n_t < 2
+    assert g(FAKE, 16, 2, 1, two, 17, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # n_t > 16
+    assert g(FAKE, 16, 2, 0, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # count < 1
+    assert g(FAKE, 16, 2, 1, two, 2, 16, 8, 1.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # alpha
+    assert g(FAKE, 16, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 9, FAKE, None, None, FAKE, ws, None) == UNSUPPORTED
+    assert g(FAKE, 16, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws - 1, None) == WORKSPACE
+    assert g(None, 16, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID
+    assert g(FAKE, 15, 2, 1, two, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # mass_ld < N
     holes = (ctypes.c_void_p * 2)(FAKE, None)
-    assert g(FAKE, 2, 1, holes, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # null snapshot
+    assert g(FAKE, 16, 2, 1, holes, 2, 16, 8, 0.5, 1e-8, 1, FAKE, None, None, FAKE, ws, None) == INVALID  # null snapshot
+
+
+def test_position_and_noise_validation(lib):
+    assert lib.avits_grid_positions(FAKE, -1, 4, 0, 1, 0, None) == INVALID
+    assert lib.avits_grid_positions(FAKE, 5, 0, 0, 1, 0, None) == INVALID      # W < 1
+    assert lib.avits_grid_positions(None, 0, 4, 0, 1, 0, None) == 0            # rows == 0: no-op
+    assert lib.avits_scale_positions(None, 3, 2, FAKE, None) == INVALID
+    f = lib.avits_noise_reinject
+    assert f(FAKE, 4, 6, None, 0, 8, 8, 0.5, 1, 1, None) == INVALID           # C not a multiple of 4
+    assert f(FAKE, 4, 8, None, 0, 7, 8, 0.5, 1, 1, None) == INVALID           # odd grid
+    assert f(FAKE, 4, 8, None, 0, 8, 8, 1.5, 1, 1, None) == INVALID           # t > 1
+    assert f(FAKE, 4, 8, None, 3, 8, 8, 0.5, 1, 1, None) == INVALID           # rows_kind
+    assert f(FAKE, 65, 8, None, 0, 8, 8, 0.5, 1, 1, None) == INVALID          # more rows than pixels
+    assert f(FAKE, 17, 8, None, 2, 8, 8, 0.5, 1, 1, None) == INVALID          # more rows than blocks
+    assert f(FAKE, 4, 8, None, 1, 8, 8, 0.5, 1, 1, None) == INVALID           # half units need positions
+    assert f(FAKE, 4, 8, None, 0, 8, 8, 0.5, 1, 7, None) == UNSUPPORTED
+    assert f(None, 0, 8, None, 0, 8, 8, 0.5, 1, 1, None) == 0                 # rows == 0: no-op
+    assert lib.avits_noise_bits(-1, 4, 8, 1, FAKE, None) == INVALID
+    assert lib.avits_noise_bits(0, 4, 6, 1, FAKE, None) == INVALID
+    assert lib.avits_noise_bits(0, 0, 8, 1, None, None) == 0
