@@ -136,6 +136,9 @@ def stage_bytes(w, e: int = 2) -> dict:
     S = L + R + k
     score = N * D * e + L * D * e + 4 * H * N + 2 * N * Df * e + 12 * N
     select = 4 * N + 4 * k
+    from paper_2608_17995_amd.step import SelectiveStep
+    if N <= SelectiveStep.FUSED_MAX_N:      # the selection runs inside the scoring call (avits_score_select)
+        score, select = score + select, 0
     gather = ((L + R) * D * e + k * D * e + w.N_lr * D * e + 4 * k          # reads
               + S * D * e + (N - k) * D * e + 12 * k)                       # writes
     scatter = 2 * k * D * e + 4 * k
@@ -594,7 +597,7 @@ def _workload_legs(avits, torch, steps: int, warmup: int) -> list:
                 "block_tflops": round(fl["total"] / (per["block"] / 1e3) / 1e12, 1),
                 "block_mfma_frac": round(fl["total"] / (per["block"] / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
                 "hbm_gbs": {k: round(by[k] / (per[k] / 1e3) / 1e9, 1)
-                            for k in ("score", "select", "gather_upsample", "scatter") if per[k] > 0},
+                            for k in ("score", "select", "gather_upsample", "scatter") if per[k] > 0 and by[k] > 0},
                 "input_sets": len(sets)})
             del step
         del sets, first, bw
@@ -874,7 +877,7 @@ def main(argv=None):
     attn_tflops = fl["attention"] / (attn_ms / attn_n / 1e3) / 1e12   # one launch per step
 
     def gbs(nbytes, ms):
-        return round(nbytes / (ms / 1e3) / 1e9, 1) if ms > 0 else None
+        return round(nbytes / (ms / 1e3) / 1e9, 1) if ms > 0 and nbytes > 0 else None
 
     result = {
         "metric": METRIC,
@@ -919,8 +922,9 @@ def main(argv=None):
                   "tflops": round(fl["total"] / (stage_ms["block"] / 1e3) / 1e12, 1),
                   "mfma_frac": round(fl["total"] / (stage_ms["block"] / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
         "hbm_gbs": {s: gbs(by[s], stage_ms[s]) for s in ("score", "select", "gather_upsample", "scatter")},
-        "hbm_frac": {s: (round(gbs(by[s], stage_ms[s]) / PEAK_HBM_GBS, 4) if stage_ms[s] > 0 else None)
+        "hbm_frac": {s: (round(gbs(by[s], stage_ms[s]) / PEAK_HBM_GBS, 4) if gbs(by[s], stage_ms[s]) else None)
                      for s in ("score", "select", "gather_upsample", "scatter")},
+        "select_fused_into_score": w.N <= SelectiveStep.FUSED_MAX_N,
         "stage_traffic": measured_stage_traffic(),
         "algorithmic_bytes": by,
         "tokens_per_s": round(S / (ms_per_step / 1e3), 1),

@@ -88,6 +88,22 @@ int avits_score(const void* latent_q, const void* text_k, const float* row_lse,
                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_score_select — avits_score followed by avits_select(scores, k) in
+ * one call (Section 3.3: Eq. joint, then Eq. topk), for N <= 16384: the
+ * normalisation and the selection run in one workgroup, one launch less.
+ * scores, a_raw, v_raw and idx [k] are exactly what the two calls write.
+ * Arguments as avits_score, plus k (0 <= k <= N; k == 0 writes scores only)
+ * and idx (device int32 [k]).  N > 16384 -> AVITS_ERR_INVALID_ARG (use the
+ * two calls).  Other errors as avits_score.
+ * ---------------------------------------------------------------------- */
+int avits_score_select(const void* latent_q, const void* text_k, const float* row_lse,
+                       const void* feat_t, const void* feat_prev,
+                       int64_t N, int64_t L, int32_t H, int32_t d, int64_t D_f,
+                       float alpha, float eps, int dtype,
+                       float* scores, float* a_raw, float* v_raw, int64_t k, int32_t* idx,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_score_batched — avits_score over B equally shaped images in one
  * pass (Section 3.3, applied per image: a CFG pair, or several prompts at
  * one resolution).  Image b's min-max normalisation (Eq. joint) uses its own

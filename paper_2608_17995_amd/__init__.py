@@ -10,7 +10,8 @@ raises.
 from ._binding import (  # noqa: F401
     AvitsError, load, lib_path, version,
     F32, BF16, UP_NEAREST, UP_BILINEAR, BLOCK_DOUBLE, BLOCK_SINGLE,
-    avits_score_workspace_bytes, avits_score, avits_score_batched_workspace_bytes, avits_score_batched,
+    avits_score_workspace_bytes, avits_score, avits_score_select, avits_score_batched_workspace_bytes,
+    avits_score_batched,
     avits_select_workspace_bytes, avits_select, avits_select_perturbed, avits_select_batched,
     avits_select_noalloc, avits_select_noalloc_max_n,
     avits_gather_upsample, avits_scatter, avits_joint_lse, avits_gather_upsample_batched, avits_scatter_batched,

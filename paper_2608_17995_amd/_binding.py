@@ -45,6 +45,9 @@ _SIGS = {
     "avits_score": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i32, _i32,
                                    _i64, _f32, _f32, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                    _size, _c_void_p]),
+    "avits_score_select": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i32, _i32,
+                                          _i64, _f32, _f32, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _i64,
+                                          _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_score_batched_workspace_bytes": (_size, [_i64, _i64, _i32]),
     "avits_score_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i64,
                                            _i32, _i32, _i64, _f32, _f32, ctypes.c_int, _c_void_p, _c_void_p,
@@ -197,6 +200,24 @@ def avits_score(latent_q, text_k, row_lse, feat_t, feat_prev, alpha, eps, scores
         _dtype_code(latent_q), _dev(scores, "scores", torch.float32), _dev(a_raw, "a_raw", torch.float32),
         _dev(v_raw, "v_raw", torch.float32), wsp, wsb, _stream(stream)))
     return scores
+
+
+def avits_score_select(latent_q, text_k, row_lse, feat_t, feat_prev, alpha, eps, scores, k, idx,
+                       a_raw=None, v_raw=None, workspace=None, stream=None):
+    """avits_score then avits_select(scores, k, idx) in one call (N <= 16384)."""
+    import torch
+    N, H, d = latent_q.shape
+    L = text_k.shape[0]
+    D_f = feat_t.shape[1]
+    dt = latent_q.dtype
+    ws, wsp, wsb = _workspace(workspace, avits_score_workspace_bytes(N, H), latent_q.device)
+    _check(load().avits_score_select(
+        _dev(latent_q, "latent_q"), _dev(text_k, "text_k", dt), _dev(row_lse, "row_lse", torch.float32),
+        _dev(feat_t, "feat_t", dt), _dev(feat_prev, "feat_prev", dt), N, L, H, d, D_f, alpha, eps,
+        _dtype_code(latent_q), _dev(scores, "scores", torch.float32), _dev(a_raw, "a_raw", torch.float32),
+        _dev(v_raw, "v_raw", torch.float32), k, _dev(idx, "idx", torch.int32) if k else None, wsp, wsb,
+        _stream(stream)))
+    return scores, idx
 
 
 def avits_score_batched_workspace_bytes(B: int, N: int, H: int) -> int:

@@ -47,9 +47,10 @@ def _run(cmd):
 
 # Kernels that must compile without scratch: the GEMM's loads are
 # asynchronous inline assembly (a spilled destination would be saved before
-# the data lands), and a spill in the attention kernel's tile loop costs more
-# than half its speed.
-NO_SCRATCH = {"gemm.hip": "gemm_bf16", "attention.hip": "attn_bf16_kernel"}
+# the data lands); a spill in the attention or scoring tile loops costs more
+# than half their speed; the selections keep their keys in registers.
+NO_SCRATCH = {"gemm.hip": ("gemm_bf16",), "attention.hip": ("attn_bf16_kernel",),
+              "score.hip": ("spatial_temporal_bf16", "finalize_select"), "select.hip": ("radix_select",)}
 _USAGE = ["-Rpass-analysis=kernel-resource-usage"]
 
 
@@ -62,7 +63,7 @@ def _check_no_scratch(src: str, out: str) -> None:
             name = m.group(1)
             continue
         m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
-        if m and name and want in name and int(m.group(1)) != 0:
+        if m and name and any(w in name for w in want) and int(m.group(1)) != 0:
             raise RuntimeError(f"{src}: {name} uses {m.group(1)} bytes of scratch per lane; it must build "
                                "without spills")
 

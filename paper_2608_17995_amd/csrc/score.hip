@@ -14,6 +14,7 @@
 //  3. finalize: every workgroup reduces the same partials (min and max are
 //     exact in any order) and writes S for its slice of rows.
 #include "common.h"
+#include "select_block.h"
 
 namespace avits {
 namespace {
@@ -22,6 +23,7 @@ constexpr int kSpRows = 128;     // image rows per spatial workgroup (4 waves x 
 constexpr int kSpKeys = 64;      // text keys per LDS tile
 constexpr int kTmpBlocks = 512;  // max workgroups of the temporal pass
 constexpr int kMaxScoreImages = 4096;  // images of one batched launch (grid y / z)
+constexpr int kOneGroupMax = kThreads * kRegKeys;  // 16384: fused score + selection in one workgroup
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
@@ -96,8 +98,7 @@ __global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
     const int rr = wrow0 + j * rpi + r_in;
     if (cc == 0 && rr < N) part_v[int64_t(h) * N + rr] = acc;
   };
-  u32x4 cx, cy, nx, ny;  // pair in flight for this tile, pair for the next
-  issue_pair(0, cx, cy);
+  u32x4 cx, cy;  // the feature pair of the current key tile
 
   // ---- spatial: Q^T fragments (B operand), lane = row l32, dims 16c + 8hi .. +7 ----
   bf16x8 qf[kC];
@@ -113,8 +114,8 @@ __global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
 
   // Text keys: tile t + 2 is loaded into registers while tile t is
   // multiplied and stored to LDS at the end of tile t + 1 (two LDS buffers,
-  // two register sets, one barrier per tile), so a key load has two tiles of
-  // work to arrive in.
+  // two register sets, one barrier per tile that waits for LDS only), so a
+  // key load has two tiles of work to arrive in.
   auto load_k = [&](u32x4 (&kr)[kKP], int k0) {
 #pragma unroll
     for (int j = 0; j < kKP; ++j) {
@@ -131,46 +132,54 @@ __global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
     }
   };
   int jt = 0;  // key tiles done = temporal pairs consumed
+  // The two 32-key sub-tiles of a tile are two independent MFMA chains,
+  // both issued before any exp2, and four partial sums per lane break the
+  // chain of adds.  acc[t][r] = logit of key 32t + 8(r/4) + 4hi + r%4
+  // against this lane's row; exp2 is the hardware instruction (about 1 ulp;
+  // terms below 2^-126 flush to zero); only the last tile masks keys past L.
+  float ps[4] = {0.f, 0.f, 0.f, 0.f};
+  static_assert(kSpKeys == 64, "two 32-key sub-tiles per tile");
   // One key tile from ks[buf] at k0; knext1 holds tile k0 + 64 (in flight),
-  // knext2 receives tile k0 + 128.
+  // knext2 receives tile k0 + 128.  The tile's feature pair is issued first
+  // and consumed at the end of the tile.
   auto tile = [&](int buf, int k0, u32x4 (&knext2)[kKP], const u32x4 (&knext1)[kKP]) {
+    issue_pair(jt, cx, cy);
     if (k0 + 2 * kSpKeys < L) load_k(knext2, k0 + 2 * kSpKeys);
-    issue_pair(jt + 1, nx, ny);
-    const bool full = k0 + kSpKeys <= L;
+    f32x16 acc[2];
 #pragma unroll
-    for (int t = 0; t < kSpKeys / 32; ++t) {
-      f32x16 acc;
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+      for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
 #pragma unroll
-      for (int c = 0; c < kC; ++c) {
+    for (int c = 0; c < kC; ++c)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
         const bf16x8 kf =
             as_bf16x8(*reinterpret_cast<const u32x4*>(&ks[buf][(32 * t + l32) * kLds + 16 * c + 8 * hi]));
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], acc, 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], acc[t], 0, 0, 0);
       }
-      // acc[r] = logit of key 32t + 8(r/4) + 4hi + r%4 against this lane's
-      // row.  exp2 is the hardware instruction (about 1 ulp; terms below
-      // 2^-126 flush to zero); only the last tile masks keys past L.
-      if (full) {
+    if (k0 + kSpKeys <= L) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) psum += __builtin_amdgcn_exp2f(fmaf(acc[r], scale2, -lse2));
-      } else {
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ps[r & 3] += __builtin_amdgcn_exp2f(fmaf(acc[t][r], scale2, -lse2));
+    } else {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = k0 + 32 * t + 8 * (r / 4) + 4 * hi + (r % 4);
-          const float e = __builtin_amdgcn_exp2f(fmaf(acc[r], scale2, -lse2));
-          psum += key < L ? e : 0.f;
+          const float e = __builtin_amdgcn_exp2f(fmaf(acc[t][r], scale2, -lse2));
+          ps[r & 3] += key < L ? e : 0.f;
         }
-      }
     }
     consume_pair(jt, cx, cy);
-    cx = nx;
-    cy = ny;
     ++jt;
     // The other buffer was last read one tile ago, before the barrier that
-    // ended that tile, so it can be refilled now.
+    // ended that tile, so it can be refilled now.  The barrier waits for
+    // LDS only: the key loads in flight stay in flight.
     if (k0 + kSpKeys < L) store_k(knext1, buf ^ 1);
-    __syncthreads();
+    lds_barrier();
   };
   u32x4 ka[kKP], kb[kKP];
   load_k(ka, 0);
@@ -182,21 +191,19 @@ __global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
     if (k0 + kSpKeys >= L) break;
     tile(1, k0 + kSpKeys, kb, ka);
   }
+  psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
   psum += __shfl_xor(psum, 32, kWave);
   if (hi == 0 && row < N) part_a[int64_t(h) * N + row] = psum;
-  // Pairs left when the slice has more pairs than there are key tiles
-  // (cx, cy hold pair jt, in flight): issued in batches so their loads
-  // overlap instead of waiting one after another.
+  // Pairs left when the slice has more pairs than there are key tiles:
+  // issued in batches so their loads overlap instead of waiting one after
+  // another.
   constexpr int kBatch = 8;
   while (jt < npairs) {
     u32x4 bx[kBatch], by[kBatch];
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) issue_pair(jt + 1 + u, bx[u], by[u]);
-    consume_pair(jt, cx, cy);
+    for (int u = 0; u < kBatch; ++u) issue_pair(jt + u, bx[u], by[u]);
 #pragma unroll
-    for (int u = 0; u < kBatch - 1; ++u) consume_pair(jt + 1 + u, bx[u], by[u]);
-    cx = bx[kBatch - 1];
-    cy = by[kBatch - 1];
+    for (int u = 0; u < kBatch; ++u) consume_pair(jt + u, bx[u], by[u]);
     jt += kBatch;
   }
 
@@ -513,6 +520,45 @@ __global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__
   }
 }
 
+// 3'. The fused score and the top-k selection in one workgroup (N <= 16384):
+// the min/max partials reduced, each thread's consecutive scores computed
+// (the arithmetic of finalize_kernel, so the scores are the same bits) and
+// written, then selected from registers (Eq. topk, lowest-index ties).
+__global__ __launch_bounds__(kThreads) void finalize_select_kernel(const float* __restrict__ a,
+                                                                   const float* __restrict__ v,
+                                                                   const float4* __restrict__ mm, int n_mm, int N,
+                                                                   float alpha, float eps, float* __restrict__ scores,
+                                                                   int k, int32_t* __restrict__ idx) {
+  __shared__ float4 red[kWaves];
+  float4 r = make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
+  for (int i = threadIdx.x; i < n_mm; i += kThreads) {
+    const float4 m = mm[i];
+    r.x = fminf(r.x, m.x); r.y = fmaxf(r.y, m.y); r.z = fminf(r.z, m.z); r.w = fmaxf(r.w, m.w);
+  }
+  r.x = wave_min(r.x); r.y = wave_max(r.y); r.z = wave_min(r.z); r.w = wave_max(r.w);
+  if (threadIdx.x % kWave == 0) red[threadIdx.x / kWave] = r;
+  __syncthreads();
+  float4 t = red[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) {
+    t.x = fminf(t.x, red[w].x); t.y = fmaxf(t.y, red[w].y); t.z = fminf(t.z, red[w].z); t.w = fmaxf(t.w, red[w].w);
+  }
+  const float ia = 1.f / (t.y - t.x + eps), iv = 1.f / (t.w - t.z + eps);
+  const int q = (N + kThreads - 1) / kThreads;
+  uint32_t keys[kRegKeys];
+#pragma unroll
+  for (int j = 0; j < kRegKeys; ++j) {
+    const int i = int(threadIdx.x) * q + j;
+    const bool live = j < q && i < N;
+    const int ic = live ? i : 0;
+    const float an = (a[ic] - t.x) * ia, vn = (v[ic] - t.z) * iv;
+    const float sc = alpha * an + (1.f - alpha) * vn;
+    if (live) scores[i] = sc;
+    keys[j] = live ? order_key(sc) : 0u;
+  }
+  if (k > 0) select_block_keys(keys, N, k, idx);
+}
+
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 
 struct ScoreWs {
@@ -545,7 +591,8 @@ ScoreWs score_ws_layout(char* base, int64_t N, int32_t H, int64_t B = 1) {
 int score_launch(const char* who, const void* latent_q, const void* text_k, const float* row_lse,
                  const void* feat_t, const void* feat_prev, int64_t B, int64_t N, int64_t L, int32_t H, int32_t d,
                  int64_t D_f, float alpha, float eps, int dtype, float* scores, float* a_raw, float* v_raw,
-                 void* workspace, size_t workspace_bytes, void* stream) {
+                 void* workspace, size_t workspace_bytes, void* stream, int64_t sel_k = -1,
+                 int32_t* sel_idx = nullptr) {
   AVITS_REQUIRE(B >= 1 && B <= kMaxScoreImages, "%s: B=%lld images outside [1, %d]", who, (long long)B,
                 kMaxScoreImages);
   AVITS_REQUIRE(N >= 1 && N <= INT32_MAX, "%s: N=%lld outside [1, 2^31)", who, (long long)N);
@@ -602,6 +649,13 @@ int score_launch(const char* who, const void* latent_q, const void* text_k, cons
     hipLaunchKernelGGL(temporal_kernel<float>, dim3(nmm, nimg), dim3(256), 0, s, (const float*)feat_t,
                        (const float*)feat_prev, ws.part, N, H, D_f, a_dst, v_dst, ws.mm);
   }
+  if (sel_k >= 0) {
+    // One image, N <= kOneGroupMax: the score and the selection in one workgroup.
+    TimedLaunch timed("score_finalize", s);
+    hipLaunchKernelGGL(finalize_select_kernel, dim3(1), dim3(kThreads), 0, s, a_dst, v_dst, ws.mm, nmm, n, alpha,
+                       eps, scores, int(sel_k), sel_idx);
+    return launch_status(who);
+  }
   const int fblocks = int(std::min<int64_t>(256, (N + 255) / 256));
   TimedLaunch timed("score_finalize", s);
   hipLaunchKernelGGL(finalize_kernel, dim3(fblocks, nimg), dim3(256), 0, s, a_dst, v_dst, ws.mm, nmm, N, alpha,
@@ -630,6 +684,19 @@ extern "C" int avits_score(const void* latent_q, const void* text_k, const float
                            void* workspace, size_t workspace_bytes, void* stream) {
   return score_launch("score", latent_q, text_k, row_lse, feat_t, feat_prev, 1, N, L, H, d, D_f, alpha, eps, dtype,
                       scores, a_raw, v_raw, workspace, workspace_bytes, stream);
+}
+
+extern "C" int avits_score_select(const void* latent_q, const void* text_k, const float* row_lse,
+                                  const void* feat_t, const void* feat_prev, int64_t N, int64_t L, int32_t H,
+                                  int32_t d, int64_t D_f, float alpha, float eps, int dtype, float* scores,
+                                  float* a_raw, float* v_raw, int64_t k, int32_t* idx, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  AVITS_REQUIRE(N >= 1 && N <= kOneGroupMax, "score_select: N=%lld outside [1, %d] (use avits_score + avits_select)",
+                (long long)N, kOneGroupMax);
+  AVITS_REQUIRE(k >= 0 && k <= N, "score_select: k=%lld outside [0, N=%lld]", (long long)k, (long long)N);
+  AVITS_REQUIRE(k == 0 || idx, "score_select: null idx");
+  return score_launch("score_select", latent_q, text_k, row_lse, feat_t, feat_prev, 1, N, L, H, d, D_f, alpha, eps,
+                      dtype, scores, a_raw, v_raw, workspace, workspace_bytes, stream, k, idx);
 }
 
 extern "C" int avits_score_batched(const void* latent_q, const void* text_k, const float* row_lse,

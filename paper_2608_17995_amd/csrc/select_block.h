@@ -1,0 +1,186 @@
+// One-workgroup radix selection of the top k of N <= 16384 fp32 values held
+// in registers (Eq. topk): order-preserving uint32 keys, four 8-bit digit
+// passes with per-wave LDS histograms, and an index-ordered emission so ties
+// go to the lowest index and the output is ascending.  Shared by the
+// selection entry points and the fused score + selection.
+#pragma once
+
+#include "common.h"
+
+namespace avits {
+namespace {
+
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / kWave;
+
+__device__ __forceinline__ uint32_t order_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;  // NaN ranks lowest
+  if (u == 0x80000000u) u = 0u;                     // -0.0 == +0.0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Key of element i: of scores[i], or of the fp32 sum scores[i] + delta[i]
+// when a perturbation is given (the seeded tie-break of Eq. topk).
+__device__ __forceinline__ uint32_t key_at(const float* __restrict__ scores, const float* __restrict__ delta,
+                                           int64_t i) {
+  return order_key(delta ? scores[i] + delta[i] : scores[i]);
+}
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// Exclusive prefix sum over the workgroup; returns the total in *total.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  uint32_t incl = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t t = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += t;
+  }
+  __syncthreads();
+  if (lane == kWave - 1) wsum[wave] = incl;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t s = wsum[w];
+    before += w < wave ? s : 0u;
+    all += s;
+  }
+  *total = all;
+  return before + incl - v;
+}
+
+// kRegKeys keys per thread stay in registers: N <= 16384.
+constexpr int kRegKeys = 16;
+
+// The selection of one workgroup of kThreads threads over N <= 16384 keys
+// held in registers: thread t holds the q = ceil(N / kThreads) consecutive
+// elements t q .. t q + q - 1 in keys[0 .. q) (so the final emission needs a
+// single workgroup scan); keys past N are ignored.  Writes the indices of
+// the k largest keys (ties: lowest index) to idx in ascending order.
+__device__ __forceinline__ void select_block_keys(const uint32_t (&keys)[kRegKeys], int N, int k,
+                                                  int32_t* __restrict__ idx) {
+  __shared__ uint32_t hist[kWaves][256];   // per-wave histograms: atomics contend only inside a wave
+  __shared__ uint32_t tot_s[256], suf_s[256];
+  __shared__ uint32_t wsum[kWaves];
+  __shared__ uint32_t s_digit, s_above;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = (N + kThreads - 1) / kThreads;
+
+  uint32_t prefix = 0u, mask = 0u;
+  uint32_t remaining = uint32_t(k);  // rank of the k-th largest among the current candidates
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = tid; b < kWaves * 256; b += kThreads) (&hist[0][0])[b] = 0u;
+    __syncthreads();
+    // Scores of one exponent share their top digits, so a wave first adds
+    // its most frequent-looking digit(s) with one ballot-counted atomic
+    // (two rounds in the first pass, one later), then the rest one by one.
+    const int rounds = shift == 24 ? 2 : 1;
+#pragma unroll
+    for (int j = 0; j < kRegKeys; ++j) {
+      if (j >= q) break;  // uniform
+      const int i = tid * q + j;
+      const uint32_t key = keys[j];
+      bool pending = i < N && (key & mask) == prefix;
+      const uint32_t digit = (key >> shift) & 255u;
+      for (int it = 0; it < rounds; ++it) {
+        const uint64_t act = __ballot(pending);
+        if (act == 0) break;
+        const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
+        const uint32_t d0 = __shfl(digit, leader, kWave);
+        const uint64_t same = __ballot(pending && digit == d0);
+        if (lane == leader) atomicAdd(&hist[wave][d0], uint32_t(__popcll(same)));
+        pending = pending && digit != d0;
+      }
+      if (pending) atomicAdd(&hist[wave][digit], 1u);
+    }
+    __syncthreads();
+    // Waves 0..3 own digits 64w .. 64w + 63: the count per digit and its
+    // suffix sum inside the wave (shuffle scan from the high lanes down).
+    if (wave < 4) {
+      const int b = 64 * wave + lane;
+      uint32_t c = 0u;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) c += hist[w][b];
+      uint32_t suf = c;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t t = __shfl_down(suf, o, kWave);
+        if (lane + o < kWave) suf += t;
+      }
+      tot_s[b] = c;
+      suf_s[b] = suf;
+      if (lane == 0) wsum[wave] = suf;  // this wave's 64 digits in total
+    }
+    __syncthreads();
+    // The selected digit b has (candidates above b) < remaining <= (candidates at or above b).
+    if (wave < 4) {
+      const int b = 64 * wave + lane;
+      uint32_t higher = 0u;
+      for (int w = wave + 1; w < 4; ++w) higher += wsum[w];
+      const uint32_t c = tot_s[b];
+      const uint32_t above = suf_s[b] - c + higher;
+      if (above < remaining && above + c >= remaining) {
+        s_digit = uint32_t(b);
+        s_above = above;
+      }
+    }
+    __syncthreads();
+    prefix |= s_digit << shift;
+    mask |= 255u << shift;
+    remaining -= s_above;
+    __syncthreads();
+  }
+  // T = prefix; `remaining` elements equal to T are still needed.  One
+  // workgroup scan of the per-thread counts of keys > T and == T gives each
+  // thread its output offset; the threads' element ranges are consecutive,
+  // so the output is in index order and the first `need` keys equal to T
+  // (lowest indices) are the ones taken.
+  const uint32_t T = prefix, need = remaining;
+  uint32_t gt_c = 0u, eq_c = 0u;
+#pragma unroll
+  for (int j = 0; j < kRegKeys; ++j) {
+    if (j < q && tid * q + j < N) {
+      gt_c += keys[j] > T;
+      eq_c += keys[j] == T;
+    }
+  }
+  uint32_t tot;
+  // Packed counts: low 16 bits equal-to-T, high 16 bits greater-than-T (N <= 16384).
+  const uint32_t ex = block_exclusive_scan(eq_c | (gt_c << 16), wsum, &tot);
+  uint32_t eq_seen = ex & 0xffffu;
+  uint32_t at = (ex >> 16) + min(eq_seen, need);
+#pragma unroll
+  for (int j = 0; j < kRegKeys; ++j) {
+    const int i = tid * q + j;
+    if (j < q && i < N) {
+      const uint32_t key = keys[j];
+      if (key > T) {
+        idx[at++] = i;
+      } else if (key == T) {
+        if (eq_seen < need) idx[at++] = i;
+        ++eq_seen;
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void select_block(const float* __restrict__ scores, const float* __restrict__ delta,
+                                             int N, int k, int32_t* __restrict__ idx) {
+  const int q = (N + kThreads - 1) / kThreads;
+  uint32_t keys[kRegKeys];
+#pragma unroll
+  for (int j = 0; j < kRegKeys; ++j) {
+    const int i = int(threadIdx.x) * q + j;
+    keys[j] = j < q && i < N ? key_at(scores, delta, i) : 0u;
+  }
+  select_block_keys(keys, N, k, idx);
+}
+
+}  // namespace
+}  // namespace avits

@@ -56,12 +56,22 @@ class SelectiveStep:
             max(B.avits_block_workspace_bytes(weights.kind, s.S, s.H, d, s.mlp_hidden, code), 1),
             dtype=torch.uint8, device=device)
 
+    # Up to 8192 scored tokens the selection runs inside the scoring call
+    # (avits_score_select, one launch less); select() then has nothing left
+    # to do.  At 16384 the one-workgroup normalisation costs more than the
+    # launch it saves (measured on MI355X), so the two calls stay separate.
+    FUSED_MAX_N = 8192
+
     def score(self, latent_q, text_k, row_lse, feat_t, feat_prev, stream=None):
-        B.avits_score(latent_q, text_k, row_lse, feat_t, feat_prev, self.alpha, self.eps, self.scores,
-                      self.a_raw, self.v_raw, self.ws_score, stream)
+        if self.shape.N <= self.FUSED_MAX_N:
+            B.avits_score_select(latent_q, text_k, row_lse, feat_t, feat_prev, self.alpha, self.eps, self.scores,
+                                 self.shape.k, self.idx, self.a_raw, self.v_raw, self.ws_score, stream)
+        else:
+            B.avits_score(latent_q, text_k, row_lse, feat_t, feat_prev, self.alpha, self.eps, self.scores,
+                          self.a_raw, self.v_raw, self.ws_score, stream)
 
     def select(self, stream=None):
-        if self.shape.k:
+        if self.shape.k and self.shape.N > self.FUSED_MAX_N:
             B.avits_select(self.scores, self.shape.k, self.idx, self.ws_select, stream)
 
     def gather(self, lowres, highres_prev, prefix, stream=None):

@@ -63,6 +63,42 @@ def test_score(gpu, w):
     np.testing.assert_allclose(host(V), v_ref, rtol=1e-4)
 
 
+def _score_select_case(gpu, w, k, scores_override=None):
+    si = G.score_inputs(w)
+    lse = _lse_gpu(gpu, w, si)
+    args = [dev(si["latent_q"], w.dtype), dev(si["text_k"], w.dtype), lse, dev(si["feat_t"], w.dtype),
+            dev(si["feat_prev"], w.dtype), w.alpha, w.eps_minmax]
+    S1, A1, V1 = (torch.empty(w.N, device="cuda") for _ in range(3))
+    S2, A2, V2 = (torch.full((w.N,), float("nan"), device="cuda") for _ in range(3))
+    idx1 = torch.empty(k, dtype=torch.int32, device="cuda")
+    idx2 = torch.full((k,), -1, dtype=torch.int32, device="cuda")
+    gpu.avits_score(*args, S1, A1, V1)
+    if k:
+        gpu.avits_select(S1, k, idx1)
+    gpu.avits_score_select(*args, S2, k, idx2, A2, V2)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(S2.cpu().numpy(), S1.cpu().numpy())
+    np.testing.assert_array_equal(A2.cpu().numpy(), A1.cpu().numpy())
+    np.testing.assert_array_equal(V2.cpu().numpy(), V1.cpu().numpy())
+    np.testing.assert_array_equal(idx2.cpu().numpy(), idx1.cpu().numpy())
+    np.testing.assert_array_equal(idx2.cpu().numpy(), oracle.select_topk(S2.cpu().numpy(), k))
+
+
+@pytest.mark.parametrize("w", TINY, ids=IDS)
+def test_score_select_matches_the_two_calls(gpu, w):
+    # The fused call writes the same scores and raw terms, bit for bit, and
+    # the selection of them; every k regime (none, a few, the workload's, all).
+    for k in sorted({0, 1, w.k, w.N - 1, w.N}):
+        _score_select_case(gpu, w, k)
+
+
+@pytest.mark.parametrize("lr", [(32, 32), (64, 64), (40, 51)], ids=["N4096", "N16384", "N8160"])
+def test_score_select_sizes(gpu, lr):
+    # Up to the one-workgroup limit, with a ragged size and the FLUX head layout shrunk to 2 heads.
+    w = C.TINY_BF16.replace(H_lr=lr[0], W_lr=lr[1])
+    _score_select_case(gpu, w, C.keep_count(0.3, w.N))
+
+
 @pytest.mark.parametrize("w", [C.TINY_F32, C.TINY_BF16], ids=["f32", "bf16"])
 def test_score_without_optional_outputs_and_small_feature_width(gpu, w):
     # D_f = 64 (the packed-latent reading of the snapshots); A/V outputs omitted.
