@@ -72,7 +72,7 @@ def measured_traffic() -> dict | None:
 # scatter), from the same two counter passes over the step's kernels; reported
 # only while the sources of those kernels hash to what they were then.
 STAGE_TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "stages_flux1024_hbm_traffic.md")
-STAGE_SOURCES = ("score.hip", "select.hip", "relayout.hip", "common.h")
+STAGE_SOURCES = ("score.hip", "select.hip", "select_block.h", "relayout.hip", "common.h")
 
 LEGS = ("fused_scoring", "block_mass", "select_sweep", "mixed_stage2", "batched", "workloads", "stack",
         "three_stage")

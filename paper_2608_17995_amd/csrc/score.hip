@@ -50,10 +50,24 @@ __global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
   constexpr int kKP = kSpKeys * DH / 8 / 256; // 16-byte K pieces per thread per tile
   __shared__ __attribute__((aligned(16))) bf16_t ks[2][kSpKeys * kLds];
 
-  const int h = blockIdx.y;
+  // Workgroup b of an image's n = row blocks x heads runs on XCD b mod 8;
+  // renumber so that each XCD takes a contiguous range of (head, row block)
+  // ids, head-major: the row blocks of a head share one L2, which then
+  // fetches that head's text keys once.
+  int h, rb;
+  {
+    const int n_rb = int(gridDim.x), n = n_rb * int(gridDim.y);
+    const int b = int(blockIdx.x) + n_rb * int(blockIdx.y);
+    const int x = b % 8;
+    int start = 0;
+    for (int y = 0; y < x; ++y) start += (n - y + 7) / 8;
+    const int u = start + b / 8;
+    h = u / n_rb;
+    rb = u % n_rb;
+  }
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int l32 = lane % 32, hi = lane / 32;
-  const int wrow0 = blockIdx.x * kSpRows + wave * 32;  // this wave's 32 rows
+  const int wrow0 = rb * kSpRows + wave * 32;  // this wave's 32 rows
   const int row = wrow0 + l32;
   const int64_t qstride = int64_t(H) * DH;
   {  // image blockIdx.z of a stack of equally shaped images
