@@ -141,7 +141,7 @@ def stage_bytes(w, e: int = 2) -> dict:
         score, select = score + select, 0
     gather = ((L + R) * D * e + k * D * e + w.N_lr * D * e + 4 * k          # reads
               + S * D * e + (N - k) * D * e + 12 * k)                       # writes
-    scatter = 2 * k * D * e + 4 * k
+    scatter = 0         # the scatter rides on the block's last projection (the block stage's bytes)
     return {"score": score, "select": select, "gather_upsample": gather, "scatter": scatter}
 
 
@@ -925,6 +925,7 @@ def main(argv=None):
         "hbm_frac": {s: (round(gbs(by[s], stage_ms[s]) / PEAK_HBM_GBS, 4) if gbs(by[s], stage_ms[s]) else None)
                      for s in ("score", "select", "gather_upsample", "scatter")},
         "select_fused_into_score": w.N <= SelectiveStep.FUSED_MAX_N,
+        "scatter_fused_into_block": True,
         "stage_traffic": measured_stage_traffic(),
         "algorithmic_bytes": by,
         "tokens_per_s": round(S / (ms_per_step / 1e3), 1),

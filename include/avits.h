@@ -310,14 +310,26 @@ int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, float
  * running maximum, so it costs no second Q K^T pass.  With
  * mass_accumulate != 0 it is added to what `mass` holds (the aggregation
  * over blocks and collection steps of Section 3.3.1; avits_score_from_mass
- * divides by their count).  outs may be NULL (= avits_block_forward without
- * lse).  lse and mass [H, S] fp32 device buffers or NULL; other arguments
- * and errors as avits_block_forward.
+ * divides by their count).
+ * The Stage-3 scatter of Section 3.2 can ride on the block's last
+ * projection: with scatter_k > 0, the output rows of the last scatter_k
+ * image rows (x_out rows S - scatter_k + j) are also written to
+ * canvas[scatter_idx[j]] (bit-identical to avits_scatter after the block;
+ * an index outside [0, n_canvas) is skipped).  canvas [n_canvas, D] of
+ * dtype, not aliasing x_in or x_out; scatter_idx [scatter_k] int32; 0 <=
+ * scatter_k <= n_img.
+ * outs may be NULL (= avits_block_forward without lse).  lse and mass
+ * [H, S] fp32 device buffers or NULL; other arguments and errors as
+ * avits_block_forward.
  * ---------------------------------------------------------------------- */
 typedef struct avits_block_outputs {
-  float* lse;               /* [H, S] or NULL */
-  float* mass;              /* [H, S] or NULL */
-  int32_t mass_accumulate;  /* nonzero: mass += this block's mass */
+  float* lse;                  /* [H, S] or NULL */
+  float* mass;                 /* [H, S] or NULL */
+  int32_t mass_accumulate;     /* nonzero: mass += this block's mass */
+  const int32_t* scatter_idx;  /* [scatter_k] or NULL */
+  int64_t scatter_k;           /* 0: no fused scatter */
+  void* canvas;                /* [n_canvas, D] or NULL */
+  int64_t n_canvas;
 } avits_block_outputs;
 
 int avits_block_forward_ex(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,

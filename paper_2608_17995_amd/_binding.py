@@ -30,7 +30,9 @@ class _Single(ctypes.Structure):
 
 
 class _BlockOutputs(ctypes.Structure):
-    _fields_ = [("lse", ctypes.c_void_p), ("mass", ctypes.c_void_p), ("mass_accumulate", ctypes.c_int32)]
+    _fields_ = [("lse", ctypes.c_void_p), ("mass", ctypes.c_void_p), ("mass_accumulate", ctypes.c_int32),
+                ("scatter_idx", ctypes.c_void_p), ("scatter_k", ctypes.c_int64), ("canvas", ctypes.c_void_p),
+                ("n_canvas", ctypes.c_int64)]
 
 
 class _BlockWeights(ctypes.Structure):
@@ -481,18 +483,24 @@ def avits_block_forward(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H
 
 
 def avits_block_forward_ex(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H, lse_out=None, mass_out=None,
-                           mass_accumulate=False, workspace=None, stream=None, pos_scale=1.0):
+                           mass_accumulate=False, workspace=None, stream=None, pos_scale=1.0, scatter_idx=None,
+                           canvas=None):
     """avits_block_forward with the joint attention's statistics: lse_out and
     mass_out [H, S] fp32 (the softmax mass of each row on the text keys
-    [0, n_txt), added to mass_out's contents when mass_accumulate)."""
+    [0, n_txt), added to mass_out's contents when mass_accumulate); with
+    scatter_idx [k] and canvas, the last k image rows' outputs also go to
+    canvas[scatter_idx] (the fused Stage-3 scatter)."""
     import torch
     S, D = x_in.shape
     d = D // H
     code = _dtype_code(x_in)
     ws, wsp, wsb = _workspace(
         workspace, avits_block_workspace_bytes(weights.kind, S, H, d, weights.c.mlp_hidden, code), x_in.device)
+    k = 0 if scatter_idx is None else scatter_idx.shape[0]
     outs = _BlockOutputs(_dev(lse_out, "lse_out", torch.float32), _dev(mass_out, "mass_out", torch.float32),
-                         1 if mass_accumulate else 0)
+                         1 if mass_accumulate else 0, _dev(scatter_idx, "scatter_idx", torch.int32) if k else None, k,
+                         _dev(canvas, "canvas", x_in.dtype) if canvas is not None else None,
+                         canvas.shape[0] if canvas is not None else 0)
     _check(load().avits_block_forward_ex(
         _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), pos_scale, n_txt, n_img,
         ctypes.byref(weights.c), H, d, code, ctypes.byref(outs), wsp, wsb, _stream(stream)))

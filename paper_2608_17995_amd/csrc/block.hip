@@ -333,7 +333,8 @@ int run_block_qk(const void* x_in, const int32_t* pos, float pos_scale, int64_t 
 template <typename T>
 int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale, int64_t n_txt, int64_t n_img,
               const avits_block_weights* w, int H, int d, int dtype, float* lse_out, const BlockWs& ws,
-              hipStream_t s, const AttnSegs* segs = nullptr, float* mass_out = nullptr, int mass_accumulate = 0) {
+              hipStream_t s, const AttnSegs* segs = nullptr, float* mass_out = nullptr, int mass_accumulate = 0,
+              const avits_block_outputs* sc = nullptr) {
   const int64_t S = n_txt + n_img, D = int64_t(H) * d, F = w->mlp_hidden;
   const bool dbl = w->kind == AVITS_BLOCK_DOUBLE;
   const T* x = static_cast<const T*>(x_in);
@@ -412,12 +413,23 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
   }
 
   T* out = static_cast<T*>(x_out);
+  // The Stage-3 scatter rides on the last projection: the output rows of the
+  // last scatter_k image rows also go to their canvas rows.
+  auto set_scatter = [&](GemmProblem& p, int64_t rows) {
+    if (!sc || !sc->canvas || sc->scatter_k == 0) return;
+    p.scat = sc->canvas;
+    p.scat_idx = sc->scatter_idx;
+    p.scat_row0 = rows - sc->scatter_k;
+    p.scat_ld = D;
+    p.scat_n = sc->n_canvas;
+  };
   if (!dbl) {
     GemmArgs g{};
     g.N = D; g.K = D + F; g.n_split = g.n_split2 = g.N; g.mode0 = EPI_RESID_GATE; g.nprob = 1;
     GemmProblem& p = g.p[0];
     p.A = ws.o; p.lda = D + F; p.W = w->single.w_out; p.bias = w->single.b_out; p.M = S;
     p.out0 = out; p.ld0 = D; p.resid = x; p.ldr = D; p.gate = mod_row(w->single.mod, 2);
+    set_scatter(p, S);
     return launch_gemm(g, dtype, s, "gemm_single_out", ws.partial, ws.partial_bytes);
   }
 
@@ -472,6 +484,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
       p.A = mlp + r0 * F; p.lda = F; p.W = streams[i].dw->w_mlp2; p.bias = streams[i].dw->b_mlp2;
       p.M = streams[i].rows; p.out0 = out + r0 * D; p.ld0 = D; p.resid = xmid + r0 * D; p.ldr = D;
       p.gate = mod_row(streams[i].dw->mod, 5);
+      if (r0 == n_txt && n_img > 0) set_scatter(p, n_img);   // the image stream
     }
     if ((rc = launch_gemm(g, dtype, s, "gemm_mlp_out", ws.partial, ws.partial_bytes)) != AVITS_OK) return rc;
   }
@@ -580,12 +593,20 @@ extern "C" int avits_block_forward_ex(const void* x_in, void* x_out, const int32
     return set_error(AVITS_ERR_WORKSPACE, "block_forward: workspace of %zu bytes, need %zu", workspace_bytes,
                      need.bytes);
   const BlockWs ws = block_ws_layout(static_cast<char*>(workspace), w->kind, S, H, d, w->mlp_hidden, esz);
+  if (outs->canvas || outs->scatter_k) {
+    AVITS_REQUIRE(outs->scatter_k >= 0 && outs->scatter_k <= n_img,
+                  "block_forward_ex: scatter_k=%lld outside [0, n_img=%lld]", (long long)outs->scatter_k,
+                  (long long)n_img);
+    AVITS_REQUIRE(outs->scatter_k == 0 || (outs->canvas && outs->scatter_idx && outs->n_canvas >= 1),
+                  "block_forward_ex: scatter needs canvas, scatter_idx and n_canvas >= 1");
+    AVITS_REQUIRE(outs->canvas != x_in && outs->canvas != x_out, "block_forward_ex: canvas must not alias x_in/x_out");
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == AVITS_BF16)
     return run_block<bf16_t>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, outs->lse, ws, s, nullptr,
-                             outs->mass, outs->mass_accumulate);
+                             outs->mass, outs->mass_accumulate, outs);
   return run_block<float>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, outs->lse, ws, s, nullptr,
-                          outs->mass, outs->mass_accumulate);
+                          outs->mass, outs->mass_accumulate, outs);
 }
 
 extern "C" int avits_block_forward_batched(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,

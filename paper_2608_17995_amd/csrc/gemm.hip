@@ -52,6 +52,16 @@ __device__ __forceinline__ f32x16 mfma32x32x16(const bf16x8& a, const bf16x8& b,
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// The fused scatter: region 0's final row m (columns from col, stored as
+// the vector w) also goes to its canvas row, when the problem has one.
+template <typename T, typename V>
+__device__ __forceinline__ void scatter_copy(const GemmProblem& p, int64_t m, int64_t col, const V& w) {
+  if (!p.scat || m < p.scat_row0) return;
+  const int64_t q = p.scat_idx[m - p.scat_row0];
+  if (q < 0 || q >= p.scat_n) return;
+  *reinterpret_cast<V*>(static_cast<T*>(p.scat) + q * p.scat_ld + col) = w;
+}
+
 // Epilogue for four consecutive columns n..n+3 of row m of problem p (the
 // four columns never straddle a region boundary: region starts are
 // multiples of 4).
@@ -91,8 +101,11 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, const GemmProblem& 
   if constexpr (sizeof(T) == 2) {
     u32x2 w = {pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
     *reinterpret_cast<u32x2*>(dst) = w;
+    if (n < a.n_split) scatter_copy<T>(p, m, col, w);
   } else {
-    *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+    const float4 w = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4*>(dst) = w;
+    if (n < a.n_split) scatter_copy<T>(p, m, col, w);
   }
 }
 
@@ -142,6 +155,7 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& a, const GemmProblem& 
   }
   const u32x4 w = {pack_bf2(x[0], x[1]), pack_bf2(x[2], x[3]), pack_bf2(x[4], x[5]), pack_bf2(x[6], x[7])};
   *reinterpret_cast<u32x4*>(out + m * ldo + col) = w;
+  if (r0) scatter_copy<bf16_t>(p, m, col, w);
 }
 
 // Split-K reduce fused with the modulated layer norm that follows the
@@ -413,6 +427,7 @@ __device__ __forceinline__ void staged_epilogue(const GemmArgs& a, const GemmPro
           }
           const u32x2 w = {pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
           *reinterpret_cast<u32x2*>(out + m * ldo + col) = w;
+          if (n < a.n_split) scatter_copy<bf16_t>(p, m, col, w);
         }
       }
     }

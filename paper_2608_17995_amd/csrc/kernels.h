@@ -36,6 +36,13 @@ struct GemmProblem {
   const void* resid;   // EPI_RESID_GATE: [M, ldr], same columns as the region
   int64_t ldr;
   const void* gate;    // EPI_RESID_GATE: [N]
+  // Optional second destination of region 0's final rows (the Stage-3
+  // scatter fused into a block's last projection): row m >= scat_row0 also
+  // goes to scat[scat_idx[m - scat_row0] * scat_ld + column] when that index
+  // lies in [0, scat_n).
+  void* scat;
+  const int32_t* scat_idx;
+  int64_t scat_row0, scat_ld, scat_n;
 };
 
 struct GemmArgs {

@@ -47,6 +47,7 @@ class SelectiveStep:
         self.pos[: s.L + s.R].copy_(prefix_pos)
         self.x_out = torch.empty(s.S, s.D, dtype=dtype, device=device)
         self.canvas = canvas  # None: the canvas aliases highres_prev (in-place update)
+        self._step_canvas = canvas
         self.lse = torch.empty(s.H, s.S, dtype=f32, device=device) if keep_lse else None
         d = s.D // s.H
         self.ws_score = torch.empty(max(B.avits_score_workspace_bytes(s.N, s.H), 1), dtype=torch.uint8, device=device)
@@ -79,17 +80,20 @@ class SelectiveStep:
         canvas = highres_prev if self.canvas is None else self.canvas
         B.avits_gather_upsample(lowres, highres_prev, prefix, self.idx, s.H_lr, s.W_lr, self.compact,
                                 self.pos[s.L + s.R:], canvas, self.mode, stream)
+        self._step_canvas = canvas
 
+    # The scatter rides on the block's last projection (the image rows'
+    # outputs go to their canvas rows from the same epilogue); scatter()
+    # then has nothing left to do.
     def block(self, stream=None):
         s = self.shape
-        B.avits_block_forward(self.compact, self.x_out, self.pos, s.L, s.R + s.k, self.weights, s.H,
-                              self.lse, self.ws_block, stream)
+        B.avits_block_forward_ex(self.compact, self.x_out, self.pos, s.L, s.R + s.k, self.weights, s.H,
+                                 lse_out=self.lse, workspace=self.ws_block, stream=stream,
+                                 scatter_idx=self.idx if s.k else None,
+                                 canvas=self._step_canvas if s.k else None)
 
     def scatter(self, highres_prev, stream=None):
-        s = self.shape
-        canvas = highres_prev if self.canvas is None else self.canvas
-        if s.k:
-            B.avits_scatter(self.x_out, self.idx, s.L + s.R, canvas, stream)
+        pass
 
     def run(self, latent_q, text_k, row_lse, feat_t, feat_prev, lowres, highres_prev, prefix, stream=None):
         self.score(latent_q, text_k, row_lse, feat_t, feat_prev, stream)

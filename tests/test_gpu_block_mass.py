@@ -1,6 +1,5 @@
-"""The text attention mass from the block's own joint attention
-(avits_block_forward_ex): per head, each row's softmax share on the text
-keys (Eq. spatial with the softmax of Eq. dit_attn), taken inside the block's
+"""avits_block_forward_ex: the text attention mass from the block's own
+joint attention, per head each row's softmax share on the text keys (Eq. spatial with the softmax of Eq. dit_attn), taken inside the block's
 attention pass, against the oracle's text mass of the block's own normalised,
 rotated q and k (oracle.block_qk then oracle.text_attention_mass).
 
@@ -8,7 +7,8 @@ The block output with the mass requested is bit-identical to the plain
 block; the accumulate flag adds to the buffer (two calls give twice one);
 forced key-piece plans (the combine kernel merging the pieces' text sums)
 give the same mass; the FLUX 1024^2 block (whose attention runs its overrun
-units in key pieces) is checked on every row.
+units in key pieces) is checked on every row.  The fused Stage-3 scatter
+is bit-identical to the block followed by avits_scatter.
 """
 import numpy as np
 import pytest
@@ -121,3 +121,47 @@ def test_block_mass_flux_1024(gpu):
     ref = _oracle_mass(w, x, pos, n_txt, ow)
     assert_close(r["mass"], ref, w.dtype, "block text mass")
     assert np.abs(r["mass"] - ref).max() < 2e-3
+
+
+# ---------------------------------------------------------------------------
+# The Stage-3 scatter fused into the block's last projection
+# (avits_block_forward_ex with scatter_idx / canvas): canvas and block output
+# bit-identical to the block followed by avits_scatter, whatever the GEMM plan
+# of that projection (split-K with its reduce kernel, unsplit, 128-wide).
+
+def _fused_vs_two_calls(gpu, w, kind, k, seed=13):
+    n_txt, n_img = w.L, w.R + w.k
+    x, pos = _inputs(w, n_txt, n_img, seed)
+    bw, _ = _weights(gpu, w, kind)
+    S = n_txt + n_img
+    t_x, t_pos = dev(x, w.dtype), dev(pos)
+    g = np.random.default_rng(seed)
+    idx = np.sort(g.permutation(w.N)[:k]).astype(np.int32)
+    canvas0 = dev(G.block_input(w, w.N, seed + 1), w.dtype)
+    c1, c2 = canvas0.clone(), canvas0.clone()
+    o1, o2 = torch.empty_like(t_x), torch.empty_like(t_x)
+    t_idx = dev(idx)
+    gpu.avits_block_forward(t_x, o1, t_pos, n_txt, n_img, bw, w.H)
+    if k:
+        gpu.avits_scatter(o1, t_idx, S - k, c1)
+    gpu.avits_block_forward_ex(t_x, o2, t_pos, n_txt, n_img, bw, w.H, scatter_idx=t_idx if k else None,
+                               canvas=c2 if k else None)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(o2), host(o1))
+    np.testing.assert_array_equal(host(c2), host(c1))
+
+
+@pytest.mark.parametrize("plan", [None, "256,3", "256,1", "128,1"])
+@pytest.mark.parametrize("kind", ["double", "single"])
+@pytest.mark.parametrize("w", [C.TINY_F32, C.TINY_BF16, C.TINY_BF16_REF], ids=lambda w: w.name)
+def test_block_fused_scatter(gpu, monkeypatch, w, kind, plan):
+    if plan:
+        monkeypatch.setenv("AVITS_GEMM_TILE_gemm_mlp_out", plan)
+        monkeypatch.setenv("AVITS_GEMM_TILE_gemm_single_out", plan)
+    for k in sorted({0, 1, w.k}):
+        _fused_vs_two_calls(gpu, w, kind, k)
+
+
+@pytest.mark.slow
+def test_block_fused_scatter_flux_1024(gpu):
+    _fused_vs_two_calls(gpu, C.FLUX_1024, "double", C.FLUX_1024.k)
