@@ -40,7 +40,8 @@ def test_stage_bytes_flux_1024():
     b = bench.stage_bytes(C.FLUX_1024)
     assert abs(b["score"] / 1e6 - 79.1) < 0.1
     assert abs(b["gather_upsample"] / 1e6 - 45.3) < 0.1
-    assert abs(b["scatter"] / 1e6 - 15.1) < 0.1
+    assert b["select"] == 0            # N = 4096: the selection runs inside the scoring call
+    assert b["scatter"] == 0           # the scatter is the last projection's second store
 
 
 def test_gemm_compulsory_bytes():
