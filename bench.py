@@ -74,6 +74,10 @@ def measured_traffic() -> dict | None:
 STAGE_TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "stages_flux1024_hbm_traffic.md")
 STAGE_SOURCES = ("score.hip", "select.hip", "select_block.h", "relayout.hip", "common.h")
 
+# Launch families (the library's per-launch timing names) of each streaming stage.
+STAGE_FAMILIES = {"score": ("score_spatial", "score_combine", "score_finalize"), "select": ("select",),
+                  "gather_upsample": ("gather_upsample",), "scatter": ("scatter",)}
+
 LEGS = ("fused_scoring", "block_mass", "select_sweep", "mixed_stage2", "batched", "workloads", "stack",
         "three_stage")
 
@@ -924,6 +928,11 @@ def main(argv=None):
         "hbm_gbs": {s: gbs(by[s], stage_ms[s]) for s in ("score", "select", "gather_upsample", "scatter")},
         "hbm_frac": {s: (round(gbs(by[s], stage_ms[s]) / PEAK_HBM_GBS, 4) if gbs(by[s], stage_ms[s]) else None)
                      for s in ("score", "select", "gather_upsample", "scatter")},
+        # The same bytes over the stage's kernels alone: the sum of their
+        # per-launch event times (no stage-boundary events or launch gaps).
+        "hbm_gbs_kernels": {s: gbs(by[s], sum(fam[f]["avg_launch_us"] * fam[f]["launches_per_step"]
+                                              for f in fs) / 1e3)
+                            for s, fs in STAGE_FAMILIES.items()},
         "select_fused_into_score": w.N <= SelectiveStep.FUSED_MAX_N,
         "scatter_fused_into_block": True,
         "stage_traffic": measured_stage_traffic(),
