@@ -357,6 +357,29 @@ int avits_block_forward_batched(const void* x_in, void* x_out, const int32_t* po
                                 float* lse_out, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_block_forward_batched_ex — avits_block_forward_batched with one set
+ * of modulation vectors per image, for images at different timesteps in
+ * one pass (Section 3.2: every image of a batch runs its own denoising
+ * schedule; with a diffusion transformer the timestep enters each block
+ * through its modulation vectors).  Image b's rows (its text rows with the
+ * text stream, its image rows with the image stream; every row with the
+ * single kind) use the modulation rows at mod + b * mod_stride elements,
+ * where mod is the stream's `mod` pointer in w: the caller lays the images'
+ * [6, D] (double) or [3, D] (single) blocks out mod_stride elements apart,
+ * e.g. as [B, 6, D] with mod_stride = 6 D.  mod_stride == 0 shares one set
+ * across the images (exactly avits_block_forward_batched).  Every other
+ * weight is shared.  The gated projections apply their per-image gates in
+ * their split-K reduce, so they always run split (the workspace of
+ * avits_block_workspace_bytes covers it).  Errors as
+ * avits_block_forward_batched; AVITS_ERR_INVALID_ARG for mod_stride < 0.
+ * ---------------------------------------------------------------------- */
+int avits_block_forward_batched_ex(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,
+                                   int32_t B, const int64_t* txt_off, const int64_t* img_off,
+                                   const avits_block_weights* w, int64_t mod_stride, int32_t H, int32_t d,
+                                   int dtype, float* lse_out, void* workspace, size_t workspace_bytes,
+                                   void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_block_qk — the first stage of a block alone (the attention probe of
  * Section 3.3.1: the queries and keys whose joint softmax defines the
  * image-to-text attention mass of Eq. spatial): for each row,

@@ -16,6 +16,7 @@ from ._binding import (  # noqa: F401
     avits_select_noalloc, avits_select_noalloc_max_n,
     avits_gather_upsample, avits_scatter, avits_joint_lse, avits_gather_upsample_batched, avits_scatter_batched,
     avits_block_workspace_bytes, avits_block_forward, avits_block_forward_ex, avits_block_forward_batched,
+    avits_block_forward_batched_ex,
     BlockWeights,
     avits_block_qk_workspace_bytes, avits_block_qk,
     avits_joint_attention_stats, avits_score_from_mass,

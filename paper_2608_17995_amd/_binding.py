@@ -80,6 +80,9 @@ _SIGS = {
     "avits_block_forward_batched": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _f32, _i32, _c_void_p, _c_void_p,
                                                    ctypes.POINTER(_BlockWeights), _i32, _i32, ctypes.c_int,
                                                    _c_void_p, _c_void_p, _size, _c_void_p]),
+    "avits_block_forward_batched_ex": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _f32, _i32, _c_void_p,
+                                                      _c_void_p, ctypes.POINTER(_BlockWeights), _i64, _i32, _i32,
+                                                      ctypes.c_int, _c_void_p, _c_void_p, _size, _c_void_p]),
     "avits_block_qk_workspace_bytes": (_size, [_i64, _i32, _i32, ctypes.c_int]),
     "avits_block_qk": (ctypes.c_int, [_c_void_p, _c_void_p, _f32, _i64, _i64, ctypes.POINTER(_BlockWeights), _i32, _i32,
                                       ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _size, _c_void_p]),
@@ -567,6 +570,26 @@ def avits_block_forward_batched(x_in, x_out, pos, txt_off, img_off, weights: Blo
     _check(load().avits_block_forward_batched(
         _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), pos_scale, B, to, io,
         ctypes.byref(weights.c), H, d, code, _dev(lse_out, "lse_out", torch.float32), wsp, wsb, _stream(stream)))
+    return x_out
+
+
+def avits_block_forward_batched_ex(x_in, x_out, pos, txt_off, img_off, weights: BlockWeights, H, mod_stride: int,
+                                   lse_out=None, workspace=None, stream=None, pos_scale=1.0):
+    """avits_block_forward_batched with image b's modulation rows at the
+    stream's mod + b * mod_stride elements (0: one set for all images)."""
+    import torch
+    S, D = x_in.shape
+    d = D // H
+    B = len(txt_off) - 1
+    code = _dtype_code(x_in)
+    ws, wsp, wsb = _workspace(workspace, avits_block_workspace_bytes(weights.kind, S, H, d, weights.c.mlp_hidden,
+                                                                     code), x_in.device)
+    to = (ctypes.c_int64 * (B + 1))(*[int(v) for v in txt_off])
+    io = (ctypes.c_int64 * (B + 1))(*[int(v) for v in img_off])
+    _check(load().avits_block_forward_batched_ex(
+        _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), pos_scale, B, to, io,
+        ctypes.byref(weights.c), int(mod_stride), H, d, code, _dev(lse_out, "lse_out", torch.float32), wsp, wsb,
+        _stream(stream)))
     return x_out
 
 

@@ -32,13 +32,14 @@ template <typename T>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, T* __restrict__ h, int64_t S,
                                                      int64_t D, int64_t n_a, const T* __restrict__ shift_a,
                                                      const T* __restrict__ scale_a, const T* __restrict__ shift_b,
-                                                     const T* __restrict__ scale_b) {
+                                                     const T* __restrict__ scale_b, const ModRows mods) {
   const int lane = threadIdx.x % kWave;
   const int64_t row = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave;
   if (row >= S) return;
   const T* xr = x + row * D;
-  const T* sh = row < n_a ? shift_a : shift_b;
-  const T* sc = row < n_a ? scale_a : scale_b;
+  const int64_t moff = mod_offset(mods, row);  // this row's image (several images in one pass)
+  const T* sh = (row < n_a ? shift_a : shift_b) + moff;
+  const T* sc = (row < n_a ? scale_a : scale_b) + moff;
   T* hr = h + row * D;
   if constexpr (sizeof(T) == 2) {
     const int64_t nchunk = D / 8;
@@ -245,7 +246,7 @@ const T* mod_row(const void* mod, int r, int64_t D) { return static_cast<const T
 // each stream (the single kind has one set for every row).
 template <typename T>
 int launch_ln_mod(const T* x, T* h, int64_t S, int64_t D, int64_t n_txt, const avits_block_weights* w, int r_shift,
-                  hipStream_t s) {
+                  hipStream_t s, const ModRows& mods = ModRows{}) {
   const dim3 rows_grid(unsigned(ceil_div64(S, 4))), blk(256);
   TimedLaunch timed("ln_mod", s);
   if (w->kind == AVITS_BLOCK_DOUBLE) {
@@ -253,11 +254,11 @@ int launch_ln_mod(const T* x, T* h, int64_t S, int64_t D, int64_t n_txt, const a
     const avits_double_stream_weights& wb = n_txt < S ? w->img : w->txt;
     hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, n_txt, mod_row<T>(wa.mod, r_shift, D),
                        mod_row<T>(wa.mod, r_shift + 1, D), mod_row<T>(wb.mod, r_shift, D),
-                       mod_row<T>(wb.mod, r_shift + 1, D));
+                       mod_row<T>(wb.mod, r_shift + 1, D), mods);
   } else {
     const void* m = w->single.mod;
     hipLaunchKernelGGL(ln_mod_kernel<T>, rows_grid, blk, 0, s, x, h, S, D, S, mod_row<T>(m, 0, D),
-                       mod_row<T>(m, 1, D), mod_row<T>(m, 0, D), mod_row<T>(m, 1, D));
+                       mod_row<T>(m, 1, D), mod_row<T>(m, 0, D), mod_row<T>(m, 1, D), mods);
   }
   return launch_status("block ln_mod");
 }
@@ -334,7 +335,7 @@ template <typename T>
 int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale, int64_t n_txt, int64_t n_img,
               const avits_block_weights* w, int H, int d, int dtype, float* lse_out, const BlockWs& ws,
               hipStream_t s, const AttnSegs* segs = nullptr, float* mass_out = nullptr, int mass_accumulate = 0,
-              const avits_block_outputs* sc = nullptr) {
+              const avits_block_outputs* sc = nullptr, const ModRows& mods = ModRows{}) {
   const int64_t S = n_txt + n_img, D = int64_t(H) * d, F = w->mlp_hidden;
   const bool dbl = w->kind == AVITS_BLOCK_DOUBLE;
   const T* x = static_cast<const T*>(x_in);
@@ -354,7 +355,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
   auto mod_row = [&](const void* mod, int r) { return static_cast<const T*>(mod) + r * D; };
 
   // 1. modulated layer norm.
-  if ((rc = launch_ln_mod<T>(x, h, S, D, n_txt, w, 0, s)) != AVITS_OK) return rc;
+  if ((rc = launch_ln_mod<T>(x, h, S, D, n_txt, w, 0, s, mods)) != AVITS_OK) return rc;
 
   // 2. QKV projection: q | k token-major, v transposed per head
   //    (+ the single block's MLP input, GELU'd beside o).
@@ -426,6 +427,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
   if (!dbl) {
     GemmArgs g{};
     g.N = D; g.K = D + F; g.n_split = g.n_split2 = g.N; g.mode0 = EPI_RESID_GATE; g.nprob = 1;
+    g.mod = mods;
     GemmProblem& p = g.p[0];
     p.A = ws.o; p.lda = D + F; p.W = w->single.w_out; p.bias = w->single.b_out; p.M = S;
     p.out0 = out; p.ld0 = D; p.resid = x; p.ldr = D; p.gate = mod_row(w->single.mod, 2);
@@ -438,9 +440,11 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
   {
     GemmArgs g{};
     g.N = D; g.K = D; g.n_split = g.n_split2 = g.N; g.mode0 = EPI_RESID_GATE; g.nprob = nst;
+    g.mod = mods;
     for (int i = 0; i < nst; ++i) {
       GemmProblem& p = g.p[i];
       const int64_t r0 = streams[i].r0;
+      p.row0 = r0;
       p.A = reinterpret_cast<T*>(ws.o) + r0 * D; p.lda = D;
       p.W = streams[i].dw->w_o; p.bias = streams[i].dw->b_o; p.M = streams[i].rows;
       p.out0 = xmid + r0 * D; p.ld0 = D; p.resid = x + r0 * D; p.ldr = D;
@@ -458,7 +462,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
     if ((rc = launch_gemm(g, dtype, s, "gemm_o", ws.partial, ws.partial_bytes,
                           sizeof(T) == 2 ? &ln : nullptr)) != AVITS_OK)
       return rc;
-    if (!(sizeof(T) == 2 && ln.done) && (rc = launch_ln_mod<T>(xmid, h, S, D, n_txt, w, 3, s)) != AVITS_OK)
+    if (!(sizeof(T) == 2 && ln.done) && (rc = launch_ln_mod<T>(xmid, h, S, D, n_txt, w, 3, s, mods)) != AVITS_OK)
       return rc;
   }
   // 7. MLP in + GELU.
@@ -478,9 +482,11 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
   {
     GemmArgs g{};
     g.N = D; g.K = F; g.n_split = g.n_split2 = g.N; g.mode0 = EPI_RESID_GATE; g.nprob = nst;
+    g.mod = mods;
     for (int i = 0; i < nst; ++i) {
       GemmProblem& p = g.p[i];
       const int64_t r0 = streams[i].r0;
+      p.row0 = r0;
       p.A = mlp + r0 * F; p.lda = F; p.W = streams[i].dw->w_mlp2; p.bias = streams[i].dw->b_mlp2;
       p.M = streams[i].rows; p.out0 = out + r0 * D; p.ld0 = D; p.resid = xmid + r0 * D; p.ldr = D;
       p.gate = mod_row(streams[i].dw->mod, 5);
@@ -614,7 +620,17 @@ extern "C" int avits_block_forward_batched(const void* x_in, void* x_out, const 
                                            const avits_block_weights* w, int32_t H, int32_t d, int dtype,
                                            float* lse_out, void* workspace, size_t workspace_bytes,
                                            void* stream) {
+  return avits_block_forward_batched_ex(x_in, x_out, pos, pos_scale, B, txt_off, img_off, w, 0, H, d, dtype, lse_out,
+                                        workspace, workspace_bytes, stream);
+}
+
+extern "C" int avits_block_forward_batched_ex(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,
+                                              int32_t B, const int64_t* txt_off, const int64_t* img_off,
+                                              const avits_block_weights* w, int64_t mod_stride, int32_t H,
+                                              int32_t d, int dtype, float* lse_out, void* workspace,
+                                              size_t workspace_bytes, void* stream) {
   AVITS_REQUIRE(B >= 1 && B <= kMaxSeqs, "block_forward_batched: B=%d outside [1, %d]", B, kMaxSeqs);
+  AVITS_REQUIRE(mod_stride >= 0, "block_forward_batched: mod_stride=%lld < 0", (long long)mod_stride);
   AVITS_REQUIRE(txt_off && img_off, "block_forward_batched: null txt_off/img_off");
   AVITS_REQUIRE(txt_off[0] == 0 && img_off[0] == 0, "block_forward_batched: offsets must start at 0");
   AttnSegs segs{};
@@ -642,8 +658,19 @@ extern "C" int avits_block_forward_batched(const void* x_in, void* x_out, const 
     return set_error(AVITS_ERR_WORKSPACE, "block_forward_batched: workspace of %zu bytes, need %zu",
                      workspace_bytes, need.bytes);
   const BlockWs ws = block_ws_layout(static_cast<char*>(workspace), w->kind, S, H, d, w->mlp_hidden, 2);
+  // Per-image modulation: segment b ends at image b's last text row,
+  // segment B + b at its last image row (rows packed by stream).
+  ModRows mods{};
+  if (mod_stride > 0 && B > 1) {
+    mods.B = B;
+    mods.stride = mod_stride;
+    for (int b = 0; b < B; ++b) {
+      mods.end[b] = txt_off[b + 1];
+      mods.end[B + b] = n_txt + img_off[b + 1];
+    }
+  }
   return run_block<bf16_t>(x_in, x_out, pos, pos_scale, n_txt, n_img, w, H, d, dtype, lse_out, ws,
-                           static_cast<hipStream_t>(stream), &segs);
+                           static_cast<hipStream_t>(stream), &segs, nullptr, 0, nullptr, mods);
 }
 
 // ---------------------------------------------------------------------------
@@ -730,11 +757,11 @@ extern "C" int avits_final_layer(const void* x, int64_t M, int64_t D, const void
     if (dtype == AVITS_BF16) {
       const bf16_t *sh = static_cast<const bf16_t*>(mod), *sc = sh + D;
       hipLaunchKernelGGL(ln_mod_kernel<bf16_t>, rows_grid, blk, 0, s, static_cast<const bf16_t*>(x),
-                         static_cast<bf16_t*>(workspace), M, D, M, sh, sc, sh, sc);
+                         static_cast<bf16_t*>(workspace), M, D, M, sh, sc, sh, sc, ModRows{});
     } else {
       const float *sh = static_cast<const float*>(mod), *sc = sh + D;
       hipLaunchKernelGGL(ln_mod_kernel<float>, rows_grid, blk, 0, s, static_cast<const float*>(x),
-                         static_cast<float*>(workspace), M, D, M, sh, sc, sh, sc);
+                         static_cast<float*>(workspace), M, D, M, sh, sc, sh, sc, ModRows{});
     }
   }
   if ((rc = launch_status("final_layer ln_mod")) != AVITS_OK) return rc;

@@ -177,8 +177,10 @@ __global__ __launch_bounds__(256) void splitk_reduce_ln_kernel(const GemmArgs a,
   const int64_t m = second ? grow - a.p[0].M : grow;
   const GemmProblem& p = second ? a.p[1] : a.p[0];
   const int64_t nchunk = a.N / 8;
+  // This row's image's gate and LN modulation (one set when a.mod.B == 0).
+  const int64_t moff = mod_offset(a.mod, p.row0 + m);
   const bf16_t* bias = static_cast<const bf16_t*>(p.bias);
-  const bf16_t* gate = static_cast<const bf16_t*>(p.gate);
+  const bf16_t* gate = static_cast<const bf16_t*>(p.gate) + moff;
   const bf16_t* res = static_cast<const bf16_t*>(p.resid) + m * p.ldr;
   bf16_t* y = static_cast<bf16_t*>(p.out0) + m * p.ld0;
   u32x4 yv[kRlnChunks];
@@ -210,8 +212,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_ln_kernel(const GemmArgs a,
     *reinterpret_cast<u32x4*>(y + n) = yv[c];
   }
   // Modulated layer norm of the bf16 row.
-  const bf16_t* sc = static_cast<const bf16_t*>(post.scale[second ? 1 : 0]);
-  const bf16_t* sh = static_cast<const bf16_t*>(post.shift[second ? 1 : 0]);
+  const bf16_t* sc = static_cast<const bf16_t*>(post.scale[second ? 1 : 0]) + moff;
+  const bf16_t* sh = static_cast<const bf16_t*>(post.shift[second ? 1 : 0]) + moff;
   bf16_t* hr = static_cast<bf16_t*>(post.out) + grow * post.ld;
   float s = 0.f;
 #pragma unroll
@@ -851,8 +853,10 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmArgs a, co
     v[0] += x0.x; v[1] += x0.y; v[2] += x0.z; v[3] += x0.w; v[4] += x1.x; v[5] += x1.y; v[6] += x1.z; v[7] += x1.w;
   }
   const bool second = grow >= a.p[0].M;
-  const GemmProblem p = second ? a.p[1] : a.p[0];
-  epilogue8(a, p, second ? grow - a.p[0].M : grow, n, v);
+  GemmProblem p = second ? a.p[1] : a.p[0];
+  const int64_t m = second ? grow - a.p[0].M : grow;
+  if (a.mod.B) p.gate = static_cast<const bf16_t*>(p.gate) + mod_offset(a.mod, p.row0 + m);  // this row's image
+  epilogue8(a, p, m, n, v);
 }
 
 // fp32 VALU GEMM: 64x64 tile, 16x16 threads, 4x4 outputs per thread.
@@ -1007,11 +1011,24 @@ int launch_gemm(const GemmArgs& a, int dtype, hipStream_t s, const char* family,
                 size_t partial_bytes, GemmPostLN* post_ln) {
   GemmPlan pl = plan_gemm(a, dtype, partial ? partial_bytes : 0, family);
   if (pl.tiles == 0) return AVITS_OK;
+  // Per-image gates are applied by the split-K reduce (the GEMM's own
+  // epilogue has one gate per launch): such a projection always runs split.
+  const bool per_image_gate = a.mod.B > 0 && a.mode0 == EPI_RESID_GATE;
+  if (per_image_gate && (pl.splits < 2 || pl.tail > 0)) {
+    pl.splits = 2;
+    pl.tail = 0;
+    pl.tail_splits = 1;
+  }
   // The reduce kernels take eight columns per thread.
   if ((pl.splits > 1 || pl.tail > 0) && (!partial || partial_bytes < gemm_partial_bytes(a, pl) || a.N % 8 != 0)) {
+    if (per_image_gate)
+      return set_error(AVITS_ERR_UNSUPPORTED, "gemm %s: per-image gates need a split-K scratch of %zu bytes and N %% 8 == 0",
+                       family ? family : "", gemm_partial_bytes(a, pl));
     pl.splits = 1;
     pl.tail = 0;
   }
+  if (per_image_gate && dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "gemm %s: per-image gates need bf16", family ? family : "");
   if (dtype == AVITS_BF16) {
     const dim3 grid(unsigned(pl.tiles * pl.splits + pl.tail * (pl.tail_splits - 1)));
     {

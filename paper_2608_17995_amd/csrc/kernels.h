@@ -18,6 +18,31 @@ enum EpiMode : int {
   EPI_STORE_T = 3,     // out[col * ld + m] = C (transposed store)
 };
 
+// Several images packed in one block pass (rows packed by stream: the text
+// rows of images 0..B-1, then their image rows), each with its own
+// modulation vectors: rows [end[i-1], end[i]) of the packed sequence form
+// segment i (end[-1] = 0), segments 0..B-1 hold the images' text rows and
+// B..2B-1 their image rows, and segment i's rows use the modulation block of
+// image i mod B, `stride` elements after the previous image's.  B == 0: one
+// modulation for every row.
+constexpr int kMaxSeqs = 16;
+struct ModRows {
+  int32_t B;
+  int64_t stride;
+  int64_t end[2 * kMaxSeqs];
+};
+
+// Element offset of packed row `row`'s modulation block.  The loop is
+// unrolled over the whole array so every index is static (a dynamically
+// indexed kernel-argument array would be copied to private memory).
+__device__ __forceinline__ int64_t mod_offset(const ModRows& m, int64_t row) {
+  if (m.B == 0) return 0;
+  int seg = 0;
+#pragma unroll
+  for (int i = 0; i < 2 * kMaxSeqs - 1; ++i) seg += (i < 2 * m.B - 1 && row >= m.end[i]) ? 1 : 0;
+  return int64_t(seg < m.B ? seg : seg - m.B) * m.stride;
+}
+
 // Output columns are split into up to three regions, [0, n_split),
 // [n_split, n_split2) and [n_split2, N); region r writes out_r with row
 // stride ld_r at column (n - region start) and applies mode_r.
@@ -43,6 +68,7 @@ struct GemmProblem {
   void* scat;
   const int32_t* scat_idx;
   int64_t scat_row0, scat_ld, scat_n;
+  int64_t row0;        // packed row of the problem's row 0 (for `mod` below)
 };
 
 struct GemmArgs {
@@ -51,6 +77,10 @@ struct GemmArgs {
   int64_t N, K;
   int64_t n_split, n_split2;  // region starts; >= N when unused
   int mode0, mode1, mode2;
+  // Per-image gates (EPI_RESID_GATE) and post-LN modulation: row m of
+  // problem p takes gate + mod_offset(mod, p.row0 + m).  Applied by the
+  // split-K reduce kernels, so launch_gemm runs such a projection split.
+  ModRows mod;
 };
 
 struct GemmPlan {
@@ -69,7 +99,8 @@ size_t gemm_partial_bytes(const GemmArgs& a, const GemmPlan& pl);
 // `family` names the timing family of the launch (see avits_timing_read).
 // Optional modulated layer norm of the GEMM's output rows, fused into the
 // split-K reduce when the GEMM is split: out = LN(y) * (1 + scale[p]) +
-// shift[p] for the rows of problem p, y the bf16 result rows (layer norm
+// shift[p] for the rows of problem p (offset per image by the launch's
+// ModRows), y the bf16 result rows (layer norm
 // without affine, eps 1e-6, biased variance, as the block's other LN).
 // `done` reports whether it ran; when not, the caller normalises itself.
 struct GemmPostLN {
@@ -96,7 +127,6 @@ inline size_t gemm_partial_reserve(int64_t S, int64_t D) { return size_t(4) * si
 // Block-diagonal attention over packed sequences: sequence b is the union
 // of two row ranges (its text rows and its image rows when the rows are
 // packed by stream); its rows attend to its own rows only.
-constexpr int kMaxSeqs = 16;
 struct AttnSegs {
   int n;                        // 0: one sequence, all rows (no segments)
   int64_t start[kMaxSeqs][2];

@@ -344,7 +344,9 @@ class BatchedStep:
                rows), [ref_b; X_prev,b[idx_b]] into image b's area and its
                canvas filled by upsampling (avits_gather_upsample, or one
                avits_gather_upsample_batched launch for stacked images)
-      block    avits_block_forward_batched over the packed rows
+      block    avits_block_forward_batched_ex over the packed rows (with
+               mod_stride > 0 each image takes its own modulation block,
+               images at different timesteps)
       scatter  canvas_b[idx_b] = image b's selected output rows (one
                avits_scatter_batched launch for stacked canvases)
 
@@ -352,10 +354,11 @@ class BatchedStep:
     """
 
     def __init__(self, shape: StepShape, ks: list, weights: B.BlockWeights, prefix_pos, dtype, device="cuda",
-                 alpha=0.5, eps=1e-8, mode=B.UP_NEAREST):
+                 alpha=0.5, eps=1e-8, mode=B.UP_NEAREST, mod_stride: int = 0):
         import torch
         s = shape
         self.shape, self.ks, self.weights, self.alpha, self.eps, self.mode = s, list(ks), weights, alpha, eps, mode
+        self.mod_stride = mod_stride
         Bn = len(self.ks)
         if not 1 <= Bn <= 16 or any(not 0 <= k <= s.N for k in self.ks):
             raise ValueError("1 <= B <= 16 images with 0 <= k_b <= N")
@@ -430,8 +433,8 @@ class BatchedStep:
                 B.avits_gather_upsample(lowres[b], highres_prev[b], ref[b] if s.R else None, idx_b, s.H_lr,
                                         s.W_lr, self.x[a0:a0 + s.R + self.ks[b]],
                                         self.pos[a0 + s.R:a0 + s.R + self.ks[b]], highres_prev[b], self.mode, stream)
-        B.avits_block_forward_batched(self.x, self.x_out, self.pos, self.txt_off, self.img_off, self.weights, s.H,
-                                      workspace=self.ws_block, stream=stream)
+        B.avits_block_forward_batched_ex(self.x, self.x_out, self.pos, self.txt_off, self.img_off, self.weights, s.H,
+                                         self.mod_stride, workspace=self.ws_block, stream=stream)
         if torch.is_tensor(highres_prev):
             B.avits_scatter_batched(self.x_out, self.idx, self.out_off, [a + s.R for a in img_rows], highres_prev,
                                     stream)
