@@ -145,6 +145,10 @@ def stage_bytes(w, e: int = 2) -> dict:
         score, select = score + select, 0
     gather = ((L + R) * D * e + k * D * e + w.N_lr * D * e + 4 * k          # reads
               + S * D * e + (N - k) * D * e + 12 * k)                       # writes
+    if e == 2 and D % 8 == 0 and D <= 4096:
+        # bf16: the gather also writes the block's first stage (the modulated
+        # layer norm of every compact row; avits_gather_upsample_ln).
+        gather += S * D * e
     scatter = 0         # the scatter rides on the block's last projection (the block stage's bytes)
     return {"score": score, "select": select, "gather_upsample": gather, "scatter": scatter}
 
@@ -949,6 +953,7 @@ def main(argv=None):
                             for s, fs in STAGE_FAMILIES.items()},
         "select_fused_into_score": w.N <= SelectiveStep.FUSED_MAX_N,
         "scatter_fused_into_block": True,
+        "ln1_fused_into_gather": step.ln_vectors is not None,
         "stage_traffic": measured_stage_traffic(),
         "algorithmic_bytes": by,
         "tokens_per_s": round(S / (ms_per_step / 1e3), 1),

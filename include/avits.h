@@ -233,6 +233,30 @@ int avits_gather_upsample_batched(const void* lowres, const void* highres_prev, 
                                   void* canvas, void* stream);
 
 /* ------------------------------------------------------------------------
+ * avits_gather_upsample_ln — avits_gather_upsample (one image, bf16) that
+ * also writes the first stage of the double block the compacted rows feed
+ * (Section 3.3.1, the block on the compacted sequence): for every compact
+ * row r < n_prefix + k,
+ *   h[r] = LN(compact[r]) (1 + scale) + shift
+ * (layer norm without affine, eps 1e-6, biased variance, fp32 arithmetic,
+ * rounded to bf16), with (shift_txt, scale_txt) for rows r < n_txt (the
+ * text rows leading the prefix) and (shift_img, scale_img) for the others
+ * (the reference rows and the selected rows: the image stream).  The
+ * shift / scale vectors are [D] bf16: rows 0 and 1 of each stream's
+ * modulation.  h is bit-identical to the block's own first stage, so
+ * avits_block_forward_ex with h_in = h_out gives the block output bit for
+ * bit.  h_out [n_prefix + k, D] bf16, not aliasing compact.  D a multiple
+ * of 8 in [8, 4096]; 0 <= n_txt <= n_prefix.  Other arguments, outputs
+ * and errors as avits_gather_upsample; dtype other than bf16 ->
+ * AVITS_ERR_UNSUPPORTED.
+ * ---------------------------------------------------------------------- */
+int avits_gather_upsample_ln(const void* lowres, const void* highres_prev, const void* prefix,
+                             const int32_t* idx, int64_t k, int32_t H_lr, int32_t W_lr, int64_t n_prefix,
+                             int64_t D, int mode, int dtype, void* compact, int32_t* pos_sel, void* canvas,
+                             int64_t n_txt, const void* shift_txt, const void* scale_txt,
+                             const void* shift_img, const void* scale_img, void* h_out, void* stream);
+
+/* ------------------------------------------------------------------------
  * avits_block_forward — one MMDiT joint-attention block on the compacted
  * sequence (Section 3.3.1: joint self-attention over [C; Z], Eq. joint_qk,
  * with the model's QK-normalisation), FLUX-style:
@@ -318,6 +342,12 @@ int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, float
  * an index outside [0, n_canvas) is skipped).  canvas [n_canvas, D] of
  * dtype, not aliasing x_in or x_out; scatter_idx [scatter_k] int32; 0 <=
  * scatter_k <= n_img.
+ * The block's first stage can come in precomputed: h_in [S, D] of dtype
+ * holds h = LN(x_in)(1 + scale1) + shift1 of every row with its stream's
+ * first two modulation rows (the single kind: its own), e.g. written by
+ * avits_gather_upsample_ln as it gathers x_in; the block then starts from
+ * it and skips its own layer norm (x_in still supplies the residual).  Not
+ * aliasing x_in, x_out or the workspace.
  * outs may be NULL (= avits_block_forward without lse).  lse and mass
  * [H, S] fp32 device buffers or NULL; other arguments and errors as
  * avits_block_forward.
@@ -330,6 +360,7 @@ typedef struct avits_block_outputs {
   int64_t scatter_k;           /* 0: no fused scatter */
   void* canvas;                /* [n_canvas, D] or NULL */
   int64_t n_canvas;
+  const void* h_in;            /* [S, D]: the first modulated layer norm, precomputed; or NULL */
 } avits_block_outputs;
 
 int avits_block_forward_ex(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,

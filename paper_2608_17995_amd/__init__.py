@@ -14,7 +14,8 @@ from ._binding import (  # noqa: F401
     avits_score_batched,
     avits_select_workspace_bytes, avits_select, avits_select_perturbed, avits_select_batched,
     avits_select_noalloc, avits_select_noalloc_max_n,
-    avits_gather_upsample, avits_scatter, avits_joint_lse, avits_gather_upsample_batched, avits_scatter_batched,
+    avits_gather_upsample, avits_gather_upsample_ln, avits_scatter, avits_joint_lse, avits_gather_upsample_batched,
+    avits_scatter_batched,
     avits_block_workspace_bytes, avits_block_forward, avits_block_forward_ex, avits_block_forward_batched,
     avits_block_forward_batched_ex,
     BlockWeights,

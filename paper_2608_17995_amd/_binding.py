@@ -32,7 +32,7 @@ class _Single(ctypes.Structure):
 class _BlockOutputs(ctypes.Structure):
     _fields_ = [("lse", ctypes.c_void_p), ("mass", ctypes.c_void_p), ("mass_accumulate", ctypes.c_int32),
                 ("scatter_idx", ctypes.c_void_p), ("scatter_k", ctypes.c_int64), ("canvas", ctypes.c_void_p),
-                ("n_canvas", ctypes.c_int64)]
+                ("n_canvas", ctypes.c_int64), ("h_in", ctypes.c_void_p)]
 
 
 class _BlockWeights(ctypes.Structure):
@@ -86,6 +86,10 @@ _SIGS = {
     "avits_block_qk_workspace_bytes": (_size, [_i64, _i32, _i32, ctypes.c_int]),
     "avits_block_qk": (ctypes.c_int, [_c_void_p, _c_void_p, _f32, _i64, _i64, ctypes.POINTER(_BlockWeights), _i32, _i32,
                                       ctypes.c_int, _c_void_p, _c_void_p, _c_void_p, _size, _c_void_p]),
+    "avits_gather_upsample_ln": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _i64, _i32, _i32, _i64,
+                                                 _i64, ctypes.c_int, ctypes.c_int, _c_void_p, _c_void_p, _c_void_p,
+                                                 _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                                                 _c_void_p]),
     "avits_scatter": (ctypes.c_int, [_c_void_p, _c_void_p, _i64, _i64, _i64, _i64, ctypes.c_int, _c_void_p,
                                      _c_void_p]),
     "avits_linear": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _i64, ctypes.c_int, _c_void_p,
@@ -310,6 +314,23 @@ def avits_gather_upsample(lowres, highres_prev, prefix, idx, H_lr, W_lr, compact
     return compact, pos_sel, canvas
 
 
+def avits_gather_upsample_ln(lowres, highres_prev, prefix, idx, H_lr, W_lr, compact, pos_sel, canvas, n_txt,
+                             shift_txt, scale_txt, shift_img, scale_img, h_out, mode=UP_NEAREST, stream=None):
+    """avits_gather_upsample plus h_out = LN(compact)(1 + scale) + shift per
+    row (text-stream vectors for the first n_txt rows, image-stream after)."""
+    import torch
+    dt = lowres.dtype
+    n_prefix = 0 if prefix is None else prefix.shape[0]
+    _check(load().avits_gather_upsample_ln(
+        _dev(lowres, "lowres"), _dev(highres_prev, "highres_prev", dt),
+        _dev(prefix, "prefix", dt) if n_prefix else None, _dev(idx, "idx", torch.int32), idx.shape[0],
+        H_lr, W_lr, n_prefix, lowres.shape[1], mode, _dtype_code(lowres), _dev(compact, "compact", dt),
+        _dev(pos_sel, "pos_sel", torch.int32), _dev(canvas, "canvas", dt), n_txt, _dev(shift_txt, "shift_txt", dt),
+        _dev(scale_txt, "scale_txt", dt), _dev(shift_img, "shift_img", dt), _dev(scale_img, "scale_img", dt),
+        _dev(h_out, "h_out", dt), _stream(stream)))
+    return compact, pos_sel, canvas, h_out
+
+
 def avits_linear(x, w, b, out, stream=None):
     """out [M, N] = x [M, K] w[N, K]^T + b [N] (b may be None)."""
     M, K = x.shape
@@ -487,12 +508,13 @@ def avits_block_forward(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H
 
 def avits_block_forward_ex(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H, lse_out=None, mass_out=None,
                            mass_accumulate=False, workspace=None, stream=None, pos_scale=1.0, scatter_idx=None,
-                           canvas=None):
+                           canvas=None, h_in=None):
     """avits_block_forward with the joint attention's statistics: lse_out and
     mass_out [H, S] fp32 (the softmax mass of each row on the text keys
     [0, n_txt), added to mass_out's contents when mass_accumulate); with
     scatter_idx [k] and canvas, the last k image rows' outputs also go to
-    canvas[scatter_idx] (the fused Stage-3 scatter)."""
+    canvas[scatter_idx] (the fused Stage-3 scatter); with h_in [S, D], the
+    first modulated layer norm comes precomputed (avits_gather_upsample_ln)."""
     import torch
     S, D = x_in.shape
     d = D // H
@@ -503,7 +525,8 @@ def avits_block_forward_ex(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights
     outs = _BlockOutputs(_dev(lse_out, "lse_out", torch.float32), _dev(mass_out, "mass_out", torch.float32),
                          1 if mass_accumulate else 0, _dev(scatter_idx, "scatter_idx", torch.int32) if k else None, k,
                          _dev(canvas, "canvas", x_in.dtype) if canvas is not None else None,
-                         canvas.shape[0] if canvas is not None else 0)
+                         canvas.shape[0] if canvas is not None else 0,
+                         _dev(h_in, "h_in", x_in.dtype) if h_in is not None else None)
     _check(load().avits_block_forward_ex(
         _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), pos_scale, n_txt, n_img,
         ctypes.byref(weights.c), H, d, code, ctypes.byref(outs), wsp, wsb, _stream(stream)))

@@ -308,7 +308,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
     for (int t = 0; t < kKT / 32; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[t][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale2;
+    mx = max_xor32(mx) * scale2;
     const bool raise = mx > mrow + 8.f;
     float corr = 1.f;
     if (raise) {
@@ -390,8 +390,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const AttnArgs a) {
     }
   }
 
-  float l = lrow + __shfl_xor(lrow, 32, kWave);
-  const float tm = trow + __shfl_xor(trow, 32, kWave);
+  float l = sum_xor32(lrow);
+  const float tm = sum_xor32(trow);
   if (row >= un.q_hi) return;
   if constexpr (WITH_V) {
     if (piece >= 0) {

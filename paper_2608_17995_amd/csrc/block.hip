@@ -16,13 +16,13 @@
 // GELU(m) beside the attention output (cat = [o, GELU(m)], [S, D + F]) ->
 // qk_norm_rope -> attention into cat -> x + gate (cat W_out^T + b).
 #include "kernels.h"
+#include "ln_row.h"
 
 namespace avits {
 namespace {
 
-constexpr float kLnEps = 1e-6f, kRmsEps = 1e-6f;
+constexpr float kRmsEps = 1e-6f;
 constexpr float kLog2Theta = 13.287712379549449f;  // log2(10000)
-constexpr int kLnMaxChunks = 8;                    // bf16 rows up to 64 * 8 * 8 = 4096 elements in registers
 
 // h = LN(x) (1 + scale) + shift, one wavefront per row; rows [0, n_a) use
 // (shift_a, scale_a), the rest (shift_b, scale_b).  bf16 rows of up to 4096
@@ -44,57 +44,13 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, T*
   if constexpr (sizeof(T) == 2) {
     const int64_t nchunk = D / 8;
     if (D % 8 == 0 && nchunk <= int64_t(kWave) * kLnMaxChunks) {
-      // All loads (row, scale, shift) are issued before the reductions.
-      u32x4 v[kLnMaxChunks], g[kLnMaxChunks], t[kLnMaxChunks];
+      u32x4 v[kLnMaxChunks];
 #pragma unroll
       for (int c = 0; c < kLnMaxChunks; ++c) {
         const int64_t idx = lane + kWave * c;
-        if (idx < nchunk) {
-          v[c] = reinterpret_cast<const u32x4*>(xr)[idx];
-          g[c] = reinterpret_cast<const u32x4*>(sc)[idx];
-          t[c] = reinterpret_cast<const u32x4*>(sh)[idx];
-        }
+        if (idx < nchunk) v[c] = reinterpret_cast<const u32x4*>(xr)[idx];
       }
-      float s = 0.f;
-#pragma unroll
-      for (int c = 0; c < kLnMaxChunks; ++c) {
-        const int64_t idx = lane + kWave * c;
-        if (idx < nchunk) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) s += __uint_as_float(v[c][e] << 16) + __uint_as_float(v[c][e] & 0xffff0000u);
-        }
-      }
-      const float mean = wave_sum(s) / float(D);
-      float q = 0.f;
-#pragma unroll
-      for (int c = 0; c < kLnMaxChunks; ++c) {
-        const int64_t idx = lane + kWave * c;
-        if (idx < nchunk) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float a = __uint_as_float(v[c][e] << 16) - mean, b = __uint_as_float(v[c][e] & 0xffff0000u) - mean;
-            q = fmaf(a, a, fmaf(b, b, q));
-          }
-        }
-      }
-      const float rstd = rsqrtf(wave_sum(q) / float(D) + kLnEps);
-#pragma unroll
-      for (int c = 0; c < kLnMaxChunks; ++c) {
-        const int64_t idx = lane + kWave * c;
-        if (idx < nchunk) {
-          u32x4 o;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float a = (__uint_as_float(v[c][e] << 16) - mean) * rstd * (1.f + __uint_as_float(g[c][e] << 16)) +
-                            __uint_as_float(t[c][e] << 16);
-            const float b = (__uint_as_float(v[c][e] & 0xffff0000u) - mean) * rstd *
-                                (1.f + __uint_as_float(g[c][e] & 0xffff0000u)) +
-                            __uint_as_float(t[c][e] & 0xffff0000u);
-            o[e] = pack_bf2(a, b);
-          }
-          reinterpret_cast<u32x4*>(hr)[idx] = o;
-        }
-      }
+      ln_mod_row_bf16<true>(v, nchunk, D, lane, sh, sc, hr);
       return;
     }
   }
@@ -182,8 +138,7 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ q, T*
     float ss = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
-#pragma unroll
-    for (int o = 1; o < kLanesPerHead; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+    ss = group_sum(ss, kLanesPerHead);
     const float r = rsqrtf(ss / float(DH) + kRmsEps);
     const float* g = head < H ? gq : gk;
 #pragma unroll
@@ -354,8 +309,10 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
   }
   auto mod_row = [&](const void* mod, int r) { return static_cast<const T*>(mod) + r * D; };
 
-  // 1. modulated layer norm.
-  if ((rc = launch_ln_mod<T>(x, h, S, D, n_txt, w, 0, s, mods)) != AVITS_OK) return rc;
+  // 1. modulated layer norm (or the caller's, computed as it gathered x).
+  const T* hq = h;
+  if (sc && sc->h_in) hq = static_cast<const T*>(sc->h_in);
+  else if ((rc = launch_ln_mod<T>(x, h, S, D, n_txt, w, 0, s, mods)) != AVITS_OK) return rc;
 
   // 2. QKV projection: q | k token-major, v transposed per head
   //    (+ the single block's MLP input, GELU'd beside o).
@@ -372,7 +329,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
       for (int i = 0; i < nst; ++i) {
         GemmProblem& p = g.p[i];
         const int64_t r0 = streams[i].r0;
-        p.A = h + r0 * D; p.lda = D;
+        p.A = hq + r0 * D; p.lda = D;
         p.W = streams[i].dw->w_qkv; p.bias = streams[i].dw->b_qkv; p.M = streams[i].rows;
         p.out0 = qk + r0 * 2 * D; p.ld0 = 2 * D;
         p.out1 = vt + r0; p.ld1 = ws.ldvt;
@@ -381,7 +338,7 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
     } else {
       g.N = 3 * D + F;
       GemmProblem& p = g.p[0];
-      p.A = h; p.lda = D; p.W = w->single.w_in; p.bias = w->single.b_in; p.M = S;
+      p.A = hq; p.lda = D; p.W = w->single.w_in; p.bias = w->single.b_in; p.M = S;
       p.out0 = qk; p.ld0 = 2 * D;
       p.out1 = vt; p.ld1 = ws.ldvt;
       p.out2 = reinterpret_cast<T*>(ws.o) + D; p.ld2 = D + F;
@@ -606,6 +563,12 @@ extern "C" int avits_block_forward_ex(const void* x_in, void* x_out, const int32
     AVITS_REQUIRE(outs->scatter_k == 0 || (outs->canvas && outs->scatter_idx && outs->n_canvas >= 1),
                   "block_forward_ex: scatter needs canvas, scatter_idx and n_canvas >= 1");
     AVITS_REQUIRE(outs->canvas != x_in && outs->canvas != x_out, "block_forward_ex: canvas must not alias x_in/x_out");
+  }
+  if (outs->h_in) {
+    const char* hb = static_cast<const char*>(outs->h_in);
+    const char* wb = static_cast<const char*>(workspace);
+    AVITS_REQUIRE(outs->h_in != x_in && outs->h_in != x_out && !(hb >= wb && hb < wb + need.bytes),
+                  "block_forward_ex: h_in must not alias x_in, x_out or the workspace");
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == AVITS_BF16)

@@ -46,21 +46,81 @@ template <> struct Elem<bf16_t> {
 template <typename T> __device__ __forceinline__ float ld(const T* p, int64_t i) { return Elem<T>::load(p, i); }
 template <typename T> __device__ __forceinline__ void st(T* p, int64_t i, float v) { Elem<T>::store(p, i, v); }
 
-// Wavefront reductions (all 64 lanes receive the result).
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+// Cross-lane exchanges that stay off the LDS pipe (a shuffle through
+// ds_bpermute waits on it for each step): DPP moves inside 16-lane rows,
+// v_permlane32_swap between the two halves of the wave, readlane.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141; // lane i <- 7 - i in each group of 8
+constexpr int kDppMirror = 0x140;     // lane i <- 15 - i in each row of 16
+
+// Lane l % 32 of each half: lo = v[l % 32], hi = v[l % 32 + 32].
+__device__ __forceinline__ void wave_halves(float v, float& lo, float& hi) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  lo = __uint_as_float(p[0]);
+  hi = __uint_as_float(p[1]);
+}
+// v + v[l ^ 32] and max(v, v[l ^ 32]) (the same bits as the shuffle forms).
+__device__ __forceinline__ float sum_xor32(float v) {
+  float lo, hi;
+  wave_halves(v, lo, hi);
+  return lo + hi;
+}
+__device__ __forceinline__ float max_xor32(float v) {
+  float lo, hi;
+  wave_halves(v, lo, hi);
+  return fmaxf(lo, hi);
+}
+
+// Sum over aligned groups of n lanes (n = 1, 2, 4, 8 or 16), every lane of a
+// group receiving it: the butterfly over lane bits 0, 1, 2, 3 in that
+// order.  Once bits below b are summed a group of 2^b lanes holds one
+// value, so the mirror moves pair the same groups as lane ^ 2^b, and the
+// result is bit for bit the xor-shuffle butterfly's.
+__device__ __forceinline__ float group_sum(float v, int n) {
+  if (n > 1) v += dpp_move<kDppXor1>(v);
+  if (n > 2) v += dpp_move<kDppXor2>(v);
+  if (n > 4) v += dpp_move<kDppHalfMirror>(v);
+  if (n > 8) v += dpp_move<kDppMirror>(v);
   return v;
+}
+
+// Wavefront reductions (all 64 lanes receive the result): each 16-lane row
+// by DPP, then the four row values, read once each, combined as
+// (row 0 + row 1) + (row 2 + row 3).
+__device__ __forceinline__ float wave_sum(float v) {
+  v = group_sum(v, 16);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (r0 + r1) + (r2 + r3);
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+  v = fmaxf(v, dpp_move<kDppXor1>(v));
+  v = fmaxf(v, dpp_move<kDppXor2>(v));
+  v = fmaxf(v, dpp_move<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_move<kDppMirror>(v));
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
 __device__ __forceinline__ float wave_min(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, kWave));
-  return v;
+  v = fminf(v, dpp_move<kDppXor1>(v));
+  v = fminf(v, dpp_move<kDppXor2>(v));
+  v = fminf(v, dpp_move<kDppHalfMirror>(v));
+  v = fminf(v, dpp_move<kDppMirror>(v));
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return fminf(fminf(r0, r1), fminf(r2, r3));
 }
 
 // Block-wide sum of one float per thread; `red` holds >= blockDim.x/64 floats.

@@ -6,6 +6,7 @@
 // chip: prefix copies, selected-row copies (+ their positions) and the
 // upsampled fill of unselected canvas rows.
 #include "common.h"
+#include "ln_row.h"
 
 namespace avits {
 namespace {
@@ -31,6 +32,16 @@ __device__ __forceinline__ void store_chunks(u32x4* __restrict__ d, int n, int i
 #pragma unroll
   for (int u = 0; u < kCopyBatch; ++u)
     if (u * kWave < left) dl[u * kWave] = r[u];
+}
+
+// A row of n <= 64 kCopyBatch chunks into registers with unconditional
+// loads: lanes past the row's end read its last chunk again (the value is
+// never used), so there is no branch per chunk and the compiler keeps one
+// copy of the array.
+__device__ __forceinline__ void load_row_clamped(const u32x4* __restrict__ s, int n, int lane,
+                                                 u32x4 (&r)[kCopyBatch]) {
+#pragma unroll
+  for (int u = 0; u < kCopyBatch; ++u) r[u] = s[min(lane + u * kWave, n - 1)];
 }
 
 // Copy `bytes` (multiple of 16) from src to dst; chunks from `from` on.
@@ -107,13 +118,33 @@ struct ImageRows {
   int64_t pos_off[kMaxRelayoutImages];
 };
 
+// Optional output of the gather (one image, bf16): the modulated layer norm
+// of every compact row, h = LN(row)(1 + scale) + shift, with (shift_a,
+// scale_a) for rows [0, n_a) and (shift_b, scale_b) for the others: the
+// first stage of the block that takes the compact rows, computed while the
+// row is in registers.
+struct LnOut {
+  bf16_t* h;  // [n_prefix + k, D], or null: no layer norm
+  int64_t n_a;
+  const bf16_t *shift_a, *scale_a, *shift_b, *scale_b;
+};
+static_assert(kCopyBatch == kLnMaxChunks, "a fused row must fit the layer norm's register layout");
+
+// Compact row `row` (its 16-byte chunks already in r, lane + 64 u): its LN.
+__device__ __forceinline__ void ln_of_row(const LnOut& ln, int64_t row, int64_t D, int lane,
+                                          const u32x4 (&r)[kCopyBatch]) {
+  const bool a = row < ln.n_a;
+  ln_mod_row_bf16<false>(r, D / 8, D, lane, a ? ln.shift_a : ln.shift_b, a ? ln.scale_a : ln.scale_b, ln.h + row * D);
+}
+
 // Image blockIdx.y of a stack of equally shaped images (lowres [B, N/4, D],
 // highres / canvas [B, N, D], prefix [B, n_prefix, D]).
 template <typename T>
 __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
     const T* __restrict__ lowres, const T* highres, const T* __restrict__ prefix,
     const int32_t* __restrict__ idx, const ImageRows im, int H_lr, int W_lr, int64_t n_prefix, int64_t D,
-    int mode, T* __restrict__ compact, int32_t* __restrict__ pos_sel, T* canvas, int canvas_aliases) {
+    int mode, T* __restrict__ compact, int32_t* __restrict__ pos_sel, T* canvas, int canvas_aliases,
+    const LnOut ln) {
   const int lane = threadIdx.x % kWave;
   const int64_t job = int64_t(blockIdx.x) * kRowsPerBlock + threadIdx.x / kWave;
   const int W_hr = 2 * W_lr;
@@ -129,6 +160,16 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
   compact += im.row_off[b] * D;
   pos_sel += im.pos_off[b] * 3;
   if (job < n_prefix) {
+    if constexpr (sizeof(T) == 2) {
+      if (ln.h) {  // the row fits one batch (the host checks D)
+        const int n = int(row_bytes / 16);
+        u32x4 r[kCopyBatch];
+        load_row_clamped(reinterpret_cast<const u32x4*>(prefix + job * D), n, lane, r);
+        store_chunks(reinterpret_cast<u32x4*>(compact + job * D), n, 0, lane, r);
+        ln_of_row(ln, job, D, lane, r);
+        return;
+      }
+    }
     wave_copy_row(reinterpret_cast<const char*>(prefix + job * D),
                   reinterpret_cast<char*>(compact + job * D), row_bytes, lane);
     return;
@@ -143,8 +184,19 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
     u32x4* to_compact = reinterpret_cast<u32x4*>(compact + (n_prefix + j) * D);
     u32x4* to_canvas = reinterpret_cast<u32x4*>(canvas + p * D);
     const int n = int(row_bytes / 16);
+    bool done = false;
+    if constexpr (sizeof(T) == 2) {
+      if (ln.h) {  // one batch holds the row
+        u32x4 r[kCopyBatch];
+        load_row_clamped(src, n, lane, r);
+        store_chunks(to_compact, n, 0, lane, r);
+        if (!canvas_aliases) store_chunks(to_canvas, n, 0, lane, r);
+        ln_of_row(ln, n_prefix + j, D, lane, r);
+        done = true;
+      }
+    }
 #pragma unroll 1
-    for (int i0 = 0; i0 < n; i0 += kCopyBatch * kWave) {
+    for (int i0 = 0; !done && i0 < n; i0 += kCopyBatch * kWave) {
       u32x4 r[kCopyBatch];
       load_chunks(src, n, i0, lane, r);
       store_chunks(to_compact, n, i0, lane, r);
@@ -320,7 +372,7 @@ namespace {
 int launch_gather(const void* lowres, const void* highres_prev, const void* prefix, const int32_t* idx,
                   const ImageRows& im, int B, int64_t k_max, int32_t H_lr, int32_t W_lr, int64_t n_prefix,
                   int64_t D, int mode, int dtype, void* compact, int32_t* pos_sel, void* canvas, void* stream,
-                  const char* who) {
+                  const char* who, const LnOut& ln = LnOut{}) {
   const int64_t N = int64_t(4) * H_lr * W_lr;
   const int64_t jobs = n_prefix + k_max + N;
   const dim3 grid(unsigned(ceil_div(jobs, kRowsPerBlock)), unsigned(B)), block(kWave * kRowsPerBlock);
@@ -330,11 +382,11 @@ int launch_gather(const void* lowres, const void* highres_prev, const void* pref
   if (dtype == AVITS_F32)
     hipLaunchKernelGGL(gather_upsample_kernel<float>, grid, block, 0, s, (const float*)lowres,
                        (const float*)highres_prev, (const float*)prefix, idx, im, H_lr, W_lr, n_prefix, D,
-                       mode, (float*)compact, pos_sel, (float*)canvas, alias);
+                       mode, (float*)compact, pos_sel, (float*)canvas, alias, LnOut{});
   else
     hipLaunchKernelGGL(gather_upsample_kernel<bf16_t>, grid, block, 0, s, (const bf16_t*)lowres,
                        (const bf16_t*)highres_prev, (const bf16_t*)prefix, idx, im, H_lr, W_lr, n_prefix, D,
-                       mode, (bf16_t*)compact, pos_sel, (bf16_t*)canvas, alias);
+                       mode, (bf16_t*)compact, pos_sel, (bf16_t*)canvas, alias, ln);
   return launch_status(who);
 }
 
@@ -412,6 +464,44 @@ extern "C" int avits_gather_upsample(const void* lowres, const void* highres_pre
   im.idx_off[1] = k;
   return launch_gather(lowres, highres_prev, prefix, idx, im, 1, k, H_lr, W_lr, n_prefix, D, mode, dtype, compact,
                        pos_sel, canvas, stream, "gather_upsample");
+}
+
+extern "C" int avits_gather_upsample_ln(const void* lowres, const void* highres_prev, const void* prefix,
+                                        const int32_t* idx, int64_t k, int32_t H_lr, int32_t W_lr,
+                                        int64_t n_prefix, int64_t D, int mode, int dtype, void* compact,
+                                        int32_t* pos_sel, void* canvas, int64_t n_txt, const void* shift_txt,
+                                        const void* scale_txt, const void* shift_img, const void* scale_img,
+                                        void* h_out, void* stream) {
+  if (dtype != AVITS_BF16)
+    return set_error(AVITS_ERR_UNSUPPORTED, "gather_upsample_ln: dtype %d unsupported (bf16 only)", dtype);
+  AVITS_REQUIRE(D >= 8 && D % 8 == 0 && D <= int64_t(kWave) * kCopyBatch * 8,
+                "gather_upsample_ln: D=%lld must be a multiple of 8 in [8, %d]", (long long)D, kWave * kCopyBatch * 8);
+  AVITS_REQUIRE(n_txt >= 0 && n_txt <= n_prefix, "gather_upsample_ln: n_txt=%lld outside [0, n_prefix=%lld]",
+                (long long)n_txt, (long long)n_prefix);
+  AVITS_REQUIRE(n_prefix + k == 0 || h_out, "gather_upsample_ln: null h_out");
+  AVITS_REQUIRE(h_out == nullptr || h_out != compact, "gather_upsample_ln: h_out must not alias compact");
+  AVITS_REQUIRE(n_txt == 0 || (shift_txt && scale_txt), "gather_upsample_ln: null text-stream shift/scale");
+  AVITS_REQUIRE(n_prefix + k == n_txt || (shift_img && scale_img), "gather_upsample_ln: null image-stream shift/scale");
+  AVITS_REQUIRE(H_lr >= 1 && W_lr >= 1, "gather_upsample_ln: H_lr=%d W_lr=%d must be >= 1", H_lr, W_lr);
+  const int64_t N = int64_t(4) * H_lr * W_lr;
+  AVITS_REQUIRE(k >= 0 && k <= N, "gather_upsample_ln: k=%lld outside [0, N=%lld]", (long long)k, (long long)N);
+  AVITS_REQUIRE(n_prefix >= 0, "gather_upsample_ln: n_prefix=%lld < 0", (long long)n_prefix);
+  AVITS_REQUIRE(mode == AVITS_UP_NEAREST || mode == AVITS_UP_BILINEAR, "gather_upsample_ln: bad mode %d", mode);
+  AVITS_REQUIRE(lowres && highres_prev && canvas, "gather_upsample_ln: null lowres/highres_prev/canvas");
+  AVITS_REQUIRE(n_prefix == 0 || prefix, "gather_upsample_ln: null prefix with n_prefix=%lld", (long long)n_prefix);
+  AVITS_REQUIRE(n_prefix + k == 0 || compact, "gather_upsample_ln: null compact");
+  AVITS_REQUIRE(k == 0 || (idx && pos_sel), "gather_upsample_ln: null idx/pos_sel with k=%lld", (long long)k);
+  ImageRows im{};
+  im.idx_off[1] = k;
+  LnOut ln{};
+  ln.h = static_cast<bf16_t*>(h_out);
+  ln.n_a = n_txt;
+  ln.shift_a = static_cast<const bf16_t*>(shift_txt);
+  ln.scale_a = static_cast<const bf16_t*>(scale_txt);
+  ln.shift_b = static_cast<const bf16_t*>(shift_img);
+  ln.scale_b = static_cast<const bf16_t*>(scale_img);
+  return launch_gather(lowres, highres_prev, prefix, idx, im, 1, k, H_lr, W_lr, n_prefix, D, mode, dtype, compact,
+                       pos_sel, canvas, stream, "gather_upsample_ln", ln);
 }
 
 extern "C" int avits_scatter(const void* out, const int32_t* idx, int64_t k, int64_t row_offset, int64_t D,

@@ -108,7 +108,11 @@ __global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
       const float d1 = __uint_as_float(x[e] & 0xffff0000u) - __uint_as_float(y[e] & 0xffff0000u);
       acc = fmaf(d0, d0, fmaf(d1, d1, acc));
     }
-    for (int o = 1; o < nch; o <<= 1) acc += __shfl_xor(acc, o, kWave);
+    if (nch <= 16) {
+      acc = group_sum(acc, int(nch));
+    } else {
+      for (int o = 1; o < nch; o <<= 1) acc += __shfl_xor(acc, o, kWave);
+    }
     const int rr = wrow0 + j * rpi + r_in;
     if (cc == 0 && rr < N) part_v[int64_t(h) * N + rr] = acc;
   };
@@ -206,7 +210,7 @@ __global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
     tile(1, k0 + kSpKeys, kb, ka);
   }
   psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
-  psum += __shfl_xor(psum, 32, kWave);
+  psum = sum_xor32(psum);
   if (hi == 0 && row < N) part_a[int64_t(h) * N + row] = psum;
   // Pairs left when the slice has more pairs than there are key tiles:
   // issued in batches so their loads overlap instead of waiting one after

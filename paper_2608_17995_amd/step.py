@@ -56,6 +56,16 @@ class SelectiveStep:
         self.ws_block = torch.empty(
             max(B.avits_block_workspace_bytes(weights.kind, s.S, s.H, d, s.mlp_hidden, code), 1),
             dtype=torch.uint8, device=device)
+        # bf16 double block: the gather also writes the block's first stage
+        # (the modulated layer norm of every compact row) while each row is
+        # in registers, and the block starts from it.
+        self.ln_vectors = None
+        if code == B.BF16 and weights.kind == B.BLOCK_DOUBLE and s.D % 8 == 0 and s.D <= 4096:
+            mt, mi = weights.tensors["txt"].get("mod"), weights.tensors["img"].get("mod")
+            if mi is not None:
+                mt = mi if mt is None else mt
+                self.ln_vectors = (mt[0], mt[1], mi[0], mi[1])
+                self.h = torch.empty(s.S, s.D, dtype=dtype, device=device)
 
     # Up to 8192 scored tokens the selection runs inside the scoring call
     # (avits_score_select, one launch less); select() then has nothing left
@@ -78,8 +88,13 @@ class SelectiveStep:
     def gather(self, lowres, highres_prev, prefix, stream=None):
         s = self.shape
         canvas = highres_prev if self.canvas is None else self.canvas
-        B.avits_gather_upsample(lowres, highres_prev, prefix, self.idx, s.H_lr, s.W_lr, self.compact,
-                                self.pos[s.L + s.R:], canvas, self.mode, stream)
+        if self.ln_vectors is not None:
+            B.avits_gather_upsample_ln(lowres, highres_prev, prefix, self.idx, s.H_lr, s.W_lr, self.compact,
+                                       self.pos[s.L + s.R:], canvas, s.L, *self.ln_vectors, self.h, self.mode,
+                                       stream)
+        else:
+            B.avits_gather_upsample(lowres, highres_prev, prefix, self.idx, s.H_lr, s.W_lr, self.compact,
+                                    self.pos[s.L + s.R:], canvas, self.mode, stream)
         self._step_canvas = canvas
 
     # The scatter rides on the block's last projection (the image rows'
@@ -90,7 +105,8 @@ class SelectiveStep:
         B.avits_block_forward_ex(self.compact, self.x_out, self.pos, s.L, s.R + s.k, self.weights, s.H,
                                  lse_out=self.lse, workspace=self.ws_block, stream=stream,
                                  scatter_idx=self.idx if s.k else None,
-                                 canvas=self._step_canvas if s.k else None)
+                                 canvas=self._step_canvas if s.k else None,
+                                 h_in=self.h if self.ln_vectors is not None else None)
 
     def scatter(self, highres_prev, stream=None):
         pass

@@ -39,7 +39,7 @@ def test_stage_bytes_flux_1024():
     from synth import configs as C
     b = bench.stage_bytes(C.FLUX_1024)
     assert abs(b["score"] / 1e6 - 79.1) < 0.1
-    assert abs(b["gather_upsample"] / 1e6 - 45.3) < 0.1
+    assert abs(b["gather_upsample"] / 1e6 - 56.0) < 0.1   # 45.3 MB of relayout + the block's first stage (10.7 MB)
     assert b["select"] == 0            # N = 4096: the selection runs inside the scoring call
     assert b["scatter"] == 0           # the scatter is the last projection's second store
 
