@@ -348,6 +348,15 @@ int avits_block_forward(const void* x_in, void* x_out, const int32_t* pos, float
  * avits_gather_upsample_ln as it gathers x_in; the block then starts from
  * it and skips its own layer norm (x_in still supplies the residual).  Not
  * aliasing x_in, x_out or the workspace.
+ * And the next block's first stage can go out: with h_next and next_w set,
+ * h_next [S, D] of dtype receives LN(x_out)(1 + scale1) + shift1 with the
+ * next block's first two modulation rows (double: its text-stream rows for
+ * rows < n_txt, its image-stream rows after; single: its own), bit for bit
+ * what that block computes first; pass it there as h_in.  In a stack of
+ * blocks this replaces one layer-norm launch per block (it rides on the
+ * split-K reduce of the last projection, as the block's second layer norm
+ * rides on the output projection's).  Not aliasing x_in, x_out, h_in or the
+ * workspace; next_w is read on the host only.
  * outs may be NULL (= avits_block_forward without lse).  lse and mass
  * [H, S] fp32 device buffers or NULL; other arguments and errors as
  * avits_block_forward.
@@ -361,6 +370,8 @@ typedef struct avits_block_outputs {
   void* canvas;                /* [n_canvas, D] or NULL */
   int64_t n_canvas;
   const void* h_in;            /* [S, D]: the first modulated layer norm, precomputed; or NULL */
+  void* h_next;                /* [S, D]: the next block's first stage, or NULL */
+  const struct avits_block_weights* next_w;  /* that block's weights (host struct), or NULL */
 } avits_block_outputs;
 
 int avits_block_forward_ex(const void* x_in, void* x_out, const int32_t* pos, float pos_scale,

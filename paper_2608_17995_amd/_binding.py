@@ -32,7 +32,8 @@ class _Single(ctypes.Structure):
 class _BlockOutputs(ctypes.Structure):
     _fields_ = [("lse", ctypes.c_void_p), ("mass", ctypes.c_void_p), ("mass_accumulate", ctypes.c_int32),
                 ("scatter_idx", ctypes.c_void_p), ("scatter_k", ctypes.c_int64), ("canvas", ctypes.c_void_p),
-                ("n_canvas", ctypes.c_int64), ("h_in", ctypes.c_void_p)]
+                ("n_canvas", ctypes.c_int64), ("h_in", ctypes.c_void_p), ("h_next", ctypes.c_void_p),
+                ("next_w", ctypes.c_void_p)]
 
 
 class _BlockWeights(ctypes.Structure):
@@ -508,13 +509,15 @@ def avits_block_forward(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H
 
 def avits_block_forward_ex(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights, H, lse_out=None, mass_out=None,
                            mass_accumulate=False, workspace=None, stream=None, pos_scale=1.0, scatter_idx=None,
-                           canvas=None, h_in=None):
+                           canvas=None, h_in=None, h_next=None, next_weights=None):
     """avits_block_forward with the joint attention's statistics: lse_out and
     mass_out [H, S] fp32 (the softmax mass of each row on the text keys
     [0, n_txt), added to mass_out's contents when mass_accumulate); with
     scatter_idx [k] and canvas, the last k image rows' outputs also go to
     canvas[scatter_idx] (the fused Stage-3 scatter); with h_in [S, D], the
-    first modulated layer norm comes precomputed (avits_gather_upsample_ln)."""
+    first modulated layer norm comes precomputed (avits_gather_upsample_ln
+    or the previous block's h_next); with h_next [S, D] and next_weights,
+    the next block's first stage is written from this block's output."""
     import torch
     S, D = x_in.shape
     d = D // H
@@ -526,7 +529,9 @@ def avits_block_forward_ex(x_in, x_out, pos, n_txt, n_img, weights: BlockWeights
                          1 if mass_accumulate else 0, _dev(scatter_idx, "scatter_idx", torch.int32) if k else None, k,
                          _dev(canvas, "canvas", x_in.dtype) if canvas is not None else None,
                          canvas.shape[0] if canvas is not None else 0,
-                         _dev(h_in, "h_in", x_in.dtype) if h_in is not None else None)
+                         _dev(h_in, "h_in", x_in.dtype) if h_in is not None else None,
+                         _dev(h_next, "h_next", x_in.dtype) if h_next is not None else None,
+                         ctypes.addressof(next_weights.c) if next_weights is not None else None)
     _check(load().avits_block_forward_ex(
         _dev(x_in, "x_in"), _dev(x_out, "x_out", x_in.dtype), _dev(pos, "pos", torch.int32), pos_scale, n_txt, n_img,
         ctypes.byref(weights.c), H, d, code, ctypes.byref(outs), wsp, wsb, _stream(stream)))

@@ -371,6 +371,15 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
   }
 
   T* out = static_cast<T*>(x_out);
+  // The next block's first stage (its LN + modulation of this block's
+  // output) rides on the last projection's split-K reduce when the GEMM is
+  // split and each problem's rows take one set of the next block's vectors;
+  // otherwise the LN kernel runs on x_out.
+  const bool want_next = sc && sc->h_next && sc->next_w;
+  auto finish_next = [&](const T* y, const GemmPostLN& nl, bool fused) -> int {
+    if (!want_next || (fused && sizeof(T) == 2 && nl.done)) return AVITS_OK;
+    return launch_ln_mod<T>(y, static_cast<T*>(sc->h_next), S, D, n_txt, sc->next_w, 0, s, mods);
+  };
   // The Stage-3 scatter rides on the last projection: the output rows of the
   // last scatter_k image rows also go to their canvas rows.
   auto set_scatter = [&](GemmProblem& p, int64_t rows) {
@@ -389,7 +398,20 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
     p.A = ws.o; p.lda = D + F; p.W = w->single.w_out; p.bias = w->single.b_out; p.M = S;
     p.out0 = out; p.ld0 = D; p.resid = x; p.ldr = D; p.gate = mod_row(w->single.mod, 2);
     set_scatter(p, S);
-    return launch_gemm(g, dtype, s, "gemm_single_out", ws.partial, ws.partial_bytes);
+    // The next block's first stage on the reduce when that block is single
+    // too (one set of vectors for the launch's one problem).
+    GemmPostLN nl{};
+    const bool fuse_next = want_next && sc->next_w->kind == AVITS_BLOCK_SINGLE;
+    if (fuse_next) {
+      nl.out = sc->h_next;
+      nl.ld = D;
+      nl.shift[0] = mod_row(sc->next_w->single.mod, 0);
+      nl.scale[0] = mod_row(sc->next_w->single.mod, 1);
+    }
+    if ((rc = launch_gemm(g, dtype, s, "gemm_single_out", ws.partial, ws.partial_bytes,
+                          sizeof(T) == 2 && fuse_next ? &nl : nullptr)) != AVITS_OK)
+      return rc;
+    return finish_next(out, nl, fuse_next);
   }
 
   // 5. output projection + gated residual.
@@ -449,9 +471,24 @@ int run_block(const void* x_in, void* x_out, const int32_t* pos, float pos_scale
       p.gate = mod_row(streams[i].dw->mod, 5);
       if (r0 == n_txt && n_img > 0) set_scatter(p, n_img);   // the image stream
     }
-    if ((rc = launch_gemm(g, dtype, s, "gemm_mlp_out", ws.partial, ws.partial_bytes)) != AVITS_OK) return rc;
+    GemmPostLN nl{};
+    if (want_next) {
+      nl.out = sc->h_next;
+      nl.ld = D;
+      for (int i = 0; i < nst; ++i) {
+        const avits_block_weights* nw = sc->next_w;
+        const void* m = nw->kind == AVITS_BLOCK_SINGLE ? nw->single.mod
+                        : streams[i].r0 < n_txt       ? nw->txt.mod
+                                                      : nw->img.mod;
+        nl.shift[i] = mod_row(m, 0);
+        nl.scale[i] = mod_row(m, 1);
+      }
+    }
+    if ((rc = launch_gemm(g, dtype, s, "gemm_mlp_out", ws.partial, ws.partial_bytes,
+                          sizeof(T) == 2 && want_next ? &nl : nullptr)) != AVITS_OK)
+      return rc;
+    return finish_next(out, nl, want_next);
   }
-  return AVITS_OK;
 }
 
 bool all_set(const avits_double_stream_weights& w) {
@@ -564,11 +601,22 @@ extern "C" int avits_block_forward_ex(const void* x_in, void* x_out, const int32
                   "block_forward_ex: scatter needs canvas, scatter_idx and n_canvas >= 1");
     AVITS_REQUIRE(outs->canvas != x_in && outs->canvas != x_out, "block_forward_ex: canvas must not alias x_in/x_out");
   }
+  const char* wb = static_cast<const char*>(workspace);
   if (outs->h_in) {
     const char* hb = static_cast<const char*>(outs->h_in);
-    const char* wb = static_cast<const char*>(workspace);
     AVITS_REQUIRE(outs->h_in != x_in && outs->h_in != x_out && !(hb >= wb && hb < wb + need.bytes),
                   "block_forward_ex: h_in must not alias x_in, x_out or the workspace");
+  }
+  if (outs->h_next || outs->next_w) {
+    AVITS_REQUIRE(outs->h_next && outs->next_w, "block_forward_ex: h_next and next_w go together");
+    const avits_block_weights* nw = outs->next_w;
+    AVITS_REQUIRE(nw->kind == AVITS_BLOCK_DOUBLE ? (nw->txt.mod || n_txt == 0) && (nw->img.mod || n_img == 0)
+                                                 : nw->kind == AVITS_BLOCK_SINGLE && nw->single.mod != nullptr,
+                  "block_forward_ex: next_w lacks the modulation its rows need");
+    const char* hb = static_cast<const char*>(outs->h_next);
+    AVITS_REQUIRE(outs->h_next != x_in && outs->h_next != x_out && outs->h_next != outs->h_in &&
+                      !(hb >= wb && hb < wb + need.bytes),
+                  "block_forward_ex: h_next must not alias x_in, x_out, h_in or the workspace");
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dtype == AVITS_BF16)

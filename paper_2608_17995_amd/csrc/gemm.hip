@@ -210,6 +210,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_ln_kernel(const GemmArgs a,
       yv[c][e] = pack_bf2(lo, hi);
     }
     *reinterpret_cast<u32x4*>(y + n) = yv[c];
+    scatter_copy<bf16_t>(p, m, n, yv[c]);
   }
   // Modulated layer norm of the bf16 row.
   const bf16_t* sc = static_cast<const bf16_t*>(post.scale[second ? 1 : 0]) + moff;

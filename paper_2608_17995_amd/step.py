@@ -31,6 +31,28 @@ class StepShape:
         return self.L + self.R + self.k
 
 
+def run_chain(blocks, cur, out_of, hbuf, pos, L: int, S: int, H: int, ws, stream=None, pos_scale=1.0,
+              on_block=None, mass=None, n_mass: int = 0):
+    """The blocks in order on the rows cur [S, D]: block i writes out_of(i);
+    each block's first stage (LN + modulation) comes from the block before
+    it, written by that block's last split-K reduce into hbuf[i % 2]
+    (avits_block_forward_ex h_next -> h_in), so a stack of n blocks runs one
+    layer-norm launch instead of n.  mass (with n_mass) accumulates the text
+    mass of the first n_mass blocks.  Returns the last output."""
+    n = len(blocks)
+    for i, w in enumerate(blocks):
+        nxt = out_of(i)
+        nw = blocks[i + 1] if i + 1 < n else None
+        B.avits_block_forward_ex(cur, nxt, pos, L, S - L, w, H, mass_out=mass if i < n_mass else None,
+                                 mass_accumulate=True, workspace=ws, stream=stream, pos_scale=pos_scale,
+                                 h_in=hbuf[i % 2][:S] if i else None,
+                                 h_next=hbuf[(i + 1) % 2][:S] if nw is not None else None, next_weights=nw)
+        if on_block is not None:
+            on_block(i, cur, nxt)
+        cur = nxt
+    return cur
+
+
 class SelectiveStep:
     def __init__(self, shape: StepShape, weights: B.BlockWeights, prefix_pos, dtype, device="cuda",
                  alpha=0.5, eps=1e-8, mode=B.UP_NEAREST, canvas=None, keep_lse=False):
@@ -176,6 +198,7 @@ class StackStep:
         self.pos = torch.empty(s.S, 3, dtype=i32, device=device)
         self.pos[:LR].copy_(self.prefix_pos)
         self.x = [torch.empty(s.S, s.D, dtype=dtype, device=device) for _ in range(2)]
+        self.hbuf = [torch.empty(s.S, s.D, dtype=dtype, device=device) for _ in range(2)]
         self.ws_score = torch.empty(max(B.avits_score_workspace_bytes(s.N, s.H), 1), dtype=torch.uint8, device=device)
         self.ws_select = torch.empty(max(B.avits_select_workspace_bytes(s.N), 1), dtype=torch.uint8, device=device)
         need = max(B.avits_block_qk_workspace_bytes(max(LR, s.N), s.H, d, code),
@@ -224,14 +247,8 @@ class StackStep:
             B.avits_select(self.scores, s.k, self.idx, self.ws_select, stream)
         B.avits_gather_upsample(lowres, x_prev, prefix if LR else None, self.idx, s.H_lr, s.W_lr, self.compact,
                                 self.pos[LR:], canvas, self.mode, stream)
-        cur = self.compact
-        blocks = self.doubles + self.singles
-        for i, w in enumerate(blocks):
-            nxt = self.x[i % 2]
-            B.avits_block_forward(cur, nxt, self.pos, s.L, s.R + s.k, w, s.H, None, self.ws_block, stream)
-            if on_block is not None:
-                on_block(i, cur, nxt)
-            cur = nxt
+        cur = run_chain(self.doubles + self.singles, self.compact, lambda i: self.x[i % 2], self.hbuf, self.pos, s.L,
+                        s.S, s.H, self.ws_block, stream, on_block=on_block)
         self.out = cur
         if s.k:
             B.avits_scatter(cur, self.idx, LR, canvas, stream)
@@ -296,6 +313,7 @@ class MixedStage2:
         if LR:
             B.avits_scale_positions(prefix_pos, 2, self.pos[:LR])   # half units
         self.buf = [torch.empty(self.S, D, dtype=dtype, device=device) for _ in range(2)]
+        self.hbuf = [torch.empty(self.S, D, dtype=dtype, device=device) for _ in range(2)]
         self.ws_score = torch.empty(max(B.avits_score_workspace_bytes(Mp, H), 1), dtype=torch.uint8, device=device)
         self.ws_select = torch.empty(max(B.avits_select_workspace_bytes(Mp), 1), dtype=torch.uint8, device=device)
         need = max(B.avits_block_qk_workspace_bytes(max(LR, Mp), H, d, code),
@@ -327,14 +345,8 @@ class MixedStage2:
     def step(self, stream=None, on_block=None):
         """One pass of the block stack over the mixed sequence; the result
         becomes the sequence the next step reads."""
-        cur = self.x
-        for i, w in enumerate(self.doubles + self.singles):
-            nxt = self.buf[i % 2]
-            B.avits_block_forward(cur, nxt, self.pos, self.L, self.S - self.L, w, self.H, None, self.ws_block,
-                                  stream, pos_scale=0.5)
-            if on_block is not None:
-                on_block(i, cur, nxt)
-            cur = nxt
+        cur = run_chain(self.doubles + self.singles, self.x, lambda i: self.buf[i % 2], self.hbuf, self.pos, self.L,
+                        self.S, self.H, self.ws_block, stream, pos_scale=0.5, on_block=on_block)
         self.x, self.buf[(len(self.doubles) + len(self.singles) - 1) % 2] = cur, self.x
         return self.x
 
@@ -493,6 +505,7 @@ class SelectedEuler:
         if tuple(self.pos.shape) != (S, 3):
             raise ValueError("pos must hold the positions of [text; ref; selected] rows")
         self.x = [torch.empty(S, D, dtype=dtype, device=device) for _ in range(2)]
+        self.hbuf = [torch.empty(S, D, dtype=dtype, device=device) for _ in range(2)]
         self.v = torch.empty(k, C, dtype=dtype, device=device)
         self.prefix_rows = torch.arange(L + R, dtype=torch.int32, device=device)
         d = D // H
@@ -511,14 +524,10 @@ class SelectedEuler:
         if s0:
             B.avits_scatter(prefix, self.prefix_rows, 0, self.x[0], stream)
         B.avits_linear(z_sel, self.embed_w, self.embed_b, self.x[0][s0:], stream)
-        cur = 0
-        for i, w in enumerate(self.doubles + self.singles):
-            B.avits_block_forward(self.x[cur], self.x[1 - cur], self.pos, self.L, self.R + self.k, w, self.H,
-                                  workspace=self.ws_block, stream=stream)
-            if on_block is not None:
-                on_block(i, self.x[cur], self.x[1 - cur])
-            cur = 1 - cur
-        self.last = self.x[cur]
+        S = self.L + self.R + self.k
+        last = run_chain(self.doubles + self.singles, self.x[0], lambda i: self.x[(i + 1) % 2], self.hbuf, self.pos,
+                         self.L, S, self.H, self.ws_block, stream, on_block=on_block)
+        self.last = last
         B.avits_final_layer(self.last[s0:], self.final_mod, self.final_w, self.final_b, self.v,
                             workspace=self.ws_final, stream=stream)
         B.avits_euler_update(z_sel, self.v, dt, stream)
@@ -590,6 +599,7 @@ class ThreeStageSampler:
         self.state = mk(Mp, C)
         self.g_rows, self.g_pos = mk(max(4 * K, 1), C), mk(max(4 * K, 1), 3, dt=i32)
         self.x = [mk(self.S3, D) for _ in range(2)]
+        self.hbuf = [mk(self.S3, D) for _ in range(2)]
         prefix_pos = torch.as_tensor(prefix_pos, dtype=i32).to(device)
         self.pos1, self.pos2, self.pos3 = mk(self.S1, 3, dt=i32), mk(self.S2, 3, dt=i32), mk(self.S3, 3, dt=i32)
         if L:
@@ -615,12 +625,9 @@ class ThreeStageSampler:
         if L:
             B.avits_scatter(prefix, self.prefix_rows[:L], 0, x0, stream)
         B.avits_linear(z, self.sw["embed_w"], self.sw["embed_b"], x0[L:], stream)
-        cur, nxt = x0, x1
-        for i, w in enumerate(self.doubles + self.singles):
-            mass = self.mass if collect and i < len(self.doubles) else None
-            B.avits_block_forward_ex(cur, nxt, pos, L, S - L, w, self.H, mass_out=mass, mass_accumulate=True,
-                                     workspace=self.ws_block, stream=stream, pos_scale=pos_scale)
-            cur, nxt = nxt, cur
+        cur = run_chain(self.doubles + self.singles, x0, lambda i: (x1, x0)[i % 2], self.hbuf, pos, L, S, self.H,
+                        self.ws_block, stream, pos_scale=pos_scale, mass=self.mass if collect else None,
+                        n_mass=len(self.doubles))
         B.avits_final_layer(cur[L:], self.sw["final_mod"], self.sw["final_w"], self.sw["final_b"], v,
                             workspace=self.ws_final, stream=stream)
         B.avits_euler_update(z, v, dt, stream)
