@@ -858,6 +858,23 @@ def main(argv=None):
     torch.cuda.synchronize()
     ms_with_lse = (time.perf_counter() - t0) * 1e3 / args.steps
 
+    # Timed region 1c: the distribution of single steps (>= 50, each between
+    # two events on the stream, the input sets rotating) -> median, p10, p90.
+    n_dist = max(50, args.steps)
+    ev_d = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_dist)]
+    torch.cuda.synchronize()
+    for i in range(n_dist):
+        ev_d[i][0].record()
+        run_step(i)
+        ev_d[i][1].record()
+    torch.cuda.synchronize()
+    step_ms = sorted(a.elapsed_time(b) for a, b in ev_d)
+
+    def pct(q):
+        return round(step_ms[min(len(step_ms) - 1, int(round(q * (len(step_ms) - 1))))], 4)
+    step_dist = {"steps": n_dist, "median_ms": pct(0.5), "p10_ms": pct(0.1), "p90_ms": pct(0.9),
+                 "note": "each step between two HIP events on the launch stream"}
+
     # Timed region 2: the same K steps with stage events on the stream and the
     # library's own HIP events around every internal launch -> per-stage and
     # per-kernel times, the roofline of the dominant kernel.
@@ -956,7 +973,9 @@ def main(argv=None):
         "ln1_fused_into_gather": step.ln_vectors is not None,
         "stage_traffic": measured_stage_traffic(),
         "algorithmic_bytes": by,
+        "step_ms_distribution": step_dist,
         "tokens_per_s": round(S / (ms_per_step / 1e3), 1),
+        "tokens_per_s_block": round(S / (stage_ms["block"] / 1e3), 1),
         "canvas_tokens_per_s": round(w.N / (ms_per_step / 1e3), 1),
         "joint_lse_ms_untimed_setup": round(joint_lse_ms, 4),
         "input_generation_s": round(t_gen, 1),
