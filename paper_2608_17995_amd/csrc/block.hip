@@ -93,20 +93,25 @@ __device__ __forceinline__ void store8(float* p, const float (&x)[8]) {
 // ld = 2D; the probe passes two [S, D] arrays, ld = D).  Each lane owns 8 consecutive elements
 // (4 rotation pairs) of one head, so a d-wide head spans d/8 lanes and the
 // RMS reduction stays inside that lane group.  Rows [0, n_a) use the gains
-// of stream a.  One wavefront walks the 2H heads of a row, 64*8/d heads at a
-// time.
+// of stream a.  A wavefront takes kQkPasses passes of 64*8/d heads of one
+// row (a row's 2H heads are split over `parts` wavefronts, so that short
+// sequences still put several wavefronts on every SIMD); all its loads are
+// in flight before its first store.
+constexpr int kQkPasses = 4;
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ q, T* __restrict__ k, int64_t ld,
                                                            const int32_t* __restrict__ pos, float pos_scale,
-                                                           int64_t S, int H, int64_t n_a, const T* __restrict__ gq_a,
-                                                           const T* __restrict__ gk_a, const T* __restrict__ gq_b,
-                                                           const T* __restrict__ gk_b) {
+                                                           int64_t S, int H, int parts, int64_t n_a,
+                                                           const T* __restrict__ gq_a, const T* __restrict__ gk_a,
+                                                           const T* __restrict__ gq_b, const T* __restrict__ gk_b) {
   constexpr int kLanesPerHead = DH / 8;
   constexpr int kHeadsPerPass = kWave / kLanesPerHead;
   constexpr int p0 = DH / 16, p1 = 7 * DH / 32;  // rotation pairs per axis: (p0, p1, p1)
   const int lane = threadIdx.x % kWave;
-  const int64_t row = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave;
+  const int64_t gw = int64_t(blockIdx.x) * 4 + threadIdx.x / kWave;
+  const int64_t row = gw / parts;
   if (row >= S) return;
+  const int h0 = int(gw % parts) * kQkPasses * kHeadsPerPass;
   const int sub = lane % kLanesPerHead;           // position of the lane inside its head
   const int hoff = lane / kLanesPerHead;          // head slot within a pass
   const bool a_rows = row < n_a;
@@ -128,27 +133,36 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ q, T*
   float gq[8], gk[8];
   load8(a_rows ? gq_a : gq_b, 8 * sub, gq);
   load8(a_rows ? gk_a : gk_b, 8 * sub, gk);
-  for (int h0 = 0; h0 < 2 * H; h0 += kHeadsPerPass) {
-    const int head = h0 + hoff;                  // 0..H-1 query heads, H..2H-1 key heads
-    const bool live = head < 2 * H;
-    const int hh = live ? head : 0;
-    T* p = (hh < H ? qrow + int64_t(hh) * DH : krow + int64_t(hh - H) * DH) + 8 * sub;
-    float x[8];
-    load8(p, 0, x);
-    float ss = 0.f;
+  // Head slots 0..H-1 are query heads, H..2H-1 key heads; a slot past the
+  // end loads head 0 and is not stored.
+  auto at = [&](int head) {
+    return (head < H ? qrow + int64_t(head) * DH : krow + int64_t(head - H) * DH) + 8 * sub;
+  };
+  {
+    float x[kQkPasses][8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
-    ss = group_sum(ss, kLanesPerHead);
-    const float r = rsqrtf(ss / float(DH) + kRmsEps);
-    const float* g = head < H ? gq : gk;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float y0 = x[2 * j] * r * g[2 * j];
-      const float y1 = x[2 * j + 1] * r * g[2 * j + 1];
-      x[2 * j] = y0 * cs[j] - y1 * sn[j];
-      x[2 * j + 1] = y0 * sn[j] + y1 * cs[j];
+    for (int i = 0; i < kQkPasses; ++i) {
+      const int head = h0 + i * kHeadsPerPass + hoff;
+      load8(at(head < 2 * H ? head : 0), 0, x[i]);
     }
-    if (live) store8(p, x);
+#pragma unroll
+    for (int i = 0; i < kQkPasses; ++i) {
+      const int head = h0 + i * kHeadsPerPass + hoff;
+      float ss = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss = fmaf(x[i][e], x[i][e], ss);
+      ss = group_sum(ss, kLanesPerHead);
+      const float r = rsqrtf(ss / float(DH) + kRmsEps);
+      const float* g = head < H ? gq : gk;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float y0 = x[i][2 * j] * r * g[2 * j];
+        const float y1 = x[i][2 * j + 1] * r * g[2 * j + 1];
+        x[i][2 * j] = y0 * cs[j] - y1 * sn[j];
+        x[i][2 * j + 1] = y0 * sn[j] + y1 * cs[j];
+      }
+      if (head < 2 * H) store8(at(head), x[i]);
+    }
   }
 }
 
@@ -235,14 +249,15 @@ int launch_qk_norm_rope(T* q, T* k, int64_t ld, const int32_t* pos, float pos_sc
     gka = gkb = static_cast<const T*>(w->single.g_k);
     na = S;
   }
-  const dim3 rows_grid(unsigned(ceil_div64(S, 4))), blk(256);
+  const int parts = int(ceil_div64(2 * int64_t(H), int64_t(kQkPasses) * (kWave * 8 / d)));
+  const dim3 grid(unsigned(ceil_div64(S * parts, 4))), blk(256);
   TimedLaunch timed("qk_rope", s);
   if (d == 128)
-    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 128>), rows_grid, blk, 0, s, q, k, ld, pos, pos_scale, S, H, na, gqa,
-                       gka, gqb, gkb);
+    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 128>), grid, blk, 0, s, q, k, ld, pos, pos_scale, S, H, parts, na,
+                       gqa, gka, gqb, gkb);
   else
-    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 64>), rows_grid, blk, 0, s, q, k, ld, pos, pos_scale, S, H, na, gqa,
-                       gka, gqb, gkb);
+    hipLaunchKernelGGL((qk_norm_rope_kernel<T, 64>), grid, blk, 0, s, q, k, ld, pos, pos_scale, S, H, parts, na,
+                       gqa, gka, gqb, gkb);
   return launch_status("block qk_norm_rope");
 }
 
