@@ -50,7 +50,9 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const T* __restrict__ x, T*
         const int64_t idx = lane + kWave * c;
         if (idx < nchunk) v[c] = reinterpret_cast<const u32x4*>(xr)[idx];
       }
-      ln_mod_row_bf16<true>(v, nchunk, D, lane, sh, sc, hr);
+      u32x4 g[kLnMaxChunks], t[kLnMaxChunks];
+      ln_mod_vectors(sh, sc, nchunk, lane, g, t);
+      ln_mod_row_bf16(v, g, t, nchunk, D, lane, hr);
       return;
     }
   }

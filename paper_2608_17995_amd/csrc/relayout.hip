@@ -130,11 +130,18 @@ struct LnOut {
 };
 static_assert(kCopyBatch == kLnMaxChunks, "a fused row must fit the layer norm's register layout");
 
-// Compact row `row` (its 16-byte chunks already in r, lane + 64 u): its LN.
-__device__ __forceinline__ void ln_of_row(const LnOut& ln, int64_t row, int64_t D, int lane,
-                                          const u32x4 (&r)[kCopyBatch]) {
+// Compact row `row`: its scale and shift chunks (issued right after the
+// row's own loads, so both latencies overlap), then its LN once the row is
+// in r (lane + 64 u).
+__device__ __forceinline__ void ln_vectors_of_row(const LnOut& ln, int64_t row, int64_t D, int lane,
+                                                  u32x4 (&g)[kLnMaxChunks], u32x4 (&t)[kLnMaxChunks]) {
   const bool a = row < ln.n_a;
-  ln_mod_row_bf16<false>(r, D / 8, D, lane, a ? ln.shift_a : ln.shift_b, a ? ln.scale_a : ln.scale_b, ln.h + row * D);
+  ln_mod_vectors(a ? ln.shift_a : ln.shift_b, a ? ln.scale_a : ln.scale_b, D / 8, lane, g, t);
+}
+__device__ __forceinline__ void ln_of_row(const LnOut& ln, int64_t row, int64_t D, int lane,
+                                          const u32x4 (&r)[kCopyBatch], const u32x4 (&g)[kLnMaxChunks],
+                                          const u32x4 (&t)[kLnMaxChunks]) {
+  ln_mod_row_bf16(r, g, t, D / 8, D, lane, ln.h + row * D);
 }
 
 // Image blockIdx.y of a stack of equally shaped images (lowres [B, N/4, D],
@@ -163,10 +170,11 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
     if constexpr (sizeof(T) == 2) {
       if (ln.h) {  // the row fits one batch (the host checks D)
         const int n = int(row_bytes / 16);
-        u32x4 r[kCopyBatch];
+        u32x4 r[kCopyBatch], g[kLnMaxChunks], t[kLnMaxChunks];
         load_row_clamped(reinterpret_cast<const u32x4*>(prefix + job * D), n, lane, r);
+        ln_vectors_of_row(ln, job, D, lane, g, t);
         store_chunks(reinterpret_cast<u32x4*>(compact + job * D), n, 0, lane, r);
-        ln_of_row(ln, job, D, lane, r);
+        ln_of_row(ln, job, D, lane, r, g, t);
         return;
       }
     }
@@ -187,11 +195,12 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
     bool done = false;
     if constexpr (sizeof(T) == 2) {
       if (ln.h) {  // one batch holds the row
-        u32x4 r[kCopyBatch];
+        u32x4 r[kCopyBatch], g[kLnMaxChunks], t[kLnMaxChunks];
         load_row_clamped(src, n, lane, r);
+        ln_vectors_of_row(ln, n_prefix + j, D, lane, g, t);
         store_chunks(to_compact, n, 0, lane, r);
         if (!canvas_aliases) store_chunks(to_canvas, n, 0, lane, r);
-        ln_of_row(ln, n_prefix + j, D, lane, r);
+        ln_of_row(ln, n_prefix + j, D, lane, r, g, t);
         done = true;
       }
     }
