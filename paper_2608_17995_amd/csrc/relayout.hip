@@ -4,7 +4,9 @@
 // with 16-byte vector accesses; a row is D elements (6 KiB for D = 3072 bf16).
 // One launch covers every row job of the gather so small grids never idle the
 // chip: prefix copies, selected-row copies (+ their positions) and the
-// upsampled fill of unselected canvas rows.
+// upsampled fill of unselected canvas rows (nearest: one job per low-res
+// token, which reads its row once and writes its unselected 2x2 children;
+// bilinear: one job per high-res pixel).
 #include "common.h"
 #include "ln_row.h"
 
@@ -218,17 +220,38 @@ __global__ __launch_bounds__(kWave * kRowsPerBlock) void gather_upsample_kernel(
     }
     return;
   }
+  if (mode == AVITS_UP_NEAREST) {
+    // Low-res token q: its children p00, p00 + 1 (row 2r) and p10, p10 + 1
+    // (row 2r + 1) all take its row; the selected ones (idx ascending and
+    // unique, so p00 + 1 follows p00 there if both are in it) are skipped.
+    const int64_t q = j - k;
+    if (q >= N / 4) return;
+    const int64_t p00 = 2 * (q / W_lr) * W_hr + 2 * (q % W_lr), p10 = p00 + W_hr;
+    const int64_t a0 = wave_lower_bound(idx, k, p00, lane), a1 = wave_lower_bound(idx, k, p10, lane);
+    const bool s00 = a0 < k && idx[a0] == p00;
+    const bool s01 = a0 + s00 < k && idx[a0 + s00] == p00 + 1;
+    const bool s10 = a1 < k && idx[a1] == p10;
+    const bool s11 = a1 + s10 < k && idx[a1 + s10] == p10 + 1;
+    const u32x4* src = reinterpret_cast<const u32x4*>(lowres + q * D);
+    u32x4* const dst[4] = {reinterpret_cast<u32x4*>(canvas + p00 * D), reinterpret_cast<u32x4*>(canvas + (p00 + 1) * D),
+                           reinterpret_cast<u32x4*>(canvas + p10 * D), reinterpret_cast<u32x4*>(canvas + (p10 + 1) * D)};
+    const bool keep[4] = {!s00, !s01, !s10, !s11};
+    const int n = int(row_bytes / 16);
+#pragma unroll 1
+    for (int i0 = 0; i0 < n; i0 += kCopyBatch * kWave) {
+      u32x4 r[kCopyBatch];
+      load_chunks(src, n, i0, lane, r);
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (keep[c]) store_chunks(dst[c], n, i0, lane, r);
+    }
+    return;
+  }
   const int64_t p = j - k;
   if (p >= N) return;
   const int64_t at = wave_lower_bound(idx, k, p, lane);
   if (at < k && idx[at] == p) return;  // selected: handled by its own job
-  if (mode == AVITS_UP_NEAREST) {
-    const int64_t src_row = int64_t((p / W_hr) >> 1) * W_lr + ((p % W_hr) >> 1);
-    wave_copy_row(reinterpret_cast<const char*>(lowres + src_row * D),
-                  reinterpret_cast<char*>(canvas + p * D), row_bytes, lane);
-  } else {
-    bilinear_row(lowres, canvas + p * D, p, H_lr, W_lr, D, lane);
-  }
+  bilinear_row(lowres, canvas + p * D, p, H_lr, W_lr, D, lane);
 }
 
 // Image blockIdx.y: its selection idx[idx_off[b] ..), its rows of `out`
@@ -383,7 +406,7 @@ int launch_gather(const void* lowres, const void* highres_prev, const void* pref
                   int64_t D, int mode, int dtype, void* compact, int32_t* pos_sel, void* canvas, void* stream,
                   const char* who, const LnOut& ln = LnOut{}) {
   const int64_t N = int64_t(4) * H_lr * W_lr;
-  const int64_t jobs = n_prefix + k_max + N;
+  const int64_t jobs = n_prefix + k_max + (mode == AVITS_UP_NEAREST ? N / 4 : N);
   const dim3 grid(unsigned(ceil_div(jobs, kRowsPerBlock)), unsigned(B)), block(kWave * kRowsPerBlock);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int alias = canvas == highres_prev;
