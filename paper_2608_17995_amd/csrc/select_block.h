@@ -65,22 +65,29 @@ constexpr int kRegKeys = 16;
 // the k largest keys (ties: lowest index) to idx in ascending order.
 __device__ __forceinline__ void select_block_keys(const uint32_t (&keys)[kRegKeys], int N, int k,
                                                   int32_t* __restrict__ idx) {
-  __shared__ uint32_t hist[kWaves][256];   // per-wave histograms: atomics contend only inside a wave
-  __shared__ uint32_t tot_s[256], suf_s[256];
+  // Per-wave histograms (atomics contend only inside a wave), two sets: pass
+  // p counts into set p mod 2 while the other set is cleared for pass p + 1,
+  // so a pass needs two workgroup barriers (after the counts, after the
+  // digit pick), not five.
+  __shared__ __attribute__((aligned(16))) uint32_t hist[2][kWaves][256];
   __shared__ uint32_t wsum[kWaves];
   __shared__ uint32_t s_digit, s_above;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = (N + kThreads - 1) / kThreads;
 
+  for (int b = tid; b < kWaves * 256; b += kThreads) (&hist[0][0][0])[b] = 0u;
+  __syncthreads();
   uint32_t prefix = 0u, mask = 0u;
   uint32_t remaining = uint32_t(k);  // rank of the k-th largest among the current candidates
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int b = tid; b < kWaves * 256; b += kThreads) (&hist[0][0])[b] = 0u;
-    __syncthreads();
+#pragma unroll 1
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass, cur = pass & 1;
+    if (pass < 3)
+      for (int b = tid; b < kWaves * 256; b += kThreads) (&hist[cur ^ 1][0][0])[b] = 0u;
     // Scores of one exponent share their top digits, so a wave first adds
     // its most frequent-looking digit(s) with one ballot-counted atomic
     // (two rounds in the first pass, one later), then the rest one by one.
-    const int rounds = shift == 24 ? 2 : 1;
+    const int rounds = pass == 0 ? 2 : 1;
 #pragma unroll
     for (int j = 0; j < kRegKeys; ++j) {
       if (j >= q) break;  // uniform
@@ -94,47 +101,42 @@ __device__ __forceinline__ void select_block_keys(const uint32_t (&keys)[kRegKey
         const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
         const uint32_t d0 = __shfl(digit, leader, kWave);
         const uint64_t same = __ballot(pending && digit == d0);
-        if (lane == leader) atomicAdd(&hist[wave][d0], uint32_t(__popcll(same)));
+        if (lane == leader) atomicAdd(&hist[cur][wave][d0], uint32_t(__popcll(same)));
         pending = pending && digit != d0;
       }
-      if (pending) atomicAdd(&hist[wave][digit], 1u);
+      if (pending) atomicAdd(&hist[cur][wave][digit], 1u);
     }
     __syncthreads();
-    // Waves 0..3 own digits 64w .. 64w + 63: the count per digit and its
-    // suffix sum inside the wave (shuffle scan from the high lanes down).
-    if (wave < 4) {
-      const int b = 64 * wave + lane;
-      uint32_t c = 0u;
+    // Wave 0 picks the digit: lane l owns digits 4 l .. 4 l + 3 (their
+    // counts over the per-wave histograms), the suffix sum over the lanes
+    // above it gives the candidates above its digits, and the selected
+    // digit b has (candidates above b) < remaining <= (candidates at or
+    // above b).
+    if (wave == 0) {
+      u32x4 c = {0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) c += hist[w][b];
-      uint32_t suf = c;
+      for (int w = 0; w < kWaves; ++w) c += *reinterpret_cast<const u32x4*>(&hist[cur][w][4 * lane]);
+      const uint32_t own = c[0] + c[1] + c[2] + c[3];
+      uint32_t suf = own;
 #pragma unroll
       for (int o = 1; o < kWave; o <<= 1) {
         const uint32_t t = __shfl_down(suf, o, kWave);
         if (lane + o < kWave) suf += t;
       }
-      tot_s[b] = c;
-      suf_s[b] = suf;
-      if (lane == 0) wsum[wave] = suf;  // this wave's 64 digits in total
-    }
-    __syncthreads();
-    // The selected digit b has (candidates above b) < remaining <= (candidates at or above b).
-    if (wave < 4) {
-      const int b = 64 * wave + lane;
-      uint32_t higher = 0u;
-      for (int w = wave + 1; w < 4; ++w) higher += wsum[w];
-      const uint32_t c = tot_s[b];
-      const uint32_t above = suf_s[b] - c + higher;
-      if (above < remaining && above + c >= remaining) {
-        s_digit = uint32_t(b);
-        s_above = above;
+      uint32_t above = suf - own;
+#pragma unroll
+      for (int e = 3; e >= 0; --e) {
+        if (above < remaining && above + c[e] >= remaining) {
+          s_digit = uint32_t(4 * lane + e);
+          s_above = above;
+        }
+        above += c[e];
       }
     }
     __syncthreads();
     prefix |= s_digit << shift;
     mask |= 255u << shift;
     remaining -= s_above;
-    __syncthreads();
   }
   // T = prefix; `remaining` elements equal to T are still needed.  One
   // workgroup scan of the per-thread counts of keys > T and == T gives each
