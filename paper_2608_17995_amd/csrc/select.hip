@@ -134,11 +134,36 @@ __global__ __launch_bounds__(kGT) void select_hist_kernel(const float* __restric
     }
     if (pending) atomicAdd(&h[digit], 1u);
   };
-  const int64_t groups = (N + 3) / 4;
-  for (int64_t g = int64_t(blockIdx.x) * kGT + tid; g - tid < groups; g += int64_t(gridDim.x) * kGT) {
+  // Grid-stride over groups of four keys, the next group's 16-byte loads in
+  // flight while the current group is counted (groups that are not whole
+  // or not 16-byte aligned take load_keys4's element path instead).
+  const int64_t groups = (N + 3) / 4, stride = int64_t(gridDim.x) * kGT;
+  const bool al = (reinterpret_cast<uintptr_t>(scores) & 15) == 0 &&
+                  (!delta || (reinterpret_cast<uintptr_t>(delta) & 15) == 0);
+  float4 rv = make_float4(0.f, 0.f, 0.f, 0.f), rd = rv;
+  auto issue = [&](int64_t i0) {
+    if (al && i0 + 3 < N) {
+      rv = *reinterpret_cast<const float4*>(scores + i0);
+      if (delta) rd = *reinterpret_cast<const float4*>(delta + i0);
+    }
+  };
+  int64_t g = int64_t(blockIdx.x) * kGT + tid;
+  issue(4 * g);
+  for (; g - tid < groups; g += stride) {
     uint32_t key[4];
     bool live[4];
-    load_keys4(scores, delta, N, 4 * g, key, live);  // past the end: live = false
+    const int64_t i0 = 4 * g;
+    if (al && i0 + 3 < N) {
+      float4 v = rv;
+      if (delta) {
+        v.x += rd.x; v.y += rd.y; v.z += rd.z; v.w += rd.w;
+      }
+      key[0] = order_key(v.x); key[1] = order_key(v.y); key[2] = order_key(v.z); key[3] = order_key(v.w);
+      live[0] = live[1] = live[2] = live[3] = true;
+    } else {
+      load_keys4(scores, delta, N, i0, key, live);  // past the end: live = false
+    }
+    issue(4 * (g + stride));
 #pragma unroll
     for (int e = 0; e < 4; ++e) count(key[e], live[e]);
   }
