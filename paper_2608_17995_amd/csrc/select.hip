@@ -127,7 +127,7 @@ __global__ __launch_bounds__(kGT) void select_hist_kernel(const float* __restric
       const uint64_t act = __ballot(pending);
       if (act == 0) break;
       const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
-      const uint32_t d0 = __shfl(digit, leader, kWave);
+      const uint32_t d0 = __builtin_amdgcn_readlane(digit, leader);  // leader is wave-uniform
       const uint64_t same = __ballot(pending && digit == d0);
       if (lane == leader) atomicAdd(&h[d0], uint32_t(__popcll(same)));
       pending = pending && digit != d0;

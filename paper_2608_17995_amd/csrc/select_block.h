@@ -99,7 +99,7 @@ __device__ __forceinline__ void select_block_keys(const uint32_t (&keys)[kRegKey
         const uint64_t act = __ballot(pending);
         if (act == 0) break;
         const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
-        const uint32_t d0 = __shfl(digit, leader, kWave);
+        const uint32_t d0 = __builtin_amdgcn_readlane(digit, leader);  // leader is wave-uniform
         const uint64_t same = __ballot(pending && digit == d0);
         if (lane == leader) atomicAdd(&hist[cur][wave][d0], uint32_t(__popcll(same)));
         pending = pending && digit != d0;
