@@ -182,12 +182,7 @@ __global__ __launch_bounds__(256) void select_scan_kernel(int pass, SelState* __
   __shared__ uint32_t wsum[4];
   const int b = threadIdx.x, wave = b / kWave, lane = b % kWave;
   const uint32_t c = st->hist[pass][b];
-  uint32_t suf = c;  // suffix sum inside the wave, high lanes down
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t t = __shfl_down(suf, o, kWave);
-    if (lane + o < kWave) suf += t;
-  }
+  const uint32_t suf = wave_incl_suffix_u32(c);  // suffix sum inside the wave, high lanes down
   if (lane == 0) wsum[wave] = suf;
   __syncthreads();
   uint32_t higher = 0u;
@@ -219,12 +214,7 @@ __device__ __forceinline__ void chunk_keys(const float* __restrict__ scores, con
 // Exclusive scan over a kGT-thread workgroup; *total gets the sum.
 __device__ __forceinline__ uint32_t grid_block_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  uint32_t incl = v;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t t = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += t;
-  }
+  const uint32_t incl = wave_incl_scan_u32(v);
   __syncthreads();
   if (lane == kWave - 1) wsum[wave] = incl;
   __syncthreads();
@@ -338,13 +328,8 @@ __global__ __launch_bounds__(kGT) void select_emit_kernel(const float* __restric
     uint32_t mine = 0u;
 #pragma unroll
     for (int e = 0; e < 4; ++e) mine += live[r][e] ? ((key[r][e] > T) << 16) | uint32_t(key[r][e] == T) : 0u;
-    uint32_t incl = mine;  // wave inclusive scan of the packed counts
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const uint32_t t = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += t;
-    }
-    const uint32_t ex = incl - mine, all = __shfl(incl, kWave - 1, kWave);
+    const uint32_t incl = wave_incl_scan_u32(mine);  // wave inclusive scan of the packed counts
+    const uint32_t ex = incl - mine, all = __builtin_amdgcn_readlane(incl, kWave - 1);
     uint32_t g = gt_b + (ex >> 16), q = eq_b + (ex & 0xffffu);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {

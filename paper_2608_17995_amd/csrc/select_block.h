@@ -27,21 +27,45 @@ __device__ __forceinline__ uint32_t key_at(const float* __restrict__ scores, con
   return order_key(delta ? scores[i] + delta[i] : scores[i]);
 }
 
+// Integer wave scans without the LDS pipe: DPP row shifts inside each
+// 16-lane row (lanes shifted in from outside the row read 0), then the row
+// totals by readlane.  Integer sums, so any order gives the same result.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, 0xf, 0xf, true));
+}
+constexpr int kDppShr1 = 0x111, kDppShl1 = 0x101;  // row_shr:n = 0x110 + n, row_shl:n = 0x100 + n
+// Inclusive prefix sum over the wave (lane l gets the sum of lanes 0 .. l).
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
+  v += dpp_u32<kDppShr1>(v);
+  v += dpp_u32<kDppShr1 + 1>(v);
+  v += dpp_u32<kDppShr1 + 3>(v);
+  v += dpp_u32<kDppShr1 + 7>(v);
+  const uint32_t t0 = __builtin_amdgcn_readlane(v, 15), t1 = __builtin_amdgcn_readlane(v, 31),
+                 t2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = int(threadIdx.x % kWave) / 16;
+  return v + (row > 0 ? t0 : 0u) + (row > 1 ? t1 : 0u) + (row > 2 ? t2 : 0u);
+}
+// Inclusive suffix sum over the wave (lane l gets the sum of lanes l .. 63).
+__device__ __forceinline__ uint32_t wave_incl_suffix_u32(uint32_t v) {
+  v += dpp_u32<kDppShl1>(v);
+  v += dpp_u32<kDppShl1 + 1>(v);
+  v += dpp_u32<kDppShl1 + 3>(v);
+  v += dpp_u32<kDppShl1 + 7>(v);
+  const uint32_t r1 = __builtin_amdgcn_readlane(v, 16), r2 = __builtin_amdgcn_readlane(v, 32),
+                 r3 = __builtin_amdgcn_readlane(v, 48);
+  const int row = int(threadIdx.x % kWave) / 16;
+  return v + (row < 1 ? r1 : 0u) + (row < 2 ? r2 : 0u) + (row < 3 ? r3 : 0u);
+}
+// Sum over the wave, every lane receiving it.
 __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  return __builtin_amdgcn_readlane(wave_incl_scan_u32(v), kWave - 1);
 }
 
 // Exclusive prefix sum over the workgroup; returns the total in *total.
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  uint32_t incl = v;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t t = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += t;
-  }
+  const uint32_t incl = wave_incl_scan_u32(v);
   __syncthreads();
   if (lane == kWave - 1) wsum[wave] = incl;
   __syncthreads();
@@ -117,13 +141,7 @@ __device__ __forceinline__ void select_block_keys(const uint32_t (&keys)[kRegKey
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) c += *reinterpret_cast<const u32x4*>(&hist[cur][w][4 * lane]);
       const uint32_t own = c[0] + c[1] + c[2] + c[3];
-      uint32_t suf = own;
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t t = __shfl_down(suf, o, kWave);
-        if (lane + o < kWave) suf += t;
-      }
-      uint32_t above = suf - own;
+      uint32_t above = wave_incl_suffix_u32(own) - own;
 #pragma unroll
       for (int e = 3; e >= 0; --e) {
         if (above < remaining && above + c[e] >= remaining) {
