@@ -119,12 +119,14 @@ __global__ __launch_bounds__(256, 3) void spatial_temporal_bf16_kernel(
   u32x4 cx, cy;  // the feature pair of the current key tile
 
   // ---- spatial: Q^T fragments (B operand), lane = row l32, dims 16c + 8hi .. +7 ----
+  // Each load reads 32 bytes from each of 32 rows, so the eight loads share
+  // every cache line: plain loads, which keep the lines for the next ones (a
+  // streaming hint here makes the query read markedly slower).
   bf16x8 qf[kC];
   {
     const bf16_t* src = q + int64_t(min(row, N - 1)) * qstride + int64_t(h) * DH + 8 * hi;
 #pragma unroll
-    for (int c = 0; c < kC; ++c)
-      qf[c] = as_bf16x8(__builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + 16 * c)));
+    for (int c = 0; c < kC; ++c) qf[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(src + 16 * c));
   }
   const float lse2 = row < N ? lse[int64_t(h) * N + row] * kLog2e : 0.f;
   const float scale2 = kLog2e * rsqrtf(float(DH));
