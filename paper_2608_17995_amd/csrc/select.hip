@@ -119,20 +119,34 @@ __global__ __launch_bounds__(kGT) void select_hist_kernel(const float* __restric
   // most frequent-looking digits with one atomic each (ballot) before the
   // remaining lanes add one by one; later passes, whose digits are spread,
   // aggregate only one (which also bounds the cost of heavily tied scores).
+  // A thread's four keys go through each round together: one leader digit,
+  // one ballot per key, one atomic for all of them.
   const int rounds = pass == 0 ? 2 : 1;
-  auto count = [&](uint32_t key, bool ok) {
-    bool pending = ok && (key & mask) == prefix;
-    const uint32_t digit = (key >> shift) & 255u;
+  auto count4 = [&](const uint32_t (&key)[4], const bool (&ok)[4]) {
+    bool pending[4];
+    uint32_t digit[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      pending[e] = ok[e] && (key[e] & mask) == prefix;
+      digit[e] = (key[e] >> shift) & 255u;
+    }
     for (int it = 0; it < rounds; ++it) {
-      const uint64_t act = __ballot(pending);
+      const uint64_t act = __ballot(pending[0] || pending[1] || pending[2] || pending[3]);
       if (act == 0) break;
       const int leader = __ffsll(static_cast<unsigned long long>(act)) - 1;
-      const uint32_t d0 = __builtin_amdgcn_readlane(digit, leader);  // leader is wave-uniform
-      const uint64_t same = __ballot(pending && digit == d0);
-      if (lane == leader) atomicAdd(&h[d0], uint32_t(__popcll(same)));
-      pending = pending && digit != d0;
+      const uint32_t first = pending[0] ? digit[0] : pending[1] ? digit[1] : pending[2] ? digit[2] : digit[3];
+      const uint32_t d0 = __builtin_amdgcn_readlane(first, leader);  // leader is wave-uniform
+      uint32_t total = 0u;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        total += uint32_t(__popcll(__ballot(pending[e] && digit[e] == d0)));
+        pending[e] = pending[e] && digit[e] != d0;
+      }
+      if (lane == leader) atomicAdd(&h[d0], total);
     }
-    if (pending) atomicAdd(&h[digit], 1u);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (pending[e]) atomicAdd(&h[digit[e]], 1u);
   };
   // Grid-stride over groups of four keys, the next group's 16-byte loads in
   // flight while the current group is counted (groups that are not whole
@@ -164,8 +178,7 @@ __global__ __launch_bounds__(kGT) void select_hist_kernel(const float* __restric
       load_keys4(scores, delta, N, i0, key, live);  // past the end: live = false
     }
     issue(4 * (g + stride));
-#pragma unroll
-    for (int e = 0; e < 4; ++e) count(key[e], live[e]);
+    count4(key, live);
   }
   __syncthreads();
   for (int b = tid; b < 256; b += kGT) {
