@@ -99,7 +99,7 @@ __device__ __forceinline__ void store8(float* p, const float (&x)[8]) {
 // row (a row's 2H heads are split over `parts` wavefronts, so that short
 // sequences still put several wavefronts on every SIMD); all its loads are
 // in flight before its first store.
-constexpr int kQkPasses = 4;
+constexpr int kQkPasses = 3;
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ q, T* __restrict__ k, int64_t ld,
                                                            const int32_t* __restrict__ pos, float pos_scale,
