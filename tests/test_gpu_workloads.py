@@ -226,3 +226,39 @@ def test_step_is_deterministic(run):
     np.testing.assert_array_equal(host(step.x_out), run["x_out"])
     np.testing.assert_array_equal(host(step.lse), run["lse_block"])
     np.testing.assert_array_equal(host(d["canvas"]), run["canvas_scatter"])
+
+
+def test_step_graph_replay(run):
+    """The whole step captured in a HIP graph (the library allocates, sets
+    and synchronises nothing inside a call): every replay, with eager steps
+    and synchronisations between the replays, equals the eager results bit
+    for bit."""
+    d = run["dev"]
+    step = d["step"]
+
+    def one():
+        step.score(d["latent_q"], d["text_k"], d["lse"], d["high"], d["feat_prev"])
+        step.select()
+        step.gather(d["low"], d["high"], d["prefix"])
+        step.block()
+        step.scatter(d["high"])
+
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        one()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        d["canvas"].fill_(0)
+        step.x_out.fill_(0)
+        graph.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(step.scores.cpu().numpy(), run["scores"], err_msg=f"replay {rep}")
+        np.testing.assert_array_equal(step.idx.cpu().numpy(), run["idx"], err_msg=f"replay {rep}")
+        np.testing.assert_array_equal(host(step.compact), run["compact"], err_msg=f"replay {rep}")
+        np.testing.assert_array_equal(host(step.x_out), run["x_out"], err_msg=f"replay {rep}")
+        np.testing.assert_array_equal(host(step.lse), run["lse_block"], err_msg=f"replay {rep}")
+        np.testing.assert_array_equal(host(d["canvas"]), run["canvas_scatter"], err_msg=f"replay {rep}")
+        one()  # eager work between replays
+        torch.cuda.synchronize()
+    del graph
